@@ -1,0 +1,178 @@
+"""Oracle of the LoPA iteration (arXiv 2512.16229, Sec. 3.1-3.2, Alg. 1, Eq. 1-2).
+
+TEST INFRASTRUCTURE ONLY (see oracle/__init__.py). Plain numpy / Python loops.
+
+State of one active block: tokens [L] (a position is unfilled iff it holds
+mask_id), conf [L] and pred [L] from the forward pass on exactly these tokens.
+
+Readings of points the paper leaves open (each also listed in the design doc):
+  * Conf / candidate: greedy token and its probability (model.py).
+  * Eq. 1 compares strictly (conf > tau); every argmax picks the lowest index
+    among equal values.
+  * Top-k of Alg. 1 step 2: order by (conf descending, position ascending);
+    k_eff = min(k, |M_B0|); the k - k_eff missing branches are copies of B0
+    marked invalid (fill position -1) and can never win.
+  * B_j = B0 plus position p_j filled with the candidate token pred[p_j] drawn
+    from p_theta(.|x_t) (greedy), so every branch's fill set contains B0's.
+  * Eq. 2 uses branch j's own verification forward, over M_{B_j}; an empty
+    M_{B_j} scores +inf (the branch completes the block); invalid -> -inf.
+  * Logit reuse (Sec. 3.2): the winner's verification conf / pred seed the next
+    iteration, so each iteration costs one forward; a block costs one initial
+    forward on the all-mask block plus one forward per iteration, including the
+    iteration whose winner completes the block (its K/V are then exact).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from .model import KVCache, OracleModel
+
+
+# ----------------------------------------------------------------- Eq. 1
+def threshold_fill(conf, unfilled, tau: float) -> np.ndarray:
+    """I_fill: the unfilled positions with Conf > tau; if none, the single unfilled
+    position of highest Conf (lowest position among ties).  Eq. 1."""
+    conf = np.asarray(conf, dtype=np.float64)
+    cand = [i for i in range(len(conf)) if unfilled[i]]
+    if not cand:
+        raise ValueError("no unfilled position")
+    high = [i for i in cand if conf[i] > tau]
+    if high:
+        return np.array(high, dtype=np.int64)
+    best = cand[0]
+    for i in cand[1:]:
+        if conf[i] > conf[best]:
+            best = i
+    return np.array([best], dtype=np.int64)
+
+
+# ------------------------------------------------------- Alg. 1 steps 1-2
+def build_branches(tokens, conf, pred, mask_id: int, tau: float, k: int):
+    """Anchor B0 (Eq. 1 fill) and k lookahead branches (top-k of M_B0).
+
+    Returns (branch_tokens [k+1, L] int64, fill_pos [k+1] int64 (-1 for B0 and
+    for padding), valid [k+1] uint8, n_valid)."""
+    tokens = np.asarray(tokens, dtype=np.int64)
+    conf = np.asarray(conf, dtype=np.float64)
+    pred = np.asarray(pred, dtype=np.int64)
+    L = len(tokens)
+    unfilled = tokens == mask_id
+    b0 = tokens.copy()
+    fill = threshold_fill(conf, unfilled, tau)
+    b0[fill] = pred[fill]
+    rem = [i for i in range(L) if b0[i] == mask_id]            # M_B0
+    rem.sort(key=lambda i: (-conf[i], i))
+    k_eff = min(k, len(rem))
+    bt = np.tile(b0, (k + 1, 1))
+    fill_pos = np.full(k + 1, -1, dtype=np.int64)
+    valid = np.zeros(k + 1, dtype=np.uint8)
+    valid[0] = 1
+    for j in range(1, k_eff + 1):
+        p = rem[j - 1]
+        bt[j, p] = pred[p]
+        fill_pos[j] = p
+        valid[j] = 1
+    return bt, fill_pos, valid, 1 + k_eff
+
+
+# ----------------------------------------------------------------- Eq. 2
+def branch_confidence(conf_row, tokens_row, mask_id: int) -> float:
+    """C(B) = mean of Conf over the branch's still-unfilled positions.  Eq. 2.
+    An empty unfilled set gives +inf (reading: such a branch completes the block)."""
+    vals = [float(c) for c, t in zip(conf_row, tokens_row) if t == mask_id]
+    if not vals:
+        return math.inf
+    return sum(vals) / len(vals)
+
+
+def select(branch_tokens, conf, valid, mask_id: int):
+    """Scores of all branches and B* = argmax (lowest branch index among ties)."""
+    nb = len(branch_tokens)
+    scores = np.empty(nb)
+    for j in range(nb):
+        scores[j] = branch_confidence(conf[j], branch_tokens[j], mask_id) if valid[j] else -math.inf
+    best = 0
+    for j in range(1, nb):
+        if scores[j] > scores[best]:
+            best = j
+    return scores, best
+
+
+# ------------------------------------------------------------- iteration
+def init_block(model: OracleModel, cache: KVCache, prefix_len: int, L: int):
+    """All-mask block and its first forward: the state the first iteration reads."""
+    tokens = np.full(L, model.cfg["mask_id"], dtype=np.int64)
+    out = model.forward_block(tokens[None], prefix_len, cache)
+    return tokens, out["conf"][0], out["pred"][0]
+
+
+def lopa_step(model: OracleModel, cache: KVCache, prefix_len: int, state, k: int, tau: float):
+    """One LoPA iteration (Alg. 1): build, verify in one pass, score, select, commit.
+
+    Returns (new_state, info).  info holds the branches, scores, winner, the
+    verification outputs and the committed offset."""
+    tokens, conf, pred = state
+    mask_id = model.cfg["mask_id"]
+    bt, fill_pos, valid, n_valid = build_branches(tokens, conf, pred, mask_id, tau, k)
+    out = model.forward_block(bt[:n_valid], prefix_len, cache)
+    nb = k + 1
+    conf_b = np.zeros((nb, len(tokens)))
+    pred_b = np.zeros((nb, len(tokens)), dtype=np.int64)
+    conf_b[:n_valid], pred_b[:n_valid] = out["conf"], out["pred"]
+    scores, w = select(bt, conf_b, valid, mask_id)
+    off = cache.commit(prefix_len, out["k"][w], out["v"][w])
+    new_state = (bt[w].copy(), conf_b[w].copy(), pred_b[w].copy())
+    info = dict(branch_tokens=bt, fill_pos=fill_pos, valid=valid, n_valid=n_valid,
+                conf=conf_b, pred=pred_b, scores=scores, winner=w, append_offset=off,
+                kv=(out["k"], out["v"]))
+    return new_state, info
+
+
+def decode_block(model, cache, prefix_len: int, L: int, k: int, tau: float, trace=None):
+    """Decode one block to completion.  Returns (tokens, iterations, forwards)."""
+    state = init_block(model, cache, prefix_len, L)
+    forwards, iters = 1, 0
+    mask_id = model.cfg["mask_id"]
+    while True:
+        state, info = lopa_step(model, cache, prefix_len, state, k, tau)
+        forwards += 1
+        iters += 1
+        if trace is not None:
+            trace.append(info)
+        if not np.any(state[0] == mask_id):
+            return state[0], iters, forwards
+        if iters > L:
+            raise RuntimeError("block did not complete in L iterations")
+
+
+def prefill(model: OracleModel, cache: KVCache, prompt, L: int) -> int:
+    """Block-causal prompt encoding in blocks of L (the last may be shorter):
+    each block attends to the committed prefix and bidirectionally within itself,
+    then its K/V are committed.  Returns the new prefix length."""
+    prompt = np.asarray(prompt, dtype=np.int64)
+    pos = 0
+    while pos < len(prompt):
+        blk = prompt[pos:pos + L]
+        out = model.forward_block(blk[None], pos, cache)
+        cache.commit(pos, out["k"][0], out["v"][0])
+        pos += len(blk)
+    return pos
+
+
+def decode(model, prompt, gen_len: int, L: int, k: int, tau: float, max_len=None):
+    """Prefill the prompt, then generate gen_len tokens (gen_len / L blocks)."""
+    prompt = np.asarray(prompt, dtype=np.int64)
+    cache = KVCache(model.cfg, max_len or (len(prompt) + gen_len))
+    P = prefill(model, cache, prompt, L)
+    out, iters, forwards = [], 0, 0
+    for _ in range(gen_len // L):
+        toks, it, fw = decode_block(model, cache, P, L, k, tau)
+        out.append(toks)
+        iters += it
+        forwards += fw
+        P += L
+    gen = np.concatenate(out) if out else np.zeros(0, dtype=np.int64)
+    return dict(tokens=gen, iterations=iters, forwards=forwards,
+                tpf=(len(gen) / forwards) if forwards else 0.0, cache=cache)

@@ -1,0 +1,170 @@
+"""Invariants of the whole LoPA iteration on the oracle (Alg. 1, Eq. 1-2, Sec. 3.2).
+
+* k = 0 reduces to plain confidence-threshold decoding (Eq. 1 alone).
+* Brute force on a tiny vocab / block: with k >= |M_B0| the winner equals the
+  best, by Eq. 2, of B0 and every one-position extension of B0, each forwarded
+  on its own.
+* Termination within L iterations; each iteration fills |I_fill| or |I_fill|+1.
+* Identical branches get identical scores; permuting the verify batch permutes
+  the outputs and leaves the winner's content unchanged.
+* Resuming from a saved state (tokens, conf, pred, cache) replays the same
+  trajectory."""
+import copy
+import math
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import KVCache, OracleModel, lopa
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    cfg = synth.config("tiny")
+    w = synth.model_weights(cfg)
+    m = OracleModel(cfg, w)
+    cache = KVCache(cfg, 64 + 64)
+    P = lopa.prefill(m, cache, synth.prompt(cfg, 64).numpy(), 16)
+    return cfg, m, cache, P
+
+
+def threshold_decode(model, cache, P, L, tau):
+    """Plain confidence-threshold decoding of one block (Eq. 1 on the current state)."""
+    mask = model.cfg["mask_id"]
+    x = np.full(L, mask)
+    steps = 0
+    while (x == mask).any():
+        o = model.forward_block(x[None], P, cache)
+        c, p = o["conf"][0], o["pred"][0]
+        M = np.flatnonzero(x == mask)
+        hi = M[c[M] > tau]
+        fill = hi if hi.size else M[[np.argmax(c[M])]]
+        x = x.copy()
+        x[fill] = p[fill]
+        steps += 1
+    return x, steps
+
+
+@pytest.mark.parametrize("tau", [0.9, 0.5, 0.2])
+def test_k0_is_threshold_decoding(tiny, tau):
+    cfg, m, cache, P = tiny
+    ref, steps = threshold_decode(m, cache.copy(), P, 16, tau)
+    toks, iters, forwards = lopa.decode_block(m, cache.copy(), P, 16, 0, tau)
+    assert np.array_equal(toks, ref)
+    assert iters == steps
+    assert forwards == steps + 1          # + the verify forward of the completing branch
+
+
+def test_termination_and_fill_growth(tiny):
+    cfg, m, cache, P = tiny
+    for k, tau in [(3, 0.9), (7, 0.5), (1, 0.99)]:
+        trace = []
+        toks, iters, fw = lopa.decode_block(m, cache.copy(), P, 16, k, tau, trace)
+        assert iters <= 16 and fw == iters + 1
+        mask = cfg["mask_id"]
+        filled_before = 0
+        for info in trace:
+            bt, w = info["branch_tokens"], info["winner"]
+            n0 = int((bt[0] != mask).sum())
+            nw = int((bt[w] != mask).sum())
+            assert nw in (n0, n0 + 1) and nw > filled_before
+            filled_before = nw
+        assert not np.any(toks == mask)
+
+
+def test_brute_force_one_step_lookahead():
+    """V = 16, L = 4, one layer, k >= |M_B0|: LoPA's winner is the Eq. 2 argmax over
+    B0 and all single-position extensions of B0, each forwarded separately."""
+    cfg = synth.config("tiny", layers=1, vocab=16, lm_std=2.0)
+    w = synth.model_weights(cfg)
+    m = OracleModel(cfg, w)
+    cache = KVCache(cfg, 16)
+    P = lopa.prefill(m, cache, synth.prompt(cfg, 8).numpy(), 4)
+    mask = cfg["mask_id"]
+    checked = 0
+    for tau in (0.95, 0.6, 0.3):
+        state = lopa.init_block(m, cache, P, 4)
+        while (state[0] == mask).any():
+            tokens, conf, pred = state
+            new_state, info = lopa.lopa_step(m, cache.copy(), P, state, k=4, tau=tau)
+            b0 = info["branch_tokens"][0]
+            cands = [b0]
+            for p in np.flatnonzero(b0 == mask):
+                c = b0.copy()
+                c[p] = pred[p]
+                cands.append(c)
+            best, best_s = None, -math.inf
+            for c in cands:
+                o = m.forward_block(c[None], P, cache)
+                s = lopa.branch_confidence(o["conf"][0], c, mask)
+                if s > best_s:
+                    best, best_s = c, s
+            assert np.array_equal(new_state[0], best)
+            assert info["scores"][info["winner"]] == pytest.approx(best_s, rel=1e-12) \
+                or (math.isinf(best_s) and math.isinf(info["scores"][info["winner"]]))
+            state = new_state
+            checked += 1
+    assert checked >= 3
+
+
+def test_identical_and_permuted_branches(tiny):
+    cfg, m, cache, P = tiny
+    mask = cfg["mask_id"]
+    state = lopa.init_block(m, cache, P, 16)
+    bt, fp, valid, nv = lopa.build_branches(*state, mask, 0.9, 5)
+    out = m.forward_block(bt, P, cache)
+    # identical branches (padding copies, or B0 duplicated) -> identical scores
+    dup = np.stack([bt[0]] * 3)
+    od = m.forward_block(dup, P, cache)
+    sd, wd = lopa.select(dup, od["conf"], np.ones(3, np.uint8), mask)
+    assert abs(sd[0] - sd[1]) < 1e-12 and abs(sd[1] - sd[2]) < 1e-12 and wd == 0
+    # permutation of the batch
+    perm = np.random.default_rng(1).permutation(len(bt))
+    op = m.forward_block(bt[perm], P, cache)
+    assert np.allclose(op["conf"], out["conf"][perm], atol=1e-12)
+    s1, w1 = lopa.select(bt, out["conf"], valid, mask)
+    s2, w2 = lopa.select(bt[perm], op["conf"], valid[perm], mask)
+    assert np.array_equal(bt[perm][w2], bt[w1])
+
+
+def test_resume_from_saved_state(tiny):
+    cfg, m, cache, P = tiny
+    c1 = cache.copy()
+    trace = []
+    ref, _, _ = lopa.decode_block(m, c1, P, 16, 3, 0.9, trace)
+    # replay: stop after two iterations, save, restore into fresh objects, continue
+    c2 = cache.copy()
+    state = lopa.init_block(m, c2, P, 16)
+    for _ in range(2):
+        state, _ = lopa.lopa_step(m, c2, P, state, 3, 0.9)
+    saved = copy.deepcopy((state, c2.k, c2.v))
+    c3 = cache.copy()
+    (state3, k3, v3) = saved
+    c3.k[:], c3.v[:] = k3, v3
+    while (state3[0] == cfg["mask_id"]).any():
+        state3, _ = lopa.lopa_step(m, c3, P, state3, 3, 0.9)
+    assert np.array_equal(state3[0], ref)
+    assert np.array_equal(c3.k, c1.k) and np.array_equal(c3.v, c1.v)
+
+
+def test_commit_writes_only_the_winner(tiny):
+    """The committed rows equal the winner's block K/V; a poisoned loser never lands."""
+    cfg, m, cache, P = tiny
+    c = cache.copy()
+    state = lopa.init_block(m, c, P, 16)
+    new_state, info = lopa.lopa_step(m, c, P, state, 3, 0.9)
+    k, v = info["kv"]
+    w = info["winner"]
+    assert np.array_equal(c.k[:, :, P:P + 16], k[w]) and info["append_offset"] == P
+    assert not np.isnan(c.k).any()
+
+
+def test_decode_small_end_to_end():
+    """Prefill + 2 blocks on the tiny config; TPF = tokens / forwards >= 1."""
+    cfg = synth.config("tiny")
+    m = OracleModel(cfg, synth.model_weights(cfg))
+    r = lopa.decode(m, synth.prompt(cfg, 64).numpy(), 32, 16, 3, 0.9)
+    assert len(r["tokens"]) == 32 and not np.any(r["tokens"] == cfg["mask_id"])
+    assert r["forwards"] == r["iterations"] + 2
+    assert r["tpf"] >= 1.0
