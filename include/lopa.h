@@ -1,0 +1,222 @@
+/*
+ * lopa.h - C ABI of an MI355X (gfx950) implementation of the per-iteration
+ * branch-verification step of LoPA, Lookahead Parallel Decoding for diffusion
+ * LLMs (arXiv 2512.16229).
+ *
+ * One LoPA iteration (Alg. 1) on one GPU is four calls, all enqueued on the
+ * caller's HIP stream, with no host synchronisation inside a step:
+ *
+ *   lopa_build_branches            Eq. 1 anchor fill + top-k lookahead branches
+ *                                  (Alg. 1 steps 1-2)
+ *   lopa_verify_forward            one batched forward of all k+1 branches of
+ *                                  the active block against the shared-prefix
+ *                                  KV cache; per-position Conf and candidate
+ *                                  (Alg. 1 step 3, Sec. 3.1, Sec. 3.3)
+ *   lopa_branch_confidence_select  Eq. 2 branch confidence, B* = argmax, and the
+ *                                  next state taken from B*'s verification
+ *                                  outputs (logit reuse, Sec. 3.2)
+ *   lopa_commit_kv                 write B*'s block K/V into the static cache
+ *                                  (single-GPU form of the Pre-Write /
+ *                                  Commit-Winner-Cache protocol, Sec. 3.4)
+ *
+ * Conventions for every call:
+ *   - All array arguments are DEVICE pointers unless stated otherwise; the
+ *     caller owns them. The library owns handles, repacked weights, the KV
+ *     cache, the per-branch K/V staging and its workspace.
+ *   - `stream` is a hipStream_t (NULL = the default stream). Outputs are valid
+ *     in stream order after the call; nothing here synchronises the host.
+ *   - Return value: LOPA_OK (0) or a negative status. Argument checks run on
+ *     the host before any HIP call, so invalid arguments never reach the GPU.
+ *     lopa_last_error() returns a message for the calling thread's last error.
+ *   - No call allocates device memory except lopa_model_create and
+ *     lopa_kv_create.
+ *   - Calls that share a lopa_kv must be ordered on one stream; concurrent
+ *     verify_forward calls on one lopa_kv race on its workspace.
+ */
+#ifndef LOPA_H
+#define LOPA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  LOPA_OK = 0,
+  LOPA_EINVAL = -1,    /* null pointer, k < 0, tau outside [0, 1], bad config  */
+  LOPA_ESHAPE = -2,    /* L, n_branches or a model dimension the kernels do   */
+                       /* not support, or larger than the lopa_kv capacity    */
+  LOPA_ECAPACITY = -3, /* prefix_len + L > max_len of the cache               */
+  LOPA_EHIP = -4,      /* a HIP call failed; the message names the hipError_t */
+  LOPA_ENOMEM = -5     /* device allocation failed                            */
+};
+
+/* Largest supported values (checked by the calls). */
+#define LOPA_MAX_BLOCK 64    /* L: positions of the active block            */
+#define LOPA_MAX_ROWS 512    /* n_branches * L rows in one verify forward   */
+
+/* Decoder shape (Qwen2.5 / LLaMA-style pre-norm decoder, the layout of the
+ * paper's Dream-7B / DiffuCoder-7B backbones; the paper names only the
+ * models). Constraints: hidden % 128 == 0, head_dim in {64, 128},
+ * heads % kv_heads == 0, heads * head_dim == hidden, ffn % 64 == 0,
+ * 0 <= mask_id < vocab. */
+typedef struct lopa_model_cfg {
+  int32_t layers;
+  int32_t hidden;
+  int32_t heads;      /* query heads                     */
+  int32_t kv_heads;   /* key/value heads (grouped query) */
+  int32_t head_dim;
+  int32_t ffn;        /* SwiGLU intermediate size        */
+  int32_t vocab;
+  int32_t mask_id;    /* the mask token: position unfilled <=> token == mask_id */
+  float rms_eps;
+  float rope_theta;   /* rotate-half RoPE base            */
+  int32_t qkv_bias;   /* 1: q/k/v projections have biases */
+} lopa_model_cfg;
+
+/* One layer's weights: bf16 DEVICE arrays in PyTorch [out, in] row-major
+ * layout. They are only read during lopa_model_create (repacked into library
+ * buffers); the caller may free them afterwards. */
+typedef struct lopa_layer_weights {
+  const void* wq;      /* [heads*head_dim, hidden]    */
+  const void* wk;      /* [kv_heads*head_dim, hidden] */
+  const void* wv;      /* [kv_heads*head_dim, hidden] */
+  const void* bq;      /* [heads*head_dim] or NULL when qkv_bias == 0 */
+  const void* bk;      /* [kv_heads*head_dim] or NULL */
+  const void* bv;      /* [kv_heads*head_dim] or NULL */
+  const void* wo;      /* [hidden, heads*head_dim]    */
+  const void* w_gate;  /* [ffn, hidden]               */
+  const void* w_up;    /* [ffn, hidden]               */
+  const void* w_down;  /* [hidden, ffn]               */
+  const void* ln1;     /* [hidden] pre-attention RMSNorm weight */
+  const void* ln2;     /* [hidden] pre-MLP RMSNorm weight       */
+} lopa_layer_weights;
+
+typedef struct lopa_weight_ptrs {
+  const void* embed;                 /* [vocab, hidden] bf16 device          */
+  const lopa_layer_weights* layers;  /* HOST array of cfg.layers entries     */
+  const void* final_norm;            /* [hidden] bf16 device                 */
+  const void* lm_head;               /* [vocab, hidden] bf16 device, untied  */
+} lopa_weight_ptrs;
+
+typedef struct lopa_model lopa_model;
+typedef struct lopa_kv lopa_kv;
+
+/* ------------------------------------------------------------- lifecycle */
+
+/* Validate cfg, allocate library buffers on the current device, repack the
+ * weights on `stream` and wait for that to finish. *out receives the handle. */
+int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w,
+                      void* stream, lopa_model** out);
+void lopa_model_destroy(lopa_model* m);
+
+/* Static KV cache of max_len positions for one sequence (Sec. 3.4: a
+ * pre-allocated static cache instead of dynamic objects), plus K/V staging for
+ * max_branches branches of a block of up to max_block positions, plus the
+ * verify workspace. Cache layout (bf16): K [layers][kv_heads][max_len][head_dim],
+ * V likewise. Zero-initialised. */
+int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches,
+                   int32_t max_block, lopa_kv** out);
+void lopa_kv_destroy(lopa_kv* kv);
+
+const char* lopa_strerror(int status);
+const char* lopa_last_error(void);
+
+/* ----------------------------------------------------------- hot path */
+
+/* Alg. 1 steps 1-2 (Eq. 1; Sec. 3.2 "Look ahead Multiple TFOs in Parallel").
+ * In:  tokens[L] int32 (the block; position i unfilled <=> tokens[i] == mask_id,
+ *      at least one must be unfilled), conf[L] float32 and pred[L] int32 from
+ *      the forward pass on exactly these tokens (values at filled positions are
+ *      ignored), tau in [0, 1], k >= 0.
+ * Anchor B0: I_fill = {unfilled i : conf[i] > tau} (strict), or, if empty, the
+ *      single unfilled position of largest conf (lowest position on ties);
+ *      B0 = tokens with pred written at I_fill.
+ * Lookahead: the k_eff = min(k, |M_B0|) unfilled positions of B0 with the
+ *      largest conf (ties: lower position first); branch j (1..k_eff) is B0
+ *      with position p_j also set to pred[p_j].
+ * Out: branch_tokens[(k+1)*L] int32, branch-major (row j = B_j); rows
+ *      j > k_eff are copies of B0. fill_pos[k+1] int32 (-1 for B0 and padding,
+ *      else p_j). valid[k+1] uint8 (1 for j <= k_eff). n_valid[1] int32 =
+ *      1 + k_eff. One workgroup; L <= LOPA_MAX_BLOCK. */
+int lopa_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
+                        int32_t L, int32_t mask_id, float tau, int32_t k,
+                        int32_t* branch_tokens, int32_t* fill_pos, uint8_t* valid,
+                        int32_t* n_valid, void* stream);
+
+/* Alg. 1 step 3 "single pass" + Sec. 3.1 Conf + Sec. 3.3 attention pattern.
+ * In:  branch_tokens[n_branches*L] int32 (block rows at positions
+ *      prefix_len .. prefix_len+L-1), the cache rows [0, prefix_len).
+ * Attention: each row sees all prefix_len committed positions and all L rows
+ *      of its own branch (full attention inside the block); branches do not
+ *      see each other.
+ * Out: conf[n_branches*L] float32 = the largest probability of the softmax over
+ *      the vocabulary with mask_id excluded; pred[n_branches*L] int32 = its
+ *      token (lowest id on ties). Both are produced for every row.
+ *      The post-RoPE K and V of every branch's block rows go to the lopa_kv's
+ *      staging (all layers), ready for lopa_commit_kv.
+ * Compute: bf16 weights and GEMM inputs, fp32 accumulation, fp32 residual
+ *      stream, norms, RoPE, softmax and logits.
+ * Limits: n_branches <= max_branches, L <= max_block of the lopa_kv,
+ *      n_branches*L <= LOPA_MAX_ROWS; prefix_len + L <= max_len. */
+int lopa_verify_forward(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                        const int32_t* branch_tokens, int32_t n_branches, int32_t L,
+                        float* conf, int32_t* pred, void* stream);
+
+/* Eq. 2 and Alg. 1 step 3 selection; Sec. 3.2 logit reuse.
+ * In:  branch_tokens[n_branches*L], conf/pred[n_branches*L] from
+ *      lopa_verify_forward on those branches, valid[n_branches].
+ * scores[j] = mean of conf over row j's positions holding mask_id (Eq. 2),
+ *      +inf if the row has none, -inf if valid[j] == 0.
+ * winner[0] = argmax_j scores[j] (lowest j on ties).
+ * next_tokens/next_conf/next_pred[L] = row winner of the inputs (the state of
+ *      the next iteration); next_unfilled[0] = number of mask_id positions in
+ *      it (0 = block complete). One workgroup. */
+int lopa_branch_confidence_select(const int32_t* branch_tokens, const float* conf,
+                                  const int32_t* pred, const uint8_t* valid,
+                                  int32_t n_branches, int32_t L, int32_t mask_id,
+                                  float* scores, int32_t* winner, int32_t* next_tokens,
+                                  float* next_conf, int32_t* next_pred,
+                                  int32_t* next_unfilled, void* stream);
+
+/* Sec. 3.4 Commit-Winner-Cache, single-GPU form: copy the staged post-RoPE
+ * K/V of branch *winner (a DEVICE int32, read by the kernel: no host sync) for
+ * all layers into cache rows [prefix_len, prefix_len + L). The staging must
+ * come from the last lopa_verify_forward on this lopa_kv with the same
+ * prefix_len and L. append_offset[0] (device int32) receives prefix_len.
+ * A winner outside [0, n_branches of that forward) writes nothing and sets
+ * append_offset[0] = -1. */
+int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,
+                   int32_t* append_offset, void* stream);
+
+/* ---------------------------------------------------------- inspection */
+
+/* Copy cache rows [start, start+len) of one layer to k_dst, v_dst (device,
+ * bf16 [kv_heads][len][head_dim] each). For tests and checkpoints. */
+int lopa_kv_read(const lopa_kv* kv, int32_t layer, int32_t start, int32_t len,
+                 void* k_dst, void* v_dst, void* stream);
+
+/* Write cache rows [start, start+len) of one layer from k_src, v_src (same
+ * layout as lopa_kv_read). Restores a checkpointed prefix. */
+int lopa_kv_write(lopa_kv* kv, int32_t layer, int32_t start, int32_t len,
+                  const void* k_src, const void* v_src, void* stream);
+
+/* Copy the staged block K/V of one branch and layer from the last
+ * lopa_verify_forward to k_dst, v_dst (device, bf16 [kv_heads][L][head_dim]). */
+int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer,
+                         void* k_dst, void* v_dst, void* stream);
+
+/* Diagnostics of the verify forward: run the embedding and the first n_layers
+ * decoder layers (0 <= n_layers <= cfg.layers) of lopa_verify_forward on the
+ * same arguments and copy the fp32 residual stream [n_branches*L][hidden]
+ * (row = branch * L + position) to x_out (device). K/V staging of those layers
+ * is written as by lopa_verify_forward; conf / pred are not produced. */
+int lopa_debug_hidden(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                      const int32_t* branch_tokens, int32_t n_branches, int32_t L,
+                      int32_t n_layers, float* x_out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LOPA_H */

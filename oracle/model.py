@@ -153,13 +153,15 @@ class OracleModel:
             out[:, h] = o / den
         return out
 
-    def forward_block(self, tokens, prefix_len: int, cache: KVCache, keep_hidden: bool = False):
+    def forward_block(self, tokens, prefix_len: int, cache: KVCache, keep_hidden: bool = False,
+                      n_layers=None):
         """One batched forward of nb branches of the active block.
 
         tokens: int [nb, L] (block rows at positions prefix_len .. prefix_len+L-1).
         Returns dict: conf [nb, L] (float64), pred [nb, L] (int64), k / v
         [nb, layers, Hkv, L, d] (post-RoPE block keys / values), and, if asked,
-        'hidden' [nb, L, H] (final-normed rows) and 'logits'."""
+        'hidden' [nb, L, H] (final-normed rows) and 'logits'. With n_layers set,
+        returns only {'x': residual stream after that many layers}."""
         cfg = self.cfg
         tokens = np.asarray(tokens, dtype=np.int64)
         nb, L = tokens.shape
@@ -170,6 +172,8 @@ class OracleModel:
         ks = np.empty((nb, cfg["layers"], Hkv, L, d))
         vs = np.empty_like(ks)
         for li, w in enumerate(self.layers):
+            if n_layers is not None and li == n_layers:
+                return {"x": x}
             h = self._store(rms_norm(x, w["ln1"], cfg["rms_eps"]))
             q = h @ w["wq"].T
             k = h @ w["wk"].T
@@ -189,6 +193,8 @@ class OracleModel:
             h2 = self._store(rms_norm(x, w["ln2"], cfg["rms_eps"]))
             a = self._store(silu(h2 @ w["w_gate"].T) * (h2 @ w["w_up"].T))
             x = x + a @ w["w_down"].T
+        if n_layers is not None:
+            return {"x": x}
         hf = self._store(rms_norm(x, self.final_norm, cfg["rms_eps"]))
         logits = hf @ self.lm_head.T                                    # [nb, L, V]
         conf, pred = confidence(logits, cfg["mask_id"])

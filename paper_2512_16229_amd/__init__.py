@@ -1,0 +1,229 @@
+"""Python binding of liblopa, the MI355X (gfx950) LoPA branch-verification step.
+
+Argument marshalling only: every step of the method runs in the HIP kernels
+behind the C ABI declared in include/lopa.h. PyTorch supplies device memory and
+the stream. The functions keep the C names:
+
+    lopa_build_branches            Eq. 1 + top-k lookahead branches (Alg. 1 steps 1-2)
+    lopa_verify_forward            one batched forward of all branches (Alg. 1 step 3)
+    lopa_branch_confidence_select  Eq. 2 scores, argmax, next state (Sec. 3.2 logit reuse)
+    lopa_commit_kv                 winner K/V -> static cache (Sec. 3.4)
+
+Importing this module loads liblopa.so built in-tree by build.py (or
+__graft_entry__.build()); there is no fallback: a missing library raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblopa.so")
+
+LOPA_OK, LOPA_EINVAL, LOPA_ESHAPE, LOPA_ECAPACITY, LOPA_EHIP, LOPA_ENOMEM = 0, -1, -2, -3, -4, -5
+MAX_BLOCK, MAX_ROWS = 64, 512
+
+
+class LopaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"liblopa status {status}: {msg}")
+        self.status = status
+
+
+class lopa_model_cfg(C.Structure):
+    _fields_ = [("layers", C.c_int32), ("hidden", C.c_int32), ("heads", C.c_int32),
+                ("kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn", C.c_int32),
+                ("vocab", C.c_int32), ("mask_id", C.c_int32), ("rms_eps", C.c_float),
+                ("rope_theta", C.c_float), ("qkv_bias", C.c_int32)]
+
+
+class lopa_layer_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in ("wq", "wk", "wv", "bq", "bk", "bv", "wo", "w_gate",
+                                           "w_up", "w_down", "ln1", "ln2")]
+
+
+class lopa_weight_ptrs(C.Structure):
+    _fields_ = [("embed", C.c_void_p), ("layers", C.POINTER(lopa_layer_weights)),
+                ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
+
+
+EXPORTS = ["lopa_model_create", "lopa_model_destroy", "lopa_kv_create", "lopa_kv_destroy",
+           "lopa_strerror", "lopa_last_error", "lopa_build_branches", "lopa_verify_forward",
+           "lopa_branch_confidence_select", "lopa_commit_kv", "lopa_kv_read", "lopa_kv_write",
+           "lopa_kv_read_staging", "lopa_debug_hidden"]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2512_16229_amd/build.py`")
+    lib = C.CDLL(LIB_PATH)
+    P, I32, F32 = C.c_void_p, C.c_int32, C.c_float
+    sig = {
+        "lopa_model_create": (C.c_int, [C.POINTER(lopa_model_cfg), C.POINTER(lopa_weight_ptrs), P,
+                                        C.POINTER(C.c_void_p)]),
+        "lopa_model_destroy": (None, [P]),
+        "lopa_kv_create": (C.c_int, [P, I32, I32, I32, C.POINTER(C.c_void_p)]),
+        "lopa_kv_destroy": (None, [P]),
+        "lopa_strerror": (C.c_char_p, [C.c_int]),
+        "lopa_last_error": (C.c_char_p, []),
+        "lopa_build_branches": (C.c_int, [P, P, P, I32, I32, F32, I32, P, P, P, P, P]),
+        "lopa_verify_forward": (C.c_int, [P, P, I32, P, I32, I32, P, P, P]),
+        "lopa_branch_confidence_select": (C.c_int, [P, P, P, P, I32, I32, I32, P, P, P, P, P, P, P]),
+        "lopa_commit_kv": (C.c_int, [P, P, I32, I32, P, P]),
+        "lopa_kv_read": (C.c_int, [P, I32, I32, I32, P, P, P]),
+        "lopa_kv_write": (C.c_int, [P, I32, I32, I32, P, P, P]),
+        "lopa_kv_read_staging": (C.c_int, [P, I32, I32, P, P, P]),
+        "lopa_debug_hidden": (C.c_int, [P, P, I32, P, I32, I32, I32, P, P]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype, f.argtypes = res, args
+    return lib
+
+
+lib = _load()
+
+
+def _check(status: int):
+    if status != LOPA_OK:
+        raise LopaError(status, lib.lopa_last_error().decode())
+
+
+def _ptr(t, dtype=None, name="tensor"):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name}: must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    return C.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+# ------------------------------------------------------------------ handles
+class Model:
+    """Repacked model weights on the device (lopa_model)."""
+
+    def __init__(self, cfg: dict, weights: dict, stream=None):
+        c = lopa_model_cfg(cfg["layers"], cfg["hidden"], cfg["heads"], cfg["kv_heads"],
+                           cfg["head_dim"], cfg["ffn"], cfg["vocab"], cfg["mask_id"],
+                           cfg["rms_eps"], cfg["rope_theta"], 1 if cfg["qkv_bias"] else 0)
+        bf = torch.bfloat16
+        n = cfg["layers"]
+        arr = (lopa_layer_weights * n)()
+        for i, lw in enumerate(weights["layers"]):
+            f = {}
+            for key in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "ln1", "ln2"):
+                f[key] = _ptr(lw[key], bf, key)
+            for key in ("bq", "bk", "bv"):
+                f[key] = _ptr(lw[key], bf, key) if cfg["qkv_bias"] else None
+            arr[i] = lopa_layer_weights(**f)
+        w = lopa_weight_ptrs(_ptr(weights["embed"], bf, "embed"), arr,
+                             _ptr(weights["final_norm"], bf, "final_norm"),
+                             _ptr(weights["lm_head"], bf, "lm_head"))
+        h = C.c_void_p()
+        _check(lib.lopa_model_create(C.byref(c), C.byref(w), _stream(stream), C.byref(h)))
+        self.handle, self.cfg = h, dict(cfg)
+
+    def close(self):
+        if getattr(self, "handle", None) and lib is not None:
+            lib.lopa_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        self.close()
+
+
+class KV:
+    """Static KV cache + per-branch staging + verify workspace (lopa_kv)."""
+
+    def __init__(self, model: Model, max_len: int, max_branches: int, max_block: int):
+        h = C.c_void_p()
+        _check(lib.lopa_kv_create(model.handle, max_len, max_branches, max_block, C.byref(h)))
+        self.handle, self.model = h, model
+        self.max_len, self.max_branches, self.max_block = max_len, max_branches, max_block
+
+    def read(self, layer: int, start: int, length: int, stream=None):
+        c = self.model.cfg
+        shp = (c["kv_heads"], length, c["head_dim"])
+        k = torch.empty(shp, dtype=torch.bfloat16, device="cuda")
+        v = torch.empty_like(k)
+        _check(lib.lopa_kv_read(self.handle, layer, start, length, _ptr(k), _ptr(v), _stream(stream)))
+        return k, v
+
+    def write(self, layer: int, start: int, k: torch.Tensor, v: torch.Tensor, stream=None):
+        _check(lib.lopa_kv_write(self.handle, layer, start, k.shape[1], _ptr(k, torch.bfloat16),
+                                 _ptr(v, torch.bfloat16), _stream(stream)))
+
+    def read_staging(self, branch: int, layer: int, L: int, stream=None):
+        c = self.model.cfg
+        k = torch.empty((c["kv_heads"], L, c["head_dim"]), dtype=torch.bfloat16, device="cuda")
+        v = torch.empty_like(k)
+        _check(lib.lopa_kv_read_staging(self.handle, branch, layer, _ptr(k), _ptr(v), _stream(stream)))
+        return k, v
+
+    def close(self):
+        if getattr(self, "handle", None) and lib is not None:
+            lib.lopa_kv_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        self.close()
+
+
+# ------------------------------------------------------------- entry points
+I32, F32, U8 = torch.int32, torch.float32, torch.uint8
+
+
+def lopa_build_branches(tokens, conf, pred, L, mask_id, tau, k, branch_tokens, fill_pos, valid,
+                        n_valid, stream=None):
+    _check(lib.lopa_build_branches(_ptr(tokens, I32, "tokens"), _ptr(conf, F32, "conf"),
+                                   _ptr(pred, I32, "pred"), L, mask_id, float(tau), k,
+                                   _ptr(branch_tokens, I32, "branch_tokens"),
+                                   _ptr(fill_pos, I32, "fill_pos"), _ptr(valid, U8, "valid"),
+                                   _ptr(n_valid, I32, "n_valid"), _stream(stream)))
+
+
+def lopa_verify_forward(model: Model, kv: KV, prefix_len, branch_tokens, n_branches, L, conf, pred,
+                        stream=None):
+    _check(lib.lopa_verify_forward(model.handle, kv.handle, prefix_len,
+                                   _ptr(branch_tokens, I32, "branch_tokens"), n_branches, L,
+                                   _ptr(conf, F32, "conf"), _ptr(pred, I32, "pred"),
+                                   _stream(stream)))
+
+
+def lopa_branch_confidence_select(branch_tokens, conf, pred, valid, n_branches, L, mask_id, scores,
+                                  winner, next_tokens, next_conf, next_pred, next_unfilled,
+                                  stream=None):
+    _check(lib.lopa_branch_confidence_select(
+        _ptr(branch_tokens, I32, "branch_tokens"), _ptr(conf, F32, "conf"), _ptr(pred, I32, "pred"),
+        _ptr(valid, U8, "valid"), n_branches, L, mask_id, _ptr(scores, F32, "scores"),
+        _ptr(winner, I32, "winner"), _ptr(next_tokens, I32, "next_tokens"),
+        _ptr(next_conf, F32, "next_conf"), _ptr(next_pred, I32, "next_pred"),
+        _ptr(next_unfilled, I32, "next_unfilled"), _stream(stream)))
+
+
+def lopa_debug_hidden(model: Model, kv: KV, prefix_len, branch_tokens, n_branches, L, n_layers,
+                      x_out, stream=None):
+    _check(lib.lopa_debug_hidden(model.handle, kv.handle, prefix_len,
+                                 _ptr(branch_tokens, I32, "branch_tokens"), n_branches, L, n_layers,
+                                 _ptr(x_out, F32, "x_out"), _stream(stream)))
+
+
+def lopa_commit_kv(kv: KV, winner, prefix_len, L, append_offset, stream=None):
+    _check(lib.lopa_commit_kv(kv.handle, _ptr(winner, I32, "winner"), prefix_len, L,
+                              _ptr(append_offset, I32, "append_offset"), _stream(stream)))
+
+
+from .decoder import Decoder  # noqa: E402,F401

@@ -1,0 +1,541 @@
+// C ABI of liblopa: argument checks, handles, device buffers and the launch
+// sequence of one verify forward. Every entry point validates its arguments on
+// the host before touching the GPU and only enqueues work on the caller's
+// stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/lopa.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                     \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess) return fail(LOPA_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+struct DevBuf {
+  void* p = nullptr;
+  size_t n = 0;
+};
+
+int dalloc(DevBuf& b, size_t bytes, std::vector<void*>& owned) {
+  if (bytes == 0) bytes = 16;
+  hipError_t e = hipMalloc(&b.p, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(LOPA_ENOMEM, "hipMalloc(%zu bytes) failed: %s", bytes, hipGetErrorString(e));
+  }
+  b.n = bytes;
+  owned.push_back(b.p);
+  return LOPA_OK;
+}
+
+struct LayerPack {
+  uint16_t* qkv;   // tiles_qkv x KC(H)
+  uint16_t* o;     // tiles_h x KC(Hq*d)
+  uint16_t* gu;    // tiles_gu x KC(H), gate/up interleaved
+  uint16_t* down;  // tiles_h x KC(F)
+  float* bias;     // [Nqkv] or null
+  float* ln1;
+  float* ln2;
+};
+
+int pow2_waves(int M) {
+  int w = (M + 63) / 64;
+  int p = 1;
+  while (p < w) p <<= 1;
+  return p;
+}
+
+}  // namespace
+
+struct lopa_model {
+  lopa_model_cfg cfg;
+  int device = 0;
+  int num_cu = 0;
+  int n_qkv = 0, tiles_qkv = 0, tiles_h = 0, tiles_gu = 0, tiles_lm = 0;
+  std::vector<LayerPack> layers;
+  uint16_t* embed = nullptr;
+  uint16_t* lm = nullptr;
+  float* final_norm = nullptr;
+  std::vector<void*> owned;
+  ~lopa_model() {
+    for (void* p : owned) (void)hipFree(p);
+  }
+};
+
+struct lopa_kv {
+  const lopa_model* m = nullptr;
+  int max_len = 0, max_branches = 0, max_block = 0, mp_max = 0;
+  uint16_t* cache = nullptr;    // [layers][2][Hkv][max_len][d]
+  uint16_t* staging = nullptr;  // [max_branches][layers][2][Hkv][max_block][d]
+  float* rope = nullptr;        // [max_len][d/2][2]
+  float* x = nullptr;           // [mp_max][H]
+  uint16_t* abuf = nullptr;     // packed [mp_max][H]
+  uint16_t* fbuf = nullptr;     // packed [mp_max][F]
+  uint16_t* qbuf = nullptr;     // [max_branches][Hq][max_block][d]
+  float* partials = nullptr;
+  int32_t* counters = nullptr;
+  float* pm = nullptr;
+  float* ps = nullptr;
+  int32_t* pi = nullptr;
+  int last_nb = -1, last_L = -1, last_P = -1;
+  std::vector<void*> owned;
+  ~lopa_kv() {
+    for (void* p : owned) (void)hipFree(p);
+  }
+};
+
+extern "C" {
+
+const char* lopa_strerror(int status) {
+  switch (status) {
+    case LOPA_OK: return "ok";
+    case LOPA_EINVAL: return "invalid argument";
+    case LOPA_ESHAPE: return "unsupported or over-capacity shape";
+    case LOPA_ECAPACITY: return "KV cache capacity exceeded";
+    case LOPA_EHIP: return "HIP runtime error";
+    case LOPA_ENOMEM: return "device allocation failed";
+  }
+  return "unknown status";
+}
+
+const char* lopa_last_error(void) { return g_err.c_str(); }
+
+static int check_cfg(const lopa_model_cfg* c) {
+  if (!c) return fail(LOPA_EINVAL, "cfg is null");
+  if (c->layers < 1 || c->hidden < 1 || c->heads < 1 || c->kv_heads < 1 || c->ffn < 1 ||
+      c->vocab < 2)
+    return fail(LOPA_EINVAL, "non-positive model dimension");
+  if (c->mask_id < 0 || c->mask_id >= c->vocab)
+    return fail(LOPA_EINVAL, "mask_id %d outside [0, %d)", c->mask_id, c->vocab);
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f) || !std::isfinite(c->rms_eps) ||
+      !std::isfinite(c->rope_theta))
+    return fail(LOPA_EINVAL, "rms_eps and rope_theta must be positive and finite");
+  if (c->hidden % 128) return fail(LOPA_ESHAPE, "hidden %d is not a multiple of 128", c->hidden);
+  if (c->head_dim != 64 && c->head_dim != 128)
+    return fail(LOPA_ESHAPE, "head_dim %d not in {64, 128}", c->head_dim);
+  if (c->heads % c->kv_heads) return fail(LOPA_ESHAPE, "heads %% kv_heads != 0");
+  if (c->heads * c->head_dim != c->hidden)
+    return fail(LOPA_ESHAPE, "heads * head_dim != hidden");
+  if (c->ffn % 64) return fail(LOPA_ESHAPE, "ffn %d is not a multiple of 64", c->ffn);
+  if (((c->heads + 2 * c->kv_heads) * c->head_dim) % 128)
+    return fail(LOPA_ESHAPE, "(heads + 2 kv_heads) * head_dim not a multiple of 128");
+  return LOPA_OK;
+}
+
+int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void* stream,
+                      lopa_model** out) {
+  if (!out) return fail(LOPA_EINVAL, "out is null");
+  *out = nullptr;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!w || !w->embed || !w->layers || !w->final_norm || !w->lm_head)
+    return fail(LOPA_EINVAL, "weight pointer is null");
+  for (int l = 0; l < cfg->layers; ++l) {
+    const lopa_layer_weights& lw = w->layers[l];
+    if (!lw.wq || !lw.wk || !lw.wv || !lw.wo || !lw.w_gate || !lw.w_up || !lw.w_down ||
+        !lw.ln1 || !lw.ln2)
+      return fail(LOPA_EINVAL, "layer %d: weight pointer is null", l);
+    if (cfg->qkv_bias && (!lw.bq || !lw.bk || !lw.bv))
+      return fail(LOPA_EINVAL, "layer %d: qkv_bias set but a bias pointer is null", l);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  lopa_model* m = new lopa_model();
+  m->cfg = *cfg;
+  const lopa_model_cfg& c = *cfg;
+  const int H = c.hidden, d = c.head_dim, F = c.ffn, V = c.vocab;
+  m->n_qkv = (c.heads + 2 * c.kv_heads) * d;
+  m->tiles_qkv = m->n_qkv / 128;
+  m->tiles_h = H / 128;
+  m->tiles_gu = F / 64;
+  m->tiles_lm = (V + 127) / 128;
+  auto bail = [&](int code) {
+    delete m;
+    return code;
+  };
+  if (hipGetDevice(&m->device) != hipSuccess ||
+      hipDeviceGetAttribute(&m->num_cu, hipDeviceAttributeMultiprocessorCount, m->device) !=
+          hipSuccess)
+    return bail(fail(LOPA_EHIP, "no HIP device"));
+  auto alloc16 = [&](uint16_t** p, size_t elems) -> int {
+    DevBuf b;
+    int r = dalloc(b, elems * 2, m->owned);
+    *p = (uint16_t*)b.p;
+    return r;
+  };
+  auto allocf = [&](float** p, size_t elems) -> int {
+    DevBuf b;
+    int r = dalloc(b, elems * 4, m->owned);
+    *p = (float*)b.p;
+    return r;
+  };
+  const size_t chunk = 128 * 64;  // elements per (tile, k-chunk)
+  m->layers.resize(c.layers);
+  for (int l = 0; l < c.layers; ++l) {
+    const lopa_layer_weights& lw = w->layers[l];
+    LayerPack& p = m->layers[l];
+    if ((rc = alloc16(&p.qkv, (size_t)m->tiles_qkv * (H / 64) * chunk)) ||
+        (rc = alloc16(&p.o, (size_t)m->tiles_h * (H / 64) * chunk)) ||
+        (rc = alloc16(&p.gu, (size_t)m->tiles_gu * (H / 64) * chunk)) ||
+        (rc = alloc16(&p.down, (size_t)m->tiles_h * (F / 64) * chunk)) ||
+        (rc = allocf(&p.ln1, H)) || (rc = allocf(&p.ln2, H)))
+      return bail(rc);
+    p.bias = nullptr;
+    if (c.qkv_bias && (rc = allocf(&p.bias, m->n_qkv))) return bail(rc);
+    const uint16_t* wq = (const uint16_t*)lw.wq;
+    const uint16_t* wk = (const uint16_t*)lw.wk;
+    const uint16_t* wv = (const uint16_t*)lw.wv;
+    hipError_t e;
+    if ((e = launch_repack(wq, c.heads * d, wk, c.kv_heads * d, wv, c.kv_heads * d, H,
+                           m->tiles_qkv, 0, p.qkv, s)) != hipSuccess ||
+        (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
+                           m->tiles_h, 0, p.o, s)) != hipSuccess ||
+        (e = launch_repack((const uint16_t*)lw.w_gate, F, (const uint16_t*)lw.w_up, F, nullptr,
+                           0, H, m->tiles_gu, 1, p.gu, s)) != hipSuccess ||
+        (e = launch_repack((const uint16_t*)lw.w_down, H, nullptr, 0, nullptr, 0, F, m->tiles_h,
+                           0, p.down, s)) != hipSuccess ||
+        (e = launch_bf16_to_f32((const uint16_t*)lw.ln1, p.ln1, H, s)) != hipSuccess ||
+        (e = launch_bf16_to_f32((const uint16_t*)lw.ln2, p.ln2, H, s)) != hipSuccess)
+      return bail(fail(LOPA_EHIP, "layer %d repack: %s", l, hipGetErrorString(e)));
+    if (p.bias) {
+      if ((e = launch_bf16_to_f32((const uint16_t*)lw.bq, p.bias, c.heads * d, s)) ||
+          (e = launch_bf16_to_f32((const uint16_t*)lw.bk, p.bias + c.heads * d, c.kv_heads * d,
+                                  s)) ||
+          (e = launch_bf16_to_f32((const uint16_t*)lw.bv,
+                                  p.bias + (c.heads + c.kv_heads) * d, c.kv_heads * d, s)))
+        return bail(fail(LOPA_EHIP, "layer %d bias: %s", l, hipGetErrorString(e)));
+    }
+  }
+  if ((rc = alloc16(&m->embed, (size_t)V * H)) ||
+      (rc = alloc16(&m->lm, (size_t)m->tiles_lm * (H / 64) * chunk)) ||
+      (rc = allocf(&m->final_norm, H)))
+    return bail(rc);
+  hipError_t e;
+  if ((e = hipMemcpyAsync(m->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s)) ||
+      (e = launch_repack((const uint16_t*)w->lm_head, V, nullptr, 0, nullptr, 0, H, m->tiles_lm,
+                         0, m->lm, s)) ||
+      (e = launch_bf16_to_f32((const uint16_t*)w->final_norm, m->final_norm, H, s)) ||
+      (e = hipStreamSynchronize(s)))
+    return bail(fail(LOPA_EHIP, "model create: %s", hipGetErrorString(e)));
+  *out = m;
+  return LOPA_OK;
+}
+
+void lopa_model_destroy(lopa_model* m) { delete m; }
+
+int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, int32_t max_block,
+                   lopa_kv** out) {
+  if (!out) return fail(LOPA_EINVAL, "out is null");
+  *out = nullptr;
+  if (!m) return fail(LOPA_EINVAL, "model is null");
+  if (max_len < 1 || max_branches < 1 || max_block < 1)
+    return fail(LOPA_EINVAL, "max_len, max_branches and max_block must be positive");
+  if (max_block > LOPA_MAX_BLOCK)
+    return fail(LOPA_ESHAPE, "max_block %d > %d", max_block, LOPA_MAX_BLOCK);
+  if ((int64_t)max_branches * max_block > LOPA_MAX_ROWS)
+    return fail(LOPA_ESHAPE, "max_branches * max_block > %d", LOPA_MAX_ROWS);
+  const lopa_model_cfg& c = m->cfg;
+  lopa_kv* kv = new lopa_kv();
+  kv->m = m;
+  kv->max_len = max_len;
+  kv->max_branches = max_branches;
+  kv->max_block = max_block;
+  kv->mp_max = 64 * pow2_waves(max_branches * max_block);
+  const int H = c.hidden, F = c.ffn, d = c.head_dim, Hkv = c.kv_heads;
+  auto bail = [&](int code) {
+    delete kv;
+    return code;
+  };
+  DevBuf b;
+  int rc;
+  const size_t cache_e = (size_t)c.layers * 2 * Hkv * max_len * d;
+  const size_t stag_e = (size_t)max_branches * c.layers * 2 * Hkv * max_block * d;
+  const int grid_max = m->num_cu;
+  const size_t part_b = (size_t)2 * grid_max * std::min(4, kv->mp_max / 64) * 32 * 64 * 16;
+  const int tiles_max = std::max(std::max(m->tiles_lm, m->tiles_gu), std::max(m->tiles_qkv, m->tiles_h));
+  const size_t rows = (size_t)kv->mp_max;
+#define KV_ALLOC(field, type, bytes)                  \
+  if ((rc = dalloc(b, (bytes), kv->owned))) return bail(rc); \
+  kv->field = (type)b.p;
+  KV_ALLOC(cache, uint16_t*, cache_e * 2);
+  KV_ALLOC(staging, uint16_t*, stag_e * 2);
+  KV_ALLOC(rope, float*, (size_t)max_len * (d / 2) * 2 * 4);
+  KV_ALLOC(x, float*, rows * H * 4);
+  KV_ALLOC(abuf, uint16_t*, rows * H * 2);
+  KV_ALLOC(fbuf, uint16_t*, rows * F * 2);
+  KV_ALLOC(qbuf, uint16_t*, (size_t)max_branches * c.heads * max_block * d * 2);
+  KV_ALLOC(partials, float*, part_b);
+  KV_ALLOC(counters, int32_t*, (size_t)tiles_max * (kv->mp_max / 256 + 1) * 4);
+  KV_ALLOC(pm, float*, rows * m->tiles_lm * 4);
+  KV_ALLOC(ps, float*, rows * m->tiles_lm * 4);
+  KV_ALLOC(pi, int32_t*, rows * m->tiles_lm * 4);
+#undef KV_ALLOC
+  // RoPE table in double precision, stored as fp32 (cos, sin) pairs.
+  std::vector<float> tab((size_t)max_len * (d / 2) * 2);
+  for (int p = 0; p < max_len; ++p)
+    for (int j = 0; j < d / 2; ++j) {
+      const double inv = std::pow((double)c.rope_theta, -2.0 * j / d);
+      const double ang = (double)p * inv;
+      tab[((size_t)p * (d / 2) + j) * 2] = (float)std::cos(ang);
+      tab[((size_t)p * (d / 2) + j) * 2 + 1] = (float)std::sin(ang);
+    }
+  hipError_t e;
+  if ((e = hipMemcpy(kv->rope, tab.data(), tab.size() * 4, hipMemcpyHostToDevice)) ||
+      (e = hipMemset(kv->cache, 0, cache_e * 2)) || (e = hipMemset(kv->staging, 0, stag_e * 2)) ||
+      (e = hipMemset(kv->abuf, 0, rows * H * 2)) || (e = hipMemset(kv->fbuf, 0, rows * F * 2)) ||
+      (e = hipMemset(kv->counters, 0, (size_t)tiles_max * (kv->mp_max / 256 + 1) * 4)) || (e = hipDeviceSynchronize()))
+    return bail(fail(LOPA_EHIP, "kv create: %s", hipGetErrorString(e)));
+  *out = kv;
+  return LOPA_OK;
+}
+
+void lopa_kv_destroy(lopa_kv* kv) { delete kv; }
+
+int lopa_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
+                        int32_t L, int32_t mask_id, float tau, int32_t k, int32_t* branch_tokens,
+                        int32_t* fill_pos, uint8_t* valid, int32_t* n_valid, void* stream) {
+  if (!tokens || !conf || !pred || !branch_tokens || !fill_pos || !valid || !n_valid)
+    return fail(LOPA_EINVAL, "null pointer argument");
+  if (k < 0) return fail(LOPA_EINVAL, "k = %d < 0", k);
+  if (!(tau >= 0.f && tau <= 1.f)) return fail(LOPA_EINVAL, "tau outside [0, 1]");
+  if (mask_id < 0) return fail(LOPA_EINVAL, "mask_id < 0");
+  if (L < 1 || L > LOPA_MAX_BLOCK) return fail(LOPA_ESHAPE, "L = %d outside [1, %d]", L, LOPA_MAX_BLOCK);
+  if (k + 1 > LOPA_MAX_ROWS) return fail(LOPA_ESHAPE, "k = %d too large", k);
+  HIP_TRY(launch_build_branches(tokens, conf, pred, L, mask_id, tau, k, branch_tokens, fill_pos,
+                                valid, n_valid, (hipStream_t)stream));
+  return LOPA_OK;
+}
+
+// The verify forward; with stop_layer >= 0 it stops after that many layers and
+// copies the fp32 residual stream to x_out instead of producing conf / pred.
+static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                       const int32_t* branch_tokens, int32_t n_branches, int32_t L, float* conf,
+                       int32_t* pred, void* stream, int stop_layer, float* x_out) {
+  const lopa_model_cfg& c = m->cfg;
+  hipStream_t s = (hipStream_t)stream;
+  const int M = n_branches * L;
+  const int Mp = 64 * pow2_waves(M);
+  const int H = c.hidden, F = c.ffn, d = c.head_dim;
+  const int KCh = H / 64, KCf = F / 64;
+
+  GemmArgs g{};
+  g.M = M;
+  g.Mp = Mp;
+  g.partials = kv->partials;
+  g.counters = kv->counters;
+  auto gemm = [&](int epi, const uint16_t* A, const uint16_t* W, int N, int KC, int tiles) {
+    g.A = A;
+    g.W = W;
+    g.N = N;
+    g.K = KC * 64;
+    g.KC = KC;
+    g.tiles = tiles;
+    const int64_t I = (int64_t)tiles * KC;
+    g.mtiles = Mp > 256 ? Mp / 256 : 1;
+    g.grid = (int)std::min<int64_t>(m->num_cu / g.mtiles, I) * g.mtiles;
+    return launch_gemm(epi, g, s);
+  };
+
+  HIP_TRY(launch_embed_norm(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M, Mp, H, kv->x,
+                            kv->abuf, s));
+  AttnArgs at{};
+  at.q = kv->qbuf;
+  at.staging = kv->staging;
+  at.out = kv->abuf;
+  at.nb = n_branches;
+  at.L = L;
+  at.P = prefix_len;
+  at.Hq = c.heads;
+  at.Hkv = c.kv_heads;
+  at.d = d;
+  at.max_len = kv->max_len;
+  at.layers = c.layers;
+  at.Lcap = kv->max_block;
+  at.Mp = Mp;
+  at.scale = 1.0f / std::sqrt((float)d);
+  const int n_layers = stop_layer >= 0 ? std::min(stop_layer, c.layers) : c.layers;
+  for (int l = 0; l < n_layers; ++l) {
+    const LayerPack& p = m->layers[l];
+    g.bias = p.bias;
+    g.rope = kv->rope;
+    g.q_out = kv->qbuf;
+    g.staging = kv->staging;
+    g.layer = l;
+    g.layers = c.layers;
+    g.Hq = c.heads;
+    g.Hkv = c.kv_heads;
+    g.d = d;
+    g.L = L;
+    g.Lcap = kv->max_block;
+    g.P = prefix_len;
+    HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, KCh, m->tiles_qkv));
+    at.layer = l;
+    at.kcache = kv->cache + ((size_t)l * 2 + 0) * c.kv_heads * kv->max_len * d;
+    at.vcache = kv->cache + ((size_t)l * 2 + 1) * c.kv_heads * kv->max_len * d;
+    HIP_TRY(launch_attention(at, s));
+    g.x = kv->x;
+    HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, KCh, m->tiles_h));
+    HIP_TRY(launch_rmsnorm_pack(kv->x, p.ln2, c.rms_eps, M, Mp, H, kv->abuf, s));
+    g.a_out = kv->fbuf;
+    HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, KCh, m->tiles_gu));
+    HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, KCf, m->tiles_h));
+    const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
+    HIP_TRY(launch_rmsnorm_pack(kv->x, next_w, c.rms_eps, M, Mp, H, kv->abuf, s));
+  }
+  if (stop_layer >= 0) {
+    HIP_TRY(hipMemcpyAsync(x_out, kv->x, (size_t)M * H * 4, hipMemcpyDeviceToDevice, s));
+    return LOPA_OK;
+  }
+  g.pm = kv->pm;
+  g.ps = kv->ps;
+  g.pi = kv->pi;
+  g.vocab = c.vocab;
+  g.mask_id = c.mask_id;
+  HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, m->tiles_lm * 128, KCh, m->tiles_lm));
+  HIP_TRY(launch_lm_merge(kv->pm, kv->ps, kv->pi, M, m->tiles_lm, conf, pred, s));
+  kv->last_nb = n_branches;
+  kv->last_L = L;
+  kv->last_P = prefix_len;
+  return LOPA_OK;
+}
+
+static int check_verify(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                        const int32_t* branch_tokens, int32_t n_branches, int32_t L) {
+  if (!m || !kv || !branch_tokens) return fail(LOPA_EINVAL, "null pointer argument");
+  if (kv->m != m) return fail(LOPA_EINVAL, "kv was created for another model");
+  if (n_branches < 1 || L < 1) return fail(LOPA_ESHAPE, "n_branches and L must be >= 1");
+  if (n_branches > kv->max_branches || L > kv->max_block)
+    return fail(LOPA_ESHAPE, "n_branches %d / L %d exceed kv capacity %d / %d", n_branches, L,
+                kv->max_branches, kv->max_block);
+  if (prefix_len < 0) return fail(LOPA_EINVAL, "prefix_len < 0");
+  if ((int64_t)prefix_len + L > kv->max_len)
+    return fail(LOPA_ECAPACITY, "prefix_len %d + L %d > max_len %d", prefix_len, L, kv->max_len);
+  return LOPA_OK;
+}
+
+int lopa_verify_forward(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                        const int32_t* branch_tokens, int32_t n_branches, int32_t L, float* conf,
+                        int32_t* pred, void* stream) {
+  if (!conf || !pred) return fail(LOPA_EINVAL, "null pointer argument");
+  int rc = check_verify(m, kv, prefix_len, branch_tokens, n_branches, L);
+  if (rc) return rc;
+  return verify_impl(m, kv, prefix_len, branch_tokens, n_branches, L, conf, pred, stream, -1,
+                     nullptr);
+}
+
+int lopa_debug_hidden(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                      const int32_t* branch_tokens, int32_t n_branches, int32_t L,
+                      int32_t n_layers, float* x_out, void* stream) {
+  if (!x_out) return fail(LOPA_EINVAL, "null pointer argument");
+  int rc = check_verify(m, kv, prefix_len, branch_tokens, n_branches, L);
+  if (rc) return rc;
+  if (n_layers < 0 || n_layers > m->cfg.layers) return fail(LOPA_EINVAL, "n_layers out of range");
+  return verify_impl(m, kv, prefix_len, branch_tokens, n_branches, L, nullptr, nullptr, stream,
+                     n_layers, x_out);
+}
+
+int lopa_branch_confidence_select(const int32_t* branch_tokens, const float* conf,
+                                  const int32_t* pred, const uint8_t* valid, int32_t n_branches,
+                                  int32_t L, int32_t mask_id, float* scores, int32_t* winner,
+                                  int32_t* next_tokens, float* next_conf, int32_t* next_pred,
+                                  int32_t* next_unfilled, void* stream) {
+  if (!branch_tokens || !conf || !pred || !valid || !scores || !winner || !next_tokens ||
+      !next_conf || !next_pred || !next_unfilled)
+    return fail(LOPA_EINVAL, "null pointer argument");
+  if (n_branches < 1 || n_branches > 1024) return fail(LOPA_ESHAPE, "n_branches %d outside [1, 1024]", n_branches);
+  if (L < 1 || L > LOPA_MAX_BLOCK) return fail(LOPA_ESHAPE, "L = %d outside [1, %d]", L, LOPA_MAX_BLOCK);
+  if (mask_id < 0) return fail(LOPA_EINVAL, "mask_id < 0");
+  HIP_TRY(launch_select(branch_tokens, conf, pred, valid, n_branches, L, mask_id, scores, winner,
+                        next_tokens, next_conf, next_pred, next_unfilled, (hipStream_t)stream));
+  return LOPA_OK;
+}
+
+int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,
+                   int32_t* append_offset, void* stream) {
+  if (!kv || !winner || !append_offset) return fail(LOPA_EINVAL, "null pointer argument");
+  if (kv->last_nb < 0) return fail(LOPA_EINVAL, "no verify forward has staged K/V yet");
+  if (prefix_len != kv->last_P || L != kv->last_L)
+    return fail(LOPA_EINVAL, "prefix_len/L (%d, %d) differ from the last verify forward (%d, %d)",
+                prefix_len, L, kv->last_P, kv->last_L);
+  if ((int64_t)prefix_len + L > kv->max_len) return fail(LOPA_ECAPACITY, "commit beyond max_len");
+  const lopa_model_cfg& c = kv->m->cfg;
+  HIP_TRY(launch_commit(kv->staging, kv->cache, winner, kv->last_nb, c.layers, c.kv_heads,
+                        kv->max_block, kv->max_len, c.head_dim, prefix_len, L, append_offset,
+                        (hipStream_t)stream));
+  return LOPA_OK;
+}
+
+int lopa_kv_read(const lopa_kv* kv, int32_t layer, int32_t start, int32_t len, void* k_dst,
+                 void* v_dst, void* stream) {
+  if (!kv || !k_dst || !v_dst) return fail(LOPA_EINVAL, "null pointer argument");
+  const lopa_model_cfg& c = kv->m->cfg;
+  if (layer < 0 || layer >= c.layers || start < 0 || len < 1 || (int64_t)start + len > kv->max_len)
+    return fail(LOPA_EINVAL, "layer/start/len out of range");
+  const int d = c.head_dim, Hkv = c.kv_heads;
+  for (int kvi = 0; kvi < 2; ++kvi) {
+    const uint16_t* src = kv->cache + (((size_t)layer * 2 + kvi) * Hkv * kv->max_len + start) * d;
+    uint16_t* dst = (uint16_t*)(kvi ? v_dst : k_dst);
+    HIP_TRY(launch_kv_copy(src, dst, (int64_t)kv->max_len * d, (int64_t)len * d, Hkv, len * d,
+                           (hipStream_t)stream));
+  }
+  return LOPA_OK;
+}
+
+int lopa_kv_write(lopa_kv* kv, int32_t layer, int32_t start, int32_t len, const void* k_src,
+                  const void* v_src, void* stream) {
+  if (!kv || !k_src || !v_src) return fail(LOPA_EINVAL, "null pointer argument");
+  const lopa_model_cfg& c = kv->m->cfg;
+  if (layer < 0 || layer >= c.layers || start < 0 || len < 1 || (int64_t)start + len > kv->max_len)
+    return fail(LOPA_EINVAL, "layer/start/len out of range");
+  const int d = c.head_dim, Hkv = c.kv_heads;
+  for (int kvi = 0; kvi < 2; ++kvi) {
+    uint16_t* dst = kv->cache + (((size_t)layer * 2 + kvi) * Hkv * kv->max_len + start) * d;
+    const uint16_t* src = (const uint16_t*)(kvi ? v_src : k_src);
+    HIP_TRY(launch_kv_copy(src, dst, (int64_t)len * d, (int64_t)kv->max_len * d, Hkv, len * d,
+                           (hipStream_t)stream));
+  }
+  return LOPA_OK;
+}
+
+int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer, void* k_dst,
+                         void* v_dst, void* stream) {
+  if (!kv || !k_dst || !v_dst) return fail(LOPA_EINVAL, "null pointer argument");
+  const lopa_model_cfg& c = kv->m->cfg;
+  if (kv->last_nb < 0) return fail(LOPA_EINVAL, "nothing staged yet");
+  if (branch < 0 || branch >= kv->last_nb || layer < 0 || layer >= c.layers)
+    return fail(LOPA_EINVAL, "branch/layer out of range");
+  const int d = c.head_dim, Hkv = c.kv_heads, L = kv->last_L;
+  for (int kvi = 0; kvi < 2; ++kvi) {
+    const uint16_t* src =
+        kv->staging + ((((size_t)branch * c.layers + layer) * 2 + kvi) * Hkv) * kv->max_block * d;
+    uint16_t* dst = (uint16_t*)(kvi ? v_dst : k_dst);
+    HIP_TRY(launch_kv_copy(src, dst, (int64_t)kv->max_block * d, (int64_t)L * d, Hkv, L * d,
+                           (hipStream_t)stream));
+  }
+  return LOPA_OK;
+}
+
+}  // extern "C"

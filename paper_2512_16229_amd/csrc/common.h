@@ -1,0 +1,61 @@
+// Shared definitions of the gfx950 kernels of the LoPA verify step.
+//
+// Fragment-packed bf16 layout (used for every GEMM operand):
+//   a matrix X with R rows and K columns (R % 16 == 0, K % 32 == 0) is stored as
+//   1 KiB fragments of 16 rows x 32 columns. Inside a fragment, lane
+//   l = (r % 16) + 16 * ((c % 32) / 8) holds the 8 consecutive columns
+//   c = 8 * (l / 16) .. +7 of row r % 16, i.e. exactly the per-lane operand of
+//   v_mfma_f32_16x16x32_bf16 (A: lane -> row, B: lane -> column of W^T).
+//   A wave reads one fragment as 64 lanes x 16 contiguous bytes.
+//
+// Activations ("A" operands, R = padded rows Mp):   fragment (rb, kb) at
+//   ((kb * (Mp/16)) + rb) * 512 elements.
+// Weights (W [N, K] in [out, in] order, "B" operand): tiles of BN = 128 output
+//   features; chunk kc of BK = 64 columns of tile t holds 16 fragments
+//   (kk in 0..1, nb in 0..7) at ((t * KC + kc) * 16 + kk * 8 + nb) * 512, so the
+//   whole weight is one linear stream in (tile, k-chunk) order.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define LOPA_BN 128
+#define LOPA_BK 64
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f2bf_bits(float f) {
+  // round to nearest even; NaN stays NaN
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf2f_bits(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// element offset of (row r, column c) in an activation matrix packed with Mp rows
+__device__ __forceinline__ int64_t packA_off(int r, int c, int Mp) {
+  int rb = r >> 4, kb = c >> 5;
+  int lane = (r & 15) + 16 * ((c & 31) >> 3);
+  return ((int64_t)(kb * (Mp >> 4) + rb) * 64 + lane) * 8 + (c & 7);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}

@@ -1,0 +1,82 @@
+// Host-side launchers of the gfx950 kernels (internal to liblopa).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// ----------------------------------------------------------- step kernels
+hipError_t launch_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
+                                 int L, int mask_id, float tau, int k, int32_t* branch_tokens,
+                                 int32_t* fill_pos, uint8_t* valid, int32_t* n_valid,
+                                 hipStream_t s);
+hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pred,
+                         const uint8_t* valid, int nb, int L, int mask_id, float* scores,
+                         int32_t* winner, int32_t* nt, float* nc, int32_t* np, int32_t* nu,
+                         hipStream_t s);
+hipError_t launch_commit(const uint16_t* staging, uint16_t* cache, const int32_t* winner,
+                         int nb_last, int layers, int Hkv, int Lcap, int max_len, int d, int P,
+                         int L, int32_t* append_offset, hipStream_t s);
+hipError_t launch_kv_copy(const uint16_t* src, uint16_t* dst, int64_t src_stride,
+                          int64_t dst_stride, int groups, int rows_elems, hipStream_t s);
+
+// ------------------------------------------------------------ weight repack
+// Pack rows of up to three [rows_i, K] bf16 sources (stacked in order) into the
+// tile-major fragment layout; N_pad = tiles * 128 rows, rows past the sources
+// are zero. interleave64: tile t takes rows [64t, 64t+64) of source 0 then the
+// same rows of source 1 (gate / up pairing for the SwiGLU epilogue).
+hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
+                         const uint16_t* s2, int r2, int K, int tiles, int interleave64,
+                         uint16_t* dst, hipStream_t s);
+hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_t s);
+
+// ---------------------------------------------------------------- per-row
+// x[r] = embed[tokens[r]] (fp32) and a[r] = pack(rmsnorm(x[r]) * w) for r < M.
+hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int vocab,
+                             const float* w, float eps, int M, int Mp, int H, float* x,
+                             uint16_t* a, hipStream_t s);
+// a[r] = pack(rmsnorm(x[r]) * w) for r < M.
+hipError_t launch_rmsnorm_pack(const float* x, const float* w, float eps, int M, int Mp, int H,
+                               uint16_t* a, hipStream_t s);
+// merge per-tile softmax partials into conf / pred
+hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, int M,
+                           int tiles, float* conf, int32_t* pred, hipStream_t s);
+
+// ---------------------------------------------------------------- GEMM
+enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
+
+struct GemmArgs {
+  const uint16_t* A;   // packed activations, Mp rows, K columns
+  const uint16_t* W;   // packed weights, tiles x KC chunks
+  int M, Mp, N, K, KC, tiles;
+  int mtiles;          // row tiles of 256 rows (Mp <= 256 -> 1)
+  int grid;            // workgroups = mtiles x column workgroups (stream-K)
+  float* partials;     // [2*grid][4 waves][32][64][4] fp32
+  int32_t* counters;   // [tiles * mtiles], zero between launches
+  // EPI_QKV
+  const float* bias;   // [N] or null
+  const float* rope;   // [max_pos][d/2][2] (cos, sin)
+  uint16_t* q_out;     // [nb][Hq][L][d]
+  uint16_t* staging;   // [nb][layers][2][Hkv][Lcap][d]
+  int layer, layers, Hq, Hkv, d, L, Lcap, P;
+  // EPI_RESID
+  float* x;            // [M][N] fp32 residual stream (row stride N)
+  // EPI_SWIGLU
+  uint16_t* a_out;     // packed, Mp rows, N/2 columns
+  // EPI_LMHEAD
+  float* pm;           // [M][tiles] running max
+  float* ps;           // [M][tiles] sum of exp(l - max)
+  int32_t* pi;         // [M][tiles] argmax
+  int vocab, mask_id;
+};
+hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  const uint16_t* q;       // [nb][Hq][L][d] bf16 (post-RoPE)
+  const uint16_t* kcache;  // layer's K cache [Hkv][max_len][d]
+  const uint16_t* vcache;  // layer's V cache
+  const uint16_t* staging; // [nb][layers][2][Hkv][Lcap][d]
+  uint16_t* out;           // packed activations (Mp rows, Hq*d columns)
+  int nb, L, P, Hq, Hkv, d, max_len, layer, layers, Lcap, Mp;
+  float scale;
+};
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

@@ -1,0 +1,184 @@
+// Branch construction (Eq. 1 + top-k, Alg. 1 steps 1-2), branch scoring and
+// selection (Eq. 2, Alg. 1 step 3), and the winner's K/V commit (Sec. 3.4).
+// Each runs as one small launch; the decision logic is integer work on fp32
+// comparisons, done by one wavefront per block row.
+#include "common.h"
+#include "kernels.h"
+
+#include <math.h>
+
+// One wavefront (64 lanes), lane i owns block position i (L <= 64).
+__global__ __launch_bounds__(64) void build_branches_kernel(
+    const int32_t* __restrict__ tokens, const float* __restrict__ conf,
+    const int32_t* __restrict__ pred, int L, int mask_id, float tau, int k,
+    int32_t* __restrict__ branch_tokens, int32_t* __restrict__ fill_pos,
+    uint8_t* __restrict__ valid, int32_t* __restrict__ n_valid) {
+  __shared__ float s_conf[64];
+  __shared__ int s_rem[64];
+  const int i = threadIdx.x;
+  const bool in = i < L;
+  const int tok = in ? tokens[i] : 0;
+  const float c = in ? conf[i] : 0.f;
+  const int pr = in ? pred[i] : 0;
+  const bool unf = in && tok == mask_id;
+
+  // Eq. 1: S_high = {i in M_t : conf_i > tau}; else the argmax of conf over M_t.
+  const bool high = unf && (c > tau);
+  const bool any_high = __ballot(high) != 0ull;
+  bool fill = high;
+  if (!any_high) {
+    // lowest position among the largest conf of the unfilled set
+    float bc = unf ? c : -INFINITY;
+    int bi = unf ? i : 0x7fffffff;
+    for (int o = 32; o > 0; o >>= 1) {
+      float oc = __shfl_xor(bc, o);
+      int oi = __shfl_xor(bi, o);
+      if (oc > bc || (oc == bc && oi < bi)) { bc = oc; bi = oi; }
+    }
+    fill = (i == bi) && unf;
+  }
+  const int b0 = fill ? pr : tok;
+  const bool rem = in && (b0 == mask_id);  // M_B0
+
+  // Rank of each position of M_B0 by (conf desc, position asc).
+  s_conf[i] = c;
+  s_rem[i] = rem ? 1 : 0;
+  __syncthreads();
+  int rank = 0;
+  if (rem) {
+    for (int j = 0; j < L; ++j) {
+      if (!s_rem[j]) continue;
+      const float cj = s_conf[j];
+      rank += (cj > c || (cj == c && j < i)) ? 1 : 0;
+    }
+  }
+  const int n_rem = __popcll(__ballot(rem));
+  const int k_eff = k < n_rem ? k : n_rem;
+
+  // Branch j: B0, plus position p_j (rank j-1) filled with pred.
+  if (in) {
+    for (int j = 0; j <= k; ++j) {
+      int v = b0;
+      if (rem && j >= 1 && rank == j - 1 && j <= k_eff) v = pr;
+      branch_tokens[(int64_t)j * L + i] = v;
+    }
+  }
+  if (rem && rank < k_eff) fill_pos[rank + 1] = i;
+  for (int j = i; j <= k; j += 64) {
+    if (j == 0 || j > k_eff) fill_pos[j] = -1;
+    valid[j] = (j <= k_eff) ? 1 : 0;
+  }
+  if (i == 0) n_valid[0] = 1 + k_eff;
+}
+
+// Eq. 2 per branch: one wavefront per branch row (fixed reduction order, so
+// identical rows give bit-identical scores), then the argmax and the next state.
+__global__ __launch_bounds__(256) void select_kernel(
+    const int32_t* __restrict__ branch_tokens, const float* __restrict__ conf,
+    const int32_t* __restrict__ pred, const uint8_t* __restrict__ valid, int nb, int L,
+    int mask_id, float* __restrict__ scores, int32_t* __restrict__ winner,
+    int32_t* __restrict__ next_tokens, float* __restrict__ next_conf,
+    int32_t* __restrict__ next_pred, int32_t* __restrict__ next_unfilled) {
+  __shared__ float s_score[1024];
+  __shared__ int s_win;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  for (int j = wv; j < nb; j += 4) {
+    const bool in = lane < L;
+    const int t = in ? branch_tokens[(int64_t)j * L + lane] : 0;
+    const bool m = in && t == mask_id;
+    float s = m ? conf[(int64_t)j * L + lane] : 0.f;
+    s = wave_sum(s);
+    const int cnt = __popcll(__ballot(m));
+    float sc = cnt ? s / (float)cnt : INFINITY;
+    if (!valid[j]) sc = -INFINITY;
+    if (lane == 0) {
+      scores[j] = sc;
+      s_score[j] = sc;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int best = 0;
+    for (int j = 1; j < nb; ++j)
+      if (s_score[j] > s_score[best]) best = j;
+    s_win = best;
+    winner[0] = best;
+  }
+  __syncthreads();
+  const int w = s_win;
+  if (threadIdx.x < 64) {
+    const int i = threadIdx.x;
+    const bool in = i < L;
+    int t = 0;
+    if (in) {
+      t = branch_tokens[(int64_t)w * L + i];
+      next_tokens[i] = t;
+      next_conf[i] = conf[(int64_t)w * L + i];
+      next_pred[i] = pred[(int64_t)w * L + i];
+    }
+    const int cnt = __popcll(__ballot(in && t == mask_id));
+    if (i == 0) next_unfilled[0] = cnt;
+  }
+}
+
+// Copy the winner's staged K/V (all layers) to cache rows [P, P+L).
+// grid = layers * 2 * Hkv; staging layout [nb][layers][2][Hkv][Lcap][d],
+// cache layout [layers][2][Hkv][max_len][d] (both bf16).
+__global__ __launch_bounds__(256) void commit_kernel(
+    const uint16_t* __restrict__ staging, uint16_t* __restrict__ cache,
+    const int32_t* __restrict__ winner, int nb_last, int layers, int Hkv, int Lcap,
+    int max_len, int d, int P, int L, int32_t* __restrict__ append_offset) {
+  const int w = winner[0];
+  const bool ok = (w >= 0 && w < nb_last);
+  if (blockIdx.x == 0 && threadIdx.x == 0) append_offset[0] = ok ? P : -1;
+  if (!ok) return;
+  const int lhg = blockIdx.x;  // (layer, kv, head) flattened
+  const uint4* src = (const uint4*)(staging + (((int64_t)w * layers * 2 * Hkv + lhg) * Lcap) * d);
+  uint4* dst = (uint4*)(cache + ((int64_t)lhg * max_len + P) * d);
+  const int n = L * d / 8;
+  for (int e = threadIdx.x; e < n; e += blockDim.x) dst[e] = src[e];
+}
+
+// Row copies between the cache and a caller buffer [Hkv][len][d] for one layer.
+__global__ __launch_bounds__(256) void kv_copy_kernel(const uint16_t* __restrict__ src,
+                                                      uint16_t* __restrict__ dst, int64_t src_stride,
+                                                      int64_t dst_stride, int rows_elems) {
+  const int g = blockIdx.x;
+  const uint16_t* s = src + g * src_stride;
+  uint16_t* t = dst + g * dst_stride;
+  for (int e = threadIdx.x; e < rows_elems; e += blockDim.x) t[e] = s[e];
+}
+
+// ------------------------------------------------------------ launchers
+hipError_t launch_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
+                                 int L, int mask_id, float tau, int k, int32_t* branch_tokens,
+                                 int32_t* fill_pos, uint8_t* valid, int32_t* n_valid,
+                                 hipStream_t s) {
+  hipLaunchKernelGGL(build_branches_kernel, dim3(1), dim3(64), 0, s, tokens, conf, pred, L,
+                     mask_id, tau, k, branch_tokens, fill_pos, valid, n_valid);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pred,
+                         const uint8_t* valid, int nb, int L, int mask_id, float* scores,
+                         int32_t* winner, int32_t* nt, float* nc, int32_t* np, int32_t* nu,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(256), 0, s, bt, conf, pred, valid, nb, L,
+                     mask_id, scores, winner, nt, nc, np, nu);
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(const uint16_t* staging, uint16_t* cache, const int32_t* winner,
+                         int nb_last, int layers, int Hkv, int Lcap, int max_len, int d, int P,
+                         int L, int32_t* append_offset, hipStream_t s) {
+  hipLaunchKernelGGL(commit_kernel, dim3(layers * 2 * Hkv), dim3(256), 0, s, staging, cache,
+                     winner, nb_last, layers, Hkv, Lcap, max_len, d, P, L, append_offset);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_copy(const uint16_t* src, uint16_t* dst, int64_t src_stride,
+                          int64_t dst_stride, int groups, int rows_elems, hipStream_t s) {
+  hipLaunchKernelGGL(kv_copy_kernel, dim3(groups), dim3(256), 0, s, src, dst, src_stride,
+                     dst_stride, rows_elems);
+  return hipGetLastError();
+}

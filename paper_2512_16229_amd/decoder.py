@@ -1,0 +1,115 @@
+"""Host driver of the LoPA decode loop over the four C-ABI calls.
+
+One iteration (Alg. 1) = build_branches -> verify_forward (all k+1 branches in
+one pass) -> branch_confidence_select -> commit_kv, all enqueued on one
+stream; the only host read per iteration is the winner's unfilled count (a
+4-byte copy) that ends the block. Prompt encoding is block-causal in blocks of
+L through the same verify forward with one branch, committed block by block.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import (KV, Model, lopa_branch_confidence_select, lopa_build_branches, lopa_commit_kv,
+               lopa_verify_forward)
+
+
+class Decoder:
+    def __init__(self, model: Model, kv: KV, L: int, k: int, tau: float):
+        self.model, self.kv, self.L, self.k, self.tau = model, kv, L, k, float(tau)
+        self.mask_id = model.cfg["mask_id"]
+        nb = k + 1
+        dev = "cuda"
+        i32 = dict(dtype=torch.int32, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.tokens = torch.full((L,), self.mask_id, **i32)
+        self.conf = torch.zeros(L, **f32)
+        self.pred = torch.zeros(L, **i32)
+        self.branch_tokens = torch.empty(nb * L, **i32)
+        self.fill_pos = torch.empty(nb, **i32)
+        self.valid = torch.empty(nb, dtype=torch.uint8, device=dev)
+        self.n_valid = torch.empty(1, **i32)
+        self.conf_b = torch.empty(nb * L, **f32)
+        self.pred_b = torch.empty(nb * L, **i32)
+        self.scores = torch.empty(nb, **f32)
+        self.winner = torch.zeros(1, **i32)
+        self.next_tokens = torch.empty(L, **i32)
+        self.next_conf = torch.empty(L, **f32)
+        self.next_pred = torch.empty(L, **i32)
+        self.next_unfilled = torch.empty(1, **i32)
+        self.append_offset = torch.empty(1, **i32)
+        self.zero = torch.zeros(1, **i32)
+        self.forwards = 0
+
+    # -------------------------------------------------------------- prompt
+    def prefill(self, prompt: torch.Tensor) -> int:
+        """Encode the prompt block-causally; returns the new prefix length."""
+        prompt = prompt.to(device="cuda", dtype=torch.int32).contiguous()
+        pos = 0
+        conf = torch.empty(self.L, dtype=torch.float32, device="cuda")
+        pred = torch.empty(self.L, dtype=torch.int32, device="cuda")
+        while pos < prompt.numel():
+            blk = prompt[pos:pos + self.L].contiguous()
+            n = blk.numel()
+            lopa_verify_forward(self.model, self.kv, pos, blk, 1, n, conf[:n], pred[:n])
+            lopa_commit_kv(self.kv, self.zero, pos, n, self.append_offset)
+            pos += n
+        return pos
+
+    # --------------------------------------------------------------- block
+    def init_block(self, P: int):
+        """All-mask block and its first forward (conf / pred of the state)."""
+        self.tokens.fill_(self.mask_id)
+        lopa_verify_forward(self.model, self.kv, P, self.tokens, 1, self.L, self.conf, self.pred)
+        self.forwards += 1
+
+    def step(self, P: int):
+        """One LoPA iteration; the next state replaces the current one."""
+        L, nb = self.L, self.k + 1
+        lopa_build_branches(self.tokens, self.conf, self.pred, L, self.mask_id, self.tau, self.k,
+                            self.branch_tokens, self.fill_pos, self.valid, self.n_valid)
+        lopa_verify_forward(self.model, self.kv, P, self.branch_tokens, nb, L, self.conf_b,
+                            self.pred_b)
+        lopa_branch_confidence_select(self.branch_tokens, self.conf_b, self.pred_b, self.valid, nb,
+                                      L, self.mask_id, self.scores, self.winner, self.next_tokens,
+                                      self.next_conf, self.next_pred, self.next_unfilled)
+        lopa_commit_kv(self.kv, self.winner, P, L, self.append_offset)
+        self.tokens, self.next_tokens = self.next_tokens, self.tokens
+        self.conf, self.next_conf = self.next_conf, self.conf
+        self.pred, self.next_pred = self.next_pred, self.pred
+        self.forwards += 1
+
+    def decode_block(self, P: int, trace=None) -> int:
+        """Run iterations until the winner has no unfilled position; returns the count."""
+        self.init_block(P)
+        it = 0
+        while True:
+            self.step(P)
+            it += 1
+            if trace is not None:
+                trace.append(self.snapshot())
+            if int(self.next_unfilled.item()) == 0:
+                return it
+            if it > self.L:
+                raise RuntimeError("block did not complete in L iterations")
+
+    def snapshot(self) -> dict:
+        nb, L = self.k + 1, self.L
+        return dict(branch_tokens=self.branch_tokens.view(nb, L).cpu(),
+                    fill_pos=self.fill_pos.cpu(), valid=self.valid.cpu(),
+                    n_valid=int(self.n_valid.item()), conf=self.conf_b.view(nb, L).cpu(),
+                    pred=self.pred_b.view(nb, L).cpu(), scores=self.scores.cpu(),
+                    winner=int(self.winner.item()), tokens=self.tokens.cpu(),
+                    append_offset=int(self.append_offset.item()))
+
+    def decode(self, prompt: torch.Tensor, gen_len: int) -> dict:
+        P = self.prefill(prompt)
+        out, iters = [], 0
+        self.forwards = 0
+        for _ in range(gen_len // self.L):
+            iters += self.decode_block(P)
+            out.append(self.tokens.clone())
+            P += self.L
+        toks = torch.cat(out) if out else torch.zeros(0, dtype=torch.int32, device="cuda")
+        return dict(tokens=toks, iterations=iters, forwards=self.forwards,
+                    tpf=(toks.numel() / self.forwards) if self.forwards else 0.0)
