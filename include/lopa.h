@@ -207,6 +207,27 @@ int lopa_kv_write(lopa_kv* kv, int32_t layer, int32_t start, int32_t len,
 int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer,
                          void* k_dst, void* v_dst, void* stream);
 
+/* Launch timing of lopa_verify_forward with HIP events on the call's stream.
+ * kinds_mask selects which launches get an event pair (bit i = kind i below);
+ * 0 turns timing off. Events between launches cost a few microseconds each. */
+enum {
+  LOPA_PROF_QKV = 0,     /* QKV projection + bias + RoPE + K/V staging  */
+  LOPA_PROF_ATTN = 1,    /* block attention                              */
+  LOPA_PROF_OPROJ = 2,   /* output projection + residual                 */
+  LOPA_PROF_GATEUP = 3,  /* gate/up projection + SwiGLU                  */
+  LOPA_PROF_DOWN = 4,    /* down projection + residual                   */
+  LOPA_PROF_LMHEAD = 5,  /* LM head + per-tile softmax partials          */
+  LOPA_PROF_NORM = 6,    /* embedding / RMSNorm row kernels              */
+  LOPA_PROF_MERGE = 7,   /* softmax merge -> conf / pred                 */
+  LOPA_PROF_KINDS = 8
+};
+int lopa_kv_profile(lopa_kv* kv, int32_t kinds_mask);
+
+/* Wait for the recorded events, and return per kind the summed launch time in
+ * milliseconds (total_ms[LOPA_PROF_KINDS], host) and the number of timed
+ * launches (launches[LOPA_PROF_KINDS], host) since the last read; resets them. */
+int lopa_kv_profile_read(lopa_kv* kv, double* total_ms, int64_t* launches);
+
 /* Diagnostics of the verify forward: run the embedding and the first n_layers
  * decoder layers (0 <= n_layers <= cfg.layers) of lopa_verify_forward on the
  * same arguments and copy the fp32 residual stream [n_branches*L][hidden]

@@ -52,7 +52,9 @@ class lopa_weight_ptrs(C.Structure):
 EXPORTS = ["lopa_model_create", "lopa_model_destroy", "lopa_kv_create", "lopa_kv_destroy",
            "lopa_strerror", "lopa_last_error", "lopa_build_branches", "lopa_verify_forward",
            "lopa_branch_confidence_select", "lopa_commit_kv", "lopa_kv_read", "lopa_kv_write",
-           "lopa_kv_read_staging", "lopa_debug_hidden"]
+           "lopa_kv_read_staging", "lopa_debug_hidden", "lopa_kv_profile",
+           "lopa_kv_profile_read"]
+PROF_KINDS = ["qkv", "attn", "oproj", "gateup", "down", "lmhead", "norm", "merge"]
 
 
 def _load():
@@ -76,6 +78,8 @@ def _load():
         "lopa_kv_write": (C.c_int, [P, I32, I32, I32, P, P, P]),
         "lopa_kv_read_staging": (C.c_int, [P, I32, I32, P, P, P]),
         "lopa_debug_hidden": (C.c_int, [P, P, I32, P, I32, I32, I32, P, P]),
+        "lopa_kv_profile": (C.c_int, [P, I32]),
+        "lopa_kv_profile_read": (C.c_int, [P, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -172,6 +176,21 @@ class KV:
         v = torch.empty_like(k)
         _check(lib.lopa_kv_read_staging(self.handle, branch, layer, _ptr(k), _ptr(v), _stream(stream)))
         return k, v
+
+    def profile(self, kinds=()):
+        """Time launches of the given kinds (names from PROF_KINDS) with HIP events."""
+        mask = 0
+        for kd in kinds:
+            mask |= 1 << PROF_KINDS.index(kd)
+        _check(lib.lopa_kv_profile(self.handle, mask))
+
+    def profile_read(self) -> dict:
+        """{kind: (total_ms, launches)} since the last read."""
+        n = len(PROF_KINDS)
+        ms = (C.c_double * n)()
+        cnt = (C.c_int64 * n)()
+        _check(lib.lopa_kv_profile_read(self.handle, ms, cnt))
+        return {PROF_KINDS[i]: (ms[i], cnt[i]) for i in range(n)}
 
     def close(self):
         if getattr(self, "handle", None) and lib is not None:

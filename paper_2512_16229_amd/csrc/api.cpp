@@ -62,12 +62,9 @@ struct LayerPack {
   float* ln2;
 };
 
-int pow2_waves(int M) {
-  int w = (M + 63) / 64;
-  int p = 1;
-  while (p < w) p <<= 1;
-  return p;
-}
+// rows of the packed activation buffers: whole 256-row tiles
+int padded_rows(int M) { return 256 * ((M + 255) / 256); }
+int round128(int k) { return 128 * ((k + 127) / 128); }
 
 }  // namespace
 
@@ -97,16 +94,52 @@ struct lopa_kv {
   uint16_t* fbuf = nullptr;     // packed [mp_max][F]
   uint16_t* qbuf = nullptr;     // [max_branches][Hq][max_block][d]
   float* partials = nullptr;
-  int32_t* counters = nullptr;
   float* pm = nullptr;
   float* ps = nullptr;
   int32_t* pi = nullptr;
   int last_nb = -1, last_L = -1, last_P = -1;
   std::vector<void*> owned;
+  // launch timing (lopa_kv_profile): events around launches of enabled kinds
+  int prof_mask = 0;
+  struct Ev {
+    int kind;
+    hipEvent_t a, b;
+  };
+  std::vector<Ev> ev_pool;
+  size_t ev_used = 0;
+  double prof_ms[LOPA_PROF_KINDS] = {};
+  int64_t prof_n[LOPA_PROF_KINDS] = {};
   ~lopa_kv() {
+    for (auto& e : ev_pool) {
+      (void)hipEventDestroy(e.a);
+      (void)hipEventDestroy(e.b);
+    }
     for (void* p : owned) (void)hipFree(p);
   }
 };
+
+namespace {
+// Record an event pair around one launch when its kind is enabled.
+struct ProfScope {
+  lopa_kv* kv;
+  lopa_kv::Ev* ev = nullptr;
+  hipStream_t s;
+  ProfScope(lopa_kv* k, int kind, hipStream_t st) : kv(k), s(st) {
+    if (!(kv->prof_mask & (1 << kind))) return;
+    if (kv->ev_used == kv->ev_pool.size()) {
+      lopa_kv::Ev e{kind, nullptr, nullptr};
+      if (hipEventCreate(&e.a) != hipSuccess || hipEventCreate(&e.b) != hipSuccess) return;
+      kv->ev_pool.push_back(e);
+    }
+    ev = &kv->ev_pool[kv->ev_used++];
+    ev->kind = kind;
+    (void)hipEventRecord(ev->a, s);
+  }
+  ~ProfScope() {
+    if (ev) (void)hipEventRecord(ev->b, s);
+  }
+};
+}  // namespace
 
 extern "C" {
 
@@ -192,7 +225,8 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     *p = (float*)b.p;
     return r;
   };
-  const size_t chunk = 128 * 64;  // elements per (tile, k-chunk)
+  const size_t chunk = 128 * 64;  // elements per (tile, 64-column chunk)
+  const int FP = round128(F);     // down projection K, zero-padded
   m->layers.resize(c.layers);
   for (int l = 0; l < c.layers; ++l) {
     const lopa_layer_weights& lw = w->layers[l];
@@ -200,7 +234,7 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     if ((rc = alloc16(&p.qkv, (size_t)m->tiles_qkv * (H / 64) * chunk)) ||
         (rc = alloc16(&p.o, (size_t)m->tiles_h * (H / 64) * chunk)) ||
         (rc = alloc16(&p.gu, (size_t)m->tiles_gu * (H / 64) * chunk)) ||
-        (rc = alloc16(&p.down, (size_t)m->tiles_h * (F / 64) * chunk)) ||
+        (rc = alloc16(&p.down, (size_t)m->tiles_h * (FP / 64) * chunk)) ||
         (rc = allocf(&p.ln1, H)) || (rc = allocf(&p.ln2, H)))
       return bail(rc);
     p.bias = nullptr;
@@ -209,14 +243,14 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     const uint16_t* wk = (const uint16_t*)lw.wk;
     const uint16_t* wv = (const uint16_t*)lw.wv;
     hipError_t e;
-    if ((e = launch_repack(wq, c.heads * d, wk, c.kv_heads * d, wv, c.kv_heads * d, H,
+    if ((e = launch_repack(wq, c.heads * d, wk, c.kv_heads * d, wv, c.kv_heads * d, H, H,
                            m->tiles_qkv, 0, p.qkv, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
-                           m->tiles_h, 0, p.o, s)) != hipSuccess ||
+                           c.heads * d, m->tiles_h, 0, p.o, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.w_gate, F, (const uint16_t*)lw.w_up, F, nullptr,
-                           0, H, m->tiles_gu, 1, p.gu, s)) != hipSuccess ||
-        (e = launch_repack((const uint16_t*)lw.w_down, H, nullptr, 0, nullptr, 0, F, m->tiles_h,
-                           0, p.down, s)) != hipSuccess ||
+                           0, H, H, m->tiles_gu, 1, p.gu, s)) != hipSuccess ||
+        (e = launch_repack((const uint16_t*)lw.w_down, H, nullptr, 0, nullptr, 0, F, FP,
+                           m->tiles_h, 0, p.down, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln1, p.ln1, H, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln2, p.ln2, H, s)) != hipSuccess)
       return bail(fail(LOPA_EHIP, "layer %d repack: %s", l, hipGetErrorString(e)));
@@ -235,8 +269,8 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     return bail(rc);
   hipError_t e;
   if ((e = hipMemcpyAsync(m->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s)) ||
-      (e = launch_repack((const uint16_t*)w->lm_head, V, nullptr, 0, nullptr, 0, H, m->tiles_lm,
-                         0, m->lm, s)) ||
+      (e = launch_repack((const uint16_t*)w->lm_head, V, nullptr, 0, nullptr, 0, H, H,
+                         m->tiles_lm, 0, m->lm, s)) ||
       (e = launch_bf16_to_f32((const uint16_t*)w->final_norm, m->final_norm, H, s)) ||
       (e = hipStreamSynchronize(s)))
     return bail(fail(LOPA_EHIP, "model create: %s", hipGetErrorString(e)));
@@ -263,7 +297,7 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   kv->max_len = max_len;
   kv->max_branches = max_branches;
   kv->max_block = max_block;
-  kv->mp_max = 64 * pow2_waves(max_branches * max_block);
+  kv->mp_max = padded_rows(max_branches * max_block);
   const int H = c.hidden, F = c.ffn, d = c.head_dim, Hkv = c.kv_heads;
   auto bail = [&](int code) {
     delete kv;
@@ -274,8 +308,7 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   const size_t cache_e = (size_t)c.layers * 2 * Hkv * max_len * d;
   const size_t stag_e = (size_t)max_branches * c.layers * 2 * Hkv * max_block * d;
   const int grid_max = m->num_cu;
-  const size_t part_b = (size_t)2 * grid_max * std::min(4, kv->mp_max / 64) * 32 * 64 * 16;
-  const int tiles_max = std::max(std::max(m->tiles_lm, m->tiles_gu), std::max(m->tiles_qkv, m->tiles_h));
+  const size_t part_b = (size_t)2 * grid_max * 4 * 32 * 64 * 16;
   const size_t rows = (size_t)kv->mp_max;
 #define KV_ALLOC(field, type, bytes)                  \
   if ((rc = dalloc(b, (bytes), kv->owned))) return bail(rc); \
@@ -285,10 +318,9 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   KV_ALLOC(rope, float*, (size_t)max_len * (d / 2) * 2 * 4);
   KV_ALLOC(x, float*, rows * H * 4);
   KV_ALLOC(abuf, uint16_t*, rows * H * 2);
-  KV_ALLOC(fbuf, uint16_t*, rows * F * 2);
+  KV_ALLOC(fbuf, uint16_t*, rows * round128(F) * 2);
   KV_ALLOC(qbuf, uint16_t*, (size_t)max_branches * c.heads * max_block * d * 2);
   KV_ALLOC(partials, float*, part_b);
-  KV_ALLOC(counters, int32_t*, (size_t)tiles_max * (kv->mp_max / 256 + 1) * 4);
   KV_ALLOC(pm, float*, rows * m->tiles_lm * 4);
   KV_ALLOC(ps, float*, rows * m->tiles_lm * 4);
   KV_ALLOC(pi, int32_t*, rows * m->tiles_lm * 4);
@@ -305,8 +337,8 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   hipError_t e;
   if ((e = hipMemcpy(kv->rope, tab.data(), tab.size() * 4, hipMemcpyHostToDevice)) ||
       (e = hipMemset(kv->cache, 0, cache_e * 2)) || (e = hipMemset(kv->staging, 0, stag_e * 2)) ||
-      (e = hipMemset(kv->abuf, 0, rows * H * 2)) || (e = hipMemset(kv->fbuf, 0, rows * F * 2)) ||
-      (e = hipMemset(kv->counters, 0, (size_t)tiles_max * (kv->mp_max / 256 + 1) * 4)) || (e = hipDeviceSynchronize()))
+      (e = hipMemset(kv->abuf, 0, rows * H * 2)) || (e = hipMemset(kv->fbuf, 0, rows * round128(F) * 2)) ||
+      (e = hipDeviceSynchronize()))
     return bail(fail(LOPA_EHIP, "kv create: %s", hipGetErrorString(e)));
   *out = kv;
   return LOPA_OK;
@@ -337,15 +369,14 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   const lopa_model_cfg& c = m->cfg;
   hipStream_t s = (hipStream_t)stream;
   const int M = n_branches * L;
-  const int Mp = 64 * pow2_waves(M);
+  const int Mp = padded_rows(M);
   const int H = c.hidden, F = c.ffn, d = c.head_dim;
-  const int KCh = H / 64, KCf = F / 64;
+  const int KCh = H / 64, KCf = round128(F) / 64;  // 64-column iterations per tile
 
   GemmArgs g{};
   g.M = M;
   g.Mp = Mp;
   g.partials = kv->partials;
-  g.counters = kv->counters;
   auto gemm = [&](int epi, const uint16_t* A, const uint16_t* W, int N, int KC, int tiles) {
     g.A = A;
     g.W = W;
@@ -354,13 +385,14 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.KC = KC;
     g.tiles = tiles;
     const int64_t I = (int64_t)tiles * KC;
-    g.mtiles = Mp > 256 ? Mp / 256 : 1;
+    g.mtiles = Mp / 256;
     g.grid = (int)std::min<int64_t>(m->num_cu / g.mtiles, I) * g.mtiles;
     return launch_gemm(epi, g, s);
   };
 
+  { ProfScope ps_(kv, LOPA_PROF_NORM, s);
   HIP_TRY(launch_embed_norm(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M, Mp, H, kv->x,
-                            kv->abuf, s));
+                            kv->abuf, s)); }
   AttnArgs at{};
   at.q = kv->qbuf;
   at.staging = kv->staging;
@@ -391,19 +423,26 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.L = L;
     g.Lcap = kv->max_block;
     g.P = prefix_len;
-    HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, KCh, m->tiles_qkv));
+    { ProfScope ps_(kv, LOPA_PROF_QKV, s);
+      HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, KCh, m->tiles_qkv)); }
     at.layer = l;
     at.kcache = kv->cache + ((size_t)l * 2 + 0) * c.kv_heads * kv->max_len * d;
     at.vcache = kv->cache + ((size_t)l * 2 + 1) * c.kv_heads * kv->max_len * d;
-    HIP_TRY(launch_attention(at, s));
+    { ProfScope ps_(kv, LOPA_PROF_ATTN, s);
+      HIP_TRY(launch_attention(at, s)); }
     g.x = kv->x;
-    HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, KCh, m->tiles_h));
-    HIP_TRY(launch_rmsnorm_pack(kv->x, p.ln2, c.rms_eps, M, Mp, H, kv->abuf, s));
+    { ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
+      HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, KCh, m->tiles_h)); }
+    { ProfScope ps_(kv, LOPA_PROF_NORM, s);
+      HIP_TRY(launch_rmsnorm_pack(kv->x, p.ln2, c.rms_eps, M, Mp, H, kv->abuf, s)); }
     g.a_out = kv->fbuf;
-    HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, KCh, m->tiles_gu));
-    HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, KCf, m->tiles_h));
+    { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
+      HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, KCh, m->tiles_gu)); }
+    { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
+      HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, KCf, m->tiles_h)); }
     const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
-    HIP_TRY(launch_rmsnorm_pack(kv->x, next_w, c.rms_eps, M, Mp, H, kv->abuf, s));
+    { ProfScope ps_(kv, LOPA_PROF_NORM, s);
+      HIP_TRY(launch_rmsnorm_pack(kv->x, next_w, c.rms_eps, M, Mp, H, kv->abuf, s)); }
   }
   if (stop_layer >= 0) {
     HIP_TRY(hipMemcpyAsync(x_out, kv->x, (size_t)M * H * 4, hipMemcpyDeviceToDevice, s));
@@ -414,8 +453,10 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   g.pi = kv->pi;
   g.vocab = c.vocab;
   g.mask_id = c.mask_id;
-  HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, m->tiles_lm * 128, KCh, m->tiles_lm));
-  HIP_TRY(launch_lm_merge(kv->pm, kv->ps, kv->pi, M, m->tiles_lm, conf, pred, s));
+  { ProfScope ps_(kv, LOPA_PROF_LMHEAD, s);
+    HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, m->tiles_lm * 128, KCh, m->tiles_lm)); }
+  { ProfScope ps_(kv, LOPA_PROF_MERGE, s);
+    HIP_TRY(launch_lm_merge(kv->pm, kv->ps, kv->pi, M, m->tiles_lm, conf, pred, s)); }
   kv->last_nb = n_branches;
   kv->last_L = L;
   kv->last_P = prefix_len;
@@ -534,6 +575,33 @@ int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer, void*
     uint16_t* dst = (uint16_t*)(kvi ? v_dst : k_dst);
     HIP_TRY(launch_kv_copy(src, dst, (int64_t)kv->max_block * d, (int64_t)L * d, Hkv, L * d,
                            (hipStream_t)stream));
+  }
+  return LOPA_OK;
+}
+
+int lopa_kv_profile(lopa_kv* kv, int32_t kinds_mask) {
+  if (!kv) return fail(LOPA_EINVAL, "null pointer argument");
+  if (kinds_mask < 0 || kinds_mask >= (1 << LOPA_PROF_KINDS)) return fail(LOPA_EINVAL, "bad mask");
+  kv->prof_mask = kinds_mask;
+  return LOPA_OK;
+}
+
+int lopa_kv_profile_read(lopa_kv* kv, double* total_ms, int64_t* launches) {
+  if (!kv || !total_ms || !launches) return fail(LOPA_EINVAL, "null pointer argument");
+  for (size_t i = 0; i < kv->ev_used; ++i) {
+    lopa_kv::Ev& e = kv->ev_pool[i];
+    HIP_TRY(hipEventSynchronize(e.b));
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, e.a, e.b));
+    kv->prof_ms[e.kind] += ms;
+    kv->prof_n[e.kind] += 1;
+  }
+  kv->ev_used = 0;
+  for (int k = 0; k < LOPA_PROF_KINDS; ++k) {
+    total_ms[k] = kv->prof_ms[k];
+    launches[k] = kv->prof_n[k];
+    kv->prof_ms[k] = 0.0;
+    kv->prof_n[k] = 0;
   }
   return LOPA_OK;
 }

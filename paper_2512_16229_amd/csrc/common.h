@@ -51,6 +51,15 @@ __device__ __forceinline__ int64_t packA_off(int r, int c, int Mp) {
   return ((int64_t)(kb * (Mp >> 4) + rb) * 64 + lane) * 8 + (c & 7);
 }
 
+// Workgroup barrier that orders LDS accesses only. __syncthreads() also orders
+// global memory, which makes the compiler drain every outstanding global load
+// (vmcnt(0)) at the barrier and so destroys any load pipelining across it.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ float wave_max(float v) {
   for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
   return v;

@@ -1,5 +1,5 @@
 // Weight-streaming bf16 GEMM for the skinny row counts of the verify step
-// (M = branches x block = 32 .. 512 rows) with fused epilogues:
+// (M = branches x block rows) with fused epilogues:
 //   EPI_QKV    bias + rotate-half RoPE on q/k, q -> attention input, k/v -> the
 //              branch K/V staging (the Pre-Write of Sec. 3.4)
 //   EPI_RESID  residual add into the fp32 residual stream (O-proj, down-proj)
@@ -7,13 +7,24 @@
 //   EPI_LMHEAD per (row, 128-token tile) softmax partials: max, argmax, sum exp
 //              (the logits never reach memory)
 //
-// Work decomposition: one workgroup covers all Mp rows (Mp/64 wavefronts, each
-// 64 rows x 128 columns of a tile) so every weight byte is read from HBM once.
-// The (tile, k-chunk) iteration space is split evenly over `grid` workgroups
-// (stream-K), so all CUs stream weights even when N has few tiles. A tile split
-// over several workgroups is finished by the last one to arrive (atomic
-// counter): it sums the partial tiles in workgroup order, so the result does
-// not depend on arrival order, and then runs the epilogue.
+// Work decomposition. A workgroup (4 wavefronts) covers one 256-row tile of the
+// activations (each wavefront 64 rows x 128 output columns), so every weight
+// byte is read from HBM once per row tile. The (column tile, 64-wide k-chunk)
+// iteration space is split evenly over the column workgroups (stream-K): every
+// CU streams the same number of weight bytes whatever the tile count. A tile
+// covered by one workgroup runs its epilogue in place; a tile split over
+// several writes per-workgroup partial sums, which gemm_fixup_kernel adds in
+// workgroup order (deterministic) after the kernel boundary and then runs the
+// epilogue. No workgroup waits for another. The QKV epilogue (bias, RoPE,
+// scatter to q / K / V staging) always runs in the fix-up kernel, which keeps
+// its register-heavy code out of the streaming loop.
+//
+// Pipeline. Weights (16 KiB per 64-wide k-chunk, through LDS) are loaded about
+// two iterations ahead into alternating register sets; activations (8
+// fragments per wavefront, straight to registers, L2-resident) one iteration
+// ahead, in halves as their registers free up. Loads are issued so that a wait on an
+// activation load never covers a younger weight load (the vmcnt queue is in
+// order).
 #include "common.h"
 #include "kernels.h"
 
@@ -21,26 +32,9 @@
 
 namespace {
 
-__device__ __forceinline__ int64_t sk_start(int g, int64_t I, int G) { return (int64_t)g * I / G; }
-
-// workgroup whose range contains iteration j
-__device__ __forceinline__ int sk_owner(int64_t j, int64_t I, int G) {
-  int g = (int)((j * G) / I);
-  while (g + 1 < G && sk_start(g + 1, I, G) <= j) ++g;
-  while (g > 0 && sk_start(g, I, G) > j) --g;
-  return g;
-}
-
-template <int WAVES>
-struct Smem {
-  u32x4 w[2][1024];                 // two 16 KiB weight chunks
-  uint16_t e[WAVES][64 * 72];       // per-wave epilogue staging (64 rows x 64 cols + pad)
-  int flag;
-};
-
 template <int D>
 __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, f32x4 (&acc)[4][8], int tile,
-                                             int row0, int lane) {
+                                             int row0, int lane, unsigned nbmask) {
   constexpr int HD = D / 2, HALF_NB = HD / 16;  // RoPE partner offset in 16-column blocks
   const int g = lane >> 4, c16 = lane & 15;
   const int qcols = a.Hq * D, kcols = a.Hkv * D;
@@ -60,6 +54,7 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, f32x4 (&acc)[4][
       const float* cs_row = a.rope + (int64_t)(a.P + i) * HD * 2;
 #pragma unroll
       for (int nb = 0; nb < 8; ++nb) {
+        if (!((nbmask >> nb) & 1)) continue;
         const bool low = (nb % (D / 16)) < HALF_NB;
         if (sect < 2 && !low) continue;  // written together with its partner
         const int nl = n0 - base + nb * 16 + c16;
@@ -88,9 +83,9 @@ __device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, f32x4 (&acc)[4][
     }
 }
 
-template <int EPI, int WAVES>
+template <int EPI>
 __device__ __forceinline__ void epilogue(const GemmArgs& a, f32x4 (&acc)[4][8], int tile, int row0,
-                                         int wv, int lane, Smem<WAVES>& sm) {
+                                         int lane, uint16_t* stage, unsigned nbmask = 0xffu) {
   const int g = lane >> 4, c16 = lane & 15;
   if constexpr (EPI == EPI_RESID) {
     #pragma unroll
@@ -101,18 +96,20 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, f32x4 (&acc)[4][8], 
         if (r >= a.M) continue;
         float* xr = a.x + (int64_t)r * a.N + tile * LOPA_BN + c16;
         #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) xr[nb * 16] += acc[mb][nb][j];
+        for (int nb = 0; nb < 8; ++nb)
+          if ((nbmask >> nb) & 1) xr[nb * 16] += acc[mb][nb][j];
       }
   } else if constexpr (EPI == EPI_SWIGLU) {
     // gate in columns 0..63, up in 64..127 of the tile; output columns
     // [64 tile, 64 tile + 64). Stage through LDS so each lane writes 16 bytes.
-    uint16_t* e = sm.e[wv];
+    uint16_t* e = stage;  // this wavefront's 64 x 72 staging tile
     #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
       #pragma unroll
       for (int nb = 0; nb < 4; ++nb)
         #pragma unroll
         for (int j = 0; j < 4; ++j) {
+          if (!((nbmask >> nb) & 1)) continue;
           const float gt = acc[mb][nb][j], up = acc[mb][nb + 4][j];
           const float h = gt / (1.0f + expf(-gt)) * up;
           e[(mb * 16 + g * 4 + j) * 72 + nb * 16 + c16] = f2bf_bits(h);
@@ -124,7 +121,7 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, f32x4 (&acc)[4][8], 
     for (int q = lane; q < 64 * 8; q += 64) {
       const int rr = q >> 3, cg = q & 7;
       const int r = row0 + rr;
-      if (r >= a.M) continue;
+      if (r >= a.M || !((nbmask >> (cg >> 1)) & 1)) continue;
       const uint4 v = *(const uint4*)(e + rr * 72 + cg * 8);
       *(uint4*)(a.a_out + packA_off(r, tile * 64 + cg * 8, a.Mp)) = v;
     }
@@ -164,149 +161,191 @@ __device__ __forceinline__ void epilogue(const GemmArgs& a, f32x4 (&acc)[4][8], 
         }
       }
   } else {  // EPI_QKV
-    if (a.d == 128) qkv_epilogue<128>(a, acc, tile, row0, lane);
-    else qkv_epilogue<64>(a, acc, tile, row0, lane);
+    if (a.d == 128) qkv_epilogue<128>(a, acc, tile, row0, lane, nbmask);
+    else qkv_epilogue<64>(a, acc, tile, row0, lane, nbmask);
   }
 }
 
-// weights of iteration itx -> registers (this thread's share of the 16 KiB chunk)
-#define GEMM_LOAD_W(dst, itx)                                                \
-  _Pragma("unroll") for (int r_ = 0; r_ < NL; ++r_)                          \
-    dst[r_] = W[(int64_t)(itx) * 1024 + r_ * NT + tid];
-// this wavefront's 8 activation fragments of k-chunk kcx -> registers
-#define GEMM_LOAD_A(dst, kcx)                                                \
-  _Pragma("unroll") for (int kk_ = 0; kk_ < 2; ++kk_)                        \
-    _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                      \
-      dst[kk_ * 4 + mb_] = A[((int64_t)((2 * (kcx) + kk_) * RB + rb0 + mb_)) * 64 + lane];
-#define GEMM_STORE_W(buf, src)                                               \
-  _Pragma("unroll") for (int r_ = 0; r_ < NL; ++r_) sm.w[buf][r_ * NT + tid] = src[r_];
-#define GEMM_COMPUTE(buf, ar)                                                \
-  _Pragma("unroll") for (int kk_ = 0; kk_ < 2; ++kk_)                        \
-    _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) {                    \
-      const u32x4 bf_ = sm.w[buf][(kk_ * 8 + nb_) * 64 + lane];              \
-      _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                    \
-        acc[mb_][nb_] = mfma16(ar[kk_ * 4 + mb_], bf_, acc[mb_][nb_]);       \
-    }
+__device__ __forceinline__ int64_t sk_start(int g, int64_t I, int G) { return (int64_t)g * I / G; }
 
-// Grid: a.grid workgroups = a.mtiles row tiles (of 256 rows) x G column
-// workgroups. The row tiles of one column workgroup sit on the same XCD and
-// stream the same weight chunks at the same time, so the second read hits L2.
-template <int EPI, int WAVES>
-__global__ __launch_bounds__(WAVES * 64, 1) void gemm_kernel(GemmArgs a) {
-  constexpr int NT = WAVES * 64;
-  constexpr int NL = 1024 / NT;  // 16-byte weight loads per thread per chunk
-  __shared__ __attribute__((aligned(16))) Smem<WAVES> sm;
+// workgroup whose range contains iteration j
+__device__ __forceinline__ int sk_owner(int64_t j, int64_t I, int G) {
+  int g = (int)((j * G) / I);
+  while (g + 1 < G && sk_start(g + 1, I, G) <= j) ++g;
+  while (g > 0 && sk_start(g, I, G) > j) --g;
+  return g;
+}
+
+// partial-sum slot of contributor gc of a tile that starts at iteration t0
+__device__ __forceinline__ int sk_slot(int gc, int g_lo, int64_t t0, int64_t I, int G) {
+  return (gc == g_lo && sk_start(gc, I, G) < t0) ? 2 * gc + 1 : 2 * gc;
+}
+
+constexpr int GEMM_THREADS = 256;
+constexpr int NLW = 1024 / GEMM_THREADS;  // 16-byte weight loads per thread per iteration
+
+#define GEMM_LOAD_W(dst, itx)                                                      \
+  _Pragma("unroll") for (int r_ = 0; r_ < NLW; ++r_)                               \
+    dst[r_] = W[(int64_t)(itx) * 1024 + r_ * GEMM_THREADS + tid];
+// activation fragments of k-group kk of chunk kcx -> registers
+#define GEMM_LOAD_A1(dst, kcx, kk)                                                 \
+  _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                              \
+    dst[(kk) * 4 + mb_] = A[((int64_t)((2 * (kcx) + (kk)) * RB + rb0 + mb_)) * 64 + lane];
+#define GEMM_STORE_W(buf, src)                                                     \
+  _Pragma("unroll") for (int r_ = 0; r_ < NLW; ++r_) sW[buf][r_ * GEMM_THREADS + tid] = src[r_];
+#define GEMM_COMPUTE1(buf, ar, kk)                                                 \
+  _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) {                            \
+    const u32x4 bf_ = sW[buf][((kk) * 8 + nb_) * 64 + lane];                       \
+    _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                            \
+      acc[mb_][nb_] = mfma16(ar[(kk) * 4 + mb_], bf_, acc[mb_][nb_]);              \
+  }
+#define GEMM_ZERO_ACC()                                                            \
+  _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                              \
+    _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) acc[mb_][nb_] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+// One iteration with weight register set / LDS buffer B. Load order matters:
+// the activations of the next iteration are fetched in two halves, each as
+// soon as its registers are consumed, and the weights two iterations ahead go
+// last, so waiting for an activation load never waits for a younger weight load.
+#define GEMM_STEP(B, wr)                                                           \
+  {                                                                                \
+    GEMM_STORE_W(B, wr);                                                           \
+    lds_barrier();                                                                 \
+    const bool more1_ = it + 1 < it1, more2_ = it + 2 < it1;                       \
+    const int kn_ = (int)((it + 1) % KC);                                          \
+    GEMM_COMPUTE1(B, ar, 0);                                                       \
+    if (more1_) { GEMM_LOAD_A1(ar, kn_, 0); }                                      \
+    GEMM_COMPUTE1(B, ar, 1);                                                       \
+    if (more1_) { GEMM_LOAD_A1(ar, kn_, 1); }                                      \
+    if (more2_) { GEMM_LOAD_W(wr, it + 2); }                                       \
+  }
+
+template <int EPI>
+__global__ __launch_bounds__(GEMM_THREADS, 1) void gemm_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) u32x4 sW[2][1024];  // two 16 KiB weight chunks
+  __shared__ __attribute__((aligned(16))) uint16_t sE[4][EPI == EPI_SWIGLU ? 64 * 72 : 8];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int MT = a.mtiles;
   const int G = a.grid / MT;
-  // Hardware places workgroup b on XCD b % 8. Logical index q = (xcd, slot):
-  // each XCD gets a contiguous piece of the iteration range.
+  // Hardware places workgroup b on XCD b % 8; each XCD gets a contiguous piece
+  // of the logical index q, so neighbouring iteration ranges share an L2 and
+  // the row tiles of one column workgroup stream the same weights together.
   const int b = blockIdx.x;
   const int q = (a.grid % 8 == 0) ? (b & 7) * (a.grid >> 3) + (b >> 3) : b;
   const int mt = q % MT, g = q / MT;
   const int KC = a.KC;
   const int64_t I = (int64_t)a.tiles * KC;
   const int64_t it0 = sk_start(g, I, G), it1 = sk_start(g + 1, I, G);
+  if (it0 >= it1) return;
   const int RB = a.Mp >> 4;
-  const int rb0 = mt * 16 + wv * 4;      // first 16-row block of this wavefront
-  const int row0 = mt * 256 + wv * 64;   // first row of this wavefront
+  const int rb0 = mt * 16 + wv * 4;     // first 16-row block of this wavefront
+  const int row0 = mt * 256 + wv * 64;  // first row of this wavefront
   const u32x4* __restrict__ W = (const u32x4*)a.W;
   const u32x4* __restrict__ A = (const u32x4*)a.A;
 
+  f32x4 acc[4][8];
+  GEMM_ZERO_ACC();
+  u32x4 w0[NLW], w1[NLW], ar[8];
+  GEMM_LOAD_A1(ar, (int)(it0 % KC), 0);
+  GEMM_LOAD_A1(ar, (int)(it0 % KC), 1);
+  GEMM_LOAD_W(w0, it0);
+  if (it0 + 1 < it1) { GEMM_LOAD_W(w1, it0 + 1); }
+  // Segments: the iterations of one column tile inside [it0, it1). The weight
+  // register set / LDS buffer alternates with the global iteration parity, so
+  // each segment runs one of two loops depending on the parity it starts at.
   int64_t it = it0;
-  bool first_seg = true;
   while (it < it1) {
+    const int64_t seg0 = it;
     const int tile = (int)(it / KC);
-    const int kc0 = (int)(it % KC);
-    const int64_t tile_end = (int64_t)(tile + 1) * KC;
-    const int nk = (int)((it1 < tile_end ? it1 : tile_end) - it);
-
-    f32x4 acc[4][8];
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-      for (int nb = 0; nb < 8; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // weights run two chunks ahead (w0 / w1), activations one chunk ahead
-    u32x4 w0[NL], w1[NL], a0[8], a1[8];
-    GEMM_LOAD_W(w0, it);
-    if (nk > 1) { GEMM_LOAD_W(w1, it + 1); }
-    GEMM_LOAD_A(a0, kc0);
-    for (int s = 0;;) {
-      GEMM_STORE_W(0, w0);
-      __syncthreads();
-      if (s + 2 < nk) { GEMM_LOAD_W(w0, it + s + 2); }
-      if (s + 1 < nk) { GEMM_LOAD_A(a1, kc0 + s + 1); }
-      GEMM_COMPUTE(0, a0);
-      if (++s >= nk) break;
-      GEMM_STORE_W(1, w1);
-      __syncthreads();
-      if (s + 2 < nk) { GEMM_LOAD_W(w1, it + s + 2); }
-      if (s + 1 < nk) { GEMM_LOAD_A(a0, kc0 + s + 1); }
-      GEMM_COMPUTE(1, a1);
-      if (++s >= nk) break;
-    }
-
-    const bool whole = (kc0 == 0) && (nk == KC);
-    if (whole) {
-      epilogue<EPI, WAVES>(a, acc, tile, row0, wv, lane, sm);
+    const int64_t seg1 = (it1 < (int64_t)(tile + 1) * KC) ? it1 : (int64_t)(tile + 1) * KC;
+    GEMM_ZERO_ACC();
+    if (((it - it0) & 1) == 0) {
+      for (;;) {
+        GEMM_STEP(0, w0);
+        if (++it >= seg1) break;
+        GEMM_STEP(1, w1);
+        if (++it >= seg1) break;
+      }
     } else {
-      // partial tile: publish, and let the last contributor finish it
-      const int slot = (2 * g + (first_seg ? 0 : 1)) * MT + mt;
-      f32x4* part = (f32x4*)a.partials + ((int64_t)slot * WAVES + wv) * 32 * 64;
+      for (;;) {
+        GEMM_STEP(1, w1);
+        if (++it >= seg1) break;
+        GEMM_STEP(0, w0);
+        if (++it >= seg1) break;
+      }
+    }
+    if (EPI != EPI_QKV && seg0 % KC == 0 && seg1 % KC == 0) {
+      epilogue<EPI>(a, acc, tile, row0, lane, sE[wv]);
+    } else {
+      const int slot = (2 * g + (seg0 == it0 ? 0 : 1)) * MT + mt;
+      f32x4* part = (f32x4*)a.partials + ((int64_t)slot * 4 + wv) * 32 * 64;
 #pragma unroll
       for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
         for (int nb = 0; nb < 8; ++nb) part[(mb * 8 + nb) * 64 + lane] = acc[mb][nb];
-      const int g_lo = sk_owner((int64_t)tile * KC, I, G);
-      const int g_hi = sk_owner(tile_end - 1, I, G);
-      const int ncontrib = g_hi - g_lo + 1;
-      __threadfence();
-      __syncthreads();
-      if (tid == 0) {
-        const int old = atomicAdd(&a.counters[tile * MT + mt], 1);
-        sm.flag = (old == ncontrib - 1);
-      }
-      __syncthreads();
-      if (sm.flag) {
-        __threadfence();
-        // sum the contributors in workgroup order, one 16-row block at a time
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-          f32x4 t[8];
-#pragma unroll
-          for (int nb = 0; nb < 8; ++nb) t[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-          for (int gc = g_lo; gc <= g_hi; ++gc) {
-            const int sl =
-                (gc == g_lo && sk_start(gc, I, G) < (int64_t)tile * KC) ? 2 * gc + 1 : 2 * gc;
-            const f32x4* p =
-                (const f32x4*)a.partials + ((int64_t)(sl * MT + mt) * WAVES + wv) * 32 * 64;
-#pragma unroll
-            for (int nb = 0; nb < 8; ++nb) t[nb] += p[(mb * 8 + nb) * 64 + lane];
-          }
-#pragma unroll
-          for (int nb = 0; nb < 8; ++nb) acc[mb][nb] = t[nb];
-        }
-        epilogue<EPI, WAVES>(a, acc, tile, row0, wv, lane, sm);
-        if (tid == 0) atomicExch(&a.counters[tile * MT + mt], 0);
-      }
     }
-    __syncthreads();
-    it += nk;
-    first_seg = false;
   }
+}
+
+// Sum the partial tiles of split tiles in workgroup order and run the epilogue.
+// One wavefront per (column tile, row tile, 64-row block, column group): the
+// groups pair the 16-column blocks an epilogue couples (RoPE halves, gate/up),
+// nb and nb + PAIR; the LM-head epilogue reduces over all 8 blocks of a row,
+// so it takes one group. Whole tiles (done in gemm_kernel) return at once.
+template <int EPI>
+__global__ __launch_bounds__(64) void gemm_fixup_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t sE[EPI == EPI_SWIGLU ? 64 * 72 : 8];
+  constexpr int GROUPS = EPI == EPI_LMHEAD ? 1 : 4;
+  const int MT = a.mtiles;
+  const int G = a.grid / MT;
+  int bid = blockIdx.x;
+  const int cg = bid % GROUPS;
+  bid /= GROUPS;
+  const int w = bid % 4;
+  bid /= 4;
+  const int mt = bid % MT, tile = bid / MT;
+  const int KC = a.KC;
+  const int64_t I = (int64_t)a.tiles * KC;
+  const int64_t t0 = (int64_t)tile * KC;
+  const int g_lo = sk_owner(t0, I, G), g_hi = sk_owner(t0 + KC - 1, I, G);
+  if (g_lo == g_hi && EPI != EPI_QKV) return;
+  const int lane = threadIdx.x;
+  const int row0 = mt * 256 + w * 64;
+  const int pair = (EPI == EPI_QKV && a.d == 64) ? 2 : 4;
+  const int nb_a = (cg % pair) + (cg / pair) * 2 * pair;
+  const unsigned mask = GROUPS == 1 ? 0xffu : ((1u << nb_a) | (1u << (nb_a + pair)));
+  f32x4 acc[4][8];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int gc = g_lo; gc <= g_hi; ++gc) {
+    const int slot = sk_slot(gc, g_lo, t0, I, G) * MT + mt;
+    const f32x4* p = (const f32x4*)a.partials + ((int64_t)slot * 4 + w) * 32 * 64;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 8; ++nb)
+        if ((mask >> nb) & 1) acc[mb][nb] += p[(mb * 8 + nb) * 64 + lane];
+  }
+  epilogue<EPI>(a, acc, tile, row0, lane, sE, mask);
 }
 
 template <int EPI>
 hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  const int waves = a.Mp >= 256 ? 4 : a.Mp / 64;
-  switch (waves) {
-    case 1: hipLaunchKernelGGL((gemm_kernel<EPI, 1>), dim3(a.grid), dim3(64), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((gemm_kernel<EPI, 2>), dim3(a.grid), dim3(128), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((gemm_kernel<EPI, 4>), dim3(a.grid), dim3(256), 0, s, a); break;
-    default: return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gemm_kernel<EPI>, dim3(a.grid), dim3(GEMM_THREADS), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // split tiles exist unless every column workgroup owns whole tiles
+  const int G = a.grid / a.mtiles;
+  if (EPI == EPI_QKV || (int64_t)a.tiles * a.KC % G != 0 ||
+      ((int64_t)a.tiles * a.KC / G) % a.KC != 0) {
+    const int groups = EPI == EPI_LMHEAD ? 1 : 4;
+    hipLaunchKernelGGL(gemm_fixup_kernel<EPI>, dim3(a.tiles * a.mtiles * 4 * groups), dim3(64), 0,
+                       s, a);
+    e = hipGetLastError();
   }
-  return hipGetLastError();
+  return e;
 }
 
 }  // namespace

@@ -23,8 +23,9 @@ hipError_t launch_kv_copy(const uint16_t* src, uint16_t* dst, int64_t src_stride
 // tile-major fragment layout; N_pad = tiles * 128 rows, rows past the sources
 // are zero. interleave64: tile t takes rows [64t, 64t+64) of source 0 then the
 // same rows of source 1 (gate / up pairing for the SwiGLU epilogue).
+// K: source row length; KP (a multiple of 128, >= K): packed width, zero-filled.
 hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
-                         const uint16_t* s2, int r2, int K, int tiles, int interleave64,
+                         const uint16_t* s2, int r2, int K, int KP, int tiles, int interleave64,
                          uint16_t* dst, hipStream_t s);
 hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_t s);
 
@@ -45,12 +46,11 @@ enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
 struct GemmArgs {
   const uint16_t* A;   // packed activations, Mp rows, K columns
-  const uint16_t* W;   // packed weights, tiles x KC chunks
-  int M, Mp, N, K, KC, tiles;
-  int mtiles;          // row tiles of 256 rows (Mp <= 256 -> 1)
+  const uint16_t* W;   // packed weights, tiles x (K/64) chunks of 64 columns
+  int M, Mp, N, K, KC, tiles;  // K % 64 == 0; KC = K / 64 iterations per tile
+  int mtiles;          // row tiles of 256 rows; Mp = 256 * mtiles
   int grid;            // workgroups = mtiles x column workgroups (stream-K)
   float* partials;     // [2*grid][4 waves][32][64][4] fp32
-  int32_t* counters;   // [tiles * mtiles], zero between launches
   // EPI_QKV
   const float* bias;   // [N] or null
   const float* rope;   // [max_pos][d/2][2] (cos, sin)

@@ -113,6 +113,7 @@ __global__ __launch_bounds__(256) void repack_kernel(const uint16_t* __restrict_
                                                      const uint16_t* __restrict__ s2, int r2,
                                                      int K, int KC, int64_t total,
                                                      int interleave64, uint16_t* __restrict__ dst) {
+  // K: length of a source row; KC * 64 >= K: packed columns, the excess is zero
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= total) return;
   const int lane = (int)(gid & 63);
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(256) void repack_kernel(const uint16_t* __restrict_
     else if (n < r0 + r1 + r2) { src = s2; row = n - r0 - r1; }
   }
   uint4 v = make_uint4(0, 0, 0, 0);
-  if (src) v = *(const uint4*)(src + (int64_t)row * K + k0);
+  if (src && k0 < K) v = *(const uint4*)(src + (int64_t)row * K + k0);
   *(uint4*)(dst + gid * 8) = v;
 }
 
@@ -168,9 +169,9 @@ hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, 
 }
 
 hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
-                         const uint16_t* s2, int r2, int K, int tiles, int interleave64,
+                         const uint16_t* s2, int r2, int K, int KP, int tiles, int interleave64,
                          uint16_t* dst, hipStream_t s) {
-  const int KC = K / LOPA_BK;
+  const int KC = KP / LOPA_BK;
   const int64_t total = (int64_t)tiles * KC * 16 * 64;
   const int64_t blocks = (total + 255) / 256;
   hipLaunchKernelGGL(repack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, s0, r0, s1, r1, s2,

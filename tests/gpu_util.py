@@ -16,11 +16,21 @@ CONF_TOL = 2e-2     # abs tolerance of confidences and branch scores (bf16 path 
 FAITHFUL_TOL = 2e-2
 
 
+def faithful_bound(bf16_own_error: float) -> float:
+    """Bound on |GPU - bf16-faithful oracle| for confidences.
+
+    Both are bf16 computations with the same rounding points that round in a
+    different order (fp32 vs fp64 sums; a running vs a global softmax maximum),
+    so each sits at about the bf16 distance e from the exact float64 result,
+    e = |faithful - float64| measured on the case itself (no GPU involved).
+    Bound: 2e, and never below the benchmark spec's 2e-2."""
+    return max(CONF_TOL, 2.0 * bf16_own_error)
+
+
 def conf_tolerance(bf16_own_error: float) -> float:
-    """Bound on |GPU - float64 oracle| for confidences: 2e-2, or, where bf16
-    arithmetic alone (bf16-faithful oracle vs float64 oracle, no GPU involved)
-    already exceeds it, 1.25 times that distance."""
-    return max(CONF_TOL, 1.25 * bf16_own_error)
+    """Bound on |GPU - float64 oracle| (the bf16 result vs the exact one): 2e-2,
+    or twice the faithful oracle's own bf16 distance where that is larger."""
+    return max(CONF_TOL, 2.0 * bf16_own_error)
 
 
 def near_tie(eps: float) -> float:

@@ -10,7 +10,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import (FAITHFUL_TOL, Setup, build_margin, conf_tolerance, f32, log, near_tie,
+from gpu_util import (FAITHFUL_TOL, Setup, build_margin, conf_tolerance, f32, faithful_bound, log,
+                      near_tie,
                       score_margin, vocab_margin)
 from oracle import lopa
 
@@ -57,7 +58,7 @@ def test_teacher_forced_iterations(cfgname, P, L, k, tau):
         gp = pred_b.view(nb, L).cpu().numpy()
         eps = np.max(np.abs(gc - out_f["conf"]))
         e_bf16 = np.max(np.abs(out_f["conf"] - out_p["conf"]))
-        assert eps < conf_tolerance(e_bf16)
+        assert eps < faithful_bound(e_bf16)
         assert np.max(np.abs(gc - out_p["conf"])) < conf_tolerance(e_bf16)
         dec = vocab_margin(out_f["logits"], mask) >= near_tie(eps)
         assert np.array_equal(gp[dec], out_f["pred"][dec])
@@ -74,7 +75,7 @@ def test_teacher_forced_iterations(cfgname, P, L, k, tau):
         gs = scores.cpu().numpy().astype(np.float64)
         fin = np.isfinite(rs)
         s_eps = np.max(np.abs(gs[fin] - rs[fin]), initial=0)
-        assert s_eps < conf_tolerance(e_bf16)
+        assert s_eps < faithful_bound(e_bf16)
         w = int(win.item())
         if score_margin(rs) >= near_tie(s_eps):
             assert np.array_equal(rbt[w], rbt[rw])

@@ -8,7 +8,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import Setup, conf_tolerance, log, near_tie, vocab_margin
+from gpu_util import Setup, conf_tolerance, faithful_bound, log, near_tie, vocab_margin
 
 pytestmark = pytest.mark.gpu
 
@@ -56,7 +56,7 @@ def test_verify_forward_parity(cfgname, P, L, k):
     decided = marg >= near_tie(e_faith)
     log(f"  max|dconf| gpu-pure={e_pure:.2e} gpu-faithful={e_faith:.2e} faithful-pure={e_bf16:.2e} "
         f"near-ties={int((~decided).sum())}/{decided.size}")
-    assert e_faith < conf_tolerance(e_bf16)
+    assert e_faith < faithful_bound(e_bf16)
     assert decided.mean() > 0.8
     assert np.array_equal(pred[decided], rf["pred"][decided]), \
         f"{int((pred[decided] != rf['pred'][decided]).sum())} decided tokens differ"
