@@ -19,12 +19,11 @@
 // scatter to q / K / V staging) always runs in the fix-up kernel, which keeps
 // its register-heavy code out of the streaming loop.
 //
-// Pipeline. Weights (16 KiB per 64-wide k-chunk, through LDS) are loaded about
-// two iterations ahead into alternating register sets; activations (8
-// fragments per wavefront, straight to registers, L2-resident) one iteration
-// ahead, in halves as their registers free up. Loads are issued so that a wait on an
-// activation load never covers a younger weight load (the vmcnt queue is in
-// order).
+// Pipeline. Per iteration (a 64-wide k-chunk) the 16 KiB weight chunk goes
+// straight from global memory into a 4-slot LDS ring (LDS-DMA, no registers)
+// and each wavefront's 8 activation fragments (L2-resident) into one of three
+// register sets, both three iterations ahead (the in-order vmcnt queue makes
+// equal lead distances the only way not to wait on younger loads).
 #include "common.h"
 #include "kernels.h"
 
@@ -182,49 +181,76 @@ __device__ __forceinline__ int sk_slot(int gc, int g_lo, int64_t t0, int64_t I, 
 }
 
 constexpr int GEMM_THREADS = 256;
-constexpr int NLW = 1024 / GEMM_THREADS;  // 16-byte weight loads per thread per iteration
+constexpr int W_SLOTS = 4;  // LDS ring of 16 KiB weight chunks (three in flight)
 
-#define GEMM_LOAD_W(dst, itx)                                                      \
-  _Pragma("unroll") for (int r_ = 0; r_ < NLW; ++r_)                               \
-    dst[r_] = W[(int64_t)(itx) * 1024 + r_ * GEMM_THREADS + tid];
-// activation fragments of k-group kk of chunk kcx -> registers
-#define GEMM_LOAD_A1(dst, kcx, kk)                                                 \
-  _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                              \
-    dst[(kk) * 4 + mb_] = A[((int64_t)((2 * (kcx) + (kk)) * RB + rb0 + mb_)) * 64 + lane];
-#define GEMM_STORE_W(buf, src)                                                     \
-  _Pragma("unroll") for (int r_ = 0; r_ < NLW; ++r_) sW[buf][r_ * GEMM_THREADS + tid] = src[r_];
-#define GEMM_COMPUTE1(buf, ar, kk)                                                 \
-  _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) {                            \
-    const u32x4 bf_ = sW[buf][((kk) * 8 + nb_) * 64 + lane];                       \
-    _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                            \
-      acc[mb_][nb_] = mfma16(ar[(kk) * 4 + mb_], bf_, acc[mb_][nb_]);              \
+// Asynchronous global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane l writes bytes [16 l, 16 l + 16) of the 1 KiB LDS block at lds_addr
+// (wave-uniform, passed in M0). The compiler does not track it: completion is
+// awaited with an explicit vmcnt wait before the workgroup barrier.
+__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_addr), "v"(gptr)
+               : "memory");
+}
+
+// weight chunk of iteration itx -> ring slot (4 x 1 KiB blocks per wavefront)
+#define GEMM_DMA_W(itx)                                                                  \
+  {                                                                                      \
+    const uint32_t slot_ = sW_base + (uint32_t)(((itx) % W_SLOTS) * 16384);              \
+    const char* src_ = (const char*)a.W + (int64_t)(itx) * 16384 + lane * 16;            \
+    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                   \
+      const int blk_ = r_ * 4 + wv;                                                      \
+      lds_dma16(src_ + blk_ * 1024, slot_ + blk_ * 1024);                                \
+    }                                                                                    \
   }
-#define GEMM_ZERO_ACC()                                                            \
-  _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                              \
+// this wavefront's 8 activation fragments of 64-wide chunk kcx -> registers
+#define GEMM_LOAD_A(dst, kcx)                                                            \
+  _Pragma("unroll") for (int kk_ = 0; kk_ < 2; ++kk_)                                    \
+    _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                                  \
+      dst[kk_ * 4 + mb_] = A[((int64_t)((2 * (kcx) + kk_) * RB + rb0 + mb_)) * 64 + lane];
+#define GEMM_ZERO_ACC()                                                                  \
+  _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                                    \
     _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) acc[mb_][nb_] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-// One iteration with weight register set / LDS buffer B. Load order matters:
-// the activations of the next iteration are fetched in two halves, each as
-// soon as its registers are consumed, and the weights two iterations ahead go
-// last, so waiting for an activation load never waits for a younger weight load.
-#define GEMM_STEP(B, wr)                                                           \
-  {                                                                                \
-    GEMM_STORE_W(B, wr);                                                           \
-    lds_barrier();                                                                 \
-    const bool more1_ = it + 1 < it1, more2_ = it + 2 < it1;                       \
-    const int kn_ = (int)((it + 1) % KC);                                          \
-    GEMM_COMPUTE1(B, ar, 0);                                                       \
-    if (more1_) { GEMM_LOAD_A1(ar, kn_, 0); }                                      \
-    GEMM_COMPUTE1(B, ar, 1);                                                       \
-    if (more1_) { GEMM_LOAD_A1(ar, kn_, 1); }                                      \
-    if (more2_) { GEMM_LOAD_W(wr, it + 2); }                                       \
+// One iteration it. Every iteration j issues, in this order, the 8 activation
+// loads then the 4 weight copies of iteration j + 3 (the prologue issues those
+// of it0 .. it0 + 2 the same way). When iteration it starts, what was issued
+// after the weight copies of `it` is iterations it + 1 and it + 2: 24
+// operations (fewer near the end of the range), so vmcnt(24) means both the
+// weights and the activations of `it` have arrived.
+#define GEMM_STEP(ar)                                                                    \
+  {                                                                                      \
+    if (it + 2 < it1) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");                  \
+    else if (it + 1 < it1) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");             \
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");                                \
+    lds_barrier();                                                                       \
+    const u32x4* wl_ = sW + (int)(it % W_SLOTS) * 1024;                                  \
+    _Pragma("unroll") for (int kk_ = 0; kk_ < 2; ++kk_)                                  \
+      _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) {                              \
+        const u32x4 bf_ = wl_[(kk_ * 8 + nb_) * 64 + lane];                              \
+        _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                              \
+          acc[mb_][nb_] = mfma16(ar[kk_ * 4 + mb_], bf_, acc[mb_][nb_]);                 \
+      }                                                                                  \
+    if (it + 3 < it1) {                                                                  \
+      GEMM_LOAD_A(ar, (int)((it + 3) % KC));                                             \
+      GEMM_DMA_W(it + 3);                                                                \
+    }                                                                                    \
+  }
+
+#define GEMM_ROTATE()                                                                    \
+  _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) {                                     \
+    const u32x4 t_ = a0[i_];                                                             \
+    a0[i_] = a1[i_];                                                                     \
+    a1[i_] = a2[i_];                                                                     \
+    a2[i_] = t_;                                                                         \
   }
 
 template <int EPI>
 __global__ __launch_bounds__(GEMM_THREADS, 1) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) u32x4 sW[2][1024];  // two 16 KiB weight chunks
+  __shared__ __attribute__((aligned(16))) u32x4 sW[W_SLOTS * 1024];  // ring of 16 KiB chunks
   __shared__ __attribute__((aligned(16))) uint16_t sE[4][EPI == EPI_SWIGLU ? 64 * 72 : 8];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t sW_base = (uint32_t)(uintptr_t)sW;
   const int MT = a.mtiles;
   const int G = a.grid / MT;
   // Hardware places workgroup b on XCD b % 8; each XCD gets a contiguous piece
@@ -240,39 +266,36 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void gemm_kernel(GemmArgs a) {
   const int RB = a.Mp >> 4;
   const int rb0 = mt * 16 + wv * 4;     // first 16-row block of this wavefront
   const int row0 = mt * 256 + wv * 64;  // first row of this wavefront
-  const u32x4* __restrict__ W = (const u32x4*)a.W;
   const u32x4* __restrict__ A = (const u32x4*)a.A;
 
   f32x4 acc[4][8];
-  GEMM_ZERO_ACC();
-  u32x4 w0[NLW], w1[NLW], ar[8];
-  GEMM_LOAD_A1(ar, (int)(it0 % KC), 0);
-  GEMM_LOAD_A1(ar, (int)(it0 % KC), 1);
-  GEMM_LOAD_W(w0, it0);
-  if (it0 + 1 < it1) { GEMM_LOAD_W(w1, it0 + 1); }
-  // Segments: the iterations of one column tile inside [it0, it1). The weight
-  // register set / LDS buffer alternates with the global iteration parity, so
-  // each segment runs one of two loops depending on the parity it starts at.
+  // activation register sets: iteration j uses set (j - it0) % 3 (after the
+  // rotations below, the set named a0 serves the current iteration)
+  u32x4 a0[8], a1[8], a2[8];
+  GEMM_LOAD_A(a0, (int)(it0 % KC));
+  GEMM_DMA_W(it0);
+  if (it0 + 1 < it1) {
+    GEMM_LOAD_A(a1, (int)((it0 + 1) % KC));
+    GEMM_DMA_W(it0 + 1);
+  }
+  if (it0 + 2 < it1) {
+    GEMM_LOAD_A(a2, (int)((it0 + 2) % KC));
+    GEMM_DMA_W(it0 + 2);
+  }
+  // Segments: the iterations of one column tile inside [it0, it1).
   int64_t it = it0;
   while (it < it1) {
     const int64_t seg0 = it;
     const int tile = (int)(it / KC);
     const int64_t seg1 = (it1 < (int64_t)(tile + 1) * KC) ? it1 : (int64_t)(tile + 1) * KC;
     GEMM_ZERO_ACC();
-    if (((it - it0) & 1) == 0) {
-      for (;;) {
-        GEMM_STEP(0, w0);
-        if (++it >= seg1) break;
-        GEMM_STEP(1, w1);
-        if (++it >= seg1) break;
-      }
-    } else {
-      for (;;) {
-        GEMM_STEP(1, w1);
-        if (++it >= seg1) break;
-        GEMM_STEP(0, w0);
-        if (++it >= seg1) break;
-      }
+    for (;;) {
+      GEMM_STEP(a0);
+      if (++it >= seg1) { GEMM_ROTATE(); break; }
+      GEMM_STEP(a1);
+      if (++it >= seg1) { GEMM_ROTATE(); GEMM_ROTATE(); break; }
+      GEMM_STEP(a2);
+      if (++it >= seg1) break;
     }
     if (EPI != EPI_QKV && seg0 % KC == 0 && seg1 % KC == 0) {
       epilogue<EPI>(a, acc, tile, row0, lane, sE[wv]);
@@ -285,6 +308,8 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void gemm_kernel(GemmArgs a) {
         for (int nb = 0; nb < 8; ++nb) part[(mb * 8 + nb) * 64 + lane] = acc[mb][nb];
     }
   }
+  // nothing may still be writing LDS when the workgroup ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // Sum the partial tiles of split tiles in workgroup order and run the epilogue.
