@@ -58,7 +58,7 @@ enum {
 
 /* Decoder shape (Qwen2.5 / LLaMA-style pre-norm decoder, the layout of the
  * paper's Dream-7B / DiffuCoder-7B backbones; the paper names only the
- * models). Constraints: hidden % 128 == 0, head_dim in {64, 128},
+ * models). Constraints: hidden % 256 == 0, head_dim in {64, 128},
  * heads % kv_heads == 0, heads * head_dim == hidden, ffn % 64 == 0,
  * 0 <= mask_id < vocab. */
 typedef struct lopa_model_cfg {

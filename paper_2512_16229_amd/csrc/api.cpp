@@ -52,11 +52,12 @@ int dalloc(DevBuf& b, size_t bytes, std::vector<void*>& owned) {
   return LOPA_OK;
 }
 
+// Packed weights: [blocks of 16 output features][K / 64][2][64][8] bf16.
 struct LayerPack {
-  uint16_t* qkv;   // tiles_qkv x KC(H)
-  uint16_t* o;     // tiles_h x KC(Hq*d)
-  uint16_t* gu;    // tiles_gu x KC(H), gate/up interleaved
-  uint16_t* down;  // tiles_h x KC(F)
+  uint16_t* qkv;   // blk_qkv blocks, K = H
+  uint16_t* o;     // blk_h blocks, K = Hq * d
+  uint16_t* gu;    // blk_gu blocks (gate / up pairs), K = H
+  uint16_t* down;  // blk_h blocks, K = round256(F)
   float* bias;     // [Nqkv] or null
   float* ln1;
   float* ln2;
@@ -64,7 +65,45 @@ struct LayerPack {
 
 // rows of the packed activation buffers: whole 256-row tiles
 int padded_rows(int M) { return 256 * ((M + 255) / 256); }
-int round128(int k) { return 128 * ((k + 127) / 128); }
+int round256(int k) { return 256 * ((k + 255) / 256); }
+int round_up(int x, int m) { return m * ((x + m - 1) / m); }
+
+// Decomposition of one GEMM (see gemm.hip): tile width nb (16-column blocks)
+// and k-splits S. SwiGLU and LM-head tiles are fixed (their epilogues need
+// whole rows of a tile and no split); for the others the pair minimising an
+// estimate of HBM time is taken: rounds of workgroups x bytes of the largest
+// split, plus the fp32 partial sums written and read back and the fix-up
+// launch when partial sums exist.
+struct GemmPlan {
+  int nb, tiles, splits;
+};
+GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu) {
+  if (epi == EPI_SWIGLU) return {10, nblocks / 10, 1};
+  if (epi == EPI_LMHEAD) return {8, nblocks / 8, 1};
+  const int Q = KC / 4;
+  const double per_round = std::max(1, num_cu / MT);
+  GemmPlan best{8, nblocks / 8, 1};
+  double best_cost = 1e300;
+  for (int nb : {4, 8}) {
+    const int tiles = nblocks / nb;
+    for (int S = 1; S <= Q; ++S) {
+      const int64_t wgs = (int64_t)MT * tiles * S;
+      const int64_t rounds = (wgs + num_cu - 1) / num_cu;
+      const double split_bytes = (double)((Q + S - 1) / S) * 4 * nb * 2048;
+      double cost = (double)rounds * split_bytes * per_round;
+      if (epi == EPI_QKV || S > 1) cost += 2.0 * wgs * nb * 16384 + 14e6;
+      if (cost < best_cost) {
+        best_cost = cost;
+        best = {nb, tiles, S};
+      }
+    }
+  }
+  return best;
+}
+// bytes of fp32 partial sums the plan writes (QKV always goes through them)
+size_t plan_partial_bytes(int epi, const GemmPlan& p, int MT) {
+  return (epi == EPI_QKV || p.splits > 1) ? (size_t)MT * p.tiles * p.splits * p.nb * 16384 : 0;
+}
 
 }  // namespace
 
@@ -72,7 +111,9 @@ struct lopa_model {
   lopa_model_cfg cfg;
   int device = 0;
   int num_cu = 0;
-  int n_qkv = 0, tiles_qkv = 0, tiles_h = 0, tiles_gu = 0, tiles_lm = 0;
+  int n_qkv = 0;
+  int blk_qkv = 0, blk_h = 0, blk_gu = 0, blk_lm = 0;  // packed 16-column blocks
+  int tiles_lm = 0;                                     // LM-head column tiles
   std::vector<LayerPack> layers;
   uint16_t* embed = nullptr;
   uint16_t* lm = nullptr;
@@ -91,7 +132,7 @@ struct lopa_kv {
   float* rope = nullptr;        // [max_len][d/2][2]
   float* x = nullptr;           // [mp_max][H]
   uint16_t* abuf = nullptr;     // packed [mp_max][H]
-  uint16_t* fbuf = nullptr;     // packed [mp_max][F]
+  uint16_t* fbuf = nullptr;     // packed [mp_max][round256(F)], padding columns zero
   uint16_t* qbuf = nullptr;     // [max_branches][Hq][max_block][d]
   float* partials = nullptr;
   float* pm = nullptr;
@@ -139,6 +180,20 @@ struct ProfScope {
     if (ev) (void)hipEventRecord(ev->b, s);
   }
 };
+// the plans of the five GEMMs of a verify forward with MT row tiles
+struct StepPlans {
+  GemmPlan qkv, o, gu, down, lm;
+};
+StepPlans step_plans(const lopa_model* m, int MT) {
+  const lopa_model_cfg& c = m->cfg;
+  StepPlans p;
+  p.qkv = plan_gemm(EPI_QKV, m->blk_qkv, c.hidden / 64, MT, m->num_cu);
+  p.o = plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu);
+  p.gu = plan_gemm(EPI_SWIGLU, m->blk_gu, c.hidden / 64, MT, m->num_cu);
+  p.down = plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu);
+  p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, c.hidden / 64, MT, m->num_cu);
+  return p;
+}
 }  // namespace
 
 extern "C" {
@@ -167,15 +222,13 @@ static int check_cfg(const lopa_model_cfg* c) {
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f) || !std::isfinite(c->rms_eps) ||
       !std::isfinite(c->rope_theta))
     return fail(LOPA_EINVAL, "rms_eps and rope_theta must be positive and finite");
-  if (c->hidden % 128) return fail(LOPA_ESHAPE, "hidden %d is not a multiple of 128", c->hidden);
+  if (c->hidden % 256) return fail(LOPA_ESHAPE, "hidden %d is not a multiple of 256", c->hidden);
   if (c->head_dim != 64 && c->head_dim != 128)
     return fail(LOPA_ESHAPE, "head_dim %d not in {64, 128}", c->head_dim);
   if (c->heads % c->kv_heads) return fail(LOPA_ESHAPE, "heads %% kv_heads != 0");
   if (c->heads * c->head_dim != c->hidden)
     return fail(LOPA_ESHAPE, "heads * head_dim != hidden");
   if (c->ffn % 64) return fail(LOPA_ESHAPE, "ffn %d is not a multiple of 64", c->ffn);
-  if (((c->heads + 2 * c->kv_heads) * c->head_dim) % 128)
-    return fail(LOPA_ESHAPE, "(heads + 2 kv_heads) * head_dim not a multiple of 128");
   return LOPA_OK;
 }
 
@@ -201,10 +254,13 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
   const lopa_model_cfg& c = *cfg;
   const int H = c.hidden, d = c.head_dim, F = c.ffn, V = c.vocab;
   m->n_qkv = (c.heads + 2 * c.kv_heads) * d;
-  m->tiles_qkv = m->n_qkv / 128;
-  m->tiles_h = H / 128;
-  m->tiles_gu = F / 64;
-  m->tiles_lm = (V + 127) / 128;
+  // blocks padded to whole tiles of every width a plan may pick (4, 8; 10 for
+  // the gate / up pairs); padding blocks hold zero weights
+  m->blk_qkv = round_up(m->n_qkv / 16, 8);
+  m->blk_h = round_up(H / 16, 8);
+  m->blk_gu = round_up(2 * F / 16, 10);
+  m->blk_lm = round_up((V + 15) / 16, 8);
+  m->tiles_lm = m->blk_lm / 8;
   auto bail = [&](int code) {
     delete m;
     return code;
@@ -225,16 +281,17 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     *p = (float*)b.p;
     return r;
   };
-  const size_t chunk = 128 * 64;  // elements per (tile, 64-column chunk)
-  const int FP = round128(F);     // down projection K, zero-padded
+  const int FP = round256(F);  // down projection K, zero-padded
+  // elements of a packed weight: blocks x K x 16
+  auto wsize = [](int blocks, int K) { return (size_t)blocks * K * 16; };
   m->layers.resize(c.layers);
   for (int l = 0; l < c.layers; ++l) {
     const lopa_layer_weights& lw = w->layers[l];
     LayerPack& p = m->layers[l];
-    if ((rc = alloc16(&p.qkv, (size_t)m->tiles_qkv * (H / 64) * chunk)) ||
-        (rc = alloc16(&p.o, (size_t)m->tiles_h * (H / 64) * chunk)) ||
-        (rc = alloc16(&p.gu, (size_t)m->tiles_gu * (H / 64) * chunk)) ||
-        (rc = alloc16(&p.down, (size_t)m->tiles_h * (FP / 64) * chunk)) ||
+    if ((rc = alloc16(&p.qkv, wsize(m->blk_qkv, H))) ||
+        (rc = alloc16(&p.o, wsize(m->blk_h, c.heads * d))) ||
+        (rc = alloc16(&p.gu, wsize(m->blk_gu, H))) ||
+        (rc = alloc16(&p.down, wsize(m->blk_h, FP))) ||
         (rc = allocf(&p.ln1, H)) || (rc = allocf(&p.ln2, H)))
       return bail(rc);
     p.bias = nullptr;
@@ -244,13 +301,13 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     const uint16_t* wv = (const uint16_t*)lw.wv;
     hipError_t e;
     if ((e = launch_repack(wq, c.heads * d, wk, c.kv_heads * d, wv, c.kv_heads * d, H, H,
-                           m->tiles_qkv, 0, p.qkv, s)) != hipSuccess ||
+                           m->blk_qkv, 0, p.qkv, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
-                           c.heads * d, m->tiles_h, 0, p.o, s)) != hipSuccess ||
+                           c.heads * d, m->blk_h, 0, p.o, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.w_gate, F, (const uint16_t*)lw.w_up, F, nullptr,
-                           0, H, H, m->tiles_gu, 1, p.gu, s)) != hipSuccess ||
+                           0, H, H, m->blk_gu, 1, p.gu, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.w_down, H, nullptr, 0, nullptr, 0, F, FP,
-                           m->tiles_h, 0, p.down, s)) != hipSuccess ||
+                           m->blk_h, 0, p.down, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln1, p.ln1, H, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln2, p.ln2, H, s)) != hipSuccess)
       return bail(fail(LOPA_EHIP, "layer %d repack: %s", l, hipGetErrorString(e)));
@@ -264,13 +321,13 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     }
   }
   if ((rc = alloc16(&m->embed, (size_t)V * H)) ||
-      (rc = alloc16(&m->lm, (size_t)m->tiles_lm * (H / 64) * chunk)) ||
+      (rc = alloc16(&m->lm, wsize(m->blk_lm, H))) ||
       (rc = allocf(&m->final_norm, H)))
     return bail(rc);
   hipError_t e;
   if ((e = hipMemcpyAsync(m->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s)) ||
       (e = launch_repack((const uint16_t*)w->lm_head, V, nullptr, 0, nullptr, 0, H, H,
-                         m->tiles_lm, 0, m->lm, s)) ||
+                         m->blk_lm, 0, m->lm, s)) ||
       (e = launch_bf16_to_f32((const uint16_t*)w->final_norm, m->final_norm, H, s)) ||
       (e = hipStreamSynchronize(s)))
     return bail(fail(LOPA_EHIP, "model create: %s", hipGetErrorString(e)));
@@ -307,9 +364,15 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   int rc;
   const size_t cache_e = (size_t)c.layers * 2 * Hkv * max_len * d;
   const size_t stag_e = (size_t)max_branches * c.layers * 2 * Hkv * max_block * d;
-  const int grid_max = m->num_cu;
-  const size_t part_b = (size_t)2 * grid_max * 4 * 32 * 64 * 16;
+  size_t part_b = 16;
+  for (int MT = 1; MT <= kv->mp_max / 256; ++MT) {
+    const StepPlans p = step_plans(m, MT);
+    part_b = std::max({part_b, plan_partial_bytes(EPI_QKV, p.qkv, MT),
+                       plan_partial_bytes(EPI_RESID, p.o, MT),
+                       plan_partial_bytes(EPI_RESID, p.down, MT)});
+  }
   const size_t rows = (size_t)kv->mp_max;
+  const int FP = round256(F);
 #define KV_ALLOC(field, type, bytes)                  \
   if ((rc = dalloc(b, (bytes), kv->owned))) return bail(rc); \
   kv->field = (type)b.p;
@@ -318,7 +381,7 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   KV_ALLOC(rope, float*, (size_t)max_len * (d / 2) * 2 * 4);
   KV_ALLOC(x, float*, rows * H * 4);
   KV_ALLOC(abuf, uint16_t*, rows * H * 2);
-  KV_ALLOC(fbuf, uint16_t*, rows * round128(F) * 2);
+  KV_ALLOC(fbuf, uint16_t*, rows * FP * 2);
   KV_ALLOC(qbuf, uint16_t*, (size_t)max_branches * c.heads * max_block * d * 2);
   KV_ALLOC(partials, float*, part_b);
   KV_ALLOC(pm, float*, rows * m->tiles_lm * 4);
@@ -337,7 +400,7 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   hipError_t e;
   if ((e = hipMemcpy(kv->rope, tab.data(), tab.size() * 4, hipMemcpyHostToDevice)) ||
       (e = hipMemset(kv->cache, 0, cache_e * 2)) || (e = hipMemset(kv->staging, 0, stag_e * 2)) ||
-      (e = hipMemset(kv->abuf, 0, rows * H * 2)) || (e = hipMemset(kv->fbuf, 0, rows * round128(F) * 2)) ||
+      (e = hipMemset(kv->abuf, 0, rows * H * 2)) || (e = hipMemset(kv->fbuf, 0, rows * FP * 2)) ||
       (e = hipDeviceSynchronize()))
     return bail(fail(LOPA_EHIP, "kv create: %s", hipGetErrorString(e)));
   *out = kv;
@@ -371,22 +434,24 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   const int M = n_branches * L;
   const int Mp = padded_rows(M);
   const int H = c.hidden, F = c.ffn, d = c.head_dim;
-  const int KCh = H / 64, KCf = round128(F) / 64;  // 64-column iterations per tile
+  const int MT = Mp / 256;
+  const StepPlans plan = step_plans(m, MT);
 
   GemmArgs g{};
   g.M = M;
   g.Mp = Mp;
+  g.mtiles = MT;
   g.partials = kv->partials;
-  auto gemm = [&](int epi, const uint16_t* A, const uint16_t* W, int N, int KC, int tiles) {
+  auto gemm = [&](int epi, const uint16_t* A, const uint16_t* W, int N, int K,
+                  const GemmPlan& p) {
     g.A = A;
     g.W = W;
     g.N = N;
-    g.K = KC * 64;
-    g.KC = KC;
-    g.tiles = tiles;
-    const int64_t I = (int64_t)tiles * KC;
-    g.mtiles = Mp / 256;
-    g.grid = (int)std::min<int64_t>(m->num_cu / g.mtiles, I) * g.mtiles;
+    g.KC = K / 64;
+    g.nb = p.nb;
+    g.tiles = p.tiles;
+    g.splits = p.splits;
+    g.gcols = p.tiles * p.splits;
     return launch_gemm(epi, g, s);
   };
 
@@ -424,7 +489,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.Lcap = kv->max_block;
     g.P = prefix_len;
     { ProfScope ps_(kv, LOPA_PROF_QKV, s);
-      HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, KCh, m->tiles_qkv)); }
+      HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, H, plan.qkv)); }
     at.layer = l;
     at.kcache = kv->cache + ((size_t)l * 2 + 0) * c.kv_heads * kv->max_len * d;
     at.vcache = kv->cache + ((size_t)l * 2 + 1) * c.kv_heads * kv->max_len * d;
@@ -432,14 +497,14 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
       HIP_TRY(launch_attention(at, s)); }
     g.x = kv->x;
     { ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
-      HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, KCh, m->tiles_h)); }
+      HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, c.heads * d, plan.o)); }
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
       HIP_TRY(launch_rmsnorm_pack(kv->x, p.ln2, c.rms_eps, M, Mp, H, kv->abuf, s)); }
     g.a_out = kv->fbuf;
     { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
-      HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, KCh, m->tiles_gu)); }
+      HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, H, plan.gu)); }
     { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
-      HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, KCf, m->tiles_h)); }
+      HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, round256(F), plan.down)); }
     const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
       HIP_TRY(launch_rmsnorm_pack(kv->x, next_w, c.rms_eps, M, Mp, H, kv->abuf, s)); }
@@ -454,7 +519,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   g.vocab = c.vocab;
   g.mask_id = c.mask_id;
   { ProfScope ps_(kv, LOPA_PROF_LMHEAD, s);
-    HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, m->tiles_lm * 128, KCh, m->tiles_lm)); }
+    HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, c.vocab, H, plan.lm)); }
   { ProfScope ps_(kv, LOPA_PROF_MERGE, s);
     HIP_TRY(launch_lm_merge(kv->pm, kv->ps, kv->pi, M, m->tiles_lm, conf, pred, s)); }
   kv->last_nb = n_branches;

@@ -10,16 +10,14 @@
 //
 // Activations ("A" operands, R = padded rows Mp):   fragment (rb, kb) at
 //   ((kb * (Mp/16)) + rb) * 512 elements.
-// Weights (W [N, K] in [out, in] order, "B" operand): tiles of BN = 128 output
-//   features; chunk kc of BK = 64 columns of tile t holds 16 fragments
-//   (kk in 0..1, nb in 0..7) at ((t * KC + kc) * 16 + kk * 8 + nb) * 512, so the
-//   whole weight is one linear stream in (tile, k-chunk) order.
+// Weights (W [N, K] in [out, in] order, "B" operand): blocks of 16 output
+//   features; block b holds its K / 64 chunks of 64 columns, each as two
+//   fragments (kk = 0, 1: columns 32 kk .. +31), fragment (b, kc, kk) at
+//   ((b * (K / 64) + kc) * 2 + kk) * 512. A GEMM tile is a run of consecutive
+//   blocks; one iteration streams one 2 KiB piece per block.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
-
-#define LOPA_BN 128
-#define LOPA_BK 64
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));

@@ -1,29 +1,32 @@
 // Weight-streaming bf16 GEMM for the skinny row counts of the verify step
-// (M = branches x block rows) with fused epilogues:
+// (M = branches x block rows, at most a few hundred) with fused epilogues:
 //   EPI_QKV    bias + rotate-half RoPE on q/k, q -> attention input, k/v -> the
-//              branch K/V staging (the Pre-Write of Sec. 3.4)
+//              branch K/V staging (the Pre-Write of Sec. 3.4); always in the
+//              fix-up kernel, where a thread sees both RoPE halves of a column
 //   EPI_RESID  residual add into the fp32 residual stream (O-proj, down-proj)
 //   EPI_SWIGLU silu(gate) * up -> packed bf16 operand of the down projection
-//   EPI_LMHEAD per (row, 128-token tile) softmax partials: max, argmax, sum exp
-//              (the logits never reach memory)
+//   EPI_LMHEAD per (row, column tile) softmax statistics: max, argmax, sum of
+//              exp (the logits never reach memory)
 //
-// Work decomposition. A workgroup (4 wavefronts) covers one 256-row tile of the
-// activations (each wavefront 64 rows x 128 output columns), so every weight
-// byte is read from HBM once per row tile. The (column tile, 64-wide k-chunk)
-// iteration space is split evenly over the column workgroups (stream-K): every
-// CU streams the same number of weight bytes whatever the tile count. A tile
-// covered by one workgroup runs its epilogue in place; a tile split over
-// several writes per-workgroup partial sums, which gemm_fixup_kernel adds in
-// workgroup order (deterministic) after the kernel boundary and then runs the
-// epilogue. No workgroup waits for another. The QKV epilogue (bias, RoPE,
-// scatter to q / K / V staging) always runs in the fix-up kernel, which keeps
-// its register-heavy code out of the streaming loop.
+// Work decomposition. The weight is a sequence of 16-column blocks; a column
+// tile is NB consecutive blocks. A workgroup (4 wavefronts, one per 64 rows)
+// covers one 256-row tile, so each weight byte crosses HBM once per row tile,
+// and one (column tile, k-split): with Q quads of k-chunks, split s owns
+// [s Q / S, (s + 1) Q / S). The tile width NB and the split count S are chosen
+// per GEMM on the host:
+//   S == 1  whole K in one workgroup, epilogue in place (no partial sums);
+//   S  > 1  fp32 partial sums; gemm_fixup_kernel adds the S partials of each
+//           element in split order (deterministic) and runs the epilogue.
 //
-// Pipeline. Per iteration (a 64-wide k-chunk) the 16 KiB weight chunk goes
-// straight from global memory into a 4-slot LDS ring (LDS-DMA, no registers)
-// and each wavefront's 8 activation fragments (L2-resident) into one of three
-// register sets, both three iterations ahead (the in-order vmcnt queue makes
-// equal lead distances the only way not to wait on younger loads).
+// Pipeline. One iteration is a 64-wide k-chunk of one tile. Its NB x 2 KiB of
+// weights go global -> LDS directly (global_load_lds, no registers) into a
+// 5-slot ring, and each wavefront's 8 activation fragments (L2-resident) into
+// one of 4 register sets; both are issued 4 iterations ahead. K is padded to a
+// multiple of 256, so a tile always spans a multiple of 4 iterations and the
+// register set of iteration j is the static j % 4: the loop is unrolled by 4
+// and no register set is ever rotated. Vector memory operations complete in
+// issue order, so "iteration j has landed" is one vmcnt wait on the number of
+// operations issued after it.
 #include "common.h"
 #include "kernels.h"
 
@@ -31,356 +34,451 @@
 
 namespace {
 
-template <int D>
-__device__ __forceinline__ void qkv_epilogue(const GemmArgs& a, f32x4 (&acc)[4][8], int tile,
-                                             int row0, int lane, unsigned nbmask) {
-  constexpr int HD = D / 2, HALF_NB = HD / 16;  // RoPE partner offset in 16-column blocks
+constexpr int GEMM_THREADS = 256;
+constexpr int LEAD = 4;         // iterations between issue and use (= activation register sets)
+constexpr int RING = LEAD + 1;  // weight chunks in LDS: in use + LEAD in flight
+
+template <int EPI, int NB>
+struct GemmSmem {
+  static constexpr int CHUNK = NB * 2048;  // bytes of weights per iteration
+  static constexpr int SWIGLU_SP = NB / 2 * 16 + 8;  // padded staging row (bf16)
+  static constexpr int BYTES = RING * CHUNK;
+  static_assert(EPI != EPI_SWIGLU || 4 * 64 * SWIGLU_SP * 2 <= RING * CHUNK, "staging fits");
+};
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Asynchronous global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane l copies base + voff(l) to bytes [16 l, 16 l + 16) of the 1 KiB LDS block
+// at lds_addr (wave-uniform, passed in M0). base is wave-uniform (SGPRs), so
+// the only per-lane address is the constant voff = 16 lane. The compiler does
+// not track the copy: completion is awaited with an explicit vmcnt wait
+// before the workgroup barrier.
+__device__ __forceinline__ const void* uniform_ptr(const void* p) {
+  // the "s" constraint alone does not keep a value the compiler thinks may
+  // diverge out of VGPRs: make the scalar copy explicit
+  const uint64_t u = (uint64_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  return (const void*)(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ void lds_dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               ::"s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(uniform_ptr(base))
+               : "memory");
+}
+
+// Four activation fragments (1 KiB apart) at a wave-uniform base -> registers.
+// Issued as inline assembly so that, like the LDS copies, the compiler does not
+// track them: its own waits would count only the loads it knows of and so
+// stall on younger loads. Nothing reads the registers before the explicit
+// vmcnt wait of the iteration that uses them; pin_landed() then hands them to
+// the compiler.
+__device__ __forceinline__ void load_frag4(u32x4& d0, u32x4& d1, u32x4& d2, u32x4& d3,
+                                           const void* base, uint32_t voff) {
+  asm volatile(
+      "global_load_dwordx4 %0, %4, %5\n\t"
+      "global_load_dwordx4 %1, %4, %5 offset:1024\n\t"
+      "global_load_dwordx4 %2, %4, %5 offset:2048\n\t"
+      "global_load_dwordx4 %3, %4, %5 offset:3072"
+      : "=&v"(d0), "=&v"(d1), "=&v"(d2), "=&v"(d3)
+      : "v"(voff), "s"(uniform_ptr(base))
+      : "memory");
+}
+__device__ __forceinline__ void pin_landed(u32x4& v) { asm volatile("" : "+v"(v)); }
+// After the loop the last iterations' loads (repeats of the last chunk) are
+// still in flight into the activation registers: wait for them, and keep the
+// registers alive until then so that nothing else is placed in them earlier.
+#define GEMM_DRAIN()                                                                     \
+  {                                                                                      \
+    wait_vmcnt<0>();                                                                     \
+    _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) {                                   \
+      pin_landed(a0[i_]);                                                                \
+      pin_landed(a1[i_]);                                                                \
+      pin_landed(a2[i_]);                                                                \
+      pin_landed(a3[i_]);                                                                \
+    }                                                                                    \
+  }
+
+// c += a^T b on a 16x16x32 bf16 tile, accumulating in place in AGPRs. Written as
+// inline assembly with a tied operand: with the builtin the register allocator
+// renames accumulators between the unrolled iterations and then copies them
+// back at the loop edge. The compiler does not see these as MFMAs, so the
+// hazard wait states are explicit: mfma_settle() before accumulators are read
+// or rewritten by other instructions, and after they are zeroed.
+__device__ __forceinline__ void mfma_acc(f32x4& c, const u32x4& a, const u32x4& b) {
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mfma_settle() {
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+}
+
+// ------------------------------------------------------------------ epilogues
+// acc[mb][nb][j]: row row0 + 16 mb + 4 g + j, column 16 (tile NB + nb) + c16
+// of this wavefront (g = lane / 16, c16 = lane % 16).
+
+template <int NB>
+__device__ __forceinline__ void resid_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
+                                               int row0, int lane) {
   const int g = lane >> 4, c16 = lane & 15;
-  const int qcols = a.Hq * D, kcols = a.Hkv * D;
-  // A 128-column tile never straddles the q / k / v sections (their widths are
-  // multiples of 128) and holds whole heads, so the section is per tile.
-  const int n0 = tile * LOPA_BN;
-  const int sect = n0 < qcols ? 0 : (n0 < qcols + kcols ? 1 : 2);
-  const int base = sect == 0 ? 0 : (sect == 1 ? qcols : qcols + kcols);
-  if (n0 >= a.N) return;
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = row0 + mb * 16 + g * 4 + j;
       if (r >= a.M) continue;
-      const int br = r / a.L, i = r % a.L;
-      const float* cs_row = a.rope + (int64_t)(a.P + i) * HD * 2;
+      float* xr = a.x + (int64_t)r * a.N;
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb) {
-        if (!((nbmask >> nb) & 1)) continue;
-        const bool low = (nb % (D / 16)) < HALF_NB;
-        if (sect < 2 && !low) continue;  // written together with its partner
-        const int nl = n0 - base + nb * 16 + c16;
-        const int head = nl / D, dim = nl % D;
-        const int n = n0 + nb * 16 + c16;
-        float o1 = acc[mb][nb][j] + (a.bias ? a.bias[n] : 0.f), o2 = 0.f;
-        if (sect < 2) {
-          const float x2 = acc[mb][(nb + HALF_NB) & 7][j] + (a.bias ? a.bias[n + HD] : 0.f);
-          const float2 cs = *(const float2*)(cs_row + dim * 2);
-          const float x1 = o1;
-          o1 = x1 * cs.x - x2 * cs.y;
-          o2 = x2 * cs.x + x1 * cs.y;
-        }
-        if (sect == 0) {
-          uint16_t* q = a.q_out + (((int64_t)br * a.Hq + head) * a.L + i) * D;
-          q[dim] = f2bf_bits(o1);
-          q[dim + HD] = f2bf_bits(o2);
-        } else {
-          uint16_t* st = a.staging +
-                         (((((int64_t)br * a.layers + a.layer) * 2 + (sect - 1)) * a.Hkv + head) *
-                              a.Lcap + i) * D;
-          st[dim] = f2bf_bits(o1);
-          if (sect == 1) st[dim + HD] = f2bf_bits(o2);
-        }
+      for (int nb = 0; nb < NB; ++nb) {
+        const int n = (tile * NB + nb) * 16 + c16;
+        if (n < a.N) xr[n] += acc[mb][nb][j];
       }
     }
 }
 
-template <int EPI>
-__device__ __forceinline__ void epilogue(const GemmArgs& a, f32x4 (&acc)[4][8], int tile, int row0,
-                                         int lane, uint16_t* stage, unsigned nbmask = 0xffu) {
+// gate / up blocks alternate (block 2p: gate columns 16p.., block 2p + 1: up);
+// output block p of the tile -> columns 16 (tile NB / 2 + p) of the packed
+// down-projection operand. Staged through LDS so each lane stores 16 bytes.
+template <int NB>
+__device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
+                                                int row0, int lane, uint16_t* e) {
+  constexpr int PAIRS = NB / 2, SP = PAIRS * 16 + 8;
   const int g = lane >> 4, c16 = lane & 15;
-  if constexpr (EPI == EPI_RESID) {
-    #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-      #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = row0 + mb * 16 + g * 4 + j;
-        if (r >= a.M) continue;
-        float* xr = a.x + (int64_t)r * a.N + tile * LOPA_BN + c16;
-        #pragma unroll
-        for (int nb = 0; nb < 8; ++nb)
-          if ((nbmask >> nb) & 1) xr[nb * 16] += acc[mb][nb][j];
-      }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    // gate in columns 0..63, up in 64..127 of the tile; output columns
-    // [64 tile, 64 tile + 64). Stage through LDS so each lane writes 16 bytes.
-    uint16_t* e = stage;  // this wavefront's 64 x 72 staging tile
-    #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-      #pragma unroll
-      for (int nb = 0; nb < 4; ++nb)
-        #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (!((nbmask >> nb) & 1)) continue;
-          const float gt = acc[mb][nb][j], up = acc[mb][nb + 4][j];
-          const float h = gt / (1.0f + expf(-gt)) * up;
-          e[(mb * 16 + g * 4 + j) * 72 + nb * 16 + c16] = f2bf_bits(h);
-        }
-    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): wave-local LDS writes done
-    __builtin_amdgcn_wave_barrier();
-    const int Nout = a.N >> 1;
-    #pragma unroll
-    for (int q = lane; q < 64 * 8; q += 64) {
-      const int rr = q >> 3, cg = q & 7;
-      const int r = row0 + rr;
-      if (r >= a.M || !((nbmask >> (cg >> 1)) & 1)) continue;
-      const uint4 v = *(const uint4*)(e + rr * 72 + cg * 8);
-      *(uint4*)(a.a_out + packA_off(r, tile * 64 + cg * 8, a.Mp)) = v;
-    }
-    (void)Nout;
-  } else if constexpr (EPI == EPI_LMHEAD) {
-    #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
-      #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = row0 + mb * 16 + g * 4 + j;
-        float m = -INFINITY;
-        int mi = 0x7fffffff;
-        float v[8];
-        #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) {
-          const int col = tile * LOPA_BN + nb * 16 + c16;
-          v[nb] = (col < a.vocab && col != a.mask_id) ? acc[mb][nb][j] : -INFINITY;
-          if (v[nb] > m) { m = v[nb]; mi = col; }
-        }
-        #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) {
-          const float om = __shfl_xor(m, o);
-          const int oi = __shfl_xor(mi, o);
-          if (om > m || (om == m && oi < mi)) { m = om; mi = oi; }
-        }
-        float s = 0.f;
-        if (m != -INFINITY)
-          #pragma unroll
-          for (int nb = 0; nb < 8; ++nb) s += expf(v[nb] - m);
-        #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o);
-        if (c16 == 0 && r < a.M) {
-          const int64_t o = (int64_t)r * a.tiles + tile;
-          a.pm[o] = m;
-          a.ps[o] = s;
-          a.pi[o] = mi;
-        }
-      }
-  } else {  // EPI_QKV
-    if (a.d == 128) qkv_epilogue<128>(a, acc, tile, row0, lane, nbmask);
-    else qkv_epilogue<64>(a, acc, tile, row0, lane, nbmask);
-  }
-}
-
-__device__ __forceinline__ int64_t sk_start(int g, int64_t I, int G) { return (int64_t)g * I / G; }
-
-// workgroup whose range contains iteration j
-__device__ __forceinline__ int sk_owner(int64_t j, int64_t I, int G) {
-  int g = (int)((j * G) / I);
-  while (g + 1 < G && sk_start(g + 1, I, G) <= j) ++g;
-  while (g > 0 && sk_start(g, I, G) > j) --g;
-  return g;
-}
-
-// partial-sum slot of contributor gc of a tile that starts at iteration t0
-__device__ __forceinline__ int sk_slot(int gc, int g_lo, int64_t t0, int64_t I, int G) {
-  return (gc == g_lo && sk_start(gc, I, G) < t0) ? 2 * gc + 1 : 2 * gc;
-}
-
-constexpr int GEMM_THREADS = 256;
-constexpr int W_SLOTS = 4;  // LDS ring of 16 KiB weight chunks (three in flight)
-
-// Asynchronous global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
-// lane l writes bytes [16 l, 16 l + 16) of the 1 KiB LDS block at lds_addr
-// (wave-uniform, passed in M0). The compiler does not track it: completion is
-// awaited with an explicit vmcnt wait before the workgroup barrier.
-__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_addr), "v"(gptr)
-               : "memory");
-}
-
-// weight chunk of iteration itx -> ring slot (4 x 1 KiB blocks per wavefront)
-#define GEMM_DMA_W(itx)                                                                  \
-  {                                                                                      \
-    const uint32_t slot_ = sW_base + (uint32_t)(((itx) % W_SLOTS) * 16384);              \
-    const char* src_ = (const char*)a.W + (int64_t)(itx) * 16384 + lane * 16;            \
-    _Pragma("unroll") for (int r_ = 0; r_ < 4; ++r_) {                                   \
-      const int blk_ = r_ * 4 + wv;                                                      \
-      lds_dma16(src_ + blk_ * 1024, slot_ + blk_ * 1024);                                \
-    }                                                                                    \
-  }
-// this wavefront's 8 activation fragments of 64-wide chunk kcx -> registers
-#define GEMM_LOAD_A(dst, kcx)                                                            \
-  _Pragma("unroll") for (int kk_ = 0; kk_ < 2; ++kk_)                                    \
-    _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                                  \
-      dst[kk_ * 4 + mb_] = A[((int64_t)((2 * (kcx) + kk_) * RB + rb0 + mb_)) * 64 + lane];
-#define GEMM_ZERO_ACC()                                                                  \
-  _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                                    \
-    _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) acc[mb_][nb_] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-// One iteration it. Every iteration j issues, in this order, the 8 activation
-// loads then the 4 weight copies of iteration j + 3 (the prologue issues those
-// of it0 .. it0 + 2 the same way). When iteration it starts, what was issued
-// after the weight copies of `it` is iterations it + 1 and it + 2: 24
-// operations (fewer near the end of the range), so vmcnt(24) means both the
-// weights and the activations of `it` have arrived.
-#define GEMM_STEP(ar)                                                                    \
-  {                                                                                      \
-    if (it + 2 < it1) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");                  \
-    else if (it + 1 < it1) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");             \
-    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");                                \
-    lds_barrier();                                                                       \
-    const u32x4* wl_ = sW + (int)(it % W_SLOTS) * 1024;                                  \
-    _Pragma("unroll") for (int kk_ = 0; kk_ < 2; ++kk_)                                  \
-      _Pragma("unroll") for (int nb_ = 0; nb_ < 8; ++nb_) {                              \
-        const u32x4 bf_ = wl_[(kk_ * 8 + nb_) * 64 + lane];                              \
-        _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                              \
-          acc[mb_][nb_] = mfma16(ar[kk_ * 4 + mb_], bf_, acc[mb_][nb_]);                 \
-      }                                                                                  \
-    if (it + 3 < it1) {                                                                  \
-      GEMM_LOAD_A(ar, (int)((it + 3) % KC));                                             \
-      GEMM_DMA_W(it + 3);                                                                \
-    }                                                                                    \
-  }
-
-#define GEMM_ROTATE()                                                                    \
-  _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) {                                     \
-    const u32x4 t_ = a0[i_];                                                             \
-    a0[i_] = a1[i_];                                                                     \
-    a1[i_] = a2[i_];                                                                     \
-    a2[i_] = t_;                                                                         \
-  }
-
-template <int EPI>
-__global__ __launch_bounds__(GEMM_THREADS, 1) void gemm_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) u32x4 sW[W_SLOTS * 1024];  // ring of 16 KiB chunks
-  __shared__ __attribute__((aligned(16))) uint16_t sE[4][EPI == EPI_SWIGLU ? 64 * 72 : 8];
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const uint32_t sW_base = (uint32_t)(uintptr_t)sW;
-  const int MT = a.mtiles;
-  const int G = a.grid / MT;
-  // Hardware places workgroup b on XCD b % 8; each XCD gets a contiguous piece
-  // of the logical index q, so neighbouring iteration ranges share an L2 and
-  // the row tiles of one column workgroup stream the same weights together.
-  const int b = blockIdx.x;
-  const int q = (a.grid % 8 == 0) ? (b & 7) * (a.grid >> 3) + (b >> 3) : b;
-  const int mt = q % MT, g = q / MT;
-  const int KC = a.KC;
-  const int64_t I = (int64_t)a.tiles * KC;
-  const int64_t it0 = sk_start(g, I, G), it1 = sk_start(g + 1, I, G);
-  if (it0 >= it1) return;
-  const int RB = a.Mp >> 4;
-  const int rb0 = mt * 16 + wv * 4;     // first 16-row block of this wavefront
-  const int row0 = mt * 256 + wv * 64;  // first row of this wavefront
-  const u32x4* __restrict__ A = (const u32x4*)a.A;
-
-  f32x4 acc[4][8];
-  // activation register sets: iteration j uses set (j - it0) % 3 (after the
-  // rotations below, the set named a0 serves the current iteration)
-  u32x4 a0[8], a1[8], a2[8];
-  GEMM_LOAD_A(a0, (int)(it0 % KC));
-  GEMM_DMA_W(it0);
-  if (it0 + 1 < it1) {
-    GEMM_LOAD_A(a1, (int)((it0 + 1) % KC));
-    GEMM_DMA_W(it0 + 1);
-  }
-  if (it0 + 2 < it1) {
-    GEMM_LOAD_A(a2, (int)((it0 + 2) % KC));
-    GEMM_DMA_W(it0 + 2);
-  }
-  // Segments: the iterations of one column tile inside [it0, it1).
-  int64_t it = it0;
-  while (it < it1) {
-    const int64_t seg0 = it;
-    const int tile = (int)(it / KC);
-    const int64_t seg1 = (it1 < (int64_t)(tile + 1) * KC) ? it1 : (int64_t)(tile + 1) * KC;
-    GEMM_ZERO_ACC();
-    for (;;) {
-      GEMM_STEP(a0);
-      if (++it >= seg1) { GEMM_ROTATE(); break; }
-      GEMM_STEP(a1);
-      if (++it >= seg1) { GEMM_ROTATE(); GEMM_ROTATE(); break; }
-      GEMM_STEP(a2);
-      if (++it >= seg1) break;
-    }
-    if (EPI != EPI_QKV && seg0 % KC == 0 && seg1 % KC == 0) {
-      epilogue<EPI>(a, acc, tile, row0, lane, sE[wv]);
-    } else {
-      const int slot = (2 * g + (seg0 == it0 ? 0 : 1)) * MT + mt;
-      f32x4* part = (f32x4*)a.partials + ((int64_t)slot * 4 + wv) * 32 * 64;
-#pragma unroll
-      for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb) part[(mb * 8 + nb) * 64 + lane] = acc[mb][nb];
-    }
-  }
-  // nothing may still be writing LDS when the workgroup ends
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-}
-
-// Sum the partial tiles of split tiles in workgroup order and run the epilogue.
-// One wavefront per (column tile, row tile, 64-row block, column group): the
-// groups pair the 16-column blocks an epilogue couples (RoPE halves, gate/up),
-// nb and nb + PAIR; the LM-head epilogue reduces over all 8 blocks of a row,
-// so it takes one group. Whole tiles (done in gemm_kernel) return at once.
-template <int EPI>
-__global__ __launch_bounds__(64) void gemm_fixup_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t sE[EPI == EPI_SWIGLU ? 64 * 72 : 8];
-  constexpr int GROUPS = EPI == EPI_LMHEAD ? 1 : 4;
-  const int MT = a.mtiles;
-  const int G = a.grid / MT;
-  int bid = blockIdx.x;
-  const int cg = bid % GROUPS;
-  bid /= GROUPS;
-  const int w = bid % 4;
-  bid /= 4;
-  const int mt = bid % MT, tile = bid / MT;
-  const int KC = a.KC;
-  const int64_t I = (int64_t)a.tiles * KC;
-  const int64_t t0 = (int64_t)tile * KC;
-  const int g_lo = sk_owner(t0, I, G), g_hi = sk_owner(t0 + KC - 1, I, G);
-  if (g_lo == g_hi && EPI != EPI_QKV) return;
-  const int lane = threadIdx.x;
-  const int row0 = mt * 256 + w * 64;
-  const int pair = (EPI == EPI_QKV && a.d == 64) ? 2 : 4;
-  const int nb_a = (cg % pair) + (cg / pair) * 2 * pair;
-  const unsigned mask = GROUPS == 1 ? 0xffu : ((1u << nb_a) | (1u << (nb_a + pair)));
-  f32x4 acc[4][8];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 8; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int gc = g_lo; gc <= g_hi; ++gc) {
-    const int slot = sk_slot(gc, g_lo, t0, I, G) * MT + mt;
-    const f32x4* p = (const f32x4*)a.partials + ((int64_t)slot * 4 + w) * 32 * 64;
+    for (int p = 0; p < PAIRS; ++p)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
+        const float h = gt / (1.0f + expf(-gt)) * up;
+        e[(mb * 16 + g * 4 + j) * SP + p * 16 + c16] = f2bf_bits(h);
+      }
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wavefront's LDS writes done
+  __builtin_amdgcn_wave_barrier();
+  const int Nout = a.N >> 1;
+  for (int q = lane; q < 64 * PAIRS * 2; q += 64) {
+    const int rr = q / (PAIRS * 2), cg = q % (PAIRS * 2);
+    const int r = row0 + rr, col = tile * PAIRS * 16 + cg * 8;
+    if (r >= a.M || col >= Nout) continue;
+    const uint4 v = *(const uint4*)(e + rr * SP + cg * 8);
+    *(uint4*)(a.a_out + packA_off(r, col, a.Mp)) = v;
+  }
+}
+
+// per-row (max, argmax, sum exp(l - max)) over this tile's valid columns
+// (column < vocab, column != mask token) -> pm / ps / pi [row][tile]
+template <int NB>
+__device__ __forceinline__ void lm_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
+                                            int row0, int lane) {
+  const int g = lane >> 4, c16 = lane & 15;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float m = -INFINITY;
+      int mi = 0x7fffffff;
+      float v[NB];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) {
+        const int col = (tile * NB + nb) * 16 + c16;
+        v[nb] = (col < a.vocab && col != a.mask_id) ? acc[mb][nb][j] : -INFINITY;
+        if (v[nb] > m) { m = v[nb]; mi = col; }
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) {
+        const float om = __shfl_xor(m, o);
+        const int oi = __shfl_xor(mi, o);
+        if (om > m || (om == m && oi < mi)) { m = om; mi = oi; }
+      }
+      float s = 0.f;
+      if (m != -INFINITY)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) s += expf(v[nb] - m);
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o);
+      const int r = row0 + mb * 16 + g * 4 + j;
+      if (c16 == 0 && r < a.M) {
+        const int64_t o = (int64_t)r * a.tiles + tile;
+        a.pm[o] = m;
+        a.ps[o] = s;
+        a.pi[o] = mi;
+      }
+    }
+}
+
+// ------------------------------------------------------------------ main loop
+// loads of one iteration (tile jt, k-chunk kct) into register set `set` and
+// ring slot `slot`; weight layout [block][KC][2][64 lanes][8]
+// Loads of one iteration (tile jt, k-chunk kct): 8 activation fragments into
+// register set `set` (two groups of 4, k-halves 0 and 1) and the NB x 2 KiB
+// weight chunk into ring slot `slot` (NB / 2 copies of 1 KiB per wavefront).
+// Weight layout [block][KC][2][64 lanes][8].
+#define GEMM_ISSUE_A(set, half, kct)                                                     \
+  load_frag4(set[4 * (half) + 0], set[4 * (half) + 1], set[4 * (half) + 2],              \
+             set[4 * (half) + 3], Ab + ((int64_t)(2 * (kct) + (half)) * RB + rb0) * 1024, voff)
+#define GEMM_ISSUE_W(r, jt, kct, slot)                                                   \
+  {                                                                                      \
+    const int u_ = (r) * 4 + wv; /* 1 KiB unit: block u_ / 2, k-half u_ % 2 */           \
+    lds_dma16(Wb + (((int64_t)(jt) * NB + (u_ >> 1)) * KC + (kct)) * 2048 + (u_ & 1) * 1024, \
+              voff, sW_base + (uint32_t)(slot) * (uint32_t)SM::CHUNK + (uint32_t)u_ * 1024u); \
+  }
+#define GEMM_ISSUE(set, jt, kct, slot)                                                   \
+  {                                                                                      \
+    GEMM_ISSUE_A(set, 0, kct);                                                           \
+    GEMM_ISSUE_A(set, 1, kct);                                                           \
+    _Pragma("unroll") for (int r_ = 0; r_ < NB / 2; ++r_) GEMM_ISSUE_W(r_, jt, kct, slot); \
+  }
+
+// next iteration to issue; past the last one the last chunk is issued again
+// (an L2 hit), which keeps every wait count and the loop body branch-free
+#define GEMM_ADVANCE_LOAD()                                                              \
+  {                                                                                      \
+    if (++lk == kc_end) {                                                                \
+      if (lt + 1 < t_hi) { lk = kc_beg; ++lt; }                                          \
+      else lk = kc_end - 1;                                                              \
+    }                                                                                    \
+  }
+
+// One iteration j. The 2 NB weight fragments of the chunk are read from LDS
+// BPF fragments ahead of the MFMAs that use them; the loads of iteration j + 4
+// are spread over the MFMA stream (activation half h once the MFMAs reading
+// it have issued, the weight copies from the second fragment on). Scheduling
+// barriers keep this order. Every iteration issues exactly OPS operations, so
+// waiting for iteration j is always vmcnt(3 OPS).
+constexpr int BPF = 4;
+#define GEMM_STEP(set)                                                                   \
+  {                                                                                      \
+    wait_vmcnt<3 * OPS>(); /* iteration j landed; j + 1 .. j + 3 may be in flight */     \
+    lds_barrier();                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) pin_landed(set[i_]);                \
+    const u32x4* wl_ = (const u32x4*)(smem + cs * SM::CHUNK);                            \
+    const int islot_ = cs == 0 ? RING - 1 : cs - 1; /* slot of iteration j - 1 */        \
+    u32x4 bf_[2 * NB];                                                                   \
+    _Pragma("unroll") for (int f_ = 0; f_ < BPF; ++f_)                                   \
+      bf_[f_] = wl_[((f_ % NB) * 2 + f_ / NB) * 64 + lane];                              \
+    __builtin_amdgcn_sched_barrier(0);                                                   \
+    _Pragma("unroll") for (int f_ = 0; f_ < 2 * NB; ++f_) {                              \
+      if (f_ + BPF < 2 * NB)                                                             \
+        bf_[f_ + BPF] = wl_[(((f_ + BPF) % NB) * 2 + (f_ + BPF) / NB) * 64 + lane];      \
+      _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                                \
+        mfma_acc(acc[mb_][f_ % NB], set[(f_ / NB) * 4 + mb_], bf_[f_]);                  \
+      if (f_ >= 1 && f_ <= NB / 2) GEMM_ISSUE_W(f_ - 1, lt, lk, islot_);                 \
+      if (f_ == NB - 1) GEMM_ISSUE_A(set, 0, lk);                                        \
+      if (f_ == 2 * NB - 1) GEMM_ISSUE_A(set, 1, lk);                                    \
+      __builtin_amdgcn_sched_barrier(0);                                                 \
+    }                                                                                    \
+    GEMM_ADVANCE_LOAD();                                                                 \
+    cs = (cs == RING - 1) ? 0 : cs + 1;                                                  \
+  }
+
+template <int EPI, int NB>
+__global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_kernel(GemmArgs a) {
+  using SM = GemmSmem<EPI, NB>;
+  constexpr int OPS = 8 + NB / 2;  // vector memory operations per wavefront per iteration
+  static_assert(NB % 2 == 0 && 3 * OPS <= 63, "tile width");
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t sW_base = (uint32_t)(uintptr_t)smem;
+
+  // Hardware places workgroup b on XCD b % 8; the remap gives each XCD a
+  // contiguous range of q, so the row tiles of one column workgroup (adjacent
+  // q) share an L2 and read each weight chunk from HBM once.
+  const int b = blockIdx.x, grid = gridDim.x;
+  const int q = (grid % 8 == 0) ? (b & 7) * (grid >> 3) + (b >> 3) : b;
+  const int MT = a.mtiles;
+  const int mt = q % MT, c = q / MT;
+  const int KC = a.KC, QT = KC >> 2;
+  // workgroup c of a row tile: column tile c / S, k-chunks of split c % S
+  const int split = c % a.splits;
+  const int t_lo = c / a.splits, t_hi = t_lo + 1;
+  const int kc_beg = 4 * (split * QT / a.splits);
+  const int kc_end = 4 * ((split + 1) * QT / a.splits);
+  if (t_lo >= a.tiles || kc_beg >= kc_end) return;
+  const int nq = (kc_end - kc_beg) >> 2;  // quads of iterations per tile
+  const int RB = a.Mp >> 4;
+  const int rb0 = mt * 16 + wv * 4;     // first 16-row block of this wavefront
+  const int row0 = mt * 256 + wv * 64;  // first row of this wavefront
+  const char* __restrict__ Ab = (const char*)a.A;  // fragment f at Ab + 1024 f
+  const char* __restrict__ Wb = (const char*)a.W;
+  const uint32_t voff = (uint32_t)lane * 16u;
+
+  f32x4 acc[4][NB];
+  u32x4 a0[8], a1[8], a2[8], a3[8];
+  int lt = t_lo, lk = kc_beg;  // next iteration to issue
+  GEMM_ISSUE(a0, lt, lk, 0);
+  GEMM_ADVANCE_LOAD();
+  GEMM_ISSUE(a1, lt, lk, 1);
+  GEMM_ADVANCE_LOAD();
+  GEMM_ISSUE(a2, lt, lk, 2);
+  GEMM_ADVANCE_LOAD();
+  GEMM_ISSUE(a3, lt, lk, 3);
+  GEMM_ADVANCE_LOAD();
+  int cs = 0;  // ring slot of the current iteration
+
+  {
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < 8; ++nb)
-        if ((mask >> nb) & 1) acc[mb][nb] += p[(mb * 8 + nb) * 64 + lane];
+      for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    mfma_settle();
+    for (int qq = 0; qq < nq; ++qq) {
+      GEMM_STEP(a0);
+      GEMM_STEP(a1);
+      GEMM_STEP(a2);
+      GEMM_STEP(a3);
+    }
+    GEMM_DRAIN();
+    mfma_settle();
+    if (EPI != EPI_QKV && a.splits == 1) {
+      if constexpr (EPI == EPI_LMHEAD) lm_epilogue<NB>(a, acc, t_lo, row0, lane);
+      if constexpr (EPI == EPI_RESID) resid_epilogue<NB>(a, acc, t_lo, row0, lane);
+      if constexpr (EPI == EPI_SWIGLU) {
+        // the weight ring becomes the staging area once every copy (including
+        // the repeated last chunk) has landed in all wavefronts
+        lds_barrier();
+        uint16_t* stage = (uint16_t*)smem + wv * 64 * SM::SWIGLU_SP;
+        swiglu_epilogue<NB>(a, acc, t_lo, row0, lane, stage);
+      }
+    } else {
+      const int64_t slot = ((int64_t)mt * a.tiles + t_lo) * a.splits + split;
+      f32x4* part = (f32x4*)a.partials + (slot * 4 + wv) * 4 * NB * 64;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) part[(mb * NB + nb) * 64 + lane] = acc[mb][nb];
+    }
   }
-  epilogue<EPI>(a, acc, tile, row0, lane, sE, mask);
+  wait_vmcnt<0>();  // nothing may still be writing LDS when the workgroup ends
 }
 
-template <int EPI>
-hipError_t launch_epi(const GemmArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(gemm_kernel<EPI>, dim3(a.grid), dim3(GEMM_THREADS), 0, s, a);
+// Sum the S partials of one f32x4 of the output (4 rows, 1 column) in split
+// order and run the epilogue. One thread per (row tile, column tile, wave,
+// 16-row block, 16-column block, lane): the same indexing as gemm_kernel's
+// partial store, so each warp-wide load is 1 KiB contiguous.
+template <int EPI, int NB>
+__global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int lane = (int)(gid & 63);
+  int64_t rest = gid >> 6;
+  const int nb = (int)(rest % NB);
+  rest /= NB;
+  const int mb = (int)(rest & 3);
+  rest >>= 2;
+  const int wv = (int)(rest & 3);
+  rest >>= 2;
+  const int tile = (int)(rest % a.tiles);
+  const int mt = (int)(rest / a.tiles);
+  if (mt >= a.mtiles) return;
+  const int g = lane >> 4, c16 = lane & 15;
+  const int r0 = mt * 256 + wv * 64 + mb * 16 + g * 4;
+  const int n = (tile * NB + nb) * 16 + c16;
+  if (n >= a.N || r0 >= a.M) return;
+  const int64_t sstride = (int64_t)4 * 4 * NB * 64;  // f32x4 between consecutive splits
+  auto sum = [&](int t2, int nb2) {
+    const f32x4* p = (const f32x4*)a.partials +
+                     ((((int64_t)mt * a.tiles + t2) * a.splits * 4 + wv) * 4 * NB + mb * NB + nb2) *
+                         64 + lane;
+    f32x4 v = p[0];
+    for (int s = 1; s < a.splits; ++s) v += p[s * sstride];
+    return v;
+  };
+  if constexpr (EPI == EPI_RESID) {
+    const f32x4 v = sum(tile, nb);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (r0 + j < a.M) a.x[(int64_t)(r0 + j) * a.N + n] += v[j];
+  } else if constexpr (EPI == EPI_QKV) {
+    const int D = a.d, HD = D >> 1;
+    const int qcols = a.Hq * D, kcols = a.Hkv * D;
+    const int sect = n < qcols ? 0 : (n < qcols + kcols ? 1 : 2);
+    const int base = sect == 0 ? 0 : (sect == 1 ? qcols : qcols + kcols);
+    const int head = (n - base) / D, dim = (n - base) % D;
+    if (sect < 2 && dim >= HD) return;  // written with its rotation partner
+    const f32x4 v1 = sum(tile, nb);
+    f32x4 v2 = {0.f, 0.f, 0.f, 0.f};
+    const int n2 = n + HD;
+    if (sect < 2) v2 = sum((n2 >> 4) / NB, (n2 >> 4) % NB);
+    const float b1 = a.bias ? a.bias[n] : 0.f;
+    const float b2 = (a.bias && sect < 2) ? a.bias[n2] : 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = r0 + j;
+      if (r >= a.M) continue;
+      const int br = r / a.L, i = r % a.L;
+      float o1 = v1[j] + b1, o2 = 0.f;
+      if (sect < 2) {
+        const float2 cs = *(const float2*)(a.rope + ((int64_t)(a.P + i) * HD + dim) * 2);
+        const float x1 = o1, x2 = v2[j] + b2;
+        o1 = x1 * cs.x - x2 * cs.y;
+        o2 = x2 * cs.x + x1 * cs.y;
+      }
+      if (sect == 0) {
+        uint16_t* qo = a.q_out + (((int64_t)br * a.Hq + head) * a.L + i) * D;
+        qo[dim] = f2bf_bits(o1);
+        qo[dim + HD] = f2bf_bits(o2);
+      } else {
+        uint16_t* st = a.staging +
+                       (((((int64_t)br * a.layers + a.layer) * 2 + (sect - 1)) * a.Hkv + head) *
+                            a.Lcap + i) * D;
+        st[dim] = f2bf_bits(o1);
+        if (sect == 1) st[dim + HD] = f2bf_bits(o2);
+      }
+    }
+  }
+}
+
+template <int EPI, int NB>
+hipError_t launch_nb(const GemmArgs& a, hipStream_t s) {
+  const int grid = a.mtiles * a.gcols;
+  hipLaunchKernelGGL((gemm_kernel<EPI, NB>), dim3(grid), dim3(GEMM_THREADS), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // split tiles exist unless every column workgroup owns whole tiles
-  const int G = a.grid / a.mtiles;
-  if (EPI == EPI_QKV || (int64_t)a.tiles * a.KC % G != 0 ||
-      ((int64_t)a.tiles * a.KC / G) % a.KC != 0) {
-    const int groups = EPI == EPI_LMHEAD ? 1 : 4;
-    hipLaunchKernelGGL(gemm_fixup_kernel<EPI>, dim3(a.tiles * a.mtiles * 4 * groups), dim3(64), 0,
-                       s, a);
-    e = hipGetLastError();
+  if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
+    if (EPI == EPI_QKV || a.splits > 1) {
+      const int64_t threads = (int64_t)a.mtiles * a.tiles * 4 * 4 * NB * 64;
+      hipLaunchKernelGGL((gemm_fixup_kernel<EPI, NB>), dim3((unsigned)((threads + 255) / 256)),
+                         dim3(256), 0, s, a);
+      e = hipGetLastError();
+    }
   }
   return e;
 }
 
 }  // namespace
 
+int gemm_smem_bytes(int epi, int nb) {
+  switch (epi * 16 + nb) {
+    case EPI_QKV * 16 + 4: return GemmSmem<EPI_QKV, 4>::BYTES;
+    case EPI_QKV * 16 + 8: return GemmSmem<EPI_QKV, 8>::BYTES;
+    case EPI_RESID * 16 + 4: return GemmSmem<EPI_RESID, 4>::BYTES;
+    case EPI_RESID * 16 + 8: return GemmSmem<EPI_RESID, 8>::BYTES;
+    case EPI_SWIGLU * 16 + 10: return GemmSmem<EPI_SWIGLU, 10>::BYTES;
+    case EPI_LMHEAD * 16 + 8: return GemmSmem<EPI_LMHEAD, 8>::BYTES;
+  }
+  return -1;
+}
+
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
-  switch (epi) {
-    case EPI_QKV: return launch_epi<EPI_QKV>(a, s);
-    case EPI_RESID: return launch_epi<EPI_RESID>(a, s);
-    case EPI_SWIGLU: return launch_epi<EPI_SWIGLU>(a, s);
-    case EPI_LMHEAD: return launch_epi<EPI_LMHEAD>(a, s);
+  // (epilogue, tile width) pairs the host planner may choose; splits > 1 only
+  // for EPI_QKV and EPI_RESID
+  if (a.splits > 1 && (epi == EPI_SWIGLU || epi == EPI_LMHEAD)) return hipErrorInvalidValue;
+  if (a.KC % 4 || a.KC < 4 || a.splits < 1 || a.splits > a.KC / 4 || a.mtiles < 1 ||
+      a.gcols < 1 || a.Mp != 256 * a.mtiles)
+    return hipErrorInvalidValue;
+  if (a.gcols != a.tiles * a.splits) return hipErrorInvalidValue;
+  switch (epi * 16 + a.nb) {
+    case EPI_QKV * 16 + 4: return launch_nb<EPI_QKV, 4>(a, s);
+    case EPI_QKV * 16 + 8: return launch_nb<EPI_QKV, 8>(a, s);
+    case EPI_RESID * 16 + 4: return launch_nb<EPI_RESID, 4>(a, s);
+    case EPI_RESID * 16 + 8: return launch_nb<EPI_RESID, 8>(a, s);
+    case EPI_SWIGLU * 16 + 10: return launch_nb<EPI_SWIGLU, 10>(a, s);
+    case EPI_LMHEAD * 16 + 8: return launch_nb<EPI_LMHEAD, 8>(a, s);
   }
   return hipErrorInvalidValue;
 }

@@ -19,13 +19,15 @@ hipError_t launch_kv_copy(const uint16_t* src, uint16_t* dst, int64_t src_stride
                           int64_t dst_stride, int groups, int rows_elems, hipStream_t s);
 
 // ------------------------------------------------------------ weight repack
-// Pack rows of up to three [rows_i, K] bf16 sources (stacked in order) into the
-// tile-major fragment layout; N_pad = tiles * 128 rows, rows past the sources
-// are zero. interleave64: tile t takes rows [64t, 64t+64) of source 0 then the
-// same rows of source 1 (gate / up pairing for the SwiGLU epilogue).
-// K: source row length; KP (a multiple of 128, >= K): packed width, zero-filled.
+// Pack the rows of up to three [rows_i, K] bf16 sources (stacked in order) into
+// the GEMM weight layout: blocks of 16 output rows, each [KC][2][64 lanes][8]
+// (one 1 KiB B-operand fragment per (block, 64-column chunk, 32-column half)).
+// `blocks` blocks are written; rows past the sources are zero. pairs: block 2p
+// holds rows [16p, 16p + 16) of source 0 and block 2p + 1 the same rows of
+// source 1 (gate / up pairing for the SwiGLU epilogue).
+// K: source row length; KP (a multiple of 256, >= K): packed width, zero-filled.
 hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
-                         const uint16_t* s2, int r2, int K, int KP, int tiles, int interleave64,
+                         const uint16_t* s2, int r2, int K, int KP, int blocks, int pairs,
                          uint16_t* dst, hipStream_t s);
 hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_t s);
 
@@ -46,11 +48,14 @@ enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
 struct GemmArgs {
   const uint16_t* A;   // packed activations, Mp rows, K columns
-  const uint16_t* W;   // packed weights, tiles x (K/64) chunks of 64 columns
-  int M, Mp, N, K, KC, tiles;  // K % 64 == 0; KC = K / 64 iterations per tile
+  const uint16_t* W;   // packed weights [tiles * nb blocks of 16 columns][KC][2][64][8]
+  int M, Mp, N, KC;    // KC = K / 64 iterations per tile, a multiple of 4
+  int nb;              // 16-column blocks per tile (an instantiated width)
+  int tiles;           // column tiles
+  int splits;          // k-splits per tile; > 1: partial sums + fix-up kernel
   int mtiles;          // row tiles of 256 rows; Mp = 256 * mtiles
-  int grid;            // workgroups = mtiles x column workgroups (stream-K)
-  float* partials;     // [2*grid][4 waves][32][64][4] fp32
+  int gcols;           // workgroups per row tile (tiles * splits when splits > 1)
+  float* partials;     // [mtiles][tiles][splits][4 waves][4][nb][64][4] fp32
   // EPI_QKV
   const float* bias;   // [N] or null
   const float* rope;   // [max_pos][d/2][2] (cos, sin)
@@ -67,6 +72,8 @@ struct GemmArgs {
   int32_t* pi;         // [M][tiles] argmax
   int vocab, mask_id;
 };
+// bytes of LDS of gemm_kernel<epi, nb> (-1: not instantiated)
+int gemm_smem_bytes(int epi, int nb);
 hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- attention

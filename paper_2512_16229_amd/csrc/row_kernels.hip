@@ -107,30 +107,30 @@ __global__ __launch_bounds__(256) void lm_merge_kernel(const float* __restrict__
   }
 }
 
-// Weight repack: one thread per (fragment, lane) writes 8 bf16 (16 bytes).
+// Weight repack: one thread per (fragment, lane) writes 8 bf16 (16 bytes);
+// thread order is the packed order [block][kc][kk][lane].
 __global__ __launch_bounds__(256) void repack_kernel(const uint16_t* __restrict__ s0, int r0,
                                                      const uint16_t* __restrict__ s1, int r1,
                                                      const uint16_t* __restrict__ s2, int r2,
-                                                     int K, int KC, int64_t total,
-                                                     int interleave64, uint16_t* __restrict__ dst) {
+                                                     int K, int KC, int64_t total, int pairs,
+                                                     uint16_t* __restrict__ dst) {
   // K: length of a source row; KC * 64 >= K: packed columns, the excess is zero
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= total) return;
   const int lane = (int)(gid & 63);
-  const int64_t f = gid >> 6;
-  const int per_tile = KC * 16;
-  const int t = (int)(f / per_tile);
-  const int rem = (int)(f % per_tile);
-  const int kc = rem >> 4, kk = (rem >> 3) & 1, nb = rem & 7;
-  const int k0 = kc * LOPA_BK + kk * 32 + (lane >> 4) * 8;
+  const int64_t u = gid >> 6;
+  const int kk = (int)(u & 1);
+  const int kc = (int)((u >> 1) % KC);
+  const int blk = (int)((u >> 1) / KC);
+  const int k0 = kc * 64 + kk * 32 + (lane >> 4) * 8;
   const uint16_t* src = nullptr;
   int row = 0;
-  if (interleave64) {
-    row = t * 64 + (nb & 3) * 16 + (lane & 15);
-    if (nb < 4) { if (row < r0) src = s0; }
+  if (pairs) {
+    row = (blk >> 1) * 16 + (lane & 15);
+    if (!(blk & 1)) { if (row < r0) src = s0; }
     else { if (row < r1) src = s1; }
   } else {
-    const int n = t * LOPA_BN + nb * 16 + (lane & 15);
+    const int n = blk * 16 + (lane & 15);
     if (n < r0) { src = s0; row = n; }
     else if (n < r0 + r1) { src = s1; row = n - r0; }
     else if (n < r0 + r1 + r2) { src = s2; row = n - r0 - r1; }
@@ -169,15 +169,17 @@ hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, 
 }
 
 hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
-                         const uint16_t* s2, int r2, int K, int KP, int tiles, int interleave64,
+                         const uint16_t* s2, int r2, int K, int KP, int blocks, int pairs,
                          uint16_t* dst, hipStream_t s) {
-  const int KC = KP / LOPA_BK;
-  const int64_t total = (int64_t)tiles * KC * 16 * 64;
-  const int64_t blocks = (total + 255) / 256;
-  hipLaunchKernelGGL(repack_kernel, dim3((unsigned)blocks), dim3(256), 0, s, s0, r0, s1, r1, s2,
-                     r2, K, KC, total, interleave64, dst);
+  if (KP % 256 || KP < K) return hipErrorInvalidValue;
+  const int KC = KP / 64;
+  const int64_t total = (int64_t)blocks * KC * 2 * 64;
+  const int64_t grid = (total + 255) / 256;
+  hipLaunchKernelGGL(repack_kernel, dim3((unsigned)grid), dim3(256), 0, s, s0, r0, s1, r1, s2,
+                     r2, K, KC, total, pairs, dst);
   return hipGetLastError();
 }
+
 
 hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_t s) {
   hipLaunchKernelGGL(bf16_to_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, src, dst, n);
