@@ -127,8 +127,9 @@ struct lopa_model {
 struct lopa_kv {
   const lopa_model* m = nullptr;
   int max_len = 0, max_branches = 0, max_block = 0, mp_max = 0;
-  uint16_t* cache = nullptr;    // [layers][2][Hkv][max_len][d]
-  uint16_t* staging = nullptr;  // [max_branches][layers][2][Hkv][max_block][d]
+  int vld = 0, vlds = 0;        // V leading dimensions: max_len, max_block rounded up to 8
+  uint16_t* cache = nullptr;    // [layers][2][Hkv][d * vld]: K [pos][d], V [d][vld]
+  uint16_t* staging = nullptr;  // [max_branches][layers][2][Hkv][d * vlds]
   float* rope = nullptr;        // [max_len][d/2][2]
   float* x = nullptr;           // [mp_max][H]
   uint16_t* abuf = nullptr;     // packed [mp_max][H]
@@ -362,8 +363,10 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   };
   DevBuf b;
   int rc;
-  const size_t cache_e = (size_t)c.layers * 2 * Hkv * max_len * d;
-  const size_t stag_e = (size_t)max_branches * c.layers * 2 * Hkv * max_block * d;
+  kv->vld = round_up(max_len, 8);
+  kv->vlds = round_up(max_block, 8);
+  const size_t cache_e = (size_t)c.layers * 2 * Hkv * d * kv->vld;
+  const size_t stag_e = (size_t)max_branches * c.layers * 2 * Hkv * d * kv->vlds;
   size_t part_b = 16;
   for (int MT = 1; MT <= kv->mp_max / 256; ++MT) {
     const StepPlans p = step_plans(m, MT);
@@ -468,9 +471,9 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   at.Hq = c.heads;
   at.Hkv = c.kv_heads;
   at.d = d;
-  at.max_len = kv->max_len;
+  at.vld = kv->vld;
   at.layers = c.layers;
-  at.Lcap = kv->max_block;
+  at.vlds = kv->vlds;
   at.Mp = Mp;
   at.scale = 1.0f / std::sqrt((float)d);
   const int n_layers = stop_layer >= 0 ? std::min(stop_layer, c.layers) : c.layers;
@@ -486,13 +489,13 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.Hkv = c.kv_heads;
     g.d = d;
     g.L = L;
-    g.Lcap = kv->max_block;
+    g.vlds = kv->vlds;
     g.P = prefix_len;
     { ProfScope ps_(kv, LOPA_PROF_QKV, s);
       HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, H, plan.qkv)); }
     at.layer = l;
-    at.kcache = kv->cache + ((size_t)l * 2 + 0) * c.kv_heads * kv->max_len * d;
-    at.vcache = kv->cache + ((size_t)l * 2 + 1) * c.kv_heads * kv->max_len * d;
+    at.kcache = kv->cache + ((size_t)l * 2 + 0) * c.kv_heads * d * kv->vld;
+    at.vcache = kv->cache + ((size_t)l * 2 + 1) * c.kv_heads * d * kv->vld;
     { ProfScope ps_(kv, LOPA_PROF_ATTN, s);
       HIP_TRY(launch_attention(at, s)); }
     g.x = kv->x;
@@ -589,7 +592,7 @@ int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32
   if ((int64_t)prefix_len + L > kv->max_len) return fail(LOPA_ECAPACITY, "commit beyond max_len");
   const lopa_model_cfg& c = kv->m->cfg;
   HIP_TRY(launch_commit(kv->staging, kv->cache, winner, kv->last_nb, c.layers, c.kv_heads,
-                        kv->max_block, kv->max_len, c.head_dim, prefix_len, L, append_offset,
+                        kv->vlds, kv->vld, c.head_dim, prefix_len, L, append_offset,
                         (hipStream_t)stream));
   return LOPA_OK;
 }
@@ -601,12 +604,10 @@ int lopa_kv_read(const lopa_kv* kv, int32_t layer, int32_t start, int32_t len, v
   if (layer < 0 || layer >= c.layers || start < 0 || len < 1 || (int64_t)start + len > kv->max_len)
     return fail(LOPA_EINVAL, "layer/start/len out of range");
   const int d = c.head_dim, Hkv = c.kv_heads;
-  for (int kvi = 0; kvi < 2; ++kvi) {
-    const uint16_t* src = kv->cache + (((size_t)layer * 2 + kvi) * Hkv * kv->max_len + start) * d;
-    uint16_t* dst = (uint16_t*)(kvi ? v_dst : k_dst);
-    HIP_TRY(launch_kv_copy(src, dst, (int64_t)kv->max_len * d, (int64_t)len * d, Hkv, len * d,
-                           (hipStream_t)stream));
-  }
+  uint16_t* ck = kv->cache + ((size_t)layer * 2 + 0) * Hkv * d * kv->vld;
+  uint16_t* cv = kv->cache + ((size_t)layer * 2 + 1) * Hkv * d * kv->vld;
+  HIP_TRY(launch_kv_rows(ck, cv, (int64_t)d * kv->vld, kv->vld, Hkv, d, start, len,
+                         (uint16_t*)k_dst, (uint16_t*)v_dst, 0, (hipStream_t)stream));
   return LOPA_OK;
 }
 
@@ -617,12 +618,10 @@ int lopa_kv_write(lopa_kv* kv, int32_t layer, int32_t start, int32_t len, const 
   if (layer < 0 || layer >= c.layers || start < 0 || len < 1 || (int64_t)start + len > kv->max_len)
     return fail(LOPA_EINVAL, "layer/start/len out of range");
   const int d = c.head_dim, Hkv = c.kv_heads;
-  for (int kvi = 0; kvi < 2; ++kvi) {
-    uint16_t* dst = kv->cache + (((size_t)layer * 2 + kvi) * Hkv * kv->max_len + start) * d;
-    const uint16_t* src = (const uint16_t*)(kvi ? v_src : k_src);
-    HIP_TRY(launch_kv_copy(src, dst, (int64_t)len * d, (int64_t)kv->max_len * d, Hkv, len * d,
-                           (hipStream_t)stream));
-  }
+  uint16_t* ck = kv->cache + ((size_t)layer * 2 + 0) * Hkv * d * kv->vld;
+  uint16_t* cv = kv->cache + ((size_t)layer * 2 + 1) * Hkv * d * kv->vld;
+  HIP_TRY(launch_kv_rows(ck, cv, (int64_t)d * kv->vld, kv->vld, Hkv, d, start, len,
+                         (uint16_t*)k_src, (uint16_t*)v_src, 1, (hipStream_t)stream));
   return LOPA_OK;
 }
 
@@ -634,13 +633,11 @@ int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer, void*
   if (branch < 0 || branch >= kv->last_nb || layer < 0 || layer >= c.layers)
     return fail(LOPA_EINVAL, "branch/layer out of range");
   const int d = c.head_dim, Hkv = c.kv_heads, L = kv->last_L;
-  for (int kvi = 0; kvi < 2; ++kvi) {
-    const uint16_t* src =
-        kv->staging + ((((size_t)branch * c.layers + layer) * 2 + kvi) * Hkv) * kv->max_block * d;
-    uint16_t* dst = (uint16_t*)(kvi ? v_dst : k_dst);
-    HIP_TRY(launch_kv_copy(src, dst, (int64_t)kv->max_block * d, (int64_t)L * d, Hkv, L * d,
-                           (hipStream_t)stream));
-  }
+  const size_t head = (size_t)d * kv->vlds;
+  uint16_t* sk = kv->staging + (((size_t)branch * c.layers + layer) * 2 + 0) * Hkv * head;
+  uint16_t* sv = kv->staging + (((size_t)branch * c.layers + layer) * 2 + 1) * Hkv * head;
+  HIP_TRY(launch_kv_rows(sk, sv, (int64_t)head, kv->vlds, Hkv, d, 0, L, (uint16_t*)k_dst,
+                         (uint16_t*)v_dst, 0, (hipStream_t)stream));
   return LOPA_OK;
 }
 

@@ -36,7 +36,7 @@ namespace {
 
 constexpr int GEMM_THREADS = 256;
 constexpr int LEAD = 4;         // iterations between issue and use (= activation register sets)
-constexpr int RING = LEAD + 1;  // weight chunks in LDS: in use + LEAD in flight
+constexpr int RING = LEAD + 2;  // weight chunks in LDS: a pair in use + LEAD in flight
 
 template <int EPI, int NB>
 struct GemmSmem {
@@ -44,6 +44,7 @@ struct GemmSmem {
   static constexpr int SWIGLU_SP = NB / 2 * 16 + 8;  // padded staging row (bf16)
   static constexpr int BYTES = RING * CHUNK;
   static_assert(EPI != EPI_SWIGLU || 4 * 64 * SWIGLU_SP * 2 <= RING * CHUNK, "staging fits");
+  static_assert(EPI != EPI_LMHEAD || 4 * 64 * 16 * 12 <= RING * CHUNK, "reduction area fits");
 };
 
 template <int N>
@@ -155,7 +156,10 @@ __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
-        const float h = gt / (1.0f + expf(-gt)) * up;
+        // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
+        // 1 ulp each, far below the bf16 rounding of the result)
+        const float ex = __builtin_amdgcn_exp2f(-gt * 1.4426950408889634f);
+        const float h = gt * __builtin_amdgcn_rcpf(1.0f + ex) * up;
         e[(mb * 16 + g * 4 + j) * SP + p * 16 + c16] = f2bf_bits(h);
       }
   __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wavefront's LDS writes done
@@ -171,11 +175,18 @@ __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[
 }
 
 // per-row (max, argmax, sum exp(l - max)) over this tile's valid columns
-// (column < vocab, column != mask token) -> pm / ps / pi [row][tile]
+// (column < vocab, column != mask token) -> pm / ps / pi [row][tile]. Each lane
+// first reduces its NB columns of each of its 16 rows; the 16 lane partials of
+// a row then meet in LDS (red: this wavefront's 64 x 16 x 3 words) and one lane
+// per row merges them in column order (ties: lowest column).
 template <int NB>
 __device__ __forceinline__ void lm_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
-                                            int row0, int lane) {
+                                            int row0, int lane, float* red) {
+  constexpr float LOG2E = 1.4426950408889634f;
   const int g = lane >> 4, c16 = lane & 15;
+  float* rm = red;
+  float* rs = red + 64 * 16;
+  int* ri = (int*)(red + 2 * 64 * 16);
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -187,93 +198,120 @@ __device__ __forceinline__ void lm_epilogue(const GemmArgs& a, f32x4 (&acc)[4][N
       for (int nb = 0; nb < NB; ++nb) {
         const int col = (tile * NB + nb) * 16 + c16;
         v[nb] = (col < a.vocab && col != a.mask_id) ? acc[mb][nb][j] : -INFINITY;
-        if (v[nb] > m) { m = v[nb]; mi = col; }
-      }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) {
-        const float om = __shfl_xor(m, o);
-        const int oi = __shfl_xor(mi, o);
-        if (om > m || (om == m && oi < mi)) { m = om; mi = oi; }
+        mi = v[nb] > m ? col : mi;  // strict: the lowest column of equal maxima
+        m = fmaxf(m, v[nb]);
       }
       float s = 0.f;
-      if (m != -INFINITY)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) s += expf(v[nb] - m);
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o);
-      const int r = row0 + mb * 16 + g * 4 + j;
-      if (c16 == 0 && r < a.M) {
-        const int64_t o = (int64_t)r * a.tiles + tile;
-        a.pm[o] = m;
-        a.ps[o] = s;
-        a.pi[o] = mi;
-      }
+      for (int nb = 0; nb < NB; ++nb) s += __builtin_amdgcn_exp2f((v[nb] - m) * LOG2E);
+      if (m == -INFINITY) s = 0.f;
+      const int o = (mb * 16 + g * 4 + j) * 16 + c16;
+      rm[o] = m;
+      rs[o] = s;
+      ri[o] = mi;
     }
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wavefront's LDS writes done
+  __builtin_amdgcn_wave_barrier();
+  float M = -INFINITY, S = 0.f;
+  int I = 0x7fffffff;
+#pragma unroll
+  for (int c = 0; c < 16; ++c) {
+    const float mc = rm[lane * 16 + c], sc = rs[lane * 16 + c];
+    const int ic = ri[lane * 16 + c];
+    if (mc > M) {
+      S = S * __builtin_amdgcn_exp2f((M - mc) * LOG2E) + sc;
+      M = mc;
+      I = ic;
+    } else if (mc == M) {
+      S += sc;
+      I = ic < I ? ic : I;
+    } else {
+      S += sc * __builtin_amdgcn_exp2f((mc - M) * LOG2E);
+    }
+  }
+  const int r = row0 + lane;
+  if (r < a.M) {
+    const int64_t o = (int64_t)r * a.tiles + tile;
+    a.pm[o] = M;
+    a.ps[o] = M == -INFINITY ? 0.f : S;
+    a.pi[o] = I;
+  }
 }
 
 // ------------------------------------------------------------------ main loop
-// loads of one iteration (tile jt, k-chunk kct) into register set `set` and
-// ring slot `slot`; weight layout [block][KC][2][64 lanes][8]
-// Loads of one iteration (tile jt, k-chunk kct): 8 activation fragments into
-// register set `set` (two groups of 4, k-halves 0 and 1) and the NB x 2 KiB
-// weight chunk into ring slot `slot` (NB / 2 copies of 1 KiB per wavefront).
-// Weight layout [block][KC][2][64 lanes][8].
-#define GEMM_ISSUE_A(set, half, kct)                                                     \
+// Loads of one iteration: 8 activation fragments into register set `set` (two
+// groups of 4, k-halves 0 and 1) and the NB x 2 KiB weight chunk into ring
+// slot `slot` (NB / 2 copies of 1 KiB per wavefront). Weight layout
+// [block][KC][2][64 lanes][8]: wavefront wv copies k-half wv % 2 of blocks
+// 2 r + wv / 2, r < NB / 2. The addresses advance by one k-chunk per issued
+// iteration (a_next, w_next); past the last k-chunk the last one is issued
+// again (an L2 hit), which keeps every wait count and the loop branch-free.
+#define GEMM_ISSUE_A(set, half)                                                          \
   load_frag4(set[4 * (half) + 0], set[4 * (half) + 1], set[4 * (half) + 2],              \
-             set[4 * (half) + 3], Ab + ((int64_t)(2 * (kct) + (half)) * RB + rb0) * 1024, voff)
-#define GEMM_ISSUE_W(r, jt, kct, slot)                                                   \
-  {                                                                                      \
-    const int u_ = (r) * 4 + wv; /* 1 KiB unit: block u_ / 2, k-half u_ % 2 */           \
-    lds_dma16(Wb + (((int64_t)(jt) * NB + (u_ >> 1)) * KC + (kct)) * 2048 + (u_ & 1) * 1024, \
-              voff, sW_base + (uint32_t)(slot) * (uint32_t)SM::CHUNK + (uint32_t)u_ * 1024u); \
-  }
-#define GEMM_ISSUE(set, jt, kct, slot)                                                   \
-  {                                                                                      \
-    GEMM_ISSUE_A(set, 0, kct);                                                           \
-    GEMM_ISSUE_A(set, 1, kct);                                                           \
-    _Pragma("unroll") for (int r_ = 0; r_ < NB / 2; ++r_) GEMM_ISSUE_W(r_, jt, kct, slot); \
-  }
-
-// next iteration to issue; past the last one the last chunk is issued again
-// (an L2 hit), which keeps every wait count and the loop body branch-free
+             set[4 * (half) + 3], a_next + (half) * a_half, voff)
+#define GEMM_ISSUE_W(r, slot)                                                            \
+  lds_dma16(w_next + (int64_t)(r) * w_rstride, voff,                                     \
+            lds_wave + (uint32_t)(slot) * (uint32_t)SM::CHUNK + (uint32_t)(r) * 4096u)
 #define GEMM_ADVANCE_LOAD()                                                              \
   {                                                                                      \
-    if (++lk == kc_end) {                                                                \
-      if (lt + 1 < t_hi) { lk = kc_beg; ++lt; }                                          \
-      else lk = kc_end - 1;                                                              \
+    if (lk + 1 < kc_end) {                                                               \
+      ++lk;                                                                              \
+      a_next += a_kstep;                                                                 \
+      w_next += 2048;                                                                    \
     }                                                                                    \
   }
-
-// One iteration j. The 2 NB weight fragments of the chunk are read from LDS
-// BPF fragments ahead of the MFMAs that use them; the loads of iteration j + 4
-// are spread over the MFMA stream (activation half h once the MFMAs reading
-// it have issued, the weight copies from the second fragment on). Scheduling
-// barriers keep this order. Every iteration issues exactly OPS operations, so
-// waiting for iteration j is always vmcnt(3 OPS).
-constexpr int BPF = 4;
-#define GEMM_STEP(set)                                                                   \
+#define GEMM_ISSUE(set, slot)                                                            \
   {                                                                                      \
-    wait_vmcnt<3 * OPS>(); /* iteration j landed; j + 1 .. j + 3 may be in flight */     \
+    GEMM_ISSUE_A(set, 0);                                                                \
+    GEMM_ISSUE_A(set, 1);                                                                \
+    _Pragma("unroll") for (int r_ = 0; r_ < NB / 2; ++r_) GEMM_ISSUE_W(r_, slot);        \
+    GEMM_ADVANCE_LOAD();                                                                 \
+  }
+
+// Two iterations j, j + 1 per workgroup barrier. Their 4 NB weight fragments
+// are read from LDS BPF fragments ahead of the MFMAs that use them (across
+// the iteration boundary); the loads of iterations j + 4 and j + 5 are spread
+// over the MFMA stream (an activation half once the MFMAs reading it have
+// issued, the weight copies from the second fragment of each iteration on).
+// Scheduling barriers keep this order. Every iteration issues exactly OPS
+// operations, so "j and j + 1 have landed" is vmcnt(2 OPS); the slots written
+// here held iterations j - 2 and j - 1, which every wavefront finished before
+// this barrier.
+constexpr int BPF = 4;
+#define GEMM_PAIR(s0, s1)                                                                \
+  {                                                                                      \
+    wait_vmcnt<2 * OPS>();                                                               \
     lds_barrier();                                                                       \
-    _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) pin_landed(set[i_]);                \
-    const u32x4* wl_ = (const u32x4*)(smem + cs * SM::CHUNK);                            \
-    const int islot_ = cs == 0 ? RING - 1 : cs - 1; /* slot of iteration j - 1 */        \
-    u32x4 bf_[2 * NB];                                                                   \
+    _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) {                                   \
+      pin_landed(s0[i_]);                                                                \
+      pin_landed(s1[i_]);                                                                \
+    }                                                                                    \
+    const u32x4* wl0_ = (const u32x4*)(smem + cs * SM::CHUNK);                           \
+    const int c1_ = cs + 1 == RING ? 0 : cs + 1;                                         \
+    const u32x4* wl1_ = (const u32x4*)(smem + c1_ * SM::CHUNK);                          \
+    const int is0_ = cs >= 2 ? cs - 2 : cs + RING - 2; /* slot of iteration j - 2 */    \
+    const int is1_ = is0_ + 1 == RING ? 0 : is0_ + 1;                                    \
+    u32x4 bf_[4 * NB];                                                                   \
     _Pragma("unroll") for (int f_ = 0; f_ < BPF; ++f_)                                   \
-      bf_[f_] = wl_[((f_ % NB) * 2 + f_ / NB) * 64 + lane];                              \
+      bf_[f_] = wl0_[((f_ % NB) * 2 + f_ / NB) * 64 + lane];                             \
     __builtin_amdgcn_sched_barrier(0);                                                   \
-    _Pragma("unroll") for (int f_ = 0; f_ < 2 * NB; ++f_) {                              \
-      if (f_ + BPF < 2 * NB)                                                             \
-        bf_[f_ + BPF] = wl_[(((f_ + BPF) % NB) * 2 + (f_ + BPF) / NB) * 64 + lane];      \
+    _Pragma("unroll") for (int f_ = 0; f_ < 4 * NB; ++f_) {                              \
+      const int e_ = f_ / (2 * NB), g_ = f_ % (2 * NB); /* iteration, fragment */        \
+      if (f_ + BPF < 4 * NB) {                                                           \
+        const int fn_ = f_ + BPF, gn_ = fn_ % (2 * NB);                                  \
+        bf_[fn_] = (fn_ < 2 * NB ? wl0_ : wl1_)[((gn_ % NB) * 2 + gn_ / NB) * 64 + lane];  \
+      }                                                                                  \
       _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                                \
-        mfma_acc(acc[mb_][f_ % NB], set[(f_ / NB) * 4 + mb_], bf_[f_]);                  \
-      if (f_ >= 1 && f_ <= NB / 2) GEMM_ISSUE_W(f_ - 1, lt, lk, islot_);                 \
-      if (f_ == NB - 1) GEMM_ISSUE_A(set, 0, lk);                                        \
-      if (f_ == 2 * NB - 1) GEMM_ISSUE_A(set, 1, lk);                                    \
+        mfma_acc(acc[mb_][g_ % NB], (e_ ? s1 : s0)[(g_ / NB) * 4 + mb_], bf_[f_]);       \
+      if (g_ >= 1 && g_ <= NB / 2) GEMM_ISSUE_W(g_ - 1, e_ ? is1_ : is0_);               \
+      if (g_ == NB - 1) GEMM_ISSUE_A((e_ ? s1 : s0), 0);                                 \
+      if (g_ == 2 * NB - 1) {                                                            \
+        GEMM_ISSUE_A((e_ ? s1 : s0), 1);                                                 \
+        GEMM_ADVANCE_LOAD();                                                             \
+      }                                                                                  \
       __builtin_amdgcn_sched_barrier(0);                                                 \
     }                                                                                    \
-    GEMM_ADVANCE_LOAD();                                                                 \
-    cs = (cs == RING - 1) ? 0 : cs + 1;                                                  \
+    cs = cs + 2 >= RING ? cs + 2 - RING : cs + 2;                                        \
   }
 
 template <int EPI, int NB>
@@ -281,6 +319,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   using SM = GemmSmem<EPI, NB>;
   constexpr int OPS = 8 + NB / 2;  // vector memory operations per wavefront per iteration
   static_assert(NB % 2 == 0 && 3 * OPS <= 63, "tile width");
+  static_assert(RING == 6 && LEAD == 4, "pair schedule");
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -296,7 +335,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   const int KC = a.KC, QT = KC >> 2;
   // workgroup c of a row tile: column tile c / S, k-chunks of split c % S
   const int split = c % a.splits;
-  const int t_lo = c / a.splits, t_hi = t_lo + 1;
+  const int t_lo = c / a.splits;
   const int kc_beg = 4 * (split * QT / a.splits);
   const int kc_end = 4 * ((split + 1) * QT / a.splits);
   if (t_lo >= a.tiles || kc_beg >= kc_end) return;
@@ -304,21 +343,24 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   const int RB = a.Mp >> 4;
   const int rb0 = mt * 16 + wv * 4;     // first 16-row block of this wavefront
   const int row0 = mt * 256 + wv * 64;  // first row of this wavefront
-  const char* __restrict__ Ab = (const char*)a.A;  // fragment f at Ab + 1024 f
-  const char* __restrict__ Wb = (const char*)a.W;
   const uint32_t voff = (uint32_t)lane * 16u;
+  // activation fragment (kb, rb) at A + ((kb RB) + rb) KiB: k-chunk kc, half h
+  // of this wavefront's first row block -> a_next + h a_half
+  const int64_t a_half = (int64_t)RB * 1024, a_kstep = 2 * a_half;
+  const char* a_next = (const char*)a.A + ((int64_t)2 * kc_beg * RB + rb0) * 1024;
+  // weight piece (block, kc, half) at W + ((block KC + kc) 2 + half) KiB
+  const int64_t w_rstride = (int64_t)2 * KC * 2048;  // two blocks further
+  const char* w_next = (const char*)a.W +
+                       (((int64_t)t_lo * NB + (wv >> 1)) * KC + kc_beg) * 2048 + (wv & 1) * 1024;
+  const uint32_t lds_wave = sW_base + (uint32_t)wv * 1024u;
+  int lk = kc_beg;  // k-chunk of the next iteration to issue
 
   f32x4 acc[4][NB];
   u32x4 a0[8], a1[8], a2[8], a3[8];
-  int lt = t_lo, lk = kc_beg;  // next iteration to issue
-  GEMM_ISSUE(a0, lt, lk, 0);
-  GEMM_ADVANCE_LOAD();
-  GEMM_ISSUE(a1, lt, lk, 1);
-  GEMM_ADVANCE_LOAD();
-  GEMM_ISSUE(a2, lt, lk, 2);
-  GEMM_ADVANCE_LOAD();
-  GEMM_ISSUE(a3, lt, lk, 3);
-  GEMM_ADVANCE_LOAD();
+  GEMM_ISSUE(a0, 0);
+  GEMM_ISSUE(a1, 1);
+  GEMM_ISSUE(a2, 2);
+  GEMM_ISSUE(a3, 3);
   int cs = 0;  // ring slot of the current iteration
 
   {
@@ -328,15 +370,16 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
       for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     mfma_settle();
     for (int qq = 0; qq < nq; ++qq) {
-      GEMM_STEP(a0);
-      GEMM_STEP(a1);
-      GEMM_STEP(a2);
-      GEMM_STEP(a3);
+      GEMM_PAIR(a0, a1);
+      GEMM_PAIR(a2, a3);
     }
     GEMM_DRAIN();
     mfma_settle();
     if (EPI != EPI_QKV && a.splits == 1) {
-      if constexpr (EPI == EPI_LMHEAD) lm_epilogue<NB>(a, acc, t_lo, row0, lane);
+      if constexpr (EPI == EPI_LMHEAD) {
+        lds_barrier();  // the ring becomes the reduction area (every copy has landed)
+        lm_epilogue<NB>(a, acc, t_lo, row0, lane, (float*)smem + wv * 64 * 16 * 3);
+      }
       if constexpr (EPI == EPI_RESID) resid_epilogue<NB>(a, acc, t_lo, row0, lane);
       if constexpr (EPI == EPI_SWIGLU) {
         // the weight ring becomes the staging area once every copy (including
@@ -423,11 +466,15 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
         qo[dim] = f2bf_bits(o1);
         qo[dim + HD] = f2bf_bits(o2);
       } else {
-        uint16_t* st = a.staging +
-                       (((((int64_t)br * a.layers + a.layer) * 2 + (sect - 1)) * a.Hkv + head) *
-                            a.Lcap + i) * D;
-        st[dim] = f2bf_bits(o1);
-        if (sect == 1) st[dim + HD] = f2bf_bits(o2);
+        // staging head (K or V) of this branch and layer: K [Lcap][D], V [D][vlds]
+        uint16_t* st = a.staging + ((((int64_t)br * a.layers + a.layer) * 2 + (sect - 1)) *
+                                        a.Hkv + head) * D * a.vlds;
+        if (sect == 1) {
+          st[(int64_t)i * D + dim] = f2bf_bits(o1);
+          st[(int64_t)i * D + dim + HD] = f2bf_bits(o2);
+        } else {
+          st[(int64_t)dim * a.vlds + i] = f2bf_bits(o1);
+        }
       }
     }
   }

@@ -12,11 +12,18 @@ hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pr
                          const uint8_t* valid, int nb, int L, int mask_id, float* scores,
                          int32_t* winner, int32_t* nt, float* nc, int32_t* np, int32_t* nu,
                          hipStream_t s);
+// KV layouts. Cache: [layers][2][Hkv][d * vld] (vld = max_len rounded up to
+// 8): K position p, dim e at p * d + e; V (transposed) at e * vld + p.
+// Staging: [branches][layers][2][Hkv][d * vlds], the same with Lcap, vlds.
 hipError_t launch_commit(const uint16_t* staging, uint16_t* cache, const int32_t* winner,
-                         int nb_last, int layers, int Hkv, int Lcap, int max_len, int d, int P,
+                         int nb_last, int layers, int Hkv, int vlds, int vld, int d, int P,
                          int L, int32_t* append_offset, hipStream_t s);
-hipError_t launch_kv_copy(const uint16_t* src, uint16_t* dst, int64_t src_stride,
-                          int64_t dst_stride, int groups, int rows_elems, hipStream_t s);
+// Copy positions of one layer between the cache (or staging) and a caller
+// buffer [Hkv][len][d] for K and V. to_cache: caller -> cache. head_stride:
+// elements between heads of the cache side; ld: its V leading dimension.
+hipError_t launch_kv_rows(uint16_t* cache_k, uint16_t* cache_v, int64_t head_stride, int ld,
+                          int Hkv, int d, int start, int len, uint16_t* buf_k, uint16_t* buf_v,
+                          int to_cache, hipStream_t s);
 
 // ------------------------------------------------------------ weight repack
 // Pack the rows of up to three [rows_i, K] bf16 sources (stacked in order) into
@@ -60,8 +67,9 @@ struct GemmArgs {
   const float* bias;   // [N] or null
   const float* rope;   // [max_pos][d/2][2] (cos, sin)
   uint16_t* q_out;     // [nb][Hq][L][d]
-  uint16_t* staging;   // [nb][layers][2][Hkv][Lcap][d]
-  int layer, layers, Hq, Hkv, d, L, Lcap, P;
+  uint16_t* staging;   // [nb][layers][2][Hkv][d * vlds] (see the KV layouts)
+  int layer, layers, Hq, Hkv, d, L, P;
+  int vlds;            // staging V leading dimension
   // EPI_RESID
   float* x;            // [M][N] fp32 residual stream (row stride N)
   // EPI_SWIGLU
@@ -79,11 +87,11 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
   const uint16_t* q;       // [nb][Hq][L][d] bf16 (post-RoPE)
-  const uint16_t* kcache;  // layer's K cache [Hkv][max_len][d]
-  const uint16_t* vcache;  // layer's V cache
-  const uint16_t* staging; // [nb][layers][2][Hkv][Lcap][d]
+  const uint16_t* kcache;  // layer's K cache, heads d * vld apart, [pos][d]
+  const uint16_t* vcache;  // layer's V cache, heads d * vld apart, [d][vld]
+  const uint16_t* staging; // [nb][layers][2][Hkv][d * vlds]
   uint16_t* out;           // packed activations (Mp rows, Hq*d columns)
-  int nb, L, P, Hq, Hkv, d, max_len, layer, layers, Lcap, Mp;
+  int nb, L, P, Hq, Hkv, d, vld, layer, layers, vlds, Mp;
   float scale;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

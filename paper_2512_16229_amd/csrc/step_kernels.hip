@@ -121,32 +121,51 @@ __global__ __launch_bounds__(256) void select_kernel(
   }
 }
 
-// Copy the winner's staged K/V (all layers) to cache rows [P, P+L).
-// grid = layers * 2 * Hkv; staging layout [nb][layers][2][Hkv][Lcap][d],
-// cache layout [layers][2][Hkv][max_len][d] (both bf16).
+// Copy the winner's staged K/V of every (layer, K/V, head) into cache
+// positions [P, P + L). grid = layers * 2 * Hkv; the layouts are the KV
+// layouts of kernels.h (V transposed, leading dimensions vlds / vld).
 __global__ __launch_bounds__(256) void commit_kernel(
     const uint16_t* __restrict__ staging, uint16_t* __restrict__ cache,
-    const int32_t* __restrict__ winner, int nb_last, int layers, int Hkv, int Lcap,
-    int max_len, int d, int P, int L, int32_t* __restrict__ append_offset) {
+    const int32_t* __restrict__ winner, int nb_last, int layers, int Hkv, int vlds, int vld,
+    int d, int P, int L, int32_t* __restrict__ append_offset) {
   const int w = winner[0];
   const bool ok = (w >= 0 && w < nb_last);
   if (blockIdx.x == 0 && threadIdx.x == 0) append_offset[0] = ok ? P : -1;
   if (!ok) return;
   const int lhg = blockIdx.x;  // (layer, kv, head) flattened
-  const uint4* src = (const uint4*)(staging + (((int64_t)w * layers * 2 * Hkv + lhg) * Lcap) * d);
-  uint4* dst = (uint4*)(cache + ((int64_t)lhg * max_len + P) * d);
-  const int n = L * d / 8;
-  for (int e = threadIdx.x; e < n; e += blockDim.x) dst[e] = src[e];
+  const bool is_v = (lhg / Hkv) & 1;
+  const uint16_t* src = staging + ((int64_t)w * layers * 2 * Hkv + lhg) * d * vlds;
+  uint16_t* dst = cache + (int64_t)lhg * d * vld;
+  if (!is_v) {
+    const uint4* s4 = (const uint4*)src;
+    uint4* d4 = (uint4*)(dst + (int64_t)P * d);
+    for (int e = threadIdx.x; e < L * d / 8; e += blockDim.x) d4[e] = s4[e];
+  } else {
+    for (int e = threadIdx.x; e < L * d; e += blockDim.x) {
+      const int dim = e / L, i = e % L;
+      dst[(int64_t)dim * vld + P + i] = src[(int64_t)dim * vlds + i];
+    }
+  }
 }
 
-// Row copies between the cache and a caller buffer [Hkv][len][d] for one layer.
-__global__ __launch_bounds__(256) void kv_copy_kernel(const uint16_t* __restrict__ src,
-                                                      uint16_t* __restrict__ dst, int64_t src_stride,
-                                                      int64_t dst_stride, int rows_elems) {
-  const int g = blockIdx.x;
-  const uint16_t* s = src + g * src_stride;
-  uint16_t* t = dst + g * dst_stride;
-  for (int e = threadIdx.x; e < rows_elems; e += blockDim.x) t[e] = s[e];
+// Positions [start, start + len) of one layer's K and V between the cache
+// side (heads head_stride apart; K [pos][d], V [d][ld]) and a caller buffer
+// [Hkv][len][d]. One workgroup per (head, K/V).
+__global__ __launch_bounds__(256) void kv_rows_kernel(uint16_t* __restrict__ ck,
+                                                      uint16_t* __restrict__ cv,
+                                                      int64_t head_stride, int ld, int d,
+                                                      int start, int len,
+                                                      uint16_t* __restrict__ bk,
+                                                      uint16_t* __restrict__ bv, int to_cache) {
+  const int head = blockIdx.x >> 1, is_v = blockIdx.x & 1;
+  uint16_t* c = (is_v ? cv : ck) + (int64_t)head * head_stride;
+  uint16_t* b = (is_v ? bv : bk) + (int64_t)head * len * d;
+  for (int e = threadIdx.x; e < len * d; e += blockDim.x) {
+    const int i = e / d, dim = e % d;  // buffer element (i, dim)
+    const int64_t co = is_v ? (int64_t)dim * ld + start + i : (int64_t)(start + i) * d + dim;
+    if (to_cache) c[co] = b[e];
+    else b[e] = c[co];
+  }
 }
 
 // ------------------------------------------------------------ launchers
@@ -169,16 +188,17 @@ hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pr
 }
 
 hipError_t launch_commit(const uint16_t* staging, uint16_t* cache, const int32_t* winner,
-                         int nb_last, int layers, int Hkv, int Lcap, int max_len, int d, int P,
+                         int nb_last, int layers, int Hkv, int vlds, int vld, int d, int P,
                          int L, int32_t* append_offset, hipStream_t s) {
   hipLaunchKernelGGL(commit_kernel, dim3(layers * 2 * Hkv), dim3(256), 0, s, staging, cache,
-                     winner, nb_last, layers, Hkv, Lcap, max_len, d, P, L, append_offset);
+                     winner, nb_last, layers, Hkv, vlds, vld, d, P, L, append_offset);
   return hipGetLastError();
 }
 
-hipError_t launch_kv_copy(const uint16_t* src, uint16_t* dst, int64_t src_stride,
-                          int64_t dst_stride, int groups, int rows_elems, hipStream_t s) {
-  hipLaunchKernelGGL(kv_copy_kernel, dim3(groups), dim3(256), 0, s, src, dst, src_stride,
-                     dst_stride, rows_elems);
+hipError_t launch_kv_rows(uint16_t* cache_k, uint16_t* cache_v, int64_t head_stride, int ld,
+                          int Hkv, int d, int start, int len, uint16_t* buf_k, uint16_t* buf_v,
+                          int to_cache, hipStream_t s) {
+  hipLaunchKernelGGL(kv_rows_kernel, dim3(2 * Hkv), dim3(256), 0, s, cache_k, cache_v,
+                     head_stride, ld, d, start, len, buf_k, buf_v, to_cache);
   return hipGetLastError();
 }
