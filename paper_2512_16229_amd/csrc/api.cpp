@@ -72,8 +72,8 @@ int round_up(int x, int m) { return m * ((x + m - 1) / m); }
 // and k-splits S. SwiGLU and LM-head tiles are fixed (their epilogues need
 // whole rows of a tile and no split); for the others the pair minimising an
 // estimate of HBM time is taken: rounds of workgroups x bytes of the largest
-// split, plus the fp32 partial sums written and read back and the fix-up
-// launch when partial sums exist.
+// split, plus the fp32 partial sums written and read back (and, for QKV, the
+// fix-up launch).
 struct GemmPlan {
   int nb, tiles, splits;
 };
@@ -91,7 +91,9 @@ GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu) {
       const int64_t rounds = (wgs + num_cu - 1) / num_cu;
       const double split_bytes = (double)((Q + S - 1) / S) * 4 * nb * 2048;
       double cost = (double)rounds * split_bytes * per_round;
-      if (epi == EPI_QKV || S > 1) cost += 2.0 * wgs * nb * 16384 + 14e6;
+      // partial sums written and read back; QKV also pays its fix-up launch
+      if (epi == EPI_QKV || S > 1) cost += 2.0 * wgs * nb * 16384;
+      if (epi == EPI_QKV) cost += 14e6;
       if (cost < best_cost) {
         best_cost = cost;
         best = {nb, tiles, S};
@@ -100,9 +102,11 @@ GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu) {
   }
   return best;
 }
-// bytes of fp32 partial sums the plan writes (QKV always goes through them)
+// bytes of fp32 partial sums the plan writes (QKV always goes through them;
+// the residual projections store [splits][Mp][N] row-major)
 size_t plan_partial_bytes(int epi, const GemmPlan& p, int MT) {
-  return (epi == EPI_QKV || p.splits > 1) ? (size_t)MT * p.tiles * p.splits * p.nb * 16384 : 0;
+  if (epi == EPI_QKV) return (size_t)MT * p.tiles * p.splits * p.nb * 16384;
+  return p.splits > 1 ? (size_t)p.splits * MT * 256 * p.tiles * p.nb * 16 * 4 : 0;
 }
 
 }  // namespace
@@ -502,7 +506,8 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     { ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
       HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, c.heads * d, plan.o)); }
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-      HIP_TRY(launch_rmsnorm_pack(kv->x, p.ln2, c.rms_eps, M, Mp, H, kv->abuf, s)); }
+      HIP_TRY(launch_resnorm(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
+                             c.rms_eps, M, Mp, H, kv->x, kv->abuf, s)); }
     g.a_out = kv->fbuf;
     { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
       HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, H, plan.gu)); }
@@ -510,7 +515,8 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
       HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, round256(F), plan.down)); }
     const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-      HIP_TRY(launch_rmsnorm_pack(kv->x, next_w, c.rms_eps, M, Mp, H, kv->abuf, s)); }
+      HIP_TRY(launch_resnorm(kv->partials, plan.down.splits > 1 ? plan.down.splits : 0, next_w,
+                             c.rms_eps, M, Mp, H, kv->x, kv->abuf, s)); }
   }
   if (stop_layer >= 0) {
     HIP_TRY(hipMemcpyAsync(x_out, kv->x, (size_t)M * H * 4, hipMemcpyDeviceToDevice, s));

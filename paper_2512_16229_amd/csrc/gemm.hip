@@ -15,18 +15,21 @@
 // [s Q / S, (s + 1) Q / S). The tile width NB and the split count S are chosen
 // per GEMM on the host:
 //   S == 1  whole K in one workgroup, epilogue in place (no partial sums);
-//   S  > 1  fp32 partial sums; gemm_fixup_kernel adds the S partials of each
-//           element in split order (deterministic) and runs the epilogue.
+//   S  > 1  fp32 partial sums, added in split order (deterministic): for the
+//           residual projections by the RMSNorm kernel that follows them, for
+//           QKV by gemm_fixup_kernel, which also runs the QKV epilogue (QKV
+//           always takes this path).
 //
 // Pipeline. One iteration is a 64-wide k-chunk of one tile. Its NB x 2 KiB of
 // weights go global -> LDS directly (global_load_lds, no registers) into a
-// 5-slot ring, and each wavefront's 8 activation fragments (L2-resident) into
+// 6-slot ring, and each wavefront's 8 activation fragments (L2-resident) into
 // one of 4 register sets; both are issued 4 iterations ahead. K is padded to a
 // multiple of 256, so a tile always spans a multiple of 4 iterations and the
 // register set of iteration j is the static j % 4: the loop is unrolled by 4
 // and no register set is ever rotated. Vector memory operations complete in
-// issue order, so "iteration j has landed" is one vmcnt wait on the number of
-// operations issued after it.
+// issue order, so "iterations j, j + 1 have landed" is one vmcnt wait on the
+// number of operations issued after them; one workgroup barrier per pair of
+// iterations.
 #include "common.h"
 #include "kernels.h"
 
@@ -388,6 +391,21 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
         uint16_t* stage = (uint16_t*)smem + wv * 64 * SM::SWIGLU_SP;
         swiglu_epilogue<NB>(a, acc, t_lo, row0, lane, stage);
       }
+    } else if constexpr (EPI == EPI_RESID) {
+      // row-major partial sums [split][Mp][N], added by the following RMSNorm
+      const int g = lane >> 4, c16 = lane & 15;
+      float* part = a.partials + (int64_t)split * a.Mp * a.N;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float* pr = part + (int64_t)(row0 + mb * 16 + g * 4 + j) * a.N;
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) {
+            const int n = (t_lo * NB + nb) * 16 + c16;
+            if (n < a.N) pr[n] = acc[mb][nb][j];
+          }
+        }
     } else {
       const int64_t slot = ((int64_t)mt * a.tiles + t_lo) * a.splits + split;
       f32x4* part = (f32x4*)a.partials + (slot * 4 + wv) * 4 * NB * 64;
@@ -400,8 +418,8 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   wait_vmcnt<0>();  // nothing may still be writing LDS when the workgroup ends
 }
 
-// Sum the S partials of one f32x4 of the output (4 rows, 1 column) in split
-// order and run the epilogue. One thread per (row tile, column tile, wave,
+// QKV: sum the S partials of one f32x4 of the output (4 rows, 1 column) in
+// split order and run the epilogue. One thread per (row tile, column tile, wave,
 // 16-row block, 16-column block, lane): the same indexing as gemm_kernel's
 // partial store, so each warp-wide load is 1 KiB contiguous.
 template <int EPI, int NB>
@@ -431,12 +449,7 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
     for (int s = 1; s < a.splits; ++s) v += p[s * sstride];
     return v;
   };
-  if constexpr (EPI == EPI_RESID) {
-    const f32x4 v = sum(tile, nb);
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (r0 + j < a.M) a.x[(int64_t)(r0 + j) * a.N + n] += v[j];
-  } else if constexpr (EPI == EPI_QKV) {
+  {
     const int D = a.d, HD = D >> 1;
     const int qcols = a.Hq * D, kcols = a.Hkv * D;
     const int sect = n < qcols ? 0 : (n < qcols + kcols ? 1 : 2);
@@ -486,13 +499,11 @@ hipError_t launch_nb(const GemmArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((gemm_kernel<EPI, NB>), dim3(grid), dim3(GEMM_THREADS), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if constexpr (EPI == EPI_QKV || EPI == EPI_RESID) {
-    if (EPI == EPI_QKV || a.splits > 1) {
-      const int64_t threads = (int64_t)a.mtiles * a.tiles * 4 * 4 * NB * 64;
-      hipLaunchKernelGGL((gemm_fixup_kernel<EPI, NB>), dim3((unsigned)((threads + 255) / 256)),
-                         dim3(256), 0, s, a);
-      e = hipGetLastError();
-    }
+  if constexpr (EPI == EPI_QKV) {
+    const int64_t threads = (int64_t)a.mtiles * a.tiles * 4 * 4 * NB * 64;
+    hipLaunchKernelGGL((gemm_fixup_kernel<EPI, NB>), dim3((unsigned)((threads + 255) / 256)),
+                       dim3(256), 0, s, a);
+    e = hipGetLastError();
   }
   return e;
 }

@@ -43,9 +43,10 @@ hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_
 hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int vocab,
                              const float* w, float eps, int M, int Mp, int H, float* x,
                              uint16_t* a, hipStream_t s);
-// a[r] = pack(rmsnorm(x[r]) * w) for r < M.
-hipError_t launch_rmsnorm_pack(const float* x, const float* w, float eps, int M, int Mp, int H,
-                               uint16_t* a, hipStream_t s);
+// x[r] += sum over s < S of part[s][r] (row-major [S][Mp][H]; S = 0: none),
+// then a[r] = pack(rmsnorm(x[r]) * w), for r < M. H % 256 == 0.
+hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, int M, int Mp,
+                          int H, float* x, uint16_t* a, hipStream_t s);
 // merge per-tile softmax partials into conf / pred
 hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, int M,
                            int tiles, float* conf, int32_t* pred, hipStream_t s);
@@ -62,7 +63,9 @@ struct GemmArgs {
   int splits;          // k-splits per tile; > 1: partial sums + fix-up kernel
   int mtiles;          // row tiles of 256 rows; Mp = 256 * mtiles
   int gcols;           // workgroups per row tile (tiles * splits when splits > 1)
-  float* partials;     // [mtiles][tiles][splits][4 waves][4][nb][64][4] fp32
+  float* partials;     // EPI_QKV: [mtiles][tiles][splits][4 waves][4][nb][64][4] fp32;
+                       // EPI_RESID (splits > 1): row-major [splits][Mp][N] fp32, added by
+                       // the following launch_resnorm (no fix-up kernel)
   // EPI_QKV
   const float* bias;   // [N] or null
   const float* rope;   // [max_pos][d/2][2] (cos, sin)

@@ -7,59 +7,93 @@
 
 #include <math.h>
 
-// Block-wide sum in a fixed order (wave butterfly, then waves in index order).
-__device__ __forceinline__ float block_sum256(float v, float* red) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  if (lane == 0) red[wv] = v;
-  __syncthreads();
-  float t = red[0] + red[1] + red[2] + red[3];
-  __syncthreads();
-  return t;
-}
-
-// One workgroup per row. H % 128 == 0, so H/8 groups of 8 columns.
-template <bool EMBED>
-__global__ __launch_bounds__(256) void norm_kernel(const int32_t* __restrict__ tokens,
-                                                   const uint16_t* __restrict__ embed, int vocab,
-                                                   const float* __restrict__ w, float eps, int Mp,
-                                                   int H, float* __restrict__ x,
-                                                   uint16_t* __restrict__ a) {
+// One workgroup (256 threads) per row; thread t holds the 4-column groups
+// q = t + 256 i (columns 4 q .. 4 q + 3, q < H / 4, H % 256 == 0, H <= 1024 CPT).
+// The row is formed in registers:
+//   EMBED:  x = embedding of the token (bf16 -> fp32)
+//   else:   x += sum of the S split-K partial sums of the preceding projection
+//           (row-major fp32 [S][Mp][H], summed in split order first)
+// then x is stored back and a = pack(x / rms(x) * w) (RMSNorm; the sum of
+// squares is reduced in a fixed order: lanes, then wavefronts 0..3). Groups
+// past the row read the row's last group again and are discarded by a
+// select: no load sits under a branch, so all of them can be in flight
+// together.
+constexpr int CPT = 8;  // 4-column groups per thread at most
+template <bool EMBED, int SC>
+__global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict__ tokens,
+                                                      const uint16_t* __restrict__ embed,
+                                                      int vocab, const float* __restrict__ part,
+                                                      int S, const float* __restrict__ w,
+                                                      float eps, int M, int Mp, int H,
+                                                      float* __restrict__ x,
+                                                      uint16_t* __restrict__ a) {
   __shared__ float red[4];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int r = blockIdx.x;
+  const int nq = H >> 2;
   float* xr = x + (int64_t)r * H;
-  const int groups = H >> 3;
+  float4 v[CPT];
   float ss = 0.f;
   if (EMBED) {
     // a token outside [0, vocab) reads row 0 instead of memory past the table
     int tok = tokens[r];
     tok = (tok >= 0 && tok < vocab) ? tok : 0;
     const uint16_t* er = embed + (int64_t)tok * H;
-    for (int gi = threadIdx.x; gi < groups; gi += 256) {
-      uint4 raw = *(const uint4*)(er + gi * 8);
-      const uint16_t* h = (const uint16_t*)&raw;
-      float v[8];
-      for (int e = 0; e < 8; ++e) {
-        v[e] = bf2f_bits(h[e]);
-        ss += v[e] * v[e];
-      }
-      *(float4*)(xr + gi * 8) = make_float4(v[0], v[1], v[2], v[3]);
-      *(float4*)(xr + gi * 8 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int q = tid + 256 * i;
+      const bool ok = q < nq;
+      const uint2 raw = *(const uint2*)(er + (ok ? q : nq - 1) * 4);
+      v[i] = make_float4(ok ? bf2f_bits(raw.x & 0xffff) : 0.f, ok ? bf2f_bits(raw.x >> 16) : 0.f,
+                         ok ? bf2f_bits(raw.y & 0xffff) : 0.f, ok ? bf2f_bits(raw.y >> 16) : 0.f);
     }
   } else {
-    for (int gi = threadIdx.x; gi < groups; gi += 256) {
-      float4 p = *(const float4*)(xr + gi * 8), q = *(const float4*)(xr + gi * 8 + 4);
-      ss += p.x * p.x + p.y * p.y + p.z * p.z + p.w * p.w + q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+    // partial sums in split order, then the residual. SC >= 0: the split count
+    // is a compile-time constant; SC < 0: S, known at run time.
+    float4 t[CPT];
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) t[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    const int ns = SC >= 0 ? SC : S;
+    for (int sp = 0; sp < ns; ++sp) {
+      const float4* pr = (const float4*)(part + ((int64_t)sp * Mp + r) * H);
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int q = tid + 256 * i;
+        const float4 u = pr[q < nq ? q : nq - 1];
+        t[i].x += u.x; t[i].y += u.y; t[i].z += u.z; t[i].w += u.w;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int q = tid + 256 * i;
+      const bool ok = q < nq;
+      const float4 u = ((const float4*)xr)[ok ? q : nq - 1];
+      v[i] = make_float4(ok ? u.x + t[i].x : 0.f, ok ? u.y + t[i].y : 0.f,
+                         ok ? u.z + t[i].z : 0.f, ok ? u.w + t[i].w : 0.f);
     }
   }
-  const float tot = block_sum256(ss, red);
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int q = tid + 256 * i;
+    if (q < nq && (EMBED || (SC >= 0 ? SC : S) > 0)) ((float4*)xr)[q] = v[i];
+    ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+  }
+  ss = wave_sum(ss);
+  if (lane == 0) red[wv] = ss;
+  __syncthreads();
+  const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
-  for (int gi = threadIdx.x; gi < groups; gi += 256) {
-    float4 p = *(const float4*)(xr + gi * 8), q = *(const float4*)(xr + gi * 8 + 4);
-    float v[8] = {p.x, p.y, p.z, p.w, q.x, q.y, q.z, q.w};
-    uint16_t o[8];
-    for (int e = 0; e < 8; ++e) o[e] = f2bf_bits(v[e] * inv * w[gi * 8 + e]);
-    *(uint4*)(a + packA_off(r, gi * 8, Mp)) = *(const uint4*)o;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int q = tid + 256 * i;
+    if (q < nq) {
+      const float4 wt = ((const float4*)w)[q];
+      const uint32_t lo = (uint32_t)f2bf_bits(v[i].x * inv * wt.x) |
+                          ((uint32_t)f2bf_bits(v[i].y * inv * wt.y) << 16);
+      const uint32_t hi = (uint32_t)f2bf_bits(v[i].z * inv * wt.z) |
+                          ((uint32_t)f2bf_bits(v[i].w * inv * wt.w) << 16);
+      *(uint2*)(a + packA_off(r, q * 4, Mp)) = make_uint2(lo, hi);
+    }
   }
 }
 
@@ -149,15 +183,30 @@ __global__ void bf16_to_f32_kernel(const uint16_t* __restrict__ s, float* __rest
 hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int vocab,
                              const float* w, float eps, int M, int Mp, int H, float* x,
                              uint16_t* a, hipStream_t s) {
-  hipLaunchKernelGGL(norm_kernel<true>, dim3(M), dim3(256), 0, s, tokens, embed, vocab, w, eps, Mp,
-                     H, x, a);
+  if (H % 256 || H > 1024 * CPT) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((resnorm_kernel<true, 0>), dim3(M), dim3(256), 0, s, tokens, embed,
+                     vocab, nullptr, 0, w, eps, M, Mp, H, x, a);
   return hipGetLastError();
 }
 
-hipError_t launch_rmsnorm_pack(const float* x, const float* w, float eps, int M, int Mp, int H,
-                               uint16_t* a, hipStream_t s) {
-  hipLaunchKernelGGL(norm_kernel<false>, dim3(M), dim3(256), 0, s, nullptr, nullptr, 0, w, eps,
-                     Mp, H, const_cast<float*>(x), a);
+hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, int M, int Mp,
+                          int H, float* x, uint16_t* a, hipStream_t s) {
+  if (H % 256 || H > 1024 * CPT || S < 0) return hipErrorInvalidValue;
+#define RESNORM(SC)                                                                         \
+  hipLaunchKernelGGL((resnorm_kernel<false, SC>), dim3(M), dim3(256), 0, s, nullptr, nullptr, \
+                     0, part, S, w, eps, M, Mp, H, x, a)
+  switch (S) {
+    case 0: RESNORM(0); break;
+    case 2: RESNORM(2); break;
+    case 3: RESNORM(3); break;
+    case 4: RESNORM(4); break;
+    case 5: RESNORM(5); break;
+    case 6: RESNORM(6); break;
+    case 7: RESNORM(7); break;
+    case 8: RESNORM(8); break;
+    default: RESNORM(-1); break;
+  }
+#undef RESNORM
   return hipGetLastError();
 }
 
