@@ -55,10 +55,122 @@ def gateup_launch_bytes(cfg, M):
     return 2 * F * H * 2 + M * H * 2 + M * F * 2
 
 
-def cpu_baseline(cfg_full, weights_dev, P, L, k, layers_sample=4):
+def gemm_source_sha():
+    """Short hash of the GEMM kernel source (the measured HBM traffic is only
+    valid for the source it was taken on)."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm.hip", "common.h"):
+        with open(os.path.join(ROOT, "paper_2512_16229_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(path):
+    """HBM bytes per gate/up launch from the rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary in profiles/ (copy-kernel calibrated), or None when the summary is
+    missing or was taken on another GEMM source."""
+    try:
+        txt = open(path).read()
+    except OSError:
+        return None
+    vals = dict(l.split(":", 1) for l in txt.splitlines() if l.startswith(("sha:", "traffic_bytes:")))
+    if vals.get("sha", "").strip() != gemm_source_sha():
+        return None
+    try:
+        return int(float(vals["traffic_bytes"]))
+    except (KeyError, ValueError):
+        return None
+
+
+class _Hip:
+    """The few HIP runtime calls the torch-free counter runs need."""
+
+    def __init__(self):
+        import ctypes as C
+        self.C = C
+        self.rt = C.CDLL("libamdhip64.so")
+        for name, args in (("hipMalloc", [C.POINTER(C.c_void_p), C.c_size_t]),
+                           ("hipFree", [C.c_void_p]),
+                           ("hipMemsetD16", [C.c_void_p, C.c_ushort, C.c_size_t]),
+                           ("hipMemset", [C.c_void_p, C.c_int, C.c_size_t]),
+                           ("hipMemcpy", [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int]),
+                           ("hipDeviceSynchronize", [])):
+            getattr(self.rt, name).argtypes = args
+            getattr(self.rt, name).restype = C.c_int
+
+    def check(self, rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} failed with hipError {rc}")
+
+    def alloc(self, nbytes, fill16=None):
+        p = self.C.c_void_p()
+        self.check(self.rt.hipMalloc(self.C.byref(p), nbytes), "hipMalloc")
+        if fill16 is not None:
+            self.check(self.rt.hipMemsetD16(p, fill16, nbytes // 2), "hipMemsetD16")
+        else:
+            self.check(self.rt.hipMemset(p, 0, nbytes), "hipMemset")
+        return p
+
+
+def copy_calibration(nbytes=1 << 30, reps=5):
+    """A plain device-to-device copy of known size (the runtime's copy kernel),
+    for scaling the HBM counters. Torch-free, like hbm_counter_run."""
+    hip = _Hip()
+    src, dst = hip.alloc(nbytes, fill16=0x3F80), hip.alloc(nbytes)
+    for _ in range(reps):
+        hip.check(hip.rt.hipMemcpy(dst, src, nbytes, 3), "hipMemcpy")  # device to device
+    hip.check(hip.rt.hipDeviceSynchronize(), "hipDeviceSynchronize")
+    print(json.dumps({"copy_bytes": nbytes, "reps": reps}))
+
+
+def hbm_counter_run(cfg, P, L, k, reps=3):
+    """Torch-free verify forwards on the given shape for the HBM counter runs
+    (rocprofv3 --pmc): weights are constant fills, which changes no traffic."""
+    import ctypes as C
+    import importlib.util
+    spec = importlib.util.spec_from_file_location(
+        "lopa_abi", os.path.join(ROOT, "paper_2512_16229_amd", "_abi.py"))
+    abi = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(abi)
+    hip = _Hip()
+    H, F, V, d = cfg["hidden"], cfg["ffn"], cfg["vocab"], cfg["head_dim"]
+    Hq, Hkv = cfg["heads"], cfg["kv_heads"]
+    W = lambda n, v=0x3C00: hip.alloc(2 * n, fill16=v)  # bf16 0.0078 (norm weights 1.0)
+    layers = (abi.lopa_layer_weights * cfg["layers"])()
+    for i in range(cfg["layers"]):
+        b = (lambda n: W(n)) if cfg["qkv_bias"] else (lambda n: None)
+        layers[i] = abi.lopa_layer_weights(
+            W(Hq * d * H), W(Hkv * d * H), W(Hkv * d * H), b(Hq * d), b(Hkv * d), b(Hkv * d),
+            W(H * Hq * d), W(F * H), W(F * H), W(H * F), W(H, 0x3F80), W(H, 0x3F80))
+    wp = abi.lopa_weight_ptrs(W(V * H), layers, W(H, 0x3F80), W(V * H))
+    c = abi.lopa_model_cfg(cfg["layers"], H, Hq, Hkv, d, F, V, cfg["mask_id"], cfg["rms_eps"],
+                           cfg["rope_theta"], 1 if cfg["qkv_bias"] else 0)
+    lib = abi.lib
+
+    def ok(rc):
+        if rc != 0:
+            raise RuntimeError(lib.lopa_last_error().decode())
+
+    model, kv = C.c_void_p(), C.c_void_p()
+    ok(lib.lopa_model_create(C.byref(c), C.byref(wp), None, C.byref(model)))
+    nb = k + 1
+    ok(lib.lopa_kv_create(model, P + L, nb, L, C.byref(kv)))
+    tokens = hip.alloc(4 * nb * L)  # token 0 everywhere
+    conf, pred = hip.alloc(4 * nb * L), hip.alloc(4 * nb * L)
+    for _ in range(reps):
+        ok(lib.lopa_verify_forward(model, kv, P, tokens, nb, L, conf, pred, None))
+    hip.check(hip.rt.hipDeviceSynchronize(), "hipDeviceSynchronize")
+    lib.lopa_kv_destroy(kv)
+    lib.lopa_model_destroy(model)
+    print(json.dumps({"verify_forwards": reps, "rows": nb * L, "prefix": P}))
+
+
+def cpu_baseline(cfg_full, weights_dev, P, L, k, layers_sample=4, min_seconds=10.0, max_reps=8):
     """Time the oracle (float64 numpy) on a bounded sample of the same step:
     `layers_sample` decoder layers of the full shape + the LM head and softmax for
-    all (k+1)*L rows, against a random prefix cache; scaled to all layers."""
+    all (k+1)*L rows, against a random prefix cache; the layer pass is repeated
+    until about `min_seconds` of CPU work, and the mean is scaled to all layers."""
     import numpy as np
     import torch
 
@@ -83,10 +195,14 @@ def cpu_baseline(cfg_full, weights_dev, P, L, k, layers_sample=4):
     tokens[:, ::2] = cfg["mask_id"]
     threads = len(os.sched_getaffinity(0))
     torch.set_num_threads(threads)
-    # layers
-    t0 = time.perf_counter()
-    out = model.forward_block(tokens, P, cache, n_layers=layers_sample)
-    t_layers = time.perf_counter() - t0
+    # layers (repeated for a stable mean)
+    t_all, reps = 0.0, 0
+    while reps < max_reps and (reps == 0 or t_all < min_seconds):
+        t0 = time.perf_counter()
+        out = model.forward_block(tokens, P, cache, n_layers=layers_sample)
+        t_all += time.perf_counter() - t0
+        reps += 1
+    t_layers = t_all / reps
     # LM head + softmax for every row (final norm included)
     from oracle.model import confidence, rms_norm
     t0 = time.perf_counter()
@@ -98,7 +214,7 @@ def cpu_baseline(cfg_full, weights_dev, P, L, k, layers_sample=4):
             "kind": "oracle",
             "sample": (f"float64 numpy oracle, {layers_sample} of {cfg_full['layers']} decoder layers "
                        f"+ LM head/softmax of the Dream-7B shape at {nb}x{L} rows, prefix {P}; "
-                       f"measured {t_layers:.2f}s layers + {t_head:.2f}s head, scaled to "
+                       f"mean of {reps} runs {t_layers:.2f}s layers + {t_head:.2f}s head, scaled to "
                        f"{step_s:.1f}s per step")}
 
 
@@ -114,11 +230,28 @@ def main():
     ap.add_argument("--tau", type=float, default=0.9)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy 5 times (HBM counter calibration)")
+    ap.add_argument("--hbm-counters", action="store_true",
+                    help="only run 3 torch-free verify forwards (for rocprofv3 --pmc)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
               "(multi-GPU branch parallelism is a design note, not built)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    if args.hbm_counters:
+        # the shape table of the synthetic generator, read without importing torch
+        import importlib.util
+        spec = importlib.util.spec_from_file_location("synth_shapes",
+                                                      os.path.join(ROOT, "synth", "shapes.py"))
+        shapes = importlib.util.module_from_spec(spec)
+        spec.loader.exec_module(shapes)
+        hbm_counter_run(shapes.config(args.config), args.prefix, args.block, args.k)
+        return
 
     import torch
 
@@ -182,18 +315,24 @@ def main():
     ms = ev0.elapsed_time(ev1) / args.steps
     log(f"{args.steps} steps: {ms:.3f} ms/step (events), {wall / args.steps * 1e3:.3f} ms/step (wall)")
 
-    # per-kind launch times with HIP events on the library's stream
+    # launch times with HIP events on the library's stream: first the gate/up
+    # launches alone (the roofline kernel; one event pair per launch), then
+    # every kind for the per-step breakdown
+    kv.profile(("gateup",))
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t, n = kv.profile_read()["gateup"]
+    gu_ms = t / n
     kv.profile(lp.PROF_KINDS)
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     prof = kv.profile_read()
     kv.profile(())
-    kernel_ms = {kd: (t / n if n else 0.0) for kd, (t, n) in prof.items()}
     per_step_ms = {kd: t / args.steps for kd, (t, n) in prof.items()}
     log("per-step ms by kind: " + ", ".join(f"{kd} {v:.3f}" for kd, v in per_step_ms.items()))
 
-    gu_ms = kernel_ms["gateup"]
     gu_bytes = gateup_launch_bytes(cfg, M)
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
     sb = step_bytes(cfg, P, L, nb)
@@ -213,7 +352,9 @@ def main():
                    "prefix": P, "block": L, "k": k, "rows": M},
         "roofline": {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (gemm_kernel<EPI_SWIGLU>)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic(os.path.join(ROOT, "profiles",
+                                                              "gemm_swiglu_dream7b_hbm_traffic.md")),
                      "bytes_per_launch": gu_bytes, "avg_launch_ms": round(gu_ms, 4)},
         "step_roofline": {"hbm_bytes": sb, "flops": sf,
                           "hbm_frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

@@ -5,7 +5,7 @@ TEST INFRASTRUCTURE ONLY (see oracle/__init__.py). Plain numpy / Python loops.
 State of one active block: tokens [L] (a position is unfilled iff it holds
 mask_id), conf [L] and pred [L] from the forward pass on exactly these tokens.
 
-Readings of points the paper leaves open (each also listed in the design doc):
+Readings of points the paper leaves open:
   * Conf / candidate: greedy token and its probability (model.py).
   * Eq. 1 compares strictly (conf > tau); every argmax picks the lowest index
     among equal values.

@@ -23,7 +23,7 @@ def faithful_bound(bf16_own_error: float) -> float:
     different order (fp32 vs fp64 sums; a running vs a global softmax maximum),
     so each sits at about the bf16 distance e from the exact float64 result,
     e = |faithful - float64| measured on the case itself (no GPU involved).
-    Bound: 2e, and never below the benchmark spec's 2e-2."""
+    Bound: 2e, and never below the 2e-2 confidence tolerance."""
     return max(CONF_TOL, 2.0 * bf16_own_error)
 
 
