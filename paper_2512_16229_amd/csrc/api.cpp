@@ -73,11 +73,12 @@ int round_up(int x, int m) { return m * ((x + m - 1) / m); }
 // whole rows of a tile and no split); for the others the pair minimising an
 // estimate of HBM time is taken: rounds of workgroups x bytes of the largest
 // split, plus the fp32 partial sums written and read back (and, for QKV, the
-// fix-up launch).
+// fix-up launch). The weights are packed per tile, so nb is chosen once, when
+// the model is created (fixed_nb = 0: choose), and later plans choose S only.
 struct GemmPlan {
   int nb, tiles, splits;
 };
-GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu) {
+GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_nb) {
   if (epi == EPI_SWIGLU) return {10, nblocks / 10, 1};
   if (epi == EPI_LMHEAD) return {8, nblocks / 8, 1};
   const int Q = KC / 4;
@@ -85,6 +86,7 @@ GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu) {
   GemmPlan best{8, nblocks / 8, 1};
   double best_cost = 1e300;
   for (int nb : {4, 8}) {
+    if (fixed_nb && nb != fixed_nb) continue;
     const int tiles = nblocks / nb;
     for (int S = 1; S <= Q; ++S) {
       const int64_t wgs = (int64_t)MT * tiles * S;
@@ -117,6 +119,7 @@ struct lopa_model {
   int num_cu = 0;
   int n_qkv = 0;
   int blk_qkv = 0, blk_h = 0, blk_gu = 0, blk_lm = 0;  // packed 16-column blocks
+  int nb_qkv = 0, nb_o = 0, nb_down = 0;                // tile widths of the packed weights
   int tiles_lm = 0;                                     // LM-head column tiles
   std::vector<LayerPack> layers;
   uint16_t* embed = nullptr;
@@ -192,11 +195,11 @@ struct StepPlans {
 StepPlans step_plans(const lopa_model* m, int MT) {
   const lopa_model_cfg& c = m->cfg;
   StepPlans p;
-  p.qkv = plan_gemm(EPI_QKV, m->blk_qkv, c.hidden / 64, MT, m->num_cu);
-  p.o = plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu);
-  p.gu = plan_gemm(EPI_SWIGLU, m->blk_gu, c.hidden / 64, MT, m->num_cu);
-  p.down = plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu);
-  p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, c.hidden / 64, MT, m->num_cu);
+  p.qkv = plan_gemm(EPI_QKV, m->blk_qkv, c.hidden / 64, MT, m->num_cu, m->nb_qkv);
+  p.o = plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu, m->nb_o);
+  p.gu = plan_gemm(EPI_SWIGLU, m->blk_gu, c.hidden / 64, MT, m->num_cu, 10);
+  p.down = plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu, m->nb_down);
+  p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, c.hidden / 64, MT, m->num_cu, 8);
   return p;
 }
 }  // namespace
@@ -274,6 +277,11 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
       hipDeviceGetAttribute(&m->num_cu, hipDeviceAttributeMultiprocessorCount, m->device) !=
           hipSuccess)
     return bail(fail(LOPA_EHIP, "no HIP device"));
+  // tile widths: those of the single-row-tile plans (up to 256 rows, the
+  // common verify batch); other row counts re-plan the k-splits only
+  m->nb_qkv = plan_gemm(EPI_QKV, m->blk_qkv, H / 64, 1, m->num_cu, 0).nb;
+  m->nb_o = plan_gemm(EPI_RESID, m->blk_h, c.heads * d / 64, 1, m->num_cu, 0).nb;
+  m->nb_down = plan_gemm(EPI_RESID, m->blk_h, round256(F) / 64, 1, m->num_cu, 0).nb;
   auto alloc16 = [&](uint16_t** p, size_t elems) -> int {
     DevBuf b;
     int r = dalloc(b, elems * 2, m->owned);
@@ -306,13 +314,13 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     const uint16_t* wv = (const uint16_t*)lw.wv;
     hipError_t e;
     if ((e = launch_repack(wq, c.heads * d, wk, c.kv_heads * d, wv, c.kv_heads * d, H, H,
-                           m->blk_qkv, 0, p.qkv, s)) != hipSuccess ||
+                           m->blk_qkv, m->nb_qkv, 0, p.qkv, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
-                           c.heads * d, m->blk_h, 0, p.o, s)) != hipSuccess ||
+                           c.heads * d, m->blk_h, m->nb_o, 0, p.o, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.w_gate, F, (const uint16_t*)lw.w_up, F, nullptr,
-                           0, H, H, m->blk_gu, 1, p.gu, s)) != hipSuccess ||
+                           0, H, H, m->blk_gu, 10, 1, p.gu, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.w_down, H, nullptr, 0, nullptr, 0, F, FP,
-                           m->blk_h, 0, p.down, s)) != hipSuccess ||
+                           m->blk_h, m->nb_down, 0, p.down, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln1, p.ln1, H, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln2, p.ln2, H, s)) != hipSuccess)
       return bail(fail(LOPA_EHIP, "layer %d repack: %s", l, hipGetErrorString(e)));
@@ -332,7 +340,7 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
   hipError_t e;
   if ((e = hipMemcpyAsync(m->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s)) ||
       (e = launch_repack((const uint16_t*)w->lm_head, V, nullptr, 0, nullptr, 0, H, H,
-                         m->blk_lm, 0, m->lm, s)) ||
+                         m->blk_lm, 8, 0, m->lm, s)) ||
       (e = launch_bf16_to_f32((const uint16_t*)w->final_norm, m->final_norm, H, s)) ||
       (e = hipStreamSynchronize(s)))
     return bail(fail(LOPA_EHIP, "model create: %s", hipGetErrorString(e)));

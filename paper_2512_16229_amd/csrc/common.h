@@ -11,10 +11,11 @@
 // Activations ("A" operands, R = padded rows Mp):   fragment (rb, kb) at
 //   ((kb * (Mp/16)) + rb) * 512 elements.
 // Weights (W [N, K] in [out, in] order, "B" operand): blocks of 16 output
-//   features; block b holds its K / 64 chunks of 64 columns, each as two
-//   fragments (kk = 0, 1: columns 32 kk .. +31), fragment (b, kc, kk) at
-//   ((b * (K / 64) + kc) * 2 + kk) * 512. A GEMM tile is a run of consecutive
-//   blocks; one iteration streams one 2 KiB piece per block.
+//   features, grouped in tiles of nb consecutive blocks (nb fixed per weight);
+//   each block's 64-column chunk kc is two fragments (kk = 0, 1: columns
+//   32 kk .. +31), fragment (tile t, kc, block j of the tile, kk) at
+//   (((t * (K / 64) + kc) * nb + j) * 2 + kk) * 512. One GEMM iteration of a
+//   tile streams one contiguous nb x 2 KiB chunk.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>

@@ -245,22 +245,23 @@ __device__ __forceinline__ void lm_epilogue(const GemmArgs& a, f32x4 (&acc)[4][N
 // Loads of one iteration: 8 activation fragments into register set `set` (two
 // groups of 4, k-halves 0 and 1) and the NB x 2 KiB weight chunk into ring
 // slot `slot` (NB / 2 copies of 1 KiB per wavefront). Weight layout
-// [block][KC][2][64 lanes][8]: wavefront wv copies k-half wv % 2 of blocks
-// 2 r + wv / 2, r < NB / 2. The addresses advance by one k-chunk per issued
-// iteration (a_next, w_next); past the last k-chunk the last one is issued
-// again (an L2 hit), which keeps every wait count and the loop branch-free.
+// [tile][KC][NB][2][64 lanes][8]: the chunk of iteration (tile, kc) is one
+// contiguous run, and so is a tile's whole k-range. The addresses advance by
+// one k-chunk per issued iteration (a_next, w_next); past the last k-chunk the
+// last one is issued again (an L2 hit), which keeps every wait count and the
+// loop branch-free.
 #define GEMM_ISSUE_A(set, half)                                                          \
   load_frag4(set[4 * (half) + 0], set[4 * (half) + 1], set[4 * (half) + 2],              \
              set[4 * (half) + 3], a_next + (half) * a_half, voff)
 #define GEMM_ISSUE_W(r, slot)                                                            \
-  lds_dma16(w_next + (int64_t)(r) * w_rstride, voff,                                     \
+  lds_dma16(w_next + (r) * 4096, voff,                                                   \
             lds_wave + (uint32_t)(slot) * (uint32_t)SM::CHUNK + (uint32_t)(r) * 4096u)
 #define GEMM_ADVANCE_LOAD()                                                              \
   {                                                                                      \
     if (lk + 1 < kc_end) {                                                               \
       ++lk;                                                                              \
       a_next += a_kstep;                                                                 \
-      w_next += 2048;                                                                    \
+      w_next += SM::CHUNK;                                                               \
     }                                                                                    \
   }
 #define GEMM_ISSUE(set, slot)                                                            \
@@ -336,9 +337,12 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   const int MT = a.mtiles;
   const int mt = q % MT, c = q / MT;
   const int KC = a.KC, QT = KC >> 2;
-  // workgroup c of a row tile: column tile c / S, k-chunks of split c % S
-  const int split = c % a.splits;
-  const int t_lo = c / a.splits;
+  // workgroup c of a row tile: k-split c / T, column tile c % T. Split-major, so
+  // that the workgroups of one XCD (consecutive q) share a k-range and with it
+  // the slice of the activation operand they stream: it stays in that XCD's
+  // L2 instead of being fetched once per column tile.
+  const int split = c / a.tiles;
+  const int t_lo = c % a.tiles;
   const int kc_beg = 4 * (split * QT / a.splits);
   const int kc_end = 4 * ((split + 1) * QT / a.splits);
   if (t_lo >= a.tiles || kc_beg >= kc_end) return;
@@ -351,10 +355,9 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   // of this wavefront's first row block -> a_next + h a_half
   const int64_t a_half = (int64_t)RB * 1024, a_kstep = 2 * a_half;
   const char* a_next = (const char*)a.A + ((int64_t)2 * kc_beg * RB + rb0) * 1024;
-  // weight piece (block, kc, half) at W + ((block KC + kc) 2 + half) KiB
-  const int64_t w_rstride = (int64_t)2 * KC * 2048;  // two blocks further
-  const char* w_next = (const char*)a.W +
-                       (((int64_t)t_lo * NB + (wv >> 1)) * KC + kc_beg) * 2048 + (wv & 1) * 1024;
+  // weight chunk (tile, kc) at W + (tile KC + kc) CHUNK; its 1 KiB unit u (block
+  // u / 2, k-half u % 2) at + u KiB; wavefront wv copies units 4 r + wv
+  const char* w_next = (const char*)a.W + ((int64_t)t_lo * KC + kc_beg) * SM::CHUNK + wv * 1024;
   const uint32_t lds_wave = sW_base + (uint32_t)wv * 1024u;
   int lk = kc_beg;  // k-chunk of the next iteration to issue
 

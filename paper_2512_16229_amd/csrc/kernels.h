@@ -27,14 +27,16 @@ hipError_t launch_kv_rows(uint16_t* cache_k, uint16_t* cache_v, int64_t head_str
 
 // ------------------------------------------------------------ weight repack
 // Pack the rows of up to three [rows_i, K] bf16 sources (stacked in order) into
-// the GEMM weight layout: blocks of 16 output rows, each [KC][2][64 lanes][8]
-// (one 1 KiB B-operand fragment per (block, 64-column chunk, 32-column half)).
-// `blocks` blocks are written; rows past the sources are zero. pairs: block 2p
-// holds rows [16p, 16p + 16) of source 0 and block 2p + 1 the same rows of
-// source 1 (gate / up pairing for the SwiGLU epilogue).
+// the GEMM weight layout: 16-row blocks grouped in tiles of nb blocks, stored
+// [tile][KC][nb][2][64 lanes][8] (one 1 KiB B-operand fragment per (block,
+// 64-column chunk, 32-column half)), so that one GEMM iteration streams one
+// contiguous nb x 2 KiB chunk and a tile's k-range is one contiguous run.
+// `blocks` (a multiple of nb) blocks are written; rows past the sources are
+// zero. pairs: block 2p holds rows [16p, 16p + 16) of source 0 and block 2p + 1
+// the same rows of source 1 (gate / up pairing for the SwiGLU epilogue).
 // K: source row length; KP (a multiple of 256, >= K): packed width, zero-filled.
 hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
-                         const uint16_t* s2, int r2, int K, int KP, int blocks, int pairs,
+                         const uint16_t* s2, int r2, int K, int KP, int blocks, int nb, int pairs,
                          uint16_t* dst, hipStream_t s);
 hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_t s);
 
@@ -56,7 +58,7 @@ enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
 struct GemmArgs {
   const uint16_t* A;   // packed activations, Mp rows, K columns
-  const uint16_t* W;   // packed weights [tiles * nb blocks of 16 columns][KC][2][64][8]
+  const uint16_t* W;   // packed weights [tiles][KC][nb blocks of 16 columns][2][64][8]
   int M, Mp, N, KC;    // KC = K / 64 iterations per tile, a multiple of 4
   int nb;              // 16-column blocks per tile (an instantiated width)
   int tiles;           // column tiles

@@ -142,20 +142,23 @@ __global__ __launch_bounds__(256) void lm_merge_kernel(const float* __restrict__
 }
 
 // Weight repack: one thread per (fragment, lane) writes 8 bf16 (16 bytes);
-// thread order is the packed order [block][kc][kk][lane].
+// thread order is the packed order [tile][kc][block in tile][kk][lane].
 __global__ __launch_bounds__(256) void repack_kernel(const uint16_t* __restrict__ s0, int r0,
                                                      const uint16_t* __restrict__ s1, int r1,
                                                      const uint16_t* __restrict__ s2, int r2,
-                                                     int K, int KC, int64_t total, int pairs,
-                                                     uint16_t* __restrict__ dst) {
+                                                     int K, int KC, int NB, int64_t total,
+                                                     int pairs, uint16_t* __restrict__ dst) {
   // K: length of a source row; KC * 64 >= K: packed columns, the excess is zero
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (gid >= total) return;
   const int lane = (int)(gid & 63);
-  const int64_t u = gid >> 6;
+  int64_t u = gid >> 6;
   const int kk = (int)(u & 1);
-  const int kc = (int)((u >> 1) % KC);
-  const int blk = (int)((u >> 1) / KC);
+  u >>= 1;
+  const int nbi = (int)(u % NB);
+  u /= NB;
+  const int kc = (int)(u % KC);
+  const int blk = (int)(u / KC) * NB + nbi;
   const int k0 = kc * 64 + kk * 32 + (lane >> 4) * 8;
   const uint16_t* src = nullptr;
   int row = 0;
@@ -218,14 +221,14 @@ hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, 
 }
 
 hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
-                         const uint16_t* s2, int r2, int K, int KP, int blocks, int pairs,
+                         const uint16_t* s2, int r2, int K, int KP, int blocks, int nb, int pairs,
                          uint16_t* dst, hipStream_t s) {
-  if (KP % 256 || KP < K) return hipErrorInvalidValue;
+  if (KP % 256 || KP < K || nb < 1 || blocks % nb) return hipErrorInvalidValue;
   const int KC = KP / 64;
   const int64_t total = (int64_t)blocks * KC * 2 * 64;
   const int64_t grid = (total + 255) / 256;
   hipLaunchKernelGGL(repack_kernel, dim3((unsigned)grid), dim3(256), 0, s, s0, r0, s1, r1, s2,
-                     r2, K, KC, total, pairs, dst);
+                     r2, K, KC, nb, total, pairs, dst);
   return hipGetLastError();
 }
 
