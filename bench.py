@@ -218,6 +218,52 @@ def cpu_baseline(cfg_full, weights_dev, P, L, k, layers_sample=4, min_seconds=10
                        f"{step_s:.1f}s per step")}
 
 
+def e2e_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7, tau=0.9):
+    """End-to-end LoPA decode (Alg. 1 driven block by block): a uniform-random
+    prompt encoded block-causally, then gen / L blocks, each an initial forward
+    plus LoPA iterations until the winner has no unfilled position, committing
+    the winner's K/V every iteration. Iterations are timed one by one on the
+    host (each ends with the 4-byte read of the winner's unfilled count)."""
+    import torch
+    kv = lp.KV(model, prompt_len + gen, k + 1, L)
+    dec = lp.Decoder(model, kv, L, k, tau)
+    prompt = synth.prompt(cfg, prompt_len, device="cuda")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    P = dec.prefill(prompt)
+    torch.cuda.synchronize()
+    t_prefill = time.perf_counter() - t0
+    dec.forwards = 0
+    steps, init_s = [], 0.0
+    t1 = time.perf_counter()
+    for _ in range(gen // L):
+        ti = time.perf_counter()
+        dec.init_block(P)
+        torch.cuda.synchronize()
+        init_s += time.perf_counter() - ti
+        while True:
+            ts = time.perf_counter()
+            dec.step(P)
+            done = int(dec.next_unfilled.item()) == 0
+            steps.append(time.perf_counter() - ts)
+            if done:
+                break
+            if len(steps) > 2 * gen:
+                raise RuntimeError("decode did not converge")
+        P += L
+    torch.cuda.synchronize()
+    t_dec = time.perf_counter() - t1
+    st = sorted(steps)
+    q = lambda f: st[min(len(st) - 1, int(f * len(st)))] * 1e3
+    return {"workload": (f"{cfg['name']} shape, {prompt_len}-token uniform-random prompt, "
+                         f"{gen} generated tokens in {gen // L} blocks of {L}, k={k}, tau {tau}"),
+            "tokens_per_s": round(gen / t_dec, 1), "tokens_per_forward": round(gen / dec.forwards, 3),
+            "forwards": dec.forwards, "iterations": len(steps),
+            "step_ms_median": round(q(0.5), 3), "step_ms_p10": round(q(0.1), 3),
+            "step_ms_p90": round(q(0.9), 3), "initial_forward_ms_mean": round(init_s / (gen // L) * 1e3, 3),
+            "prefill_s": round(t_prefill, 4), "decode_s": round(t_dec, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -230,6 +276,7 @@ def main():
     ap.add_argument("--tau", type=float, default=0.9)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=4)
+    ap.add_argument("--no-e2e", action="store_true", help="skip the end-to-end decode run")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy 5 times (HBM counter calibration)")
     ap.add_argument("--hbm-counters", action="store_true",
@@ -361,6 +408,11 @@ def main():
                           "mfma_frac": round(sf / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)},
         "kernel_ms_per_step": {kd: round(v, 4) for kd, v in per_step_ms.items()},
     }
+    if not args.no_e2e:
+        t0 = time.perf_counter()
+        result["e2e_decode"] = e2e_decode(lp, synth, model, cfg, L=L, k=k, tau=tau)
+        log(f"end-to-end decode in {time.perf_counter() - t0:.1f}s: "
+            f"{result['e2e_decode']['tokens_per_s']} tok/s, TPF {result['e2e_decode']['tokens_per_forward']}")
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         try:

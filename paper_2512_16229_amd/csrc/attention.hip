@@ -5,12 +5,14 @@
 //
 // One workgroup per (query head, branch) with four wavefronts; each wavefront
 // takes a quarter of the key tiles (32 keys each) for all L rows, and the
-// four partial softmax states are merged through LDS at the end. No K or V
-// byte goes through LDS: both are read straight from global memory (L2) in
-// MFMA operand layout. Scores are formed transposed, S^T = K Q^T, so a lane
-// owns one query column and the probabilities land directly in the operand
-// layout of O^T = V^T P^T; V is stored transposed ([d][position]) in the cache
-// and the staging so that a lane's 8 keys of one dimension are two 8-byte runs.
+// four partial softmax states are merged through LDS at the end. Each
+// wavefront streams its tiles through a private two-slot LDS ring with
+// asynchronous global -> LDS copies (one tile in flight while the previous one
+// is computed), then reads the K and V fragments from LDS in MFMA operand
+// layout. Scores are formed transposed, S^T = K Q^T, so a lane owns one query
+// column and the probabilities land directly in the operand layout of
+// O^T = V^T P^T; V is stored transposed ([d][position]) in the cache and the
+// staging so that a copy lane's 8 keys of one dimension are 16 contiguous bytes.
 // Prefix tiles and block tiles are kept apart (a tile reads one source, with
 // positions aligned to 4) and keys past the end of either are masked: their
 // probability and their V values are zero.
@@ -29,11 +31,42 @@ struct AttnTile {
   uint2 v[D / 16][2];  // V^T: dims 16 db + c16, keys {4g .. 4g+3} and {16 + 4g ..}
 };
 
+// Asynchronous copy of 16 bytes per lane, from base + voff(lane) (base
+// wave-uniform, in SGPRs) to bytes [16 lane, 16 lane + 16) of the 1 KiB LDS
+// block at lds_addr (wave-uniform, in M0). The compiler does not track it:
+// completion is awaited with an explicit vmcnt wait.
+__device__ __forceinline__ void attn_dma16(const void* base, uint32_t voff, uint32_t lds_addr) {
+  const uint64_t u = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+  const void* sbase = (const void*)(((uint64_t)hi << 32) | lo);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               ::"s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(sbase)
+               : "memory");
+}
+template <int N>
+__device__ __forceinline__ void attn_wait_vmcnt() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <int D, int QB>
+struct AttnSmem {
+  static constexpr int NDB = D / 16, NKK = D / 32;
+  static constexpr int KBYTES = 2 * NKK * 1024;   // K of one tile: [kb][kk][lane][16 B]
+  static constexpr int TILE = KBYTES + NDB * 1024;  // + V^T: [db][lane][16 B]
+  static constexpr int RING = 4 * 2 * TILE;         // four wavefronts x two slots
+  static constexpr int MERGE_O = NDB * QB * 64 * 4;  // floats of one merge slot
+  static constexpr int MERGE = (2 * MERGE_O + 4 * QB * 16) * 4;
+  static constexpr int BYTES = RING > MERGE ? RING : MERGE;
+  static constexpr int OPS = 2 * NKK + NDB;  // copies per tile and wavefront
+};
+
 template <int D, int QB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+  using SM = AttnSmem<D, QB>;
   constexpr int NDB = D / 16, NKK = D / 32;
-  __shared__ float sO[2][NDB * QB * 64 * 4];
-  __shared__ float sM[2][QB * 16], sL[2][QB * 16];
+  __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
   const int h = blockIdx.x, br = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -44,49 +77,86 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int t_lo = wv * T / 4, t_hi = (wv + 1) * T / 4;
   const float sl2 = a.scale * 1.4426950408889634f;  // scale * log2(e)
 
+  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;  // [pos][D]
+  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;  // [D][vld]
+  const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
+  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;  // [pos][D]
+  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;  // [D][vlds]
+  const uint32_t ring = (uint32_t)(uintptr_t)smem + (uint32_t)(wv * 2) * SM::TILE;
+
+  // tile t -> ring slot: OPS copies, each from a wave-uniform base at the
+  // tile's first position plus a per-lane byte offset. A K copy lane takes key
+  // row 16 kb + c16, dims 32 kk + 8 g .. +8; a V copy lane dimension
+  // 16 db + c16, keys 8 g .. 8 g + 7. In a tile that runs past the end of its
+  // source, K rows past the end read the last row and V runs that start past
+  // the end read the first run (compute() masks both): every copy stays inside
+  // the source, whose row lengths are multiples of 8.
+  const uint32_t koff_full[2] = {(uint32_t)((c16 * D + g * 8) * 2),
+                                 (uint32_t)(((16 + c16) * D + g * 8) * 2)};
+  const uint32_t voff_pre = (uint32_t)((c16 * a.vld + 8 * g) * 2);
+  const uint32_t voff_blk = (uint32_t)((c16 * a.vlds + 8 * g) * 2);
+  auto issue = [&](int t, int slot) {
+    const bool pre = t < pt;
+    const int p0 = (pre ? t : t - pt) * KT;
+    const int lim = pre ? P : L;
+    const int64_t vld = pre ? a.vld : a.vlds;
+    const uint16_t* kb_ = (pre ? kc : ks) + (int64_t)p0 * D;
+    const uint16_t* vb_ = (pre ? vc : vs) + p0;
+    uint32_t koff[2] = {koff_full[0], koff_full[1]};
+    uint32_t voff = pre ? voff_pre : voff_blk;
+    if (p0 + KT > lim) {  // wave-uniform: the last, partial tile of a source
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const int r = kb * 16 + c16 < lim - p0 ? kb * 16 + c16 : lim - 1 - p0;
+        koff[kb] = (uint32_t)((r * D + g * 8) * 2);
+      }
+      voff = (uint32_t)((c16 * vld + (8 * g < lim - p0 ? 8 * g : 0)) * 2);
+    }
+    const uint32_t sb = ring + (uint32_t)slot * SM::TILE;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) attn_dma16(kb_ + kk * 32, koff[kb], sb + (kb * NKK + kk) * 1024);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      attn_dma16(vb_ + (int64_t)db * 16 * vld, voff, sb + SM::KBYTES + db * 1024);
+  };
+
+  // ring slot -> registers (operand layouts)
+  auto fetch = [&](int slot, AttnTile<D, QB>& x) {
+    const char* sb = smem + (wv * 2 + slot) * SM::TILE;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+        x.k[kb][kk] = *(const u32x4*)(sb + ((kb * NKK + kk) * 64 + lane) * 16);
+    // keys 4g .. 4g+3 sit in copy lane c16 + 16 (g / 2) at byte 8 (g % 2);
+    // keys 16 + 4g .. in copy lane c16 + 16 (2 + g / 2)
+    const char* vb = sb + SM::KBYTES + (c16 + 16 * (g >> 1)) * 16 + 8 * (g & 1);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      x.v[db][0] = *(const uint2*)(vb + db * 1024);
+      x.v[db][1] = *(const uint2*)(vb + db * 1024 + 32 * 16);
+    }
+  };
+
+  // the first two tiles are in flight while Q is loaded
+  const int n = t_hi - t_lo;
+  if (n > 0) {
+    issue(t_lo, 0);
+    issue(t_lo + (n > 1 ? 1 : 0), 1);
+  }
+
   // Q^T operand: query column 16 qb + c16, dims 32 kk + 8 g .. +8
   u32x4 qf[QB][NKK];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int row = qb * 16 + c16;
     const uint16_t* qrow = a.q + (((int64_t)br * a.Hq + h) * L + (row < L ? row : 0)) * D;
+    const unsigned keep = row < L ? ~0u : 0u;  // rows past L: zero queries
 #pragma unroll
-    for (int kk = 0; kk < NKK; ++kk)
-      qf[qb][kk] = row < L ? *(const u32x4*)(qrow + kk * 32 + g * 8) : u32x4{0u, 0u, 0u, 0u};
+    for (int kk = 0; kk < NKK; ++kk) qf[qb][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
   }
-
-  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;  // [pos][D]
-  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;  // [D][vld]
-  const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
-  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;  // [pos][D]
-  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;  // [D][vlds]
-
-  // tile t -> registers (positions past the end of the source read position 0)
-  auto fetch = [&](int t, AttnTile<D, QB>& x) {
-    const bool pre = t < pt;
-    const int p0 = (pre ? t : t - pt) * KT;  // first position of the tile in its source
-    const int lim = pre ? P : L;
-    const uint16_t* kb_ = pre ? kc : ks;
-    const uint16_t* vb_ = pre ? vc : vs;
-    const int64_t vld = pre ? a.vld : a.vlds;  // multiples of 8: a 4-key run stays in its row
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      int pos = p0 + kb * 16 + c16;
-      pos = pos < lim ? pos : 0;
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-        x.k[kb][kk] = *(const u32x4*)(kb_ + (int64_t)pos * D + kk * 32 + g * 8);
-    }
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const uint16_t* vr = vb_ + (int64_t)(db * 16 + c16) * vld;
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const int pos = p0 + hf * 16 + g * 4;  // 4 keys pos .. pos + 3, 4-aligned
-        x.v[db][hf] = pos < lim ? *(const uint2*)(vr + pos) : make_uint2(0u, 0u);
-      }
-    }
-  };
 
   float m[QB], l[QB];  // running max (log2 units) and this lane's partial sum
   f32x4 o[NDB][QB];
@@ -98,21 +168,28 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int db = 0; db < NDB; ++db) o[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
+  // One key tile for all query rows. The probabilities are taken against a
+  // reference maximum m that trails the running row maximum by at most 8
+  // (log2 units): m, l and o are rescaled only when some row's maximum has
+  // grown past that (a wave-uniform decision), so p = 2^(s - m) <= 2^8.
+  // o / l and the final merge are unchanged by the choice of reference.
   auto compute = [&](int t, AttnTile<D, QB>& x) {
     const bool pre = t < pt;
     const int p0 = (pre ? t : t - pt) * KT;
     const int lim = pre ? P : L;
-    // zero V of masked keys (stale cache or staging contents may be non-finite)
+    const bool full = p0 + KT <= lim;  // wave-uniform
+    if (!full) {
+      // zero V of masked keys (stale cache or staging contents may be
+      // non-finite, and 0 * inf would poison the sums)
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int pos = p0 + hf * 16 + g * 4;
-      if (pos + 3 >= lim) {
+      for (int hf = 0; hf < 2; ++hf) {
+        const int pos = p0 + hf * 16 + g * 4;
+        const unsigned m01 = (pos < lim ? 0xFFFFu : 0u) | (pos + 1 < lim ? 0xFFFF0000u : 0u);
+        const unsigned m23 = (pos + 2 < lim ? 0xFFFFu : 0u) | (pos + 3 < lim ? 0xFFFF0000u : 0u);
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          uint16_t* e = (uint16_t*)&x.v[db][hf];
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            if (pos + j >= lim) e[j] = 0;
+          x.v[db][hf].x &= m01;
+          x.v[db][hf].y &= m23;
         }
       }
     }
@@ -132,24 +209,27 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int pos = p0 + kb * 16 + g * 4 + j;
-          s[kb][j] = pos < lim ? s[kb][j] * sl2 : -INFINITY;
+          s[kb][j] = full || pos < lim ? s[kb][j] * sl2 : -INFINITY;
           tmax = fmaxf(tmax, s[kb][j]);
         }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
       const float mn = fmaxf(m[qb], tmax);
-      // a fully masked tile leaves mn = -inf: keep everything as it is
-      const float alpha = mn == -INFINITY ? 1.f : exp2f(m[qb] - mn);
-      m[qb] = mn;
-      l[qb] *= alpha;
+      if (__builtin_amdgcn_ballot_w64(mn > m[qb] + 8.f)) {
+        // m = -inf (nothing seen yet) gives alpha = 0 on zero o and l
+        const float alpha = mn == -INFINITY ? 1.f : exp2f(m[qb] - mn);
+        m[qb] = mn;
+        l[qb] *= alpha;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db][qb] *= alpha;
+        for (int db = 0; db < NDB; ++db) o[db][qb] *= alpha;
+      }
+      const float mr = m[qb];
       uint16_t pb[8];
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const float p = mn == -INFINITY ? 0.f : exp2f(s[kb][j] - mn);
+          const float p = mr == -INFINITY ? 0.f : exp2f(s[kb][j] - mr);
           l[qb] += p;
           pb[kb * 4 + j] = f2bf_bits(p);
         }
@@ -162,17 +242,21 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     }
   };
 
-  // two tiles in flight: x0 holds tile t, x1 tile t + 1
-  AttnTile<D, QB> x0, x1;
-  if (t_lo < t_hi) fetch(t_lo, x0);
-  if (t_lo + 1 < t_hi) fetch(t_lo + 1, x1);
-  for (int t = t_lo; t < t_hi; t += 2) {
-    compute(t, x0);
-    if (t + 2 < t_hi) fetch(t + 2, x0);
-    if (t + 1 >= t_hi) break;
-    compute(t + 1, x1);
-    if (t + 3 < t_hi) fetch(t + 3, x1);
+  // tile i sits in slot i % 2. At the top of an iteration tiles i and i + 1
+  // are in flight (2 OPS copies): wait for the older one, compute it, and
+  // refill its slot with tile i + 2 once its LDS reads have completed. Past
+  // the last tile the last one is copied again (an L2 hit), so the number of
+  // copies in flight is the same in every iteration.
+  for (int i = 0; i < n; ++i) {
+    attn_wait_vmcnt<SM::OPS>();
+    AttnTile<D, QB> x;
+    fetch(i & 1, x);
+    compute(t_lo + i, x);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    issue(t_lo + (i + 2 < n ? i + 2 : n - 1), i & 1);
   }
+  attn_wait_vmcnt<0>();  // the ring is reused for the merge
+  __syncthreads();
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     l[qb] += __shfl_xor(l[qb], 16);
@@ -180,6 +264,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 
   // merge the four key ranges: (2, 3) into (0, 1), then 1 into 0
+  float(*sO)[SM::MERGE_O] = (float(*)[SM::MERGE_O])smem;
+  float(*sM)[QB * 16] = (float(*)[QB * 16])(smem + 2 * SM::MERGE_O * 4);
+  float(*sL)[QB * 16] = (float(*)[QB * 16])(smem + 2 * SM::MERGE_O * 4 + 2 * QB * 16 * 4);
   auto put = [&](int slot) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)

@@ -32,6 +32,10 @@ CONFIGS = {
     "llada8b": dict(layers=32, hidden=4096, heads=32, kv_heads=32, head_dim=128, ffn=12288,
                     vocab=126464, rms_eps=1e-5, rope_theta=5e5, qkv_bias=False,
                     std=0.02, lm_std=0.02),
+    # Same shape, LM head spread (parity cases).
+    "llada8b_spread": dict(layers=32, hidden=4096, heads=32, kv_heads=32, head_dim=128,
+                           ffn=12288, vocab=126464, rms_eps=1e-5, rope_theta=5e5,
+                           qkv_bias=False, std=0.02, lm_std=8.0 / math.sqrt(4096)),
 }
 
 

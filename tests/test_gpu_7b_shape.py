@@ -1,9 +1,12 @@
-"""GPU parity at the Dream-7B shape, in the launch configuration bench.py times
-(8 branches x 32 rows, prefix 512, every plan and kernel of the headline step).
+"""GPU parity at the full model shapes of the measured workloads, in the launch
+configuration bench.py times (every plan and kernel of the step at that size):
+  * Dream-7B, prefix 512, k = 7 (8 branches x 32 rows: one 256-row tile);
+  * Dream-7B, prefix 2048, k = 15 (16 branches x 32 rows: two row tiles);
+  * LLaDA-8B (MHA, no biases), prefix 1024, k = 7.
 
-The oracle cannot run 28 float64 layers at this size in seconds, so outputs are
-sampled where it can compute them one by one:
-  * the residual stream after the first layer for all 256 rows (one float64
+The oracle cannot run 28-32 float64 layers at these sizes in seconds, so outputs
+are sampled where it can compute them one by one:
+  * the residual stream after the first layer for every row (one float64
     layer, the prefix K/V of that layer taken from the GPU's own cache);
   * Conf / candidate token of sampled rows from the GPU's final residual stream:
     final RMSNorm + the full-vocabulary LM head + softmax in float64 (Sec. 3.1).
@@ -19,13 +22,16 @@ from oracle.model import bf16_round, confidence, rms_norm
 
 pytestmark = pytest.mark.gpu
 
-P, L, K = 512, 32, 7
+L = 32
+CASES = [("dream7b_spread", 512, 7), ("dream7b_spread", 2048, 15), ("llada8b_spread", 1024, 7)]
 
 
-@pytest.fixture(scope="module")
-def big():
+@pytest.fixture(scope="module", params=CASES, ids=lambda c: f"{c[0]}-P{c[1]}-k{c[2]}")
+def big(request):
     import paper_2512_16229_amd as lp
-    cfg = synth.config("dream7b_spread")
+    name, P, K = request.param
+    log(f"full shape {name}: prefix {P}, k {K}")
+    cfg = synth.config(name)
     w = synth.model_weights(cfg, device="cuda", dtype=torch.bfloat16)
     model = lp.Model(cfg, w)
     kv = lp.KV(model, P + L, K + 1, L)
@@ -36,13 +42,13 @@ def big():
     bt = np.where(rng.random((K + 1, L)) < 0.7, mask, rng.integers(0, cfg["vocab"] - 1, (K + 1, L)))
     bt[0] = mask
     torch.cuda.synchronize()
-    yield dict(lp=lp, cfg=cfg, w=w, model=model, kv=kv, bt=bt)
+    yield dict(lp=lp, cfg=cfg, w=w, model=model, kv=kv, bt=bt, P=P)
     del dec, kv, model, w
     torch.cuda.empty_cache()
 
 
 def _hidden(big, n_layers):
-    lp, cfg, bt = big["lp"], big["cfg"], big["bt"]
+    lp, cfg, bt, P = big["lp"], big["cfg"], big["bt"], big["P"]
     nb = bt.shape[0]
     x = torch.empty(nb * L * cfg["hidden"], dtype=torch.float32, device="cuda")
     btd = torch.tensor(bt, dtype=torch.int32, device="cuda").reshape(-1)
@@ -52,8 +58,8 @@ def _hidden(big, n_layers):
 
 
 def test_first_layer_all_rows(big):
-    cfg, w, bt = big["cfg"], big["w"], big["bt"]
-    log("7B shape: layer 0, 256 rows, prefix 512")
+    cfg, w, bt, P = big["cfg"], big["w"], big["bt"], big["P"]
+    log(f"  layer 0, {bt.size} rows, prefix {P}")
     g = _hidden(big, 1)
     cfg1 = dict(cfg, layers=1)
     host = {"embed": w["embed"].float().cpu(),
@@ -73,8 +79,8 @@ def test_first_layer_all_rows(big):
 
 
 def test_lm_head_sampled_rows(big):
-    lp, cfg, w, bt = big["lp"], big["cfg"], big["w"], big["bt"]
-    log("7B shape: LM head + Conf on sampled rows, full vocabulary")
+    lp, cfg, w, bt, P = big["lp"], big["cfg"], big["w"], big["bt"], big["P"]
+    log("  LM head + Conf on sampled rows, full vocabulary")
     nb = bt.shape[0]
     conf_g = torch.empty(nb * L, dtype=torch.float32, device="cuda")
     pred_g = torch.empty(nb * L, dtype=torch.int32, device="cuda")
