@@ -70,34 +70,41 @@ int round_up(int x, int m) { return m * ((x + m - 1) / m); }
 
 // Decomposition of one GEMM (see gemm.hip): tile width nb (16-column blocks)
 // and k-splits S. SwiGLU and LM-head tiles are fixed (their epilogues need
-// whole rows of a tile and no split); for the others the pair minimising an
-// estimate of HBM time is taken: rounds of workgroups x bytes of the largest
-// split, plus the fp32 partial sums written and read back (and, for QKV, the
-// fix-up launch). The weights are packed per tile, so nb is chosen once, when
-// the model is created (fixed_nb = 0: choose), and later plans choose S only.
+// whole rows of a tile and no split); for the others the pair with the
+// smallest estimated time is taken. Per round of workgroups the time is the
+// larger of (a) the bytes one workgroup pulls into its CU (every k-chunk: the
+// 256 x 64 bf16 activation chunk from L2 plus nb x 2 KiB of weights), at the
+// per-CU rate measured for these kernels (~60 GB/s), and (b) the round's
+// weight bytes at the sustained HBM rate (~6.5 TB/s); split-K adds its fp32
+// partial sums, written and read back (~5 TB/s), and QKV its fix-up launch.
+// The weights are packed per tile, so nb is chosen once, when the model is
+// created (fixed_nb = 0: choose), and later plans choose S only.
 struct GemmPlan {
   int nb, tiles, splits;
 };
 GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_nb) {
   if (epi == EPI_SWIGLU) return {10, nblocks / 10, 1};
   if (epi == EPI_LMHEAD) return {8, nblocks / 8, 1};
+  constexpr double CU_BPUS = 60e3, HBM_BPUS = 6.5e6, PART_BPUS = 5e6, FIXUP_US = 7.0;
   const int Q = KC / 4;
-  const double per_round = std::max(1, num_cu / MT);
   GemmPlan best{8, nblocks / 8, 1};
-  double best_cost = 1e300;
+  double best_t = 1e300;
   for (int nb : {4, 8}) {
     if (fixed_nb && nb != fixed_nb) continue;
     const int tiles = nblocks / nb;
     for (int S = 1; S <= Q; ++S) {
       const int64_t wgs = (int64_t)MT * tiles * S;
       const int64_t rounds = (wgs + num_cu - 1) / num_cu;
-      const double split_bytes = (double)((Q + S - 1) / S) * 4 * nb * 2048;
-      double cost = (double)rounds * split_bytes * per_round;
-      // partial sums written and read back; QKV also pays its fix-up launch
-      if (epi == EPI_QKV || S > 1) cost += 2.0 * wgs * nb * 16384;
-      if (epi == EPI_QKV) cost += 14e6;
-      if (cost < best_cost) {
-        best_cost = cost;
+      const double iters = 4.0 * ((Q + S - 1) / S);
+      const double per_cu = iters * (32768.0 + nb * 2048.0);
+      const double w_round = (double)std::min<int64_t>(wgs, num_cu) * iters * nb * 2048.0;
+      double t = (double)rounds * std::max(per_cu / CU_BPUS, w_round / HBM_BPUS);
+      const double part = epi == EPI_QKV ? (double)wgs * nb * 16384.0
+                                         : (S > 1 ? (double)S * MT * 256.0 * tiles * nb * 16 * 4 : 0.0);
+      t += 2.0 * part / PART_BPUS;
+      if (epi == EPI_QKV) t += FIXUP_US;
+      if (t < best_t) {
+        best_t = t;
         best = {nb, tiles, S};
       }
     }

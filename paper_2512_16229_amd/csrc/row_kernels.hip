@@ -8,7 +8,8 @@
 #include <math.h>
 
 // One workgroup (256 threads) per row; thread t holds the 4-column groups
-// q = t + 256 i (columns 4 q .. 4 q + 3, q < H / 4, H % 256 == 0, H <= 1024 CPT).
+// q = t + 256 i, i < NG (columns 4 q .. 4 q + 3, q < H / 4, H % 256 == 0,
+// H <= 1024 NG).
 // The row is formed in registers:
 //   EMBED:  x = embedding of the token (bf16 -> fp32)
 //   else:   x += sum of the S split-K partial sums of the preceding projection
@@ -19,7 +20,7 @@
 // select: no load sits under a branch, so all of them can be in flight
 // together.
 constexpr int CPT = 8;  // 4-column groups per thread at most
-template <bool EMBED, int SC>
+template <bool EMBED, int SC, int NG>
 __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict__ tokens,
                                                       const uint16_t* __restrict__ embed,
                                                       int vocab, const float* __restrict__ part,
@@ -32,7 +33,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   const int r = blockIdx.x;
   const int nq = H >> 2;
   float* xr = x + (int64_t)r * H;
-  float4 v[CPT];
+  float4 v[NG];
   float ss = 0.f;
   if (EMBED) {
     // a token outside [0, vocab) reads row 0 instead of memory past the table
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
     tok = (tok >= 0 && tok < vocab) ? tok : 0;
     const uint16_t* er = embed + (int64_t)tok * H;
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
+    for (int i = 0; i < NG; ++i) {
       const int q = tid + 256 * i;
       const bool ok = q < nq;
       const uint2 raw = *(const uint2*)(er + (ok ? q : nq - 1) * 4);
@@ -50,21 +51,21 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   } else {
     // partial sums in split order, then the residual. SC >= 0: the split count
     // is a compile-time constant; SC < 0: S, known at run time.
-    float4 t[CPT];
+    float4 t[NG];
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) t[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < NG; ++i) t[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     const int ns = SC >= 0 ? SC : S;
     for (int sp = 0; sp < ns; ++sp) {
       const float4* pr = (const float4*)(part + ((int64_t)sp * Mp + r) * H);
 #pragma unroll
-      for (int i = 0; i < CPT; ++i) {
+      for (int i = 0; i < NG; ++i) {
         const int q = tid + 256 * i;
         const float4 u = pr[q < nq ? q : nq - 1];
         t[i].x += u.x; t[i].y += u.y; t[i].z += u.z; t[i].w += u.w;
       }
     }
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
+    for (int i = 0; i < NG; ++i) {
       const int q = tid + 256 * i;
       const bool ok = q < nq;
       const float4 u = ((const float4*)xr)[ok ? q : nq - 1];
@@ -73,7 +74,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
     }
   }
 #pragma unroll
-  for (int i = 0; i < CPT; ++i) {
+  for (int i = 0; i < NG; ++i) {
     const int q = tid + 256 * i;
     if (q < nq && (EMBED || (SC >= 0 ? SC : S) > 0)) ((float4*)xr)[q] = v[i];
     ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
@@ -84,7 +85,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
 #pragma unroll
-  for (int i = 0; i < CPT; ++i) {
+  for (int i = 0; i < NG; ++i) {
     const int q = tid + 256 * i;
     if (q < nq) {
       const float4 wt = ((const float4*)w)[q];
@@ -183,21 +184,35 @@ __global__ void bf16_to_f32_kernel(const uint16_t* __restrict__ s, float* __rest
 }
 
 // ------------------------------------------------------------ launchers
+namespace {
+// 4-column groups per thread for a row of H columns
+int resnorm_groups(int H) { return H <= 1024 ? 1 : H <= 2048 ? 2 : H <= 4096 ? 4 : 8; }
+}  // namespace
+
 hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int vocab,
                              const float* w, float eps, int M, int Mp, int H, float* x,
                              uint16_t* a, hipStream_t s) {
   if (H % 256 || H > 1024 * CPT) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((resnorm_kernel<true, 0>), dim3(M), dim3(256), 0, s, tokens, embed,
-                     vocab, nullptr, 0, w, eps, M, Mp, H, x, a);
+#define EMBEDNORM(NG)                                                                     \
+  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG>), dim3(M), dim3(256), 0, s, tokens, embed, \
+                     vocab, nullptr, 0, w, eps, M, Mp, H, x, a)
+  switch (resnorm_groups(H)) {
+    case 1: EMBEDNORM(1); break;
+    case 2: EMBEDNORM(2); break;
+    case 4: EMBEDNORM(4); break;
+    default: EMBEDNORM(8); break;
+  }
+#undef EMBEDNORM
   return hipGetLastError();
 }
 
-hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, int M, int Mp,
-                          int H, float* x, uint16_t* a, hipStream_t s) {
-  if (H % 256 || H > 1024 * CPT || S < 0) return hipErrorInvalidValue;
+namespace {
+template <int NG>
+void resnorm_ng(const float* part, int S, const float* w, float eps, int M, int Mp, int H,
+                float* x, uint16_t* a, hipStream_t s) {
 #define RESNORM(SC)                                                                         \
-  hipLaunchKernelGGL((resnorm_kernel<false, SC>), dim3(M), dim3(256), 0, s, nullptr, nullptr, \
-                     0, part, S, w, eps, M, Mp, H, x, a)
+  hipLaunchKernelGGL((resnorm_kernel<false, SC, NG>), dim3(M), dim3(256), 0, s, nullptr,     \
+                     nullptr, 0, part, S, w, eps, M, Mp, H, x, a)
   switch (S) {
     case 0: RESNORM(0); break;
     case 2: RESNORM(2); break;
@@ -207,9 +222,22 @@ hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, i
     case 6: RESNORM(6); break;
     case 7: RESNORM(7); break;
     case 8: RESNORM(8); break;
+    case 9: RESNORM(9); break;
     default: RESNORM(-1); break;
   }
 #undef RESNORM
+}
+}  // namespace
+
+hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, int M, int Mp,
+                          int H, float* x, uint16_t* a, hipStream_t s) {
+  if (H % 256 || H > 1024 * CPT || S < 0) return hipErrorInvalidValue;
+  switch (resnorm_groups(H)) {
+    case 1: resnorm_ng<1>(part, S, w, eps, M, Mp, H, x, a, s); break;
+    case 2: resnorm_ng<2>(part, S, w, eps, M, Mp, H, x, a, s); break;
+    case 4: resnorm_ng<4>(part, S, w, eps, M, Mp, H, x, a, s); break;
+    default: resnorm_ng<8>(part, S, w, eps, M, Mp, H, x, a, s); break;
+  }
   return hipGetLastError();
 }
 
