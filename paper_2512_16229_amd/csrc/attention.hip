@@ -44,6 +44,26 @@ __device__ __forceinline__ void attn_dma16(const void* base, uint32_t voff, uint
                ::"s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(sbase)
                : "memory");
 }
+// max / sum of the values of lanes l and l ^ 16 (l ^ 32): the permlane swaps
+// hand each lane both values of its pair, lower lane first, so the two lanes
+// of a pair get bitwise identical results
+__device__ __forceinline__ float pair16_max(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair32_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair16_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair32_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int N>
 __device__ __forceinline__ void attn_wait_vmcnt() {
   static_assert(N >= 0 && N <= 63, "vmcnt range");
@@ -203,17 +223,21 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         for (int kk = 0; kk < NKK; ++kk) s[kb] = mfma16(x.k[kb][kk], qf[qb][kk], s[kb]);
       }
       // s[kb][j]: key p0 + 16 kb + 4 g + j, query 16 qb + c16
-      float tmax = -INFINITY;
+      if (full) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+        for (int kb = 0; kb < 2; ++kb) s[kb] *= sl2;
+      } else {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int pos = p0 + kb * 16 + g * 4 + j;
-          s[kb][j] = full || pos < lim ? s[kb][j] * sl2 : -INFINITY;
-          tmax = fmaxf(tmax, s[kb][j]);
-        }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int pos = p0 + kb * 16 + g * 4 + j;
+            s[kb][j] = pos < lim ? s[kb][j] * sl2 : -INFINITY;
+          }
+      }
+      float tmax = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+      tmax = pair32_max(pair16_max(tmax));
       const float mn = fmaxf(m[qb], tmax);
       if (__builtin_amdgcn_ballot_w64(mn > m[qb] + 8.f)) {
         // m = -inf (nothing seen yet) gives alpha = 0 on zero o and l
@@ -259,8 +283,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   __syncthreads();
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    l[qb] += __shfl_xor(l[qb], 16);
-    l[qb] += __shfl_xor(l[qb], 32);
+    l[qb] = pair32_sum(pair16_sum(l[qb]));
   }
 
   // merge the four key ranges: (2, 3) into (0, 1), then 1 into 0

@@ -1,17 +1,23 @@
-"""Assembly-level invariants of the GEMM kernels (CPU only: cross-compiles
-csrc/gemm.hip for gfx950 and reads the generated assembly).
+"""Assembly-level invariants of the kernels that issue untracked loads (CPU
+only: cross-compiles csrc/gemm.hip and csrc/attention.hip for gfx950 and reads
+the generated assembly).
 
-The activation fragments and the weight chunks are loaded by inline assembly
-that the compiler does not track (its own waits would stall on younger loads),
-which is only correct if the compiler never reads or moves those registers
-while the loads are in flight. These tests make that a checked property of
-every build instead of an assumption:
-  * a register written by an inline-assembly global_load_dwordx4 is, until an
-    s_waitcnt vmcnt(0), only read as an MFMA source (never copied, spilled,
-    or reused);
+The GEMM's activation fragments and weight copies and the attention kernel's
+K / V tiles are loaded by inline assembly that the compiler does not track (its
+own waits would stall on younger loads), which is only correct if the compiler
+never reads, moves or reuses those registers while the loads are in flight.
+These tests make that a checked property of every build instead of an
+assumption:
+  * vector memory operations complete in issue order, so after
+    `s_waitcnt vmcnt(N)` all but the N most recent ones have landed; walking
+    each kernel in program order with that rule, no instruction other than
+    the load itself touches a register whose load may still be in flight;
   * no gemm kernel uses scratch memory;
-  * the MFMA loop blocks contain no AGPR/VGPR copies (the accumulators stay in
-    place).
+  * the MFMA loop blocks of the GEMM contain no AGPR/VGPR copies (the
+    accumulators stay in place).
+The walk follows the text in order, which matches the control flow of these
+kernels: their loads are issued on every path (clamped indices instead of
+branches), so no conditional block holds a load.
 """
 import os
 import re
@@ -22,72 +28,92 @@ import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
+MEM = re.compile(r"^(global|buffer|flat|scratch)_(load|store|atomic)")
 
 
-@pytest.fixture(scope="module")
-def asm(tmp_path_factory):
+def _compile(tmp_path_factory, src):
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
-    out = str(tmp_path_factory.mktemp("asm") / "gemm.s")
+    out = str(tmp_path_factory.mktemp("asm") / (src + ".s"))
     cmd = [HIPCC, "-O3", "-std=c++17", "--offload-arch=gfx950", "-Xclang", "-target-feature",
            "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
-           "--cuda-device-only", "-S", os.path.join(ROOT, "paper_2512_16229_amd", "csrc", "gemm.hip"),
+           "--cuda-device-only", "-S", os.path.join(ROOT, "paper_2512_16229_amd", "csrc", src + ".hip"),
            "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     return open(out).read()
 
 
-def _kernels(s):
-    for name in re.findall(r"^(_Z[\w.]+gemm_kernel[\w.]+):", s, re.M):
+@pytest.fixture(scope="module")
+def asm(tmp_path_factory):
+    return _compile(tmp_path_factory, "gemm")
+
+
+@pytest.fixture(scope="module")
+def attn_asm(tmp_path_factory):
+    return _compile(tmp_path_factory, "attention")
+
+
+def _kernels(s, kind="gemm_kernel"):
+    for name in re.findall(r"^(_Z[\w.]+" + kind + r"[\w.]+):", s, re.M):
         i = s.index(name + ":")
         j = s.index(".Lfunc_end", i)
         yield name, s[i:j].split("\n")
 
 
 def _regs(tok):
-    m = re.match(r"v\[(\d+):(\d+)\]", tok)
+    m = re.match(r"([va])\[(\d+):(\d+)\]", tok)
     if m:
-        return set(range(int(m.group(1)), int(m.group(2)) + 1))
-    m = re.match(r"v(\d+)$", tok)
-    return {int(m.group(1))} if m else set()
+        return {(m.group(1), i) for i in range(int(m.group(2)), int(m.group(3)) + 1)}
+    m = re.match(r"([va])(\d+)$", tok)
+    return {(m.group(1), int(m.group(2)))} if m else set()
 
 
-def test_kernels_found(asm):
-    names = [n for n, _ in _kernels(asm)]
-    assert len(names) >= 6, names
-
-
-def test_inflight_activation_registers_untouched(asm):
-    for name, body in _kernels(asm):
-        inflight, bad = set(), []
-        for line in body:
-            t = line.strip()
-            if not t or t.startswith((";", ".")):
-                continue
-            if t.startswith("global_load_dwordx4"):
-                inflight |= _regs(t.split()[1].rstrip(","))
-                continue
-            if re.match(r"s_waitcnt vmcnt\(0\)", t):
-                inflight = set()
-                continue
-            ops = [o.strip() for o in t.split(None, 1)[1].split(",")] if " " in t else []
-            regs = set()
-            for o in ops:
-                if o:
-                    regs |= _regs(o.split()[0])
-            if not regs & inflight:
-                continue
-            if t.startswith("v_mfma") and not (_regs(ops[0]) & inflight):
-                continue
+def _inflight_violations(body):
+    """Instructions that touch a register while a load into it may be in flight."""
+    fifo, bad = [], []
+    for line in body:
+        t = line.strip()
+        if not t or t.startswith((";", ".")) or t.endswith(":"):
+            continue
+        if t.startswith("s_waitcnt"):
+            m = re.search(r"vmcnt\((\d+)\)", t)
+            if m:
+                del fifo[:max(0, len(fifo) - int(m.group(1)))]
+            continue
+        op = t.split()[0]
+        ops = [o.strip() for o in t.split(None, 1)[1].split(",")] if " " in t else []
+        used = set()
+        for o in ops:
+            if o:
+                used |= _regs(o.split()[0])
+        inflight = set().union(*fifo) if fifo else set()
+        if used & inflight:
             bad.append(t)
-        assert not bad, f"{name}: in-flight registers touched: {bad[:5]}"
+        if MEM.match(op):
+            dest = set()
+            if "_load" in op and "_lds" not in op and ops:
+                dest = _regs(ops[0].split()[0])
+            fifo.append(dest)
+    return bad
 
 
-def test_no_scratch(asm):
-    for name, body in _kernels(asm):
-        text = "\n".join(body)
-        assert "scratch_" not in text, f"{name} spills to scratch"
+def test_kernels_found(asm, attn_asm):
+    assert len(list(_kernels(asm))) >= 6
+    assert len(list(_kernels(attn_asm, "attn_kernel"))) >= 8
+
+
+def test_inflight_registers_untouched(asm, attn_asm):
+    for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel")):
+        for name, body in _kernels(s, kind):
+            bad = _inflight_violations(body)
+            assert not bad, f"{name}: in-flight registers touched: {bad[:5]}"
+
+
+def test_no_scratch(asm, attn_asm):
+    for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel")):
+        for name, body in _kernels(s, kind):
+            assert "scratch_" not in "\n".join(body), f"{name} spills to scratch"
 
 
 def test_mfma_loops_keep_accumulators_in_place(asm):
