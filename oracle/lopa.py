@@ -87,12 +87,65 @@ def branch_confidence(conf_row, tokens_row, mask_id: int) -> float:
     return sum(vals) / len(vals)
 
 
-def select(branch_tokens, conf, valid, mask_id: int):
+# Alternative branch-confidence measures named after Eq. 2 (Sec. 3.2, "other
+# methods"); the paper gives no formula, so these are readings:
+#   * window minimum ("local quality"): the unfilled positions in position
+#     order p_1 < ... < p_m, c_i = Conf(p_i); for a window size w, the means of
+#     all runs of w consecutive c_i (one run over all of them if m < w); the
+#     score is the smallest of these means;
+#   * lowest segment ("weak links"): the mean of the ceil(eta m) smallest c_i
+#     (at least one), 0 < eta <= 1.
+# Both give +inf for m = 0, as Eq. 2 does.
+METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
+
+
+def branch_confidence_window_min(conf_row, tokens_row, mask_id: int, window: int) -> float:
+    """Smallest mean over runs of `window` consecutive unfilled positions."""
+    if window < 1:
+        raise ValueError("window must be >= 1")
+    vals = [float(c) for c, t in zip(conf_row, tokens_row) if t == mask_id]
+    m = len(vals)
+    if m == 0:
+        return math.inf
+    if m < window:
+        return sum(vals) / m
+    best = math.inf
+    for r in range(m - window + 1):
+        best = min(best, sum(vals[r:r + window]) / window)
+    return best
+
+
+def branch_confidence_lowest_segment(conf_row, tokens_row, mask_id: int, eta: float) -> float:
+    """Mean of the ceil(eta m) least confident unfilled positions (at least one)."""
+    if not 0.0 < eta <= 1.0:
+        raise ValueError("eta must be in (0, 1]")
+    vals = sorted(float(c) for c, t in zip(conf_row, tokens_row) if t == mask_id)
+    m = len(vals)
+    if m == 0:
+        return math.inf
+    n = max(1, math.ceil(eta * m))
+    return sum(vals[:n]) / n
+
+
+def branch_score(conf_row, tokens_row, mask_id: int, metric: int = METRIC_MEAN,
+                 window: int = 4, eta: float = 0.25) -> float:
+    if metric == METRIC_MEAN:
+        return branch_confidence(conf_row, tokens_row, mask_id)
+    if metric == METRIC_WINDOW_MIN:
+        return branch_confidence_window_min(conf_row, tokens_row, mask_id, window)
+    if metric == METRIC_LOWEST_SEGMENT:
+        return branch_confidence_lowest_segment(conf_row, tokens_row, mask_id, eta)
+    raise ValueError(f"unknown metric {metric}")
+
+
+def select(branch_tokens, conf, valid, mask_id: int, metric: int = METRIC_MEAN,
+           window: int = 4, eta: float = 0.25):
     """Scores of all branches and B* = argmax (lowest branch index among ties)."""
     nb = len(branch_tokens)
     scores = np.empty(nb)
     for j in range(nb):
-        scores[j] = branch_confidence(conf[j], branch_tokens[j], mask_id) if valid[j] else -math.inf
+        scores[j] = (branch_score(conf[j], branch_tokens[j], mask_id, metric, window, eta)
+                     if valid[j] else -math.inf)
     best = 0
     for j in range(1, nb):
         if scores[j] > scores[best]:

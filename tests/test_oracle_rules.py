@@ -175,3 +175,79 @@ def test_confidence_softmax_properties():
         assert np.all(conf >= 1.0 / (V - 1) - 1e-15) and np.all(conf <= 1.0)
         assert np.array_equal(pred, np.argmax(sup, axis=-1))
         assert not np.any(pred == mask)
+
+
+# ------------------------------------------- alternative branch confidences
+def _rows(seed, n=300, L=12):
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        conf = rng.random(L)
+        tokens = np.where(rng.random(L) < 0.6, 7, rng.integers(0, 7, L))
+        yield conf, tokens
+
+
+def test_window_min_special_cases():
+    """w = 1: the smallest unfilled Conf; w >= m: the Eq. 2 mean; m = 0: +inf;
+    filled positions never matter."""
+    for conf, tokens in _rows(0):
+        un = tokens == 7
+        if not un.any():
+            assert lopa.branch_confidence_window_min(conf, tokens, 7, 3) == math.inf
+            continue
+        assert lopa.branch_confidence_window_min(conf, tokens, 7, 1) == pytest.approx(conf[un].min(), abs=0)
+        m = int(un.sum())
+        for w in (m, m + 1, 40):
+            assert lopa.branch_confidence_window_min(conf, tokens, 7, w) == pytest.approx(
+                lopa.branch_confidence(conf, tokens, 7), rel=1e-15)
+        c2 = np.where(un, conf, 1.0 - conf)
+        assert lopa.branch_confidence_window_min(c2, tokens, 7, 3) == \
+            lopa.branch_confidence_window_min(conf, tokens, 7, 3)
+
+
+def test_window_min_matches_convolution():
+    """Library special case: the window means are a 'valid' convolution of the
+    unfilled Conf sequence (position order) with a box of width w."""
+    for conf, tokens in _rows(1):
+        vals = conf[tokens == 7]
+        for w in (2, 3, 5):
+            if len(vals) < w:
+                continue
+            ref = np.convolve(vals, np.ones(w) / w, mode="valid").min()
+            assert lopa.branch_confidence_window_min(conf, tokens, 7, w) == pytest.approx(ref, rel=1e-12)
+            # reversing the position order gives the same windows
+            assert lopa.branch_confidence_window_min(conf[::-1], tokens[::-1], 7, w) == \
+                pytest.approx(ref, rel=1e-12)
+
+
+def test_lowest_segment_properties():
+    """eta = 1: the Eq. 2 mean; a tiny eta: the minimum; nondecreasing in eta,
+    never above the mean; equal to the mean of np.partition's k smallest."""
+    for conf, tokens in _rows(2):
+        un = tokens == 7
+        if not un.any():
+            assert lopa.branch_confidence_lowest_segment(conf, tokens, 7, 0.5) == math.inf
+            continue
+        mean = lopa.branch_confidence(conf, tokens, 7)
+        assert lopa.branch_confidence_lowest_segment(conf, tokens, 7, 1.0) == pytest.approx(mean, rel=1e-15)
+        assert lopa.branch_confidence_lowest_segment(conf, tokens, 7, 1e-9) == conf[un].min()
+        prev = -math.inf
+        for eta in (0.1, 0.25, 0.5, 0.75, 1.0):
+            v = lopa.branch_confidence_lowest_segment(conf, tokens, 7, eta)
+            assert prev <= v + 1e-15 and v <= mean + 1e-15
+            prev = v
+            k = max(1, math.ceil(eta * un.sum()))
+            assert v == pytest.approx(np.partition(conf[un], k - 1)[:k].mean(), rel=1e-12)
+
+
+def test_select_with_metrics_invalid_and_ties():
+    bt = np.array([[7, 7, 1, 7], [7, 7, 1, 7], [2, 7, 1, 7]])
+    conf = np.array([[0.2, 0.9, 0.5, 0.4], [0.2, 0.9, 0.5, 0.4], [0.1, 0.3, 0.5, 0.3]])
+    for metric in (lopa.METRIC_WINDOW_MIN, lopa.METRIC_LOWEST_SEGMENT):
+        s, w = lopa.select(bt, conf, np.array([1, 1, 1], np.uint8), 7, metric, 2, 0.5)
+        assert s[0] == s[1] and w == 0          # identical rows tie: lowest index
+        s, w = lopa.select(bt, conf, np.array([0, 1, 1], np.uint8), 7, metric, 2, 0.5)
+        assert s[0] == -math.inf and w == 1
+    # hand-worked: unfilled Conf of row 0 in position order 0.2, 0.9, 0.4
+    assert lopa.branch_score(conf[0], bt[0], 7, lopa.METRIC_WINDOW_MIN, 2, 0) == pytest.approx(0.55)
+    assert lopa.branch_score(conf[0], bt[0], 7, lopa.METRIC_LOWEST_SEGMENT, 4, 0.5) == pytest.approx(0.3)
+    assert lopa.branch_score(conf[2], bt[2], 7, lopa.METRIC_WINDOW_MIN, 2, 0) == pytest.approx(0.3)
