@@ -180,6 +180,28 @@ int lopa_branch_confidence_select(const int32_t* branch_tokens, const float* con
                                   float* next_conf, int32_t* next_pred,
                                   int32_t* next_unfilled, void* stream);
 
+/* Alternative branch confidences (Sec. 3.2 names them after Eq. 2 without a
+ * formula; these are the readings implemented). Same arguments, outputs and
+ * selection rule as lopa_branch_confidence_select, with scores[j] for a valid
+ * row j with m > 0 unfilled positions p_1 < ... < p_m, c_i = conf[j][p_i]:
+ *   LOPA_METRIC_MEAN            the Eq. 2 mean (window, eta unused);
+ *   LOPA_METRIC_WINDOW_MIN      the smallest mean of `window` consecutive c_i
+ *                               ("local quality"; the mean of all m if
+ *                               m <= window); window >= 1;
+ *   LOPA_METRIC_LOWEST_SEGMENT  the mean of the ceil(eta*m) smallest c_i, at
+ *                               least one ("weak links"; ceil of the double
+ *                               product of eta and m); 0 < eta <= 1.
+ * m = 0 gives +inf and an invalid row -inf, as in Eq. 2. Errors: LOPA_EINVAL
+ * for an unknown metric or a parameter outside its range. */
+enum { LOPA_METRIC_MEAN = 0, LOPA_METRIC_WINDOW_MIN = 1, LOPA_METRIC_LOWEST_SEGMENT = 2 };
+int lopa_branch_confidence_select_metric(const int32_t* branch_tokens, const float* conf,
+                                         const int32_t* pred, const uint8_t* valid,
+                                         int32_t n_branches, int32_t L, int32_t mask_id,
+                                         int32_t metric, int32_t window, float eta, float* scores,
+                                         int32_t* winner, int32_t* next_tokens, float* next_conf,
+                                         int32_t* next_pred, int32_t* next_unfilled,
+                                         void* stream);
+
 /* Sec. 3.4 Commit-Winner-Cache, single-GPU form: copy the staged post-RoPE
  * K/V of branch *winner (a DEVICE int32, read by the kernel: no host sync) for
  * all layers into cache rows [prefix_len, prefix_len + L). The staging must

@@ -161,8 +161,10 @@ def init_block(model: OracleModel, cache: KVCache, prefix_len: int, L: int):
     return tokens, out["conf"][0], out["pred"][0]
 
 
-def lopa_step(model: OracleModel, cache: KVCache, prefix_len: int, state, k: int, tau: float):
+def lopa_step(model: OracleModel, cache: KVCache, prefix_len: int, state, k: int, tau: float,
+              metric: int = METRIC_MEAN, window: int = 4, eta: float = 0.25):
     """One LoPA iteration (Alg. 1): build, verify in one pass, score, select, commit.
+    metric / window / eta: the branch confidence (Eq. 2 or an alternative above).
 
     Returns (new_state, info).  info holds the branches, scores, winner, the
     verification outputs and the committed offset."""
@@ -174,7 +176,7 @@ def lopa_step(model: OracleModel, cache: KVCache, prefix_len: int, state, k: int
     conf_b = np.zeros((nb, len(tokens)))
     pred_b = np.zeros((nb, len(tokens)), dtype=np.int64)
     conf_b[:n_valid], pred_b[:n_valid] = out["conf"], out["pred"]
-    scores, w = select(bt, conf_b, valid, mask_id)
+    scores, w = select(bt, conf_b, valid, mask_id, metric, window, eta)
     off = cache.commit(prefix_len, out["k"][w], out["v"][w])
     new_state = (bt[w].copy(), conf_b[w].copy(), pred_b[w].copy())
     info = dict(branch_tokens=bt, fill_pos=fill_pos, valid=valid, n_valid=n_valid,
@@ -183,13 +185,14 @@ def lopa_step(model: OracleModel, cache: KVCache, prefix_len: int, state, k: int
     return new_state, info
 
 
-def decode_block(model, cache, prefix_len: int, L: int, k: int, tau: float, trace=None):
+def decode_block(model, cache, prefix_len: int, L: int, k: int, tau: float, trace=None,
+                 metric: int = METRIC_MEAN, window: int = 4, eta: float = 0.25):
     """Decode one block to completion.  Returns (tokens, iterations, forwards)."""
     state = init_block(model, cache, prefix_len, L)
     forwards, iters = 1, 0
     mask_id = model.cfg["mask_id"]
     while True:
-        state, info = lopa_step(model, cache, prefix_len, state, k, tau)
+        state, info = lopa_step(model, cache, prefix_len, state, k, tau, metric, window, eta)
         forwards += 1
         iters += 1
         if trace is not None:

@@ -19,7 +19,8 @@ import ctypes as C
 import torch
 
 from ._abi import (EXPORTS, LIB_PATH, LOPA_ECAPACITY, LOPA_EHIP, LOPA_EINVAL, LOPA_ENOMEM,  # noqa: F401
-                   LOPA_ESHAPE, LOPA_OK, MAX_BLOCK, MAX_ROWS, PROF_KINDS, LopaError, lib,
+                   LOPA_ESHAPE, LOPA_OK, MAX_BLOCK, MAX_ROWS, METRIC_LOWEST_SEGMENT, METRIC_MEAN,
+                   METRIC_WINDOW_MIN, PROF_KINDS, LopaError, lib,
                    lopa_layer_weights, lopa_model_cfg, lopa_weight_ptrs)
 
 
@@ -164,6 +165,18 @@ def lopa_branch_confidence_select(branch_tokens, conf, pred, valid, n_branches, 
         _ptr(winner, I32, "winner"), _ptr(next_tokens, I32, "next_tokens"),
         _ptr(next_conf, F32, "next_conf"), _ptr(next_pred, I32, "next_pred"),
         _ptr(next_unfilled, I32, "next_unfilled"), _stream(stream)))
+
+
+def lopa_branch_confidence_select_metric(branch_tokens, conf, pred, valid, n_branches, L, mask_id,
+                                         metric, window, eta, scores, winner, next_tokens,
+                                         next_conf, next_pred, next_unfilled, stream=None):
+    _check(lib.lopa_branch_confidence_select_metric(
+        _ptr(branch_tokens, I32, "branch_tokens"), _ptr(conf, F32, "conf"), _ptr(pred, I32, "pred"),
+        _ptr(valid, U8, "valid"), n_branches, L, mask_id, metric, window, eta,
+        _ptr(scores, F32, "scores"), _ptr(winner, I32, "winner"),
+        _ptr(next_tokens, I32, "next_tokens"), _ptr(next_conf, F32, "next_conf"),
+        _ptr(next_pred, I32, "next_pred"), _ptr(next_unfilled, I32, "next_unfilled"),
+        _stream(stream)))
 
 
 def lopa_debug_hidden(model: Model, kv: KV, prefix_len, branch_tokens, n_branches, L, n_layers,

@@ -587,20 +587,39 @@ int lopa_debug_hidden(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
                      n_layers, x_out);
 }
 
-int lopa_branch_confidence_select(const int32_t* branch_tokens, const float* conf,
-                                  const int32_t* pred, const uint8_t* valid, int32_t n_branches,
-                                  int32_t L, int32_t mask_id, float* scores, int32_t* winner,
-                                  int32_t* next_tokens, float* next_conf, int32_t* next_pred,
-                                  int32_t* next_unfilled, void* stream) {
+int lopa_branch_confidence_select_metric(const int32_t* branch_tokens, const float* conf,
+                                         const int32_t* pred, const uint8_t* valid,
+                                         int32_t n_branches, int32_t L, int32_t mask_id,
+                                         int32_t metric, int32_t window, float eta, float* scores,
+                                         int32_t* winner, int32_t* next_tokens, float* next_conf,
+                                         int32_t* next_pred, int32_t* next_unfilled,
+                                         void* stream) {
   if (!branch_tokens || !conf || !pred || !valid || !scores || !winner || !next_tokens ||
       !next_conf || !next_pred || !next_unfilled)
     return fail(LOPA_EINVAL, "null pointer argument");
   if (n_branches < 1 || n_branches > 1024) return fail(LOPA_ESHAPE, "n_branches %d outside [1, 1024]", n_branches);
   if (L < 1 || L > LOPA_MAX_BLOCK) return fail(LOPA_ESHAPE, "L = %d outside [1, %d]", L, LOPA_MAX_BLOCK);
   if (mask_id < 0) return fail(LOPA_EINVAL, "mask_id < 0");
-  HIP_TRY(launch_select(branch_tokens, conf, pred, valid, n_branches, L, mask_id, scores, winner,
-                        next_tokens, next_conf, next_pred, next_unfilled, (hipStream_t)stream));
+  if (metric < LOPA_METRIC_MEAN || metric > LOPA_METRIC_LOWEST_SEGMENT)
+    return fail(LOPA_EINVAL, "unknown branch confidence metric %d", metric);
+  if (metric == LOPA_METRIC_WINDOW_MIN && window < 1) return fail(LOPA_EINVAL, "window %d < 1", window);
+  if (metric == LOPA_METRIC_LOWEST_SEGMENT && !(eta > 0.f && eta <= 1.f))
+    return fail(LOPA_EINVAL, "eta outside (0, 1]");
+  HIP_TRY(launch_select(branch_tokens, conf, pred, valid, n_branches, L, mask_id, metric, window,
+                        eta, scores, winner, next_tokens, next_conf, next_pred, next_unfilled,
+                        (hipStream_t)stream));
   return LOPA_OK;
+}
+
+int lopa_branch_confidence_select(const int32_t* branch_tokens, const float* conf,
+                                  const int32_t* pred, const uint8_t* valid, int32_t n_branches,
+                                  int32_t L, int32_t mask_id, float* scores, int32_t* winner,
+                                  int32_t* next_tokens, float* next_conf, int32_t* next_pred,
+                                  int32_t* next_unfilled, void* stream) {
+  return lopa_branch_confidence_select_metric(branch_tokens, conf, pred, valid, n_branches, L,
+                                              mask_id, LOPA_METRIC_MEAN, 1, 1.f, scores, winner,
+                                              next_tokens, next_conf, next_pred, next_unfilled,
+                                              stream);
 }
 
 int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,

@@ -8,10 +8,12 @@ hipError_t launch_build_branches(const int32_t* tokens, const float* conf, const
                                  int L, int mask_id, float tau, int k, int32_t* branch_tokens,
                                  int32_t* fill_pos, uint8_t* valid, int32_t* n_valid,
                                  hipStream_t s);
+// metric 0: Eq. 2 mean; 1: window minimum (window >= 1); 2: lowest-segment
+// mean (0 < eta <= 1). nb <= 1024, L <= 64.
 hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pred,
-                         const uint8_t* valid, int nb, int L, int mask_id, float* scores,
-                         int32_t* winner, int32_t* nt, float* nc, int32_t* np, int32_t* nu,
-                         hipStream_t s);
+                         const uint8_t* valid, int nb, int L, int mask_id, int metric,
+                         int window, float eta, float* scores, int32_t* winner, int32_t* nt,
+                         float* nc, int32_t* np, int32_t* nu, hipStream_t s);
 // KV layouts. Cache: [layers][2][Hkv][d * vld] (vld = max_len rounded up to
 // 8): K position p, dim e at p * d + e; V (transposed) at e * vld + p.
 // Staging: [branches][layers][2][Hkv][d * vlds], the same with Lcap, vlds.

@@ -71,25 +71,64 @@ __global__ __launch_bounds__(64) void build_branches_kernel(
   if (i == 0) n_valid[0] = 1 + k_eff;
 }
 
-// Eq. 2 per branch: one wavefront per branch row (fixed reduction order, so
-// identical rows give bit-identical scores), then the argmax and the next state.
+// Eq. 2 per branch (metric 0), or one of the alternative branch confidences
+// named after it (Sec. 3.2): 1 = the smallest mean over runs of `window`
+// consecutive unfilled positions (position order; all of them if fewer),
+// 2 = the mean of the ceil(eta m) least confident unfilled positions (at
+// least one). One wavefront per branch row with fixed reduction orders, so
+// identical rows give bit-identical scores; then the argmax and the next state.
 __global__ __launch_bounds__(256) void select_kernel(
     const int32_t* __restrict__ branch_tokens, const float* __restrict__ conf,
     const int32_t* __restrict__ pred, const uint8_t* __restrict__ valid, int nb, int L,
-    int mask_id, float* __restrict__ scores, int32_t* __restrict__ winner,
-    int32_t* __restrict__ next_tokens, float* __restrict__ next_conf,
-    int32_t* __restrict__ next_pred, int32_t* __restrict__ next_unfilled) {
+    int mask_id, int metric, int window, float eta, float* __restrict__ scores,
+    int32_t* __restrict__ winner, int32_t* __restrict__ next_tokens,
+    float* __restrict__ next_conf, int32_t* __restrict__ next_pred,
+    int32_t* __restrict__ next_unfilled) {
   __shared__ float s_score[1024];
+  __shared__ float s_row[4][64];
   __shared__ int s_win;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   for (int j = wv; j < nb; j += 4) {
     const bool in = lane < L;
     const int t = in ? branch_tokens[(int64_t)j * L + lane] : 0;
     const bool m = in && t == mask_id;
-    float s = m ? conf[(int64_t)j * L + lane] : 0.f;
-    s = wave_sum(s);
-    const int cnt = __popcll(__ballot(m));
-    float sc = cnt ? s / (float)cnt : INFINITY;
+    const float c = m ? conf[(int64_t)j * L + lane] : 0.f;
+    const uint64_t bal = __ballot(m);
+    const int cnt = __popcll(bal);
+    float sc = INFINITY;
+    if (cnt) {
+      const float mean = wave_sum(c) / (float)cnt;
+      sc = mean;
+      if (metric == 1 && cnt > window) {
+        // unfilled Conf compacted in position order, then each run start sums
+        // its run in order
+        const int rank = __popcll(bal & ((1ull << lane) - 1ull));
+        if (m) s_row[wv][rank] = c;
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+        __builtin_amdgcn_wave_barrier();
+        float v = INFINITY;
+        if (lane <= cnt - window) {
+          float acc = 0.f;
+          for (int i = 0; i < window; ++i) acc += s_row[wv][lane + i];
+          v = acc / (float)window;
+        }
+        sc = -wave_max(-v);
+        __builtin_amdgcn_wave_barrier();
+      } else if (metric == 2) {
+        // rank in (Conf ascending, position ascending) order among the unfilled
+        s_row[wv][lane] = m ? c : INFINITY;
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_wave_barrier();
+        int rank = 0;
+        for (int i = 0; i < L; ++i) {
+          const float o = s_row[wv][i];
+          rank += (o < c || (o == c && i < lane)) ? 1 : 0;
+        }
+        const int kk = max(1, (int)ceil((double)eta * (double)cnt));
+        sc = wave_sum(m && rank < kk ? c : 0.f) / (float)kk;
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
     if (!valid[j]) sc = -INFINITY;
     if (lane == 0) {
       scores[j] = sc;
@@ -179,11 +218,14 @@ hipError_t launch_build_branches(const int32_t* tokens, const float* conf, const
 }
 
 hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pred,
-                         const uint8_t* valid, int nb, int L, int mask_id, float* scores,
-                         int32_t* winner, int32_t* nt, float* nc, int32_t* np, int32_t* nu,
-                         hipStream_t s) {
+                         const uint8_t* valid, int nb, int L, int mask_id, int metric,
+                         int window, float eta, float* scores, int32_t* winner, int32_t* nt,
+                         float* nc, int32_t* np, int32_t* nu, hipStream_t s) {
+  if (nb < 1 || nb > 1024 || L < 1 || L > 64 || metric < 0 || metric > 2 ||
+      (metric == 1 && window < 1) || (metric == 2 && !(eta > 0.f && eta <= 1.f)))
+    return hipErrorInvalidValue;
   hipLaunchKernelGGL(select_kernel, dim3(1), dim3(256), 0, s, bt, conf, pred, valid, nb, L,
-                     mask_id, scores, winner, nt, nc, np, nu);
+                     mask_id, metric, window, eta, scores, winner, nt, nc, np, nu);
   return hipGetLastError();
 }
 

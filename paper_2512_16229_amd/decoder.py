@@ -10,13 +10,19 @@ from __future__ import annotations
 
 import torch
 
-from . import (KV, Model, lopa_branch_confidence_select, lopa_build_branches, lopa_commit_kv,
+from . import (KV, METRIC_MEAN, Model, lopa_branch_confidence_select,
+               lopa_branch_confidence_select_metric, lopa_build_branches, lopa_commit_kv,
                lopa_verify_forward)
 
 
 class Decoder:
-    def __init__(self, model: Model, kv: KV, L: int, k: int, tau: float):
+    """metric / window / eta choose the branch confidence of the selection
+    (METRIC_MEAN: Eq. 2; the alternatives of lopa_branch_confidence_select_metric)."""
+
+    def __init__(self, model: Model, kv: KV, L: int, k: int, tau: float, metric: int = METRIC_MEAN,
+                 window: int = 4, eta: float = 0.25):
         self.model, self.kv, self.L, self.k, self.tau = model, kv, L, k, float(tau)
+        self.metric, self.window, self.eta = int(metric), int(window), float(eta)
         self.mask_id = model.cfg["mask_id"]
         nb = k + 1
         dev = "cuda"
@@ -70,9 +76,15 @@ class Decoder:
                             self.branch_tokens, self.fill_pos, self.valid, self.n_valid)
         lopa_verify_forward(self.model, self.kv, P, self.branch_tokens, nb, L, self.conf_b,
                             self.pred_b)
-        lopa_branch_confidence_select(self.branch_tokens, self.conf_b, self.pred_b, self.valid, nb,
-                                      L, self.mask_id, self.scores, self.winner, self.next_tokens,
-                                      self.next_conf, self.next_pred, self.next_unfilled)
+        outs = (self.scores, self.winner, self.next_tokens, self.next_conf, self.next_pred,
+                self.next_unfilled)
+        if self.metric == METRIC_MEAN:
+            lopa_branch_confidence_select(self.branch_tokens, self.conf_b, self.pred_b, self.valid,
+                                          nb, L, self.mask_id, *outs)
+        else:
+            lopa_branch_confidence_select_metric(self.branch_tokens, self.conf_b, self.pred_b,
+                                                 self.valid, nb, L, self.mask_id, self.metric,
+                                                 self.window, self.eta, *outs)
         lopa_commit_kv(self.kv, self.winner, P, L, self.append_offset)
         self.tokens, self.next_tokens = self.next_tokens, self.tokens
         self.conf, self.next_conf = self.next_conf, self.conf

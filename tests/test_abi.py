@@ -69,6 +69,19 @@ def test_select_validation(lp):
     assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, -3, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
 
 
+def test_select_metric_validation(lp):
+    f = lp.lib.lopa_branch_confidence_select_metric
+    o = (FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 3, 1, 1.0, *o) == -1        # unknown metric
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, -1, 1, 1.0, *o) == -1
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 1, 0, 1.0, *o) == -1        # window < 1
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 2, 1, 0.0, *o) == -1        # eta outside (0, 1]
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 2, 1, 1.5, *o) == -1
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 2, 1, float("nan"), *o) == -1
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 65, 5, 1, 2, 1.0, *o) == -2        # L too large
+    assert f(None, FAKE, FAKE, FAKE, 4, 16, 5, 0, 1, 1.0, *o) == -1
+
+
 @pytest.mark.parametrize("field,value,code", [
     ("hidden", 200, -2), ("head_dim", 96, -2), ("kv_heads", 3, -2), ("ffn", 700, -2),
     ("mask_id", 1024, -1), ("mask_id", -1, -1), ("layers", 0, -1), ("rms_eps", 0.0, -1),

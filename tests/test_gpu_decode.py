@@ -105,16 +105,22 @@ def _first_divergence(gtrace, otrace):
     return None
 
 
-@pytest.mark.parametrize("cfgname,P,L,k,tau", [("tiny", 64, 16, 3, 0.9), ("tiny", 32, 16, 0, 0.9),
-                                               ("small", 100, 32, 7, 0.9), ("small128", 40, 16, 2, 0.7)])
-def test_free_running_block(cfgname, P, L, k, tau):
-    log(f"free-running {cfgname} P={P} L={L} k={k} tau={tau}")
+@pytest.mark.parametrize("cfgname,P,L,k,tau,metric", [
+    ("tiny", 64, 16, 3, 0.9, (0, 4, 0.25)), ("tiny", 32, 16, 0, 0.9, (0, 4, 0.25)),
+    ("small", 100, 32, 7, 0.9, (0, 4, 0.25)), ("small128", 40, 16, 2, 0.7, (0, 4, 0.25)),
+    ("tiny", 64, 16, 3, 0.9, (1, 4, 0.25)), ("tiny", 64, 16, 5, 0.9, (2, 4, 0.25))])
+def test_free_running_block(cfgname, P, L, k, tau, metric):
+    """metric = (branch confidence, window, eta): Eq. 2, or the window minimum /
+    lowest-segment alternatives."""
+    log(f"free-running {cfgname} P={P} L={L} k={k} tau={tau} metric={metric}")
     s = Setup(cfgname, P, L, k)
     dec = s.gpu_prefill(tau)
+    dec.metric, dec.window, dec.eta = metric[0], metric[1], metric[2]
     gtrace = []
     g_iters = dec.decode_block(P, gtrace)
     otrace = []
-    o_tokens, o_iters, _ = lopa.decode_block(s.faith, s.cache_f.copy(), P, L, k, f32(tau), otrace)
+    o_tokens, o_iters, _ = lopa.decode_block(s.faith, s.cache_f.copy(), P, L, k, f32(tau), otrace,
+                                             metric[0], metric[1], f32(metric[2]))
     g_tokens = dec.tokens.cpu().numpy()
     t = _first_divergence(gtrace, otrace)
     mask = s.cfg["mask_id"]

@@ -62,10 +62,18 @@ def test_build_branches_matches_oracle(lp, L, k, tau, style, seed):
     assert int(nv.item()) == rnv
 
 
+METRICS = [(0, 1, 1.0), (1, 1, 1.0), (1, 3, 1.0), (1, 8, 1.0), (2, 1, 0.1), (2, 1, 0.25),
+           (2, 1, 1.0)]
+
+
+@pytest.mark.parametrize("metric,window,eta", METRICS, ids=lambda v: str(v))
 @pytest.mark.parametrize("nb,L,seed", [(1, 16, 0), (4, 16, 1), (8, 32, 2), (16, 32, 3),
                                        (3, 7, 4), (8, 64, 5), (33, 9, 6)])
-def test_select_matches_oracle(lp, nb, L, seed):
-    log(f"select nb={nb} L={L} seed={seed}")
+def test_select_matches_oracle(lp, nb, L, seed, metric, window, eta):
+    """Eq. 2 (metric 0) and the alternative branch confidences (1: window
+    minimum, 2: lowest-segment mean) against the oracle."""
+    log(f"select nb={nb} L={L} seed={seed} metric={metric} window={window} eta={eta}")
+    eta = f32(eta)
     rng = np.random.default_rng(seed)
     mask = 77
     for trial in range(20):
@@ -85,12 +93,15 @@ def test_select_matches_oracle(lp, nb, L, seed):
                    nc=torch.empty(L, dtype=torch.float32, device="cuda"),
                    np_=torch.empty(L, dtype=torch.int32, device="cuda"),
                    nu=torch.empty(1, dtype=torch.int32, device="cuda"))
-        lp.lopa_branch_confidence_select(_dev(bt.ravel(), torch.int32), _dev(conf.ravel(), torch.float32),
-                                         _dev(pred.ravel(), torch.int32), _dev(valid, torch.uint8), nb, L,
-                                         mask, out["scores"], out["winner"], out["nt"], out["nc"],
-                                         out["np_"], out["nu"])
+        args = (_dev(bt.ravel(), torch.int32), _dev(conf.ravel(), torch.float32),
+                _dev(pred.ravel(), torch.int32), _dev(valid, torch.uint8), nb, L, mask)
+        outs = (out["scores"], out["winner"], out["nt"], out["nc"], out["np_"], out["nu"])
+        if metric == 0 and trial % 2 == 0:
+            lp.lopa_branch_confidence_select(*args, *outs)
+        else:
+            lp.lopa_branch_confidence_select_metric(*args, metric, window, eta, *outs)
         torch.cuda.synchronize()
-        rs, rw = lopa.select(bt, conf.astype(np.float64), valid, mask)
+        rs, rw = lopa.select(bt, conf.astype(np.float64), valid, mask, metric, window, eta)
         gs = out["scores"].cpu().numpy().astype(np.float64)
         fin = np.isfinite(rs)
         assert np.array_equal(np.isinf(gs), ~fin) and np.array_equal(np.sign(gs[~fin]), np.sign(rs[~fin]))
