@@ -44,9 +44,7 @@ constexpr int RING = LEAD + 2;  // weight chunks in LDS: a pair in use + LEAD in
 template <int EPI, int NB>
 struct GemmSmem {
   static constexpr int CHUNK = NB * 2048;  // bytes of weights per iteration
-  static constexpr int SWIGLU_SP = NB / 2 * 16 + 8;  // padded staging row (bf16)
   static constexpr int BYTES = RING * CHUNK;
-  static_assert(EPI != EPI_SWIGLU || 4 * 64 * SWIGLU_SP * 2 <= RING * CHUNK, "staging fits");
   static_assert(EPI != EPI_LMHEAD || 4 * 64 * 16 * 12 <= RING * CHUNK, "reduction area fits");
 };
 
@@ -132,7 +130,8 @@ __device__ __forceinline__ void mfma_settle() {
 
 // ------------------------------------------------------------------ epilogues
 // acc[mb][nb][j]: row row0 + 16 mb + 4 g + j, column 16 (tile NB + nb) + c16
-// of this wavefront (g = lane / 16, c16 = lane % 16).
+// of this wavefront (g = lane / 16, c16 = lane % 16); the SwiGLU GEMM holds
+// the transposed tile (see swiglu_epilogue).
 
 template <int NB>
 __device__ __forceinline__ void resid_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
@@ -155,34 +154,41 @@ __device__ __forceinline__ void resid_epilogue(const GemmArgs& a, f32x4 (&acc)[4
 
 // gate / up blocks alternate (block 2p: gate columns 16p.., block 2p + 1: up);
 // output block p of the tile -> columns 16 (tile NB / 2 + p) of the packed
-// down-projection operand. Staged through LDS so each lane stores 16 bytes.
+// down-projection operand. The SwiGLU GEMM accumulates the transposed tile
+// (weights as the MFMA's first operand), so acc[mb][nb][j] holds row
+// row0 + 16 mb + c16, column 16 (tile NB + nb) + 4 g + j: a lane's four
+// outputs of a block are four consecutive columns of one row, stored as one
+// 8-byte write (the packed operand keeps 8 consecutive columns of a row in one
+// 16-byte lane slot).
 template <int NB>
 __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
-                                                int row0, int lane, uint16_t* e) {
-  constexpr int PAIRS = NB / 2, SP = PAIRS * 16 + 8;
+                                                int row0, int lane) {
+  constexpr int PAIRS = NB / 2;
   const int g = lane >> 4, c16 = lane & 15;
-#pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
-#pragma unroll
-    for (int p = 0; p < PAIRS; ++p)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
-        // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
-        // 1 ulp each, far below the bf16 rounding of the result)
-        const float ex = __builtin_amdgcn_exp2f(-gt * 1.4426950408889634f);
-        const float h = gt * __builtin_amdgcn_rcpf(1.0f + ex) * up;
-        e[(mb * 16 + g * 4 + j) * SP + p * 16 + c16] = f2bf_bits(h);
-      }
-  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wavefront's LDS writes done
-  __builtin_amdgcn_wave_barrier();
   const int Nout = a.N >> 1;
-  for (int q = lane; q < 64 * PAIRS * 2; q += 64) {
-    const int rr = q / (PAIRS * 2), cg = q % (PAIRS * 2);
-    const int r = row0 + rr, col = tile * PAIRS * 16 + cg * 8;
-    if (r >= a.M || col >= Nout) continue;
-    const uint4 v = *(const uint4*)(e + rr * SP + cg * 8);
-    *(uint4*)(a.a_out + packA_off(r, col, a.Mp)) = v;
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb) {
+    const int r = row0 + mb * 16 + c16;
+#pragma unroll
+    for (int p = 0; p < PAIRS; ++p) {
+      uint32_t hv[2];
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        float h2[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int j = 2 * jj + u;
+          const float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
+          // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
+          // 1 ulp each, far below the bf16 rounding of the result)
+          const float ex = __builtin_amdgcn_exp2f(-gt * 1.4426950408889634f);
+          h2[u] = gt * __builtin_amdgcn_rcpf(1.0f + ex) * up;
+        }
+        hv[jj] = (uint32_t)f2bf_bits(h2[0]) | ((uint32_t)f2bf_bits(h2[1]) << 16);
+      }
+      const int col = (tile * PAIRS + p) * 16 + g * 4;
+      if (r < a.M && col < Nout) *(uint2*)(a.a_out + packA_off(r, col, a.Mp)) = make_uint2(hv[0], hv[1]);
+    }
   }
 }
 
@@ -315,7 +321,10 @@ constexpr int BPF = 4;
         bf_[fn_] = (fn_ < 2 * NB ? wl0_ : wl1_)[((gn_ % NB) * 2 + gn_ / NB) * 64 + lane];  \
       }                                                                                  \
       _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_)                                \
-        mfma_acc(acc[mb_][g_ % NB], (e_ ? s1 : s0)[(g_ / NB) * 4 + mb_], bf_[f_]);       \
+        if constexpr (EPI == EPI_SWIGLU) /* transposed tile: lanes hold output rows */  \
+          mfma_acc(acc[mb_][g_ % NB], bf_[f_], (e_ ? s1 : s0)[(g_ / NB) * 4 + mb_]);     \
+        else                                                                             \
+          mfma_acc(acc[mb_][g_ % NB], (e_ ? s1 : s0)[(g_ / NB) * 4 + mb_], bf_[f_]);     \
       if (g_ >= 1 && g_ <= NB / 2) GEMM_ISSUE_W(g_ - 1, e_ ? is1_ : is0_);               \
       if (g_ == NB - 1) GEMM_ISSUE_A((e_ ? s1 : s0), 0);                                 \
       if (g_ == 2 * NB - 1) {                                                            \
@@ -396,13 +405,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
         lm_epilogue<NB>(a, acc, t_lo, row0, lane, (float*)smem + wv * 64 * 16 * 3);
       }
       if constexpr (EPI == EPI_RESID) resid_epilogue<NB>(a, acc, t_lo, row0, lane);
-      if constexpr (EPI == EPI_SWIGLU) {
-        // the weight ring becomes the staging area once every copy (including
-        // the repeated last chunk) has landed in all wavefronts
-        lds_barrier();
-        uint16_t* stage = (uint16_t*)smem + wv * 64 * SM::SWIGLU_SP;
-        swiglu_epilogue<NB>(a, acc, t_lo, row0, lane, stage);
-      }
+      if constexpr (EPI == EPI_SWIGLU) swiglu_epilogue<NB>(a, acc, t_lo, row0, lane);
     } else if constexpr (EPI == EPI_RESID) {
       // row-major partial sums [split][Mp][N], added by the following RMSNorm
       const int g = lane >> 4, c16 = lane & 15;
