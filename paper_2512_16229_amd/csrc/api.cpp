@@ -76,7 +76,8 @@ int round_up(int x, int m) { return m * ((x + m - 1) / m); }
 // 256 x 64 bf16 activation chunk from L2 plus nb x 2 KiB of weights), at the
 // per-CU rate measured for these kernels (~60 GB/s), and (b) the round's
 // weight bytes at the sustained HBM rate (~6.5 TB/s); split-K adds its fp32
-// partial sums, written and read back (~5 TB/s), and QKV its fix-up launch.
+// partial sums, written (~5 TB/s) and read back by the small kernel that
+// reduces them (~3 TB/s), and QKV its fix-up launch.
 // The weights are packed per tile, so nb is chosen once, when the model is
 // created (fixed_nb = 0: choose), and later plans choose S only.
 struct GemmPlan {
@@ -85,7 +86,8 @@ struct GemmPlan {
 GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_nb) {
   if (epi == EPI_SWIGLU) return {10, nblocks / 10, 1};
   if (epi == EPI_LMHEAD) return {8, nblocks / 8, 1};
-  constexpr double CU_BPUS = 60e3, HBM_BPUS = 6.5e6, PART_BPUS = 5e6, FIXUP_US = 7.0;
+  constexpr double CU_BPUS = 60e3, HBM_BPUS = 6.5e6, PART_W_BPUS = 5e6, PART_R_BPUS = 3e6;
+  constexpr double FIXUP_US = 7.0;
   const int Q = KC / 4;
   GemmPlan best{8, nblocks / 8, 1};
   double best_t = 1e300;
@@ -101,7 +103,7 @@ GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_n
       double t = (double)rounds * std::max(per_cu / CU_BPUS, w_round / HBM_BPUS);
       const double part = epi == EPI_QKV ? (double)wgs * nb * 16384.0
                                          : (S > 1 ? (double)S * MT * 256.0 * tiles * nb * 16 * 4 : 0.0);
-      t += 2.0 * part / PART_BPUS;
+      t += part / PART_W_BPUS + part / PART_R_BPUS;
       if (epi == EPI_QKV) t += FIXUP_US;
       if (t < best_t) {
         best_t = t;
