@@ -85,7 +85,7 @@ struct GemmPlan {
 };
 GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_nb) {
   if (epi == EPI_SWIGLU) return {10, nblocks / 10, 1};
-  if (epi == EPI_LMHEAD) return {8, nblocks / 8, 1};
+  if (epi == EPI_LMHEAD) return {fixed_nb, nblocks / fixed_nb, 1};
   constexpr double CU_BPUS = 60e3, HBM_BPUS = 6.5e6, PART_W_BPUS = 5e6, PART_R_BPUS = 3e6;
   constexpr double FIXUP_US = 7.0;
   const int Q = KC / 4;
@@ -128,7 +128,7 @@ struct lopa_model {
   int num_cu = 0;
   int n_qkv = 0;
   int blk_qkv = 0, blk_h = 0, blk_gu = 0, blk_lm = 0;  // packed 16-column blocks
-  int nb_qkv = 0, nb_o = 0, nb_down = 0;                // tile widths of the packed weights
+  int nb_qkv = 0, nb_o = 0, nb_down = 0, nb_lm = 0;     // tile widths of the packed weights
   int tiles_lm = 0;                                     // LM-head column tiles
   std::vector<LayerPack> layers;
   uint16_t* embed = nullptr;
@@ -208,7 +208,7 @@ StepPlans step_plans(const lopa_model* m, int MT) {
   p.o = plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu, m->nb_o);
   p.gu = plan_gemm(EPI_SWIGLU, m->blk_gu, c.hidden / 64, MT, m->num_cu, 10);
   p.down = plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu, m->nb_down);
-  p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, c.hidden / 64, MT, m->num_cu, 8);
+  p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, c.hidden / 64, MT, m->num_cu, m->nb_lm);
   return p;
 }
 }  // namespace
@@ -276,8 +276,6 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
   m->blk_qkv = round_up(m->n_qkv / 16, 8);
   m->blk_h = round_up(H / 16, 8);
   m->blk_gu = round_up(2 * F / 16, 10);
-  m->blk_lm = round_up((V + 15) / 16, 8);
-  m->tiles_lm = m->blk_lm / 8;
   auto bail = [&](int code) {
     delete m;
     return code;
@@ -286,6 +284,22 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
       hipDeviceGetAttribute(&m->num_cu, hipDeviceAttributeMultiprocessorCount, m->device) !=
           hipSuccess)
     return bail(fail(LOPA_EHIP, "no HIP device"));
+  // LM head: 8- or 10-block tiles (whole tiles, no split: the epilogue reduces
+  // each tile's softmax statistics), whichever gives fewer rounds of
+  // workgroups x per-workgroup bytes (activation chunk + weights per k-chunk)
+  {
+    double best = 1e300;
+    for (int nb : {8, 10}) {
+      const int tiles = round_up((V + 15) / 16, nb) / nb;
+      const double t = std::ceil((double)tiles / m->num_cu) * (32768.0 + nb * 2048.0);
+      if (t < best) {
+        best = t;
+        m->nb_lm = nb;
+      }
+    }
+  }
+  m->blk_lm = round_up((V + 15) / 16, m->nb_lm);
+  m->tiles_lm = m->blk_lm / m->nb_lm;
   // tile widths: those of the single-row-tile plans (up to 256 rows, the
   // common verify batch); other row counts re-plan the k-splits only
   m->nb_qkv = plan_gemm(EPI_QKV, m->blk_qkv, H / 64, 1, m->num_cu, 0).nb;
@@ -349,7 +363,7 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
   hipError_t e;
   if ((e = hipMemcpyAsync(m->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s)) ||
       (e = launch_repack((const uint16_t*)w->lm_head, V, nullptr, 0, nullptr, 0, H, H,
-                         m->blk_lm, 8, 0, m->lm, s)) ||
+                         m->blk_lm, m->nb_lm, 0, m->lm, s)) ||
       (e = launch_bf16_to_f32((const uint16_t*)w->final_norm, m->final_norm, H, s)) ||
       (e = hipStreamSynchronize(s)))
     return bail(fail(LOPA_EHIP, "model create: %s", hipGetErrorString(e)));

@@ -533,6 +533,7 @@ int gemm_smem_bytes(int epi, int nb) {
     case EPI_RESID * 16 + 8: return GemmSmem<EPI_RESID, 8>::BYTES;
     case EPI_SWIGLU * 16 + 10: return GemmSmem<EPI_SWIGLU, 10>::BYTES;
     case EPI_LMHEAD * 16 + 8: return GemmSmem<EPI_LMHEAD, 8>::BYTES;
+    case EPI_LMHEAD * 16 + 10: return GemmSmem<EPI_LMHEAD, 10>::BYTES;
   }
   return -1;
 }
@@ -552,6 +553,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
     case EPI_RESID * 16 + 8: return launch_nb<EPI_RESID, 8>(a, s);
     case EPI_SWIGLU * 16 + 10: return launch_nb<EPI_SWIGLU, 10>(a, s);
     case EPI_LMHEAD * 16 + 8: return launch_nb<EPI_LMHEAD, 8>(a, s);
+    case EPI_LMHEAD * 16 + 10: return launch_nb<EPI_LMHEAD, 10>(a, s);
   }
   return hipErrorInvalidValue;
 }
