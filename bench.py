@@ -264,6 +264,27 @@ def e2e_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7, tau=0.
             "prefill_s": round(t_prefill, 4), "decode_s": round(t_dec, 4)}
 
 
+def e2e_window_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7, tau=0.9,
+                      tau_add=0.1, tau_act=0.95, w_max=2):
+    """End-to-end decode with the multi-block window (Sec. 3.3, integration with
+    D2F): up to w_max active blocks explored as one window, the D2F gates at the
+    appendix's GSM8K setting (tau_add 0.1, tau_act 0.95, tau_conf 0.9)."""
+    import torch
+    kv = lp.KV(model, prompt_len + gen, k + 1, L * w_max)
+    dec = lp.WindowDecoder(model, kv, L, k, tau, tau_add, tau_act, w_max)
+    prompt = synth.prompt(cfg, prompt_len, device="cuda")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    out = dec.decode(prompt, gen)
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    return {"workload": (f"{cfg['name']} shape, {prompt_len}-token uniform-random prompt (prefill "
+                         f"included), {gen} generated tokens, window of up to {w_max} blocks of {L}, "
+                         f"k={k}, tau {tau}, tau_add {tau_add}, tau_act {tau_act}"),
+            "tokens_per_s": round(gen / t, 1), "tokens_per_forward": round(out["tpf"], 3),
+            "forwards": out["forwards"], "iterations": out["iterations"], "seconds": round(t, 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -413,6 +434,12 @@ def main():
         result["e2e_decode"] = e2e_decode(lp, synth, model, cfg, L=L, k=k, tau=tau)
         log(f"end-to-end decode in {time.perf_counter() - t0:.1f}s: "
             f"{result['e2e_decode']['tokens_per_s']} tok/s, TPF {result['e2e_decode']['tokens_per_forward']}")
+        if 2 * L <= lp.MAX_BLOCK:
+            t0 = time.perf_counter()
+            result["e2e_window_decode"] = e2e_window_decode(lp, synth, model, cfg, L=L, k=k, tau=tau)
+            log(f"end-to-end window decode in {time.perf_counter() - t0:.1f}s: "
+                f"{result['e2e_window_decode']['tokens_per_s']} tok/s, "
+                f"TPF {result['e2e_window_decode']['tokens_per_forward']}")
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         try:

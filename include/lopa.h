@@ -145,6 +145,20 @@ int lopa_build_branches(const int32_t* tokens, const float* conf, const int32_t*
                         int32_t* branch_tokens, int32_t* fill_pos, uint8_t* valid,
                         int32_t* n_valid, void* stream);
 
+/* The same over a multi-block window (Sec. 3.3, integration with D2F: all
+ * active blocks form one window for branch exploration). tokens / conf / pred
+ * cover the L window positions; positions [0, n_eligible) are those of the
+ * fully activated blocks (a prefix of the window, 1 <= n_eligible <= L). The
+ * Eq. 1 threshold fill uses every unfilled position; the argmax fallback and
+ * the k lookahead positions are taken among the eligible ones only (at least
+ * one eligible position must be unfilled). n_eligible = L is
+ * lopa_build_branches. Errors as lopa_build_branches, and LOPA_EINVAL for
+ * n_eligible outside [1, L]. */
+int lopa_build_branches_window(const int32_t* tokens, const float* conf, const int32_t* pred,
+                               int32_t L, int32_t n_eligible, int32_t mask_id, float tau,
+                               int32_t k, int32_t* branch_tokens, int32_t* fill_pos,
+                               uint8_t* valid, int32_t* n_valid, void* stream);
+
 /* Alg. 1 step 3 "single pass" + Sec. 3.1 Conf + Sec. 3.3 attention pattern.
  * In:  branch_tokens[n_branches*L] int32 (block rows at positions
  *      prefix_len .. prefix_len+L-1), the cache rows [0, prefix_len).
@@ -211,6 +225,15 @@ int lopa_branch_confidence_select_metric(const int32_t* branch_tokens, const flo
  * append_offset[0] = -1. */
 int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,
                    int32_t* append_offset, void* stream);
+
+/* Commit only the first n_rows (1 <= n_rows <= L) staged positions of the
+ * winner: cache rows [prefix_len, prefix_len + n_rows). For a multi-block
+ * window (Sec. 3.3) whose first block has been filled: that block leaves the
+ * window and its K/V enter the prefix, while the later blocks stay active.
+ * prefix_len and L must be those of the last lopa_verify_forward (the window
+ * length); otherwise as lopa_commit_kv. */
+int lopa_commit_kv_rows(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,
+                        int32_t n_rows, int32_t* append_offset, void* stream);
 
 /* ---------------------------------------------------------- inspection */
 

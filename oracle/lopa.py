@@ -31,16 +31,20 @@ from .model import KVCache, OracleModel
 
 
 # ----------------------------------------------------------------- Eq. 1
-def threshold_fill(conf, unfilled, tau: float) -> np.ndarray:
+def threshold_fill(conf, unfilled, tau: float, n_eligible=None) -> np.ndarray:
     """I_fill: the unfilled positions with Conf > tau; if none, the single unfilled
-    position of highest Conf (lowest position among ties).  Eq. 1."""
+    position of highest Conf (lowest position among ties).  Eq. 1.
+    n_eligible: only positions below it may take the fallback (a multi-block
+    window's fully activated blocks; reading R29)."""
     conf = np.asarray(conf, dtype=np.float64)
-    cand = [i for i in range(len(conf)) if unfilled[i]]
-    if not cand:
-        raise ValueError("no unfilled position")
-    high = [i for i in cand if conf[i] > tau]
+    n_el = len(conf) if n_eligible is None else n_eligible
+    allc = [i for i in range(len(conf)) if unfilled[i]]
+    high = [i for i in allc if conf[i] > tau]
     if high:
         return np.array(high, dtype=np.int64)
+    cand = [i for i in allc if i < n_el]
+    if not cand:
+        raise ValueError("no eligible unfilled position")
     best = cand[0]
     for i in cand[1:]:
         if conf[i] > conf[best]:
@@ -49,8 +53,9 @@ def threshold_fill(conf, unfilled, tau: float) -> np.ndarray:
 
 
 # ------------------------------------------------------- Alg. 1 steps 1-2
-def build_branches(tokens, conf, pred, mask_id: int, tau: float, k: int):
+def build_branches(tokens, conf, pred, mask_id: int, tau: float, k: int, n_eligible=None):
     """Anchor B0 (Eq. 1 fill) and k lookahead branches (top-k of M_B0).
+    n_eligible: the lookahead positions are taken below it only (R29).
 
     Returns (branch_tokens [k+1, L] int64, fill_pos [k+1] int64 (-1 for B0 and
     for padding), valid [k+1] uint8, n_valid)."""
@@ -60,9 +65,10 @@ def build_branches(tokens, conf, pred, mask_id: int, tau: float, k: int):
     L = len(tokens)
     unfilled = tokens == mask_id
     b0 = tokens.copy()
-    fill = threshold_fill(conf, unfilled, tau)
+    fill = threshold_fill(conf, unfilled, tau, n_eligible)
     b0[fill] = pred[fill]
-    rem = [i for i in range(L) if b0[i] == mask_id]            # M_B0
+    n_el = L if n_eligible is None else n_eligible
+    rem = [i for i in range(n_el) if b0[i] == mask_id]         # eligible part of M_B0
     rem.sort(key=lambda i: (-conf[i], i))
     k_eff = min(k, len(rem))
     bt = np.tile(b0, (k + 1, 1))
@@ -229,6 +235,103 @@ def decode(model, prompt, gen_len: int, L: int, k: int, tau: float, max_len=None
         iters += it
         forwards += fw
         P += L
+    gen = np.concatenate(out) if out else np.zeros(0, dtype=np.int64)
+    return dict(tokens=gen, iterations=iters, forwards=forwards,
+                tpf=(len(gen) / forwards) if forwards else 0.0, cache=cache)
+
+
+# ------------------------------------------- multi-block window (Sec. 3.3)
+# LoPA on D2F treats all active blocks as one window for branch exploration,
+# with full attention inside the window (Sec. 3.3); the appendix's tables give
+# the D2F gates tau_add and tau_act next to tau_conf but not their rules.
+# Readings (the oracle and the GPU decoder follow both):
+#   R27 window: up to w_max consecutive blocks of L after the committed prefix;
+#       Eq. 1, the lookahead branches, the verify forward and Eq. 2 run over
+#       all its positions at once.
+#   R28 adding (tau_add): before an iteration, while the window holds fewer
+#       than w_max blocks, blocks remain, and the last block's filled fraction
+#       is >= tau_add, an all-mask block is appended; until a forward covers it
+#       its positions carry Conf 0.
+#   R29 activation (tau_act): the window's first block is fully activated;
+#       block i becomes so once block i-1 is, block i has been covered by a
+#       forward, and block i-1's filled fraction is >= tau_act. The Eq. 1
+#       fallback and the lookahead positions are taken in the fully activated
+#       blocks (a prefix of the window); the others fill only above tau.
+#   R30 commit: after an iteration the leading blocks of the winner with no
+#       unfilled position leave the window and their K/V (from that forward)
+#       enter the prefix; an empty window takes a new block with one initial
+#       forward, as a single block does.
+def decode_window(model: OracleModel, prompt, gen_len: int, L: int, k: int, tau: float,
+                  tau_add: float, tau_act: float, w_max: int, metric: int = METRIC_MEAN,
+                  window: int = 4, eta: float = 0.25, trace=None, max_len=None):
+    """Generate gen_len tokens (gen_len / L blocks) with a sliding window of up
+    to w_max active blocks. Returns tokens, iterations, forwards, tpf, cache."""
+    mask_id = model.cfg["mask_id"]
+    prompt = np.asarray(prompt, dtype=np.int64)
+    cache = KVCache(model.cfg, max_len or (len(prompt) + gen_len))
+    P = prefill(model, cache, prompt, L)
+    n_blocks = gen_len // L
+    tokens = np.zeros(0, dtype=np.int64)
+    conf = np.zeros(0)
+    pred = np.zeros(0, dtype=np.int64)
+    active, covered = [], []
+    out, added, committed, iters, forwards = [], 0, 0, 0, 0
+
+    def filled_frac(b):
+        return float(np.mean(tokens[b * L:(b + 1) * L] != mask_id))
+
+    def append_block():
+        nonlocal tokens, conf, pred, added
+        tokens = np.concatenate([tokens, np.full(L, mask_id, dtype=np.int64)])
+        conf = np.concatenate([conf, np.zeros(L)])
+        pred = np.concatenate([pred, np.full(L, mask_id, dtype=np.int64)])
+        active.append(len(active) == 0)
+        covered.append(False)
+        added += 1
+
+    while committed < n_blocks:
+        if not active:
+            append_block()
+            o = model.forward_block(tokens[None], P, cache)
+            conf, pred = o["conf"][0].copy(), o["pred"][0].copy()
+            covered[:] = [True] * len(covered)
+            forwards += 1
+        while len(active) < w_max and added < n_blocks and filled_frac(len(active) - 1) >= tau_add:
+            append_block()
+        n_el = L * next((i for i, a in enumerate(active) if not a), len(active))
+        state_in = (tokens.copy(), conf.copy(), pred.copy())
+        bt, fill_pos, valid, n_valid = build_branches(tokens, conf, pred, mask_id, tau, k, n_el)
+        o = model.forward_block(bt[:n_valid], P, cache)
+        nb, Lw = k + 1, len(tokens)
+        conf_b = np.zeros((nb, Lw))
+        pred_b = np.zeros((nb, Lw), dtype=np.int64)
+        conf_b[:n_valid], pred_b[:n_valid] = o["conf"], o["pred"]
+        scores, w = select(bt, conf_b, valid, mask_id, metric, window, eta)
+        forwards += 1
+        iters += 1
+        tokens, conf, pred = bt[w].copy(), conf_b[w].copy(), pred_b[w].copy()
+        covered[:] = [True] * len(covered)
+        for i in range(1, len(active)):
+            if not active[i] and active[i - 1] and covered[i] and filled_frac(i - 1) >= tau_act:
+                active[i] = True
+        c = 0
+        while c < len(active) and not np.any(tokens[c * L:(c + 1) * L] == mask_id):
+            c += 1
+        if trace is not None:
+            trace.append(dict(prefix_len=P, state=state_in, branch_tokens=bt, valid=valid,
+                              n_valid=n_valid, n_eligible=n_el, conf=conf_b, pred=pred_b,
+                              scores=scores, winner=w, committed_blocks=c, k=o["k"], v=o["v"]))
+        if c:
+            cache.commit(P, o["k"][w][:, :, :c * L], o["v"][w][:, :, :c * L])
+            out.append(tokens[:c * L].copy())
+            tokens, conf, pred = tokens[c * L:], conf[c * L:], pred[c * L:]
+            del active[:c], covered[:c]
+            if active:
+                active[0] = True
+            P += c * L
+            committed += c
+        if iters > 2 * gen_len + 2 * n_blocks:
+            raise RuntimeError("window decode did not converge")
     gen = np.concatenate(out) if out else np.zeros(0, dtype=np.int64)
     return dict(tokens=gen, iterations=iters, forwards=forwards,
                 tpf=(len(gen) / forwards) if forwards else 0.0, cache=cache)

@@ -148,6 +148,15 @@ def lopa_build_branches(tokens, conf, pred, L, mask_id, tau, k, branch_tokens, f
                                    _ptr(n_valid, I32, "n_valid"), _stream(stream)))
 
 
+def lopa_build_branches_window(tokens, conf, pred, L, n_eligible, mask_id, tau, k, branch_tokens,
+                               fill_pos, valid, n_valid, stream=None):
+    _check(lib.lopa_build_branches_window(_ptr(tokens, I32, "tokens"), _ptr(conf, F32, "conf"),
+                                          _ptr(pred, I32, "pred"), L, n_eligible, mask_id,
+                                          float(tau), k, _ptr(branch_tokens, I32, "branch_tokens"),
+                                          _ptr(fill_pos, I32, "fill_pos"), _ptr(valid, U8, "valid"),
+                                          _ptr(n_valid, I32, "n_valid"), _stream(stream)))
+
+
 def lopa_verify_forward(model: Model, kv: KV, prefix_len, branch_tokens, n_branches, L, conf, pred,
                         stream=None):
     _check(lib.lopa_verify_forward(model.handle, kv.handle, prefix_len,
@@ -191,4 +200,9 @@ def lopa_commit_kv(kv: KV, winner, prefix_len, L, append_offset, stream=None):
                               _ptr(append_offset, I32, "append_offset"), _stream(stream)))
 
 
-from .decoder import Decoder  # noqa: E402,F401
+def lopa_commit_kv_rows(kv: KV, winner, prefix_len, L, n_rows, append_offset, stream=None):
+    _check(lib.lopa_commit_kv_rows(kv.handle, _ptr(winner, I32, "winner"), prefix_len, L, n_rows,
+                                   _ptr(append_offset, I32, "append_offset"), _stream(stream)))
+
+
+from .decoder import Decoder, WindowDecoder  # noqa: E402,F401

@@ -39,8 +39,10 @@ class lopa_weight_ptrs(C.Structure):
 
 
 EXPORTS = ["lopa_model_create", "lopa_model_destroy", "lopa_kv_create", "lopa_kv_destroy",
-           "lopa_strerror", "lopa_last_error", "lopa_build_branches", "lopa_verify_forward",
-           "lopa_branch_confidence_select", "lopa_branch_confidence_select_metric", "lopa_commit_kv", "lopa_kv_read", "lopa_kv_write",
+           "lopa_strerror", "lopa_last_error", "lopa_build_branches", "lopa_build_branches_window",
+           "lopa_verify_forward",
+           "lopa_branch_confidence_select", "lopa_branch_confidence_select_metric", "lopa_commit_kv",
+           "lopa_commit_kv_rows", "lopa_kv_read", "lopa_kv_write",
            "lopa_kv_read_staging", "lopa_debug_hidden", "lopa_kv_profile",
            "lopa_kv_profile_read"]
 METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
@@ -61,11 +63,13 @@ def _load():
         "lopa_strerror": (C.c_char_p, [C.c_int]),
         "lopa_last_error": (C.c_char_p, []),
         "lopa_build_branches": (C.c_int, [P, P, P, I32, I32, F32, I32, P, P, P, P, P]),
+        "lopa_build_branches_window": (C.c_int, [P, P, P, I32, I32, I32, F32, I32, P, P, P, P, P]),
         "lopa_verify_forward": (C.c_int, [P, P, I32, P, I32, I32, P, P, P]),
         "lopa_branch_confidence_select": (C.c_int, [P, P, P, P, I32, I32, I32, P, P, P, P, P, P, P]),
         "lopa_branch_confidence_select_metric": (C.c_int, [P, P, P, P, I32, I32, I32, I32, I32, F32,
                                                            P, P, P, P, P, P, P]),
         "lopa_commit_kv": (C.c_int, [P, P, I32, I32, P, P]),
+        "lopa_commit_kv_rows": (C.c_int, [P, P, I32, I32, I32, P, P]),
         "lopa_kv_read": (C.c_int, [P, I32, I32, I32, P, P, P]),
         "lopa_kv_write": (C.c_int, [P, I32, I32, I32, P, P, P]),
         "lopa_kv_read_staging": (C.c_int, [P, I32, I32, P, P, P]),

@@ -447,19 +447,29 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
 
 void lopa_kv_destroy(lopa_kv* kv) { delete kv; }
 
-int lopa_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
-                        int32_t L, int32_t mask_id, float tau, int32_t k, int32_t* branch_tokens,
-                        int32_t* fill_pos, uint8_t* valid, int32_t* n_valid, void* stream) {
+int lopa_build_branches_window(const int32_t* tokens, const float* conf, const int32_t* pred,
+                               int32_t L, int32_t n_eligible, int32_t mask_id, float tau,
+                               int32_t k, int32_t* branch_tokens, int32_t* fill_pos,
+                               uint8_t* valid, int32_t* n_valid, void* stream) {
   if (!tokens || !conf || !pred || !branch_tokens || !fill_pos || !valid || !n_valid)
     return fail(LOPA_EINVAL, "null pointer argument");
   if (k < 0) return fail(LOPA_EINVAL, "k = %d < 0", k);
   if (!(tau >= 0.f && tau <= 1.f)) return fail(LOPA_EINVAL, "tau outside [0, 1]");
   if (mask_id < 0) return fail(LOPA_EINVAL, "mask_id < 0");
   if (L < 1 || L > LOPA_MAX_BLOCK) return fail(LOPA_ESHAPE, "L = %d outside [1, %d]", L, LOPA_MAX_BLOCK);
+  if (n_eligible < 1 || n_eligible > L)
+    return fail(LOPA_EINVAL, "n_eligible = %d outside [1, L = %d]", n_eligible, L);
   if (k + 1 > LOPA_MAX_ROWS) return fail(LOPA_ESHAPE, "k = %d too large", k);
-  HIP_TRY(launch_build_branches(tokens, conf, pred, L, mask_id, tau, k, branch_tokens, fill_pos,
-                                valid, n_valid, (hipStream_t)stream));
+  HIP_TRY(launch_build_branches(tokens, conf, pred, L, n_eligible, mask_id, tau, k, branch_tokens,
+                                fill_pos, valid, n_valid, (hipStream_t)stream));
   return LOPA_OK;
+}
+
+int lopa_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
+                        int32_t L, int32_t mask_id, float tau, int32_t k, int32_t* branch_tokens,
+                        int32_t* fill_pos, uint8_t* valid, int32_t* n_valid, void* stream) {
+  return lopa_build_branches_window(tokens, conf, pred, L, L < 1 ? 1 : L, mask_id, tau, k,
+                                    branch_tokens, fill_pos, valid, n_valid, stream);
 }
 
 // The verify forward; with stop_layer >= 0 it stops after that many layers and
@@ -636,6 +646,22 @@ int lopa_branch_confidence_select(const int32_t* branch_tokens, const float* con
                                               mask_id, LOPA_METRIC_MEAN, 1, 1.f, scores, winner,
                                               next_tokens, next_conf, next_pred, next_unfilled,
                                               stream);
+}
+
+int lopa_commit_kv_rows(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,
+                        int32_t n_rows, int32_t* append_offset, void* stream) {
+  if (!kv || !winner || !append_offset) return fail(LOPA_EINVAL, "null pointer argument");
+  if (kv->last_nb < 0) return fail(LOPA_EINVAL, "no verify forward has staged K/V yet");
+  if (prefix_len != kv->last_P || L != kv->last_L)
+    return fail(LOPA_EINVAL, "prefix_len/L (%d, %d) differ from the last verify forward (%d, %d)",
+                prefix_len, L, kv->last_P, kv->last_L);
+  if (n_rows < 1 || n_rows > L) return fail(LOPA_EINVAL, "n_rows = %d outside [1, L = %d]", n_rows, L);
+  if ((int64_t)prefix_len + n_rows > kv->max_len) return fail(LOPA_ECAPACITY, "commit beyond max_len");
+  const lopa_model_cfg& c = kv->m->cfg;
+  HIP_TRY(launch_commit(kv->staging, kv->cache, winner, kv->last_nb, c.layers, c.kv_heads,
+                        kv->vlds, kv->vld, c.head_dim, prefix_len, n_rows, append_offset,
+                        (hipStream_t)stream));
+  return LOPA_OK;
 }
 
 int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,

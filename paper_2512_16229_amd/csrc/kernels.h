@@ -4,10 +4,12 @@
 #include <stdint.h>
 
 // ----------------------------------------------------------- step kernels
+// Positions [0, n_elig) (1 <= n_elig <= L <= 64) are eligible for the Eq. 1
+// fallback and the lookahead fills.
 hipError_t launch_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
-                                 int L, int mask_id, float tau, int k, int32_t* branch_tokens,
-                                 int32_t* fill_pos, uint8_t* valid, int32_t* n_valid,
-                                 hipStream_t s);
+                                 int L, int n_elig, int mask_id, float tau, int k,
+                                 int32_t* branch_tokens, int32_t* fill_pos, uint8_t* valid,
+                                 int32_t* n_valid, hipStream_t s);
 // metric 0: Eq. 2 mean; 1: window minimum (window >= 1); 2: lowest-segment
 // mean (0 < eta <= 1). nb <= 1024, L <= 64.
 hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pred,

@@ -7,10 +7,12 @@
 
 #include <math.h>
 
-// One wavefront (64 lanes), lane i owns block position i (L <= 64).
+// One wavefront (64 lanes), lane i owns block position i (L <= 64). Positions
+// [0, n_elig) are eligible for the Eq. 1 fallback and the lookahead fills (all
+// of them for one block; the fully activated blocks of a multi-block window).
 __global__ __launch_bounds__(64) void build_branches_kernel(
     const int32_t* __restrict__ tokens, const float* __restrict__ conf,
-    const int32_t* __restrict__ pred, int L, int mask_id, float tau, int k,
+    const int32_t* __restrict__ pred, int L, int n_elig, int mask_id, float tau, int k,
     int32_t* __restrict__ branch_tokens, int32_t* __restrict__ fill_pos,
     uint8_t* __restrict__ valid, int32_t* __restrict__ n_valid) {
   __shared__ float s_conf[64];
@@ -27,18 +29,19 @@ __global__ __launch_bounds__(64) void build_branches_kernel(
   const bool any_high = __ballot(high) != 0ull;
   bool fill = high;
   if (!any_high) {
-    // lowest position among the largest conf of the unfilled set
-    float bc = unf ? c : -INFINITY;
-    int bi = unf ? i : 0x7fffffff;
+    // lowest position among the largest conf of the eligible unfilled set
+    const bool el = unf && i < n_elig;
+    float bc = el ? c : -INFINITY;
+    int bi = el ? i : 0x7fffffff;
     for (int o = 32; o > 0; o >>= 1) {
       float oc = __shfl_xor(bc, o);
       int oi = __shfl_xor(bi, o);
       if (oc > bc || (oc == bc && oi < bi)) { bc = oc; bi = oi; }
     }
-    fill = (i == bi) && unf;
+    fill = (i == bi) && el;
   }
   const int b0 = fill ? pr : tok;
-  const bool rem = in && (b0 == mask_id);  // M_B0
+  const bool rem = in && i < n_elig && (b0 == mask_id);  // eligible part of M_B0
 
   // Rank of each position of M_B0 by (conf desc, position asc).
   s_conf[i] = c;
@@ -209,11 +212,12 @@ __global__ __launch_bounds__(256) void kv_rows_kernel(uint16_t* __restrict__ ck,
 
 // ------------------------------------------------------------ launchers
 hipError_t launch_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
-                                 int L, int mask_id, float tau, int k, int32_t* branch_tokens,
-                                 int32_t* fill_pos, uint8_t* valid, int32_t* n_valid,
-                                 hipStream_t s) {
+                                 int L, int n_elig, int mask_id, float tau, int k,
+                                 int32_t* branch_tokens, int32_t* fill_pos, uint8_t* valid,
+                                 int32_t* n_valid, hipStream_t s) {
+  if (L < 1 || L > 64 || n_elig < 1 || n_elig > L) return hipErrorInvalidValue;
   hipLaunchKernelGGL(build_branches_kernel, dim3(1), dim3(64), 0, s, tokens, conf, pred, L,
-                     mask_id, tau, k, branch_tokens, fill_pos, valid, n_valid);
+                     n_elig, mask_id, tau, k, branch_tokens, fill_pos, valid, n_valid);
   return hipGetLastError();
 }
 

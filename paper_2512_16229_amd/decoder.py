@@ -11,7 +11,8 @@ from __future__ import annotations
 import torch
 
 from . import (KV, METRIC_MEAN, Model, lopa_branch_confidence_select,
-               lopa_branch_confidence_select_metric, lopa_build_branches, lopa_commit_kv,
+               lopa_branch_confidence_select_metric, lopa_build_branches,
+               lopa_build_branches_window, lopa_commit_kv, lopa_commit_kv_rows,
                lopa_verify_forward)
 
 
@@ -124,4 +125,128 @@ class Decoder:
             P += self.L
         toks = torch.cat(out) if out else torch.zeros(0, dtype=torch.int32, device="cuda")
         return dict(tokens=toks, iterations=iters, forwards=self.forwards,
+                    tpf=(toks.numel() / self.forwards) if self.forwards else 0.0)
+
+
+class WindowDecoder:
+    """LoPA over a window of up to w_max active blocks (Sec. 3.3, integration
+    with D2F: the active blocks form one window for branch exploration, full
+    attention inside it). The gates follow the library's readings: a block is
+    appended while the last one is at least tau_add filled; block i becomes
+    fully activated (eligible for the Eq. 1 fallback and the lookahead fills)
+    once block i-1 is fully activated and at least tau_act filled and a forward
+    has covered block i; leading blocks with no unfilled position are committed
+    (lopa_commit_kv_rows) and leave the window. The host reads the winner's
+    tokens after every iteration to apply the gates."""
+
+    def __init__(self, model: Model, kv: KV, L: int, k: int, tau: float, tau_add: float,
+                 tau_act: float, w_max: int, metric: int = METRIC_MEAN, window: int = 4,
+                 eta: float = 0.25):
+        self.model, self.kv, self.L, self.k = model, kv, L, k
+        self.tau, self.tau_add, self.tau_act, self.w_max = float(tau), float(tau_add), float(tau_act), w_max
+        self.metric, self.window, self.eta = int(metric), int(window), float(eta)
+        self.mask_id = model.cfg["mask_id"]
+        W, nb, dev = w_max * L, k + 1, "cuda"
+        i32 = dict(dtype=torch.int32, device=dev)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.tokens = torch.empty(W, **i32)
+        self.conf = torch.zeros(W, **f32)
+        self.pred = torch.empty(W, **i32)
+        self.bt = torch.empty(nb * W, **i32)
+        self.fill_pos = torch.empty(nb, **i32)
+        self.valid = torch.empty(nb, dtype=torch.uint8, device=dev)
+        self.n_valid = torch.empty(1, **i32)
+        self.conf_b = torch.empty(nb * W, **f32)
+        self.pred_b = torch.empty(nb * W, **i32)
+        self.scores = torch.empty(nb, **f32)
+        self.winner = torch.zeros(1, **i32)
+        self.next_tokens = torch.empty(W, **i32)
+        self.next_conf = torch.empty(W, **f32)
+        self.next_pred = torch.empty(W, **i32)
+        self.next_unfilled = torch.empty(1, **i32)
+        self.append_offset = torch.empty(1, **i32)
+        self.forwards = self.iterations = 0
+
+    def decode(self, prompt: torch.Tensor, gen_len: int, trace=None) -> dict:
+        L, k, nb, mask = self.L, self.k, self.k + 1, self.mask_id
+        P = Decoder(self.model, self.kv, L, 0, self.tau).prefill(prompt)
+        n_blocks = gen_len // L
+        active, covered, out = [], [], []
+        added = committed = 0
+        host = None  # host copy of the window's tokens
+
+        def filled(b):
+            return float((host[b * L:(b + 1) * L] != mask).float().mean())
+
+        def append_block():
+            nonlocal added, host
+            w = len(active)
+            self.tokens[w * L:(w + 1) * L] = mask
+            self.conf[w * L:(w + 1) * L] = 0.0
+            self.pred[w * L:(w + 1) * L] = mask
+            host = self.tokens[:(w + 1) * L].cpu()
+            active.append(w == 0)
+            covered.append(False)
+            added += 1
+
+        while committed < n_blocks:
+            if not active:
+                append_block()
+                lopa_verify_forward(self.model, self.kv, P, self.tokens[:L], 1, L, self.conf[:L],
+                                    self.pred[:L])
+                covered[:] = [True] * len(covered)
+                self.forwards += 1
+            while len(active) < self.w_max and added < n_blocks and filled(len(active) - 1) >= self.tau_add:
+                append_block()
+            Lw = len(active) * L
+            n_el = L * next((i for i, a in enumerate(active) if not a), len(active))
+            lopa_build_branches_window(self.tokens[:Lw], self.conf[:Lw], self.pred[:Lw], Lw, n_el,
+                                       mask, self.tau, k, self.bt[:nb * Lw], self.fill_pos,
+                                       self.valid, self.n_valid)
+            lopa_verify_forward(self.model, self.kv, P, self.bt[:nb * Lw], nb, Lw,
+                                self.conf_b[:nb * Lw], self.pred_b[:nb * Lw])
+            outs = (self.scores, self.winner, self.next_tokens[:Lw], self.next_conf[:Lw],
+                    self.next_pred[:Lw], self.next_unfilled)
+            if self.metric == METRIC_MEAN:
+                lopa_branch_confidence_select(self.bt[:nb * Lw], self.conf_b[:nb * Lw],
+                                              self.pred_b[:nb * Lw], self.valid, nb, Lw, mask, *outs)
+            else:
+                lopa_branch_confidence_select_metric(self.bt[:nb * Lw], self.conf_b[:nb * Lw],
+                                                     self.pred_b[:nb * Lw], self.valid, nb, Lw,
+                                                     mask, self.metric, self.window, self.eta, *outs)
+            self.tokens, self.next_tokens = self.next_tokens, self.tokens
+            self.conf, self.next_conf = self.next_conf, self.conf
+            self.pred, self.next_pred = self.next_pred, self.pred
+            self.forwards += 1
+            self.iterations += 1
+            host = self.tokens[:Lw].cpu()
+            covered[:] = [True] * len(covered)
+            for i in range(1, len(active)):
+                if not active[i] and active[i - 1] and covered[i] and filled(i - 1) >= self.tau_act:
+                    active[i] = True
+            c = 0
+            while c < len(active) and not bool((host[c * L:(c + 1) * L] == mask).any()):
+                c += 1
+            if trace is not None:
+                trace.append(dict(prefix_len=P, n_eligible=n_el, winner=int(self.winner.item()),
+                                  tokens=host.clone(), committed_blocks=c,
+                                  scores=self.scores.cpu()))
+            if c:
+                lopa_commit_kv_rows(self.kv, self.winner, P, Lw, c * L, self.append_offset)
+                out.append(host[:c * L].clone())
+                rest = Lw - c * L
+                if rest:
+                    self.tokens[:rest] = self.tokens[c * L:Lw].clone()
+                    self.conf[:rest] = self.conf[c * L:Lw].clone()
+                    self.pred[:rest] = self.pred[c * L:Lw].clone()
+                    host = host[c * L:]
+                del active[:c], covered[:c]
+                if active:
+                    active[0] = True
+                P += c * L
+                committed += c
+            if self.iterations > 2 * gen_len + 2 * n_blocks:
+                raise RuntimeError("window decode did not converge")
+        toks = torch.cat(out) if out else torch.zeros(0, dtype=torch.int32)
+        return dict(tokens=toks, iterations=self.iterations, forwards=self.forwards,
                     tpf=(toks.numel() / self.forwards) if self.forwards else 0.0)

@@ -119,18 +119,21 @@ def vocab_margin(logits: np.ndarray, mask_id: int) -> np.ndarray:
     return top2[..., 1] - top2[..., 0]
 
 
-def build_margin(tokens, conf, mask_id, tau, k) -> float:
-    """Smallest confidence gap that decides lopa_build_branches' output."""
+def build_margin(tokens, conf, mask_id, tau, k, n_eligible=None) -> float:
+    """Smallest confidence gap that decides lopa_build_branches' output
+    (n_eligible: the fallback and the lookahead fills only below it)."""
     tokens, conf = np.asarray(tokens), np.asarray(conf, dtype=np.float64)
+    n_el = len(tokens) if n_eligible is None else n_eligible
     M = np.flatnonzero(tokens == mask_id)
     if M.size == 0:
         return np.inf
     gaps = [np.min(np.abs(conf[M] - tau))]
-    c = np.sort(conf[M])[::-1]
+    Me = M[M < n_el]
+    c = np.sort(conf[Me])[::-1]
     if not np.any(conf[M] > tau) and c.size > 1:
         gaps.append(c[0] - c[1])
-    fill = lopa.threshold_fill(conf, tokens == mask_id, tau)
-    rem = np.setdiff1d(M, fill)
+    fill = lopa.threshold_fill(conf, tokens == mask_id, tau, n_eligible)
+    rem = np.setdiff1d(Me, fill)
     cr = np.sort(conf[rem])[::-1]
     if 0 < k < cr.size:
         gaps.append(cr[k - 1] - cr[k])

@@ -110,3 +110,13 @@ def test_kv_create_validation(lp):
     assert lp.lib.lopa_kv_create(FAKE, 0, 8, 32, C.byref(h)) == -1
     assert lp.lib.lopa_kv_create(FAKE, 128, 8, 65, C.byref(h)) == -2
     assert lp.lib.lopa_kv_create(FAKE, 128, 16, 64, C.byref(h)) == -2   # 1024 rows > 512
+
+
+def test_window_entry_points_validation(lp):
+    f = lp.lib.lopa_build_branches_window
+    o = (FAKE, FAKE, FAKE, FAKE, None)
+    assert f(FAKE, FAKE, FAKE, 32, 0, 5, 0.9, 3, *o) == -1        # n_eligible < 1
+    assert f(FAKE, FAKE, FAKE, 32, 33, 5, 0.9, 3, *o) == -1       # n_eligible > L
+    assert f(FAKE, FAKE, FAKE, 65, 32, 5, 0.9, 3, *o) == -2       # L too large
+    assert f(None, FAKE, FAKE, 32, 16, 5, 0.9, 3, *o) == -1
+    assert lp.lib.lopa_commit_kv_rows(None, FAKE, 0, 32, 16, FAKE, None) == -1

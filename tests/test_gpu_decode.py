@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 import torch
 
+import synth
 from gpu_util import (FAITHFUL_TOL, Setup, build_margin, conf_tolerance, f32, faithful_bound, log,
                       near_tie,
                       score_margin, vocab_margin)
@@ -148,3 +149,114 @@ def test_free_running_block(cfgname, P, L, k, tau, metric):
 def _pred_near_tie(s, state, P, L, tie):
     out = s.faith.forward_block(state[0][None], P, s.cache_f, keep_hidden=True)
     return bool(np.any(vocab_margin(out["logits"], s.cfg["mask_id"]) < tie))
+
+
+# ---------------------------------------------- multi-block window (R27-R30)
+WINDOW_CASES = [("tiny", 32, 16, 3, 0.9, 0.1, 0.5, 2, 48), ("tiny", 32, 16, 2, 0.9, 0.0, 0.3, 4, 64),
+                ("small", 64, 32, 3, 0.9, 0.1, 0.5, 2, 64)]
+
+
+def _load_rows(s, cache, upto):
+    for layer in range(s.cfg["layers"]):
+        k = torch.tensor(cache.k[layer, :, :upto], dtype=torch.bfloat16, device="cuda")
+        v = torch.tensor(cache.v[layer, :, :upto], dtype=torch.bfloat16, device="cuda")
+        s.kv.write(layer, 0, k.contiguous(), v.contiguous())
+
+
+@pytest.mark.parametrize("cfgname,P,L,k,tau,tau_add,tau_act,w_max,gen", WINDOW_CASES)
+def test_window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen):
+    """Every iteration of the oracle's multi-block window decode replayed on the
+    GPU from the oracle's state (window tokens / conf / pred, eligible prefix,
+    committed cache rows): lopa_build_branches_window bit-exact, the verify
+    forward over the whole window within the faithful tolerance, the selection,
+    and lopa_commit_kv_rows of the blocks that leave the window."""
+    log(f"window teacher-forced {cfgname} P={P} L={L} k={k} w_max={w_max} tau_add={tau_add} tau_act={tau_act}")
+    s = Setup(cfgname, 0, L * w_max, k, max_len=P + gen)
+    lp, mask, nb = s.lp, s.cfg["mask_id"], k + 1
+    tau32 = f32(tau)
+    prompt = synth.prompt(s.cfg, P).numpy()
+    otrace = []
+    res = lopa.decode_window(s.faith, prompt, gen, L, k, tau32, tau_add, tau_act, w_max, trace=otrace)
+    assert len(res["tokens"]) == gen and not np.any(res["tokens"] == mask)
+    cache = res["cache"]
+    checked = windows = 0
+    for it in otrace:
+        P_t, (tokens, conf, pred), n_el = it["prefix_len"], it["state"], it["n_eligible"]
+        Lw = len(tokens)
+        windows += Lw > L
+        _load_rows(s, cache, P_t)
+        conf32 = conf.astype(np.float32)
+        bt = torch.empty(nb * Lw, dtype=I32, device="cuda")
+        fp = torch.empty(nb, dtype=I32, device="cuda")
+        va = torch.empty(nb, dtype=U8, device="cuda")
+        nv = torch.empty(1, dtype=I32, device="cuda")
+        lp.lopa_build_branches_window(_d(tokens, I32), _d(conf32, F32), _d(pred, I32), Lw, n_el, mask,
+                                      tau, k, bt, fp, va, nv)
+        rbt, rfp, rva, rnv = lopa.build_branches(tokens, conf32.astype(np.float64), pred, mask, tau32, k, n_el)
+        if build_margin(tokens, conf32, mask, tau32, k, n_el) >= near_tie(0.0):
+            assert np.array_equal(bt.view(nb, Lw).cpu().numpy(), rbt)
+            assert np.array_equal(va.cpu().numpy(), rva) and int(nv.item()) == rnv
+        # the oracle's branches through the GPU forward over the whole window
+        obt, n_valid = it["branch_tokens"], it["n_valid"]
+        conf_b = torch.empty(nb * Lw, dtype=F32, device="cuda")
+        pred_b = torch.empty(nb * Lw, dtype=I32, device="cuda")
+        lp.lopa_verify_forward(s.model, s.kv, P_t, _d(obt.ravel(), I32), nb, Lw, conf_b, pred_b)
+        gc = conf_b.view(nb, Lw).cpu().numpy().astype(np.float64)[:n_valid]
+        gp = pred_b.view(nb, Lw).cpu().numpy()[:n_valid]
+        eps = np.max(np.abs(gc - it["conf"][:n_valid]))
+        # the case's own bf16 sensitivity: the pure oracle on the same inputs
+        e_bf16 = np.max(np.abs(it["conf"][:n_valid] - s.pure.forward_block(obt[:n_valid], P_t, cache)["conf"]))
+        assert eps < faithful_bound(e_bf16)
+        scores = torch.empty(nb, dtype=F32, device="cuda")
+        win = torch.empty(1, dtype=I32, device="cuda")
+        nt = torch.empty(Lw, dtype=I32, device="cuda")
+        ncf = torch.empty(Lw, dtype=F32, device="cuda")
+        npd = torch.empty(Lw, dtype=I32, device="cuda")
+        nu = torch.empty(1, dtype=I32, device="cuda")
+        lp.lopa_branch_confidence_select(_d(obt.ravel(), I32), conf_b, pred_b, _d(it["valid"], U8), nb,
+                                         Lw, mask, scores, win, nt, ncf, npd, nu)
+        rs = it["scores"]
+        if score_margin(rs) >= near_tie(eps):
+            assert np.array_equal(obt[int(win.item())], obt[it["winner"]])
+            checked += 1
+        c = it["committed_blocks"]
+        if c:
+            off = torch.empty(1, dtype=I32, device="cuda")
+            lp.lopa_commit_kv_rows(s.kv, _d([it["winner"]], I32), P_t, Lw, c * L, off)
+            assert int(off.item()) == P_t
+            for layer in range(s.cfg["layers"]):
+                kk, vv = s.kv.read(layer, P_t, c * L)
+                ref = it["k"][it["winner"], layer][:, :c * L]
+                assert np.max(np.abs(kk.float().cpu().numpy() - ref)) <= 0.05 * max(1.0, np.abs(ref).max())
+    log(f"  {len(otrace)} iterations ({windows} over more than one block), {checked} winners compared")
+    assert checked >= 1 and windows >= 1
+
+
+@pytest.mark.parametrize("cfgname,P,L,k,tau,tau_add,tau_act,w_max,gen", WINDOW_CASES[:2])
+def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen):
+    """The GPU WindowDecoder end to end: a filled, committed sequence, and the
+    oracle's trajectory until a decision the oracle calls a near-tie."""
+    log(f"window free-running {cfgname} P={P} L={L} k={k} w_max={w_max}")
+    s = Setup(cfgname, 0, L * w_max, k, max_len=P + gen)
+    mask = s.cfg["mask_id"]
+    prompt = synth.prompt(s.cfg, P)
+    dec = s.lp.WindowDecoder(s.model, s.kv, L, k, tau, tau_add, tau_act, w_max)
+    gtrace = []
+    out = dec.decode(prompt, gen, gtrace)
+    g_tokens = out["tokens"].numpy()
+    assert len(g_tokens) == gen and not np.any(g_tokens == mask)
+    assert out["forwards"] >= out["iterations"] >= gen // (L * w_max)
+    otrace = []
+    res = lopa.decode_window(s.faith, prompt.numpy(), gen, L, k, f32(tau), tau_add, tau_act, w_max,
+                             trace=otrace)
+    for t, (g, o) in enumerate(zip(gtrace, otrace)):
+        ow = o["branch_tokens"][o["winner"]]
+        if not np.array_equal(g["tokens"].numpy(), ow):
+            tokens, conf, pred = o["state"]
+            bm = build_margin(tokens, conf, mask, f32(tau), k, o["n_eligible"])
+            sm = score_margin(o["scores"])
+            log(f"  diverged at iteration {t}: build margin {bm:.2e}, score margin {sm:.2e}")
+            assert min(bm, sm) < near_tie(2 * FAITHFUL_TOL)
+            return
+    assert np.array_equal(g_tokens, res["tokens"]) and out["forwards"] == res["forwards"]
+    log(f"  identical trajectory: {out['iterations']} iterations, {out['forwards']} forwards, TPF {out['tpf']:.2f}")

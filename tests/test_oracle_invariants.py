@@ -168,3 +168,54 @@ def test_decode_small_end_to_end():
     assert len(r["tokens"]) == 32 and not np.any(r["tokens"] == cfg["mask_id"])
     assert r["forwards"] == r["iterations"] + 2
     assert r["tpf"] >= 1.0
+
+
+# ------------------------------------------- multi-block window (R27-R30)
+@pytest.mark.parametrize("k,tau", [(3, 0.9), (0, 0.9), (5, 0.5)])
+def test_window_of_one_block_is_block_decoding(k, tau):
+    """w_max = 1, or a tau_add no fill fraction reaches, leaves one block in the
+    window: the same tokens, iterations and forwards as block-by-block decoding."""
+    cfg = synth.config("tiny")
+    m = OracleModel(cfg, synth.model_weights(cfg), "faithful")
+    prompt = synth.prompt(cfg, 32).numpy()
+    ref = lopa.decode(m, prompt, 48, 16, k, tau)
+    for w_max, tau_add in ((1, 0.1), (3, 1.5)):
+        got = lopa.decode_window(m, prompt, 48, 16, k, tau, tau_add, 0.5, w_max)
+        assert np.array_equal(got["tokens"], ref["tokens"])
+        assert got["iterations"] == ref["iterations"] and got["forwards"] == ref["forwards"]
+        assert np.array_equal(got["cache"].k, ref["cache"].k)
+
+
+@pytest.mark.parametrize("w_max,tau_add,tau_act", [(2, 0.1, 0.5), (4, 0.0, 0.3), (3, 0.2, 0.95)])
+def test_window_invariants(w_max, tau_add, tau_act):
+    """Every generated position filled; blocks committed whole and in order;
+    every iteration fills at least one position; the window never exceeds
+    w_max blocks; the fallback and lookahead fills stay in the fully activated
+    prefix; a committed block's K/V equal the forward that completed it."""
+    cfg = synth.config("tiny")
+    m = OracleModel(cfg, synth.model_weights(cfg), "faithful")
+    mask, L, gen = cfg["mask_id"], 16, 64
+    prompt = synth.prompt(cfg, 32).numpy()
+    trace = []
+    res = lopa.decode_window(m, prompt, gen, L, 3, 0.9, tau_add, tau_act, w_max, trace=trace)
+    assert len(res["tokens"]) == gen and not np.any(res["tokens"] == mask)
+    assert res["forwards"] >= res["iterations"]
+    P = 32
+    for it in trace:
+        tokens, conf, pred = it["state"]
+        Lw, n_el = len(tokens), it["n_eligible"]
+        assert Lw % L == 0 and Lw <= w_max * L and n_el % L == 0 and L <= n_el <= Lw
+        assert it["prefix_len"] == P
+        w = it["winner"]
+        new = it["branch_tokens"][w]
+        filled = np.flatnonzero((tokens == mask) & (new != mask))
+        assert filled.size >= 1
+        # fills outside the eligible prefix come from the threshold only
+        outside = filled[filled >= n_el]
+        assert np.all(conf[outside] > 0.9)
+        c = it["committed_blocks"]
+        assert not np.any(new[:c * L] == mask)
+        if c:
+            assert np.array_equal(res["cache"].k[:, :, P:P + c * L], it["k"][w][:, :, :c * L])
+        P += c * L
+    assert P == 32 + gen

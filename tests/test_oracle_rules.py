@@ -251,3 +251,36 @@ def test_select_with_metrics_invalid_and_ties():
     assert lopa.branch_score(conf[0], bt[0], 7, lopa.METRIC_WINDOW_MIN, 2, 0) == pytest.approx(0.55)
     assert lopa.branch_score(conf[0], bt[0], 7, lopa.METRIC_LOWEST_SEGMENT, 4, 0.5) == pytest.approx(0.3)
     assert lopa.branch_score(conf[2], bt[2], 7, lopa.METRIC_WINDOW_MIN, 2, 0) == pytest.approx(0.3)
+
+
+def test_branches_with_eligible_prefix():
+    """n_eligible = L is the plain rule; otherwise the threshold fill still uses
+    every unfilled position while the fallback and the lookahead positions are
+    the plain rule applied to the eligible prefix (checked on that prefix)."""
+    rng = np.random.default_rng(5)
+    for _ in range(400):
+        L = int(rng.integers(2, 12))
+        tokens = np.where(rng.random(L) < 0.7, 7, rng.integers(0, 7, L))
+        n_el = int(rng.integers(1, L + 1))
+        if not np.any(tokens[:n_el] == 7):
+            tokens[rng.integers(n_el)] = 7
+        conf = np.round(rng.random(L), 2)
+        pred = rng.integers(0, 7, L)
+        tau = float(rng.choice([0.3, 0.6, 0.95]))
+        k = int(rng.integers(0, 4))
+        a = lopa.build_branches(tokens, conf, pred, 7, tau, k)
+        b = lopa.build_branches(tokens, conf, pred, 7, tau, k, L)
+        assert all(np.array_equal(x, y) for x, y in zip(a[:3], b[:3])) and a[3] == b[3]
+        bt, fp, valid, nv = lopa.build_branches(tokens, conf, pred, 7, tau, k, n_el)
+        un = tokens == 7
+        high = un & (conf > tau)
+        b0 = bt[0]
+        if high.any():
+            assert np.array_equal(b0 != tokens, high)
+        else:
+            # fallback: the plain rule on the eligible prefix alone
+            pb = lopa.build_branches(tokens[:n_el], conf[:n_el], pred[:n_el], 7, tau, k)
+            assert np.array_equal(b0[:n_el], pb[0][0]) and np.array_equal(b0[n_el:], tokens[n_el:])
+        assert np.all(fp[1:nv] < n_el) and np.all(fp[1:nv] >= 0)
+        rem = [i for i in range(n_el) if b0[i] == 7]
+        assert nv == 1 + min(k, len(rem))
