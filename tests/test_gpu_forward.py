@@ -14,7 +14,12 @@ pytestmark = pytest.mark.gpu
 
 # (config, P, L, k): 64 / 256 / 512 / 48 / 128 rows; ragged prefixes; two head dims
 CASES = [("tiny", 64, 16, 3), ("small", 100, 32, 7), ("small", 37, 32, 15),
-         ("small128", 40, 16, 2), ("small128", 0, 32, 3)]
+         ("small128", 40, 16, 2), ("small128", 0, 32, 3),
+         # ragged and extreme block shapes: a 7-row block (partial key tile and
+         # partial 16-row query block), 48 rows (three query blocks), the
+         # 64-row maximum with head_dim 128, and the degenerate one-row block
+         # with no prefix and no lookahead
+         ("tiny", 23, 7, 2), ("small", 50, 48, 3), ("small128", 64, 64, 1), ("tiny", 0, 1, 0)]
 
 
 def _kv_close(gpu, ref, what):
@@ -92,7 +97,8 @@ def test_hidden_states_per_layer(cfgname, P, L, k):
             assert np.array_equal(g, r)          # embedding gather is exact
 
 
-@pytest.mark.parametrize("cfgname,P,L,k", [("tiny", 64, 16, 3), ("small", 100, 32, 7)])
+@pytest.mark.parametrize("cfgname,P,L,k", [("tiny", 64, 16, 3), ("small", 100, 32, 7),
+                                           ("tiny", 23, 7, 2), ("small", 50, 48, 3)])
 def test_batch_invariance_and_determinism(cfgname, P, L, k):
     log(f"batch invariance {cfgname} P={P} L={L} k={k}")
     s = Setup(cfgname, P, L, k)
