@@ -252,6 +252,26 @@ int lopa_kv_write(lopa_kv* kv, int32_t layer, int32_t start, int32_t len,
 int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer,
                          void* k_dst, void* v_dst, void* stream);
 
+/* Attention path of lopa_verify_forward (Sec. 3.3: every branch attends to the
+ * same committed prefix). With a long prefix and several branches the prefix
+ * part runs once per query head for all branches: the prefix is cut into
+ * n_ranges key ranges of range_len positions (a multiple of 32; the last may
+ * be shorter), each range's unnormalised softmax state is written per row to a
+ * workspace owned by the cache, and the per-branch block attention merges them
+ * in range order. n_ranges = 0 is the per-(head, branch) path, which streams
+ * the prefix once per branch. The two paths agree up to floating-point
+ * rounding order.
+ * lopa_kv_set_attention_ranges chooses the path for later calls: -1 (the
+ * default) lets the library pick from the shapes, 0 forces the per-branch
+ * path, n >= 1 forces about n ranges (fewer if the prefix has fewer 32-key
+ * tiles; the per-branch path for an empty prefix). n above the device's limit
+ * (max(1, floor(2 compute units / heads))) is LOPA_EINVAL.
+ * lopa_kv_attention_plan reports the (n_ranges, range_len) a verify forward of
+ * this shape would use; host only, nothing is launched. */
+int lopa_kv_set_attention_ranges(lopa_kv* kv, int32_t n_ranges);
+int lopa_kv_attention_plan(const lopa_kv* kv, int32_t prefix_len, int32_t n_branches, int32_t L,
+                           int32_t* n_ranges, int32_t* range_len);
+
 /* Launch timing of lopa_verify_forward with HIP events on the call's stream.
  * kinds_mask selects which launches get an event pair (bit i = kind i below);
  * 0 turns timing off. Events between launches cost a few microseconds each. */

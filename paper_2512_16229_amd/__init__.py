@@ -111,6 +111,19 @@ class KV:
         _check(lib.lopa_kv_read_staging(self.handle, branch, layer, _ptr(k), _ptr(v), _stream(stream)))
         return k, v
 
+    def set_attention_ranges(self, n_ranges: int):
+        """-1: the library picks the attention path; 0: per-(head, branch);
+        n >= 1: shared prefix cut into about n key ranges."""
+        _check(lib.lopa_kv_set_attention_ranges(self.handle, n_ranges))
+
+    def attention_plan(self, prefix_len: int, n_branches: int, L: int):
+        """(n_ranges, range_len) of a verify forward of this shape; (0, 0) is
+        the per-(head, branch) path."""
+        s, ks = C.c_int32(), C.c_int32()
+        _check(lib.lopa_kv_attention_plan(self.handle, prefix_len, n_branches, L, C.byref(s),
+                                          C.byref(ks)))
+        return s.value, ks.value
+
     def profile(self, kinds=()):
         """Time launches of the given kinds (names from PROF_KINDS) with HIP events."""
         mask = 0

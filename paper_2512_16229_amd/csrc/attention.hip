@@ -3,19 +3,27 @@
 // all L rows of its own branch (full attention inside the block); branches
 // never see each other. Grouped-query: query head h reads KV head h / (Hq/Hkv).
 //
-// One workgroup per (query head, branch) with four wavefronts; each wavefront
-// takes a quarter of the key tiles (32 keys each) for all L rows, and the
-// four partial softmax states are merged through LDS at the end. Each
-// wavefront streams its tiles through a private two-slot LDS ring with
-// asynchronous global -> LDS copies (one tile in flight while the previous one
-// is computed), then reads the K and V fragments from LDS in MFMA operand
-// layout. Scores are formed transposed, S^T = K Q^T, so a lane owns one query
-// column and the probabilities land directly in the operand layout of
+// Two paths, chosen by the host from the prefix length:
+//  * attn_kernel alone: one workgroup per (query head, branch) with four
+//    wavefronts; each wavefront takes a quarter of the key tiles (32 keys
+//    each, prefix tiles from the cache and block tiles from the branch's
+//    staging) for all L rows, and the four partial softmax states are merged
+//    through LDS. Short prefixes: no state leaves the workgroup.
+//  * attn_prefix_kernel + attn_kernel: the prefix is shared by all branches,
+//    so one workgroup per (query head, key range, 256-row group) streams each
+//    prefix tile of its range once into LDS and computes it for the rows of
+//    every branch (64 rows per wavefront); its unnormalised partial state per
+//    row goes to a workspace. attn_kernel then runs only the block tiles and
+//    merges the partial states of the key ranges. Long prefixes: each prefix
+//    K/V tile is read once per query head instead of once per (head, branch).
+// Tiles go global -> LDS by asynchronous copies, then into registers in MFMA
+// operand layout. Scores are formed transposed, S^T = K Q^T, so a lane owns one
+// query column and the probabilities land directly in the operand layout of
 // O^T = V^T P^T; V is stored transposed ([d][position]) in the cache and the
-// staging so that a copy lane's 8 keys of one dimension are 16 contiguous bytes.
-// Prefix tiles and block tiles are kept apart (a tile reads one source, with
-// positions aligned to 4) and keys past the end of either are masked: their
-// probability and their V values are zero.
+// staging so that a copy lane's 8 keys of one dimension are 16 contiguous
+// bytes. Prefix tiles and block tiles are kept apart (a tile reads one source,
+// with positions aligned to 8) and keys past the end of either are masked:
+// their probability and their V values are zero.
 #include "common.h"
 #include "kernels.h"
 
@@ -25,7 +33,7 @@ namespace {
 
 constexpr int KT = 32;  // keys per tile
 
-template <int D, int QB>
+template <int D>
 struct AttnTile {
   u32x4 k[2][D / 32];  // K fragments: key block kb, dims 32 kk + 8 g .. +8
   uint2 v[D / 16][2];  // V^T: dims 16 db + c16, keys {4g .. 4g+3} and {16 + 4g ..}
@@ -44,16 +52,21 @@ __device__ __forceinline__ void attn_dma16(const void* base, uint32_t voff, uint
                ::"s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(voff), "s"(sbase)
                : "memory");
 }
+// Maximum of scores (never NaN: finite bf16 products or the -inf of a masked
+// key). This file is compiled without NaN semantics, so fmaxf maps to the
+// hardware maximum without first quieting each operand.
+__device__ __forceinline__ float max2(float a, float b) { return fmaxf(a, b); }
+__device__ __forceinline__ float max3(float a, float b, float c) { return fmaxf(fmaxf(a, b), c); }
 // max / sum of the values of lanes l and l ^ 16 (l ^ 32): the permlane swaps
 // hand each lane both values of its pair, lower lane first, so the two lanes
 // of a pair get bitwise identical results
 __device__ __forceinline__ float pair16_max(float x) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max2(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float pair32_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return max2(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float pair16_sum(float x) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -64,24 +77,185 @@ __device__ __forceinline__ float pair32_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// 2^x by the hardware instruction (no scaling of results below the normal
+// range: such probabilities are < 2^-126 of the row maximum and flush to 0)
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Reference maximum before any key: finite, so that 2^(m_old - m_new) and
+// s * scale - m stay defined (a row's first finite score always moves m).
+constexpr float M_INIT = -1e30f;
+
 template <int N>
 __device__ __forceinline__ void attn_wait_vmcnt() {
   static_assert(N >= 0 && N <= 63, "vmcnt range");
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-template <int D, int QB>
-struct AttnSmem {
+template <int D>
+struct TileLds {
   static constexpr int NDB = D / 16, NKK = D / 32;
-  static constexpr int KBYTES = 2 * NKK * 1024;   // K of one tile: [kb][kk][lane][16 B]
+  static constexpr int KBYTES = 2 * NKK * 1024;     // K of one tile: [kb][kk][lane][16 B]
   static constexpr int TILE = KBYTES + NDB * 1024;  // + V^T: [db][lane][16 B]
-  static constexpr int RING = 4 * 2 * TILE;         // four wavefronts x two slots
-  static constexpr int MERGE_O = NDB * QB * 64 * 4;  // floats of one merge slot
-  static constexpr int MERGE = (2 * MERGE_O + 4 * QB * 16) * 4;
-  static constexpr int BYTES = RING > MERGE ? RING : MERGE;
-  static constexpr int OPS = 2 * NKK + NDB;  // copies per tile and wavefront
+  static constexpr int OPS = 2 * NKK + NDB;         // 1 KiB copies per tile
 };
 
+// Copy q (0 <= q < OPS) of the tile whose first position is p0 in a source of
+// lim positions (K rows [pos][D] at kbase, V^T rows [D][vld] at vbase) into the
+// LDS slot at sb. A K copy lane takes key row 16 kb + c16, dims 32 kk + 8 g .. +8;
+// a V copy lane dimension 16 db + c16, keys 8 g .. 8 g + 7. In a tile that runs
+// past the end of its source, K rows past the end read the last row and V runs
+// that start past the end read the first run (tile_update masks both): every
+// copy stays inside the source, whose row lengths are multiples of 8.
+template <int D>
+__device__ __forceinline__ void tile_copy(int q, const uint16_t* kbase, const uint16_t* vbase,
+                                          int64_t vld, int p0, int lim, uint32_t sb, int c16,
+                                          int g) {
+  using T = TileLds<D>;
+  const uint16_t* kb_ = kbase + (int64_t)p0 * D;
+  const uint16_t* vb_ = vbase + p0;
+  if (q < 2 * T::NKK) {
+    const int kb = q / T::NKK, kk = q % T::NKK;
+    int r = kb * 16 + c16;
+    r = r < lim - p0 ? r : lim - 1 - p0;
+    attn_dma16(kb_ + kk * 32, (uint32_t)((r * D + g * 8) * 2), sb + q * 1024);
+  } else {
+    const int db = q - 2 * T::NKK;
+    const uint32_t voff = (uint32_t)((c16 * vld + (8 * g < lim - p0 ? 8 * g : 0)) * 2);
+    attn_dma16(vb_ + (int64_t)db * 16 * vld, voff, sb + q * 1024);
+  }
+}
+
+// LDS slot -> registers (operand layouts)
+template <int D>
+__device__ __forceinline__ void tile_fetch(const char* sb, int lane, AttnTile<D>& x) {
+  using T = TileLds<D>;
+  const int g = lane >> 4, c16 = lane & 15;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int kk = 0; kk < T::NKK; ++kk)
+      x.k[kb][kk] = *(const u32x4*)(sb + ((kb * T::NKK + kk) * 64 + lane) * 16);
+  // keys 4g .. 4g+3 sit in copy lane c16 + 16 (g / 2) at byte 8 (g % 2);
+  // keys 16 + 4g .. in copy lane c16 + 16 (2 + g / 2)
+  const char* vb = sb + T::KBYTES + (c16 + 16 * (g >> 1)) * 16 + 8 * (g & 1);
+#pragma unroll
+  for (int db = 0; db < T::NDB; ++db) {
+    x.v[db][0] = *(const uint2*)(vb + db * 1024);
+    x.v[db][1] = *(const uint2*)(vb + db * 1024 + 32 * 16);
+  }
+}
+
+// One key tile (keys p0 .. p0 + 31 of a source of lim positions) for NR blocks
+// of 16 query rows. With s the raw score q.k and sl2 = scale log2(e), the
+// probabilities are p = 2^(s sl2 - m) against a reference maximum m (log2
+// units) that trails the running row maximum of s sl2 by at most 8: a row's m,
+// l and o are rescaled only when its maximum has grown past that, so p <= 2^8.
+// o / l and every merge are unchanged by the choice of reference. The maximum
+// is taken over the raw scores (scaling by sl2 > 0 keeps the order and,
+// rounding being monotone, the maximum itself).
+template <int D, int NR>
+__device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR][D / 32],
+                                            float (&m)[NR], float (&l)[NR],
+                                            f32x4 (&o)[D / 16][NR], int p0, int lim, float sl2,
+                                            int g) {
+  constexpr int NDB = D / 16, NKK = D / 32;
+  const bool full = p0 + KT <= lim;  // wave-uniform
+  if (!full) {
+    // zero V of masked keys (stale cache or staging contents may be
+    // non-finite, and 0 * inf would poison the sums); branch-free
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int pos = p0 + hf * 16 + g * 4;
+      const unsigned m01 = (pos < lim ? 0xFFFFu : 0u) | (pos + 1 < lim ? 0xFFFF0000u : 0u);
+      const unsigned m23 = (pos + 2 < lim ? 0xFFFFu : 0u) | (pos + 3 < lim ? 0xFFFF0000u : 0u);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        x.v[db][hf].x &= m01;
+        x.v[db][hf].y &= m23;
+      }
+    }
+  }
+#pragma unroll
+  for (int qb = 0; qb < NR; ++qb) {
+    f32x4 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) s[kb] = mfma16(x.k[kb][kk], qf[qb][kk], s[kb]);
+    }
+    // s[kb][j]: key p0 + 16 kb + 4 g + j, query 16 qb + c16
+    if (!full) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int pos = p0 + kb * 16 + g * 4 + j;
+          s[kb][j] = pos < lim ? s[kb][j] : -INFINITY;
+        }
+    }
+    float tmax = max2(max3(s[0][0], s[0][1], s[0][2]),
+                      max3(max3(s[0][3], s[1][0], s[1][1]), s[1][2], s[1][3]));
+    tmax = pair32_max(pair16_max(tmax));
+    const float mn = max2(m[qb], tmax * sl2);
+    const bool grow = mn > m[qb] + 8.f;
+    if (__builtin_amdgcn_ballot_w64(grow)) {
+      // only the rows that need it move their reference (the others scale by
+      // exactly 1), so a row's arithmetic never depends on the other rows of
+      // the wavefront; from M_INIT alpha is 0 on zero o and l
+      const float alpha = grow ? fast_exp2(m[qb] - mn) : 1.f;
+      m[qb] = grow ? mn : m[qb];
+      l[qb] *= alpha;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db][qb] *= alpha;
+    }
+    const float nm = -m[qb];
+    uint16_t pb[8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float p = fast_exp2(__builtin_fmaf(s[kb][j], sl2, nm));  // masked: 2^-inf = 0
+        l[qb] += p;
+        pb[kb * 4 + j] = f2bf_bits(p);
+      }
+    const u32x4 pf = *(const u32x4*)pb;  // keys {4g .. 4g+3} then {16 + 4g ..}
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) {
+      const u32x4 vf = {x.v[db][0].x, x.v[db][0].y, x.v[db][1].x, x.v[db][1].y};
+      o[db][qb] = mfma16(vf, pf, o[db][qb]);  // O^T(dim 16 db + 4g + j, query)
+    }
+  }
+}
+
+// merge another softmax state (mo, lo, oo) into (m, l, o): both brought to the
+// larger reference maximum, then summed (a state that saw no key has m =
+// M_INIT and zero l, o: it scales to 0 against any real maximum)
+template <int NDB>
+__device__ __forceinline__ void merge_state(float& m, float& l, f32x4 (&o)[NDB], float mo,
+                                            float lo, const f32x4 (&oo)[NDB]) {
+  const float mn = max2(m, mo);
+  const float fa = fast_exp2(m - mn);
+  const float fb = fast_exp2(mo - mn);
+  m = mn;
+  l = l * fa + lo * fb;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) o[db] = o[db] * fa + oo[db] * fb;
+}
+
+template <int D, int QB>
+struct AttnSmem {
+  static constexpr int NDB = D / 16;
+  static constexpr int RING = 4 * 2 * TileLds<D>::TILE;  // four wavefronts x two slots
+  static constexpr int MERGE_O = NDB * QB * 64 * 4;      // floats of one merge slot
+  static constexpr int MERGE = (2 * MERGE_O + 4 * QB * 16) * 4;
+  static constexpr int BYTES = RING > MERGE ? RING : MERGE;
+  static constexpr int OPS = TileLds<D>::OPS;
+};
+
+// Per (query head, branch): the block tiles, and the prefix tiles unless the
+// prefix ran in attn_prefix_kernel (a.S > 0), whose partial states are merged
+// before the four wavefronts' states are.
 template <int D, int QB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   using SM = AttnSmem<D, QB>;
@@ -93,7 +267,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int g = lane >> 4, c16 = lane & 15;
   const int kvh = h / (a.Hq / a.Hkv);
   const int L = a.L, P = a.P;
-  const int pt = (P + KT - 1) / KT, bt = (L + KT - 1) / KT, T = pt + bt;
+  const int pt = a.S > 0 ? 0 : (P + KT - 1) / KT, bt = (L + KT - 1) / KT, T = pt + bt;
   const int t_lo = wv * T / 4, t_hi = (wv + 1) * T / 4;
   const float sl2 = a.scale * 1.4426950408889634f;  // scale * log2(e)
 
@@ -102,62 +276,17 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
   const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;  // [pos][D]
   const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;  // [D][vlds]
-  const uint32_t ring = (uint32_t)(uintptr_t)smem + (uint32_t)(wv * 2) * SM::TILE;
+  const uint32_t ring = (uint32_t)(uintptr_t)smem + (uint32_t)(wv * 2) * TileLds<D>::TILE;
 
-  // tile t -> ring slot: OPS copies, each from a wave-uniform base at the
-  // tile's first position plus a per-lane byte offset. A K copy lane takes key
-  // row 16 kb + c16, dims 32 kk + 8 g .. +8; a V copy lane dimension
-  // 16 db + c16, keys 8 g .. 8 g + 7. In a tile that runs past the end of its
-  // source, K rows past the end read the last row and V runs that start past
-  // the end read the first run (compute() masks both): every copy stays inside
-  // the source, whose row lengths are multiples of 8.
-  const uint32_t koff_full[2] = {(uint32_t)((c16 * D + g * 8) * 2),
-                                 (uint32_t)(((16 + c16) * D + g * 8) * 2)};
-  const uint32_t voff_pre = (uint32_t)((c16 * a.vld + 8 * g) * 2);
-  const uint32_t voff_blk = (uint32_t)((c16 * a.vlds + 8 * g) * 2);
+  // tile t -> this wavefront's ring slot (all OPS copies)
   auto issue = [&](int t, int slot) {
     const bool pre = t < pt;
     const int p0 = (pre ? t : t - pt) * KT;
-    const int lim = pre ? P : L;
-    const int64_t vld = pre ? a.vld : a.vlds;
-    const uint16_t* kb_ = (pre ? kc : ks) + (int64_t)p0 * D;
-    const uint16_t* vb_ = (pre ? vc : vs) + p0;
-    uint32_t koff[2] = {koff_full[0], koff_full[1]};
-    uint32_t voff = pre ? voff_pre : voff_blk;
-    if (p0 + KT > lim) {  // wave-uniform: the last, partial tile of a source
+    const uint32_t sb = ring + (uint32_t)slot * TileLds<D>::TILE;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const int r = kb * 16 + c16 < lim - p0 ? kb * 16 + c16 : lim - 1 - p0;
-        koff[kb] = (uint32_t)((r * D + g * 8) * 2);
-      }
-      voff = (uint32_t)((c16 * vld + (8 * g < lim - p0 ? 8 * g : 0)) * 2);
-    }
-    const uint32_t sb = ring + (uint32_t)slot * SM::TILE;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) attn_dma16(kb_ + kk * 32, koff[kb], sb + (kb * NKK + kk) * 1024);
-#pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      attn_dma16(vb_ + (int64_t)db * 16 * vld, voff, sb + SM::KBYTES + db * 1024);
-  };
-
-  // ring slot -> registers (operand layouts)
-  auto fetch = [&](int slot, AttnTile<D, QB>& x) {
-    const char* sb = smem + (wv * 2 + slot) * SM::TILE;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-        x.k[kb][kk] = *(const u32x4*)(sb + ((kb * NKK + kk) * 64 + lane) * 16);
-    // keys 4g .. 4g+3 sit in copy lane c16 + 16 (g / 2) at byte 8 (g % 2);
-    // keys 16 + 4g .. in copy lane c16 + 16 (2 + g / 2)
-    const char* vb = sb + SM::KBYTES + (c16 + 16 * (g >> 1)) * 16 + 8 * (g & 1);
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      x.v[db][0] = *(const uint2*)(vb + db * 1024);
-      x.v[db][1] = *(const uint2*)(vb + db * 1024 + 32 * 16);
-    }
+    for (int q = 0; q < SM::OPS; ++q)
+      tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, pre ? P : L, sb,
+                   c16, g);
   };
 
   // the first two tiles are in flight while Q is loaded
@@ -178,93 +307,15 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int kk = 0; kk < NKK; ++kk) qf[qb][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
   }
 
-  float m[QB], l[QB];  // running max (log2 units) and this lane's partial sum
+  float m[QB], l[QB];  // reference max (log2 units) and this lane's partial sum
   f32x4 o[NDB][QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    m[qb] = -INFINITY;
+    m[qb] = M_INIT;
     l[qb] = 0.f;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) o[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
-
-  // One key tile for all query rows. The probabilities are taken against a
-  // reference maximum m that trails the running row maximum by at most 8
-  // (log2 units): m, l and o are rescaled only when some row's maximum has
-  // grown past that (a wave-uniform decision), so p = 2^(s - m) <= 2^8.
-  // o / l and the final merge are unchanged by the choice of reference.
-  auto compute = [&](int t, AttnTile<D, QB>& x) {
-    const bool pre = t < pt;
-    const int p0 = (pre ? t : t - pt) * KT;
-    const int lim = pre ? P : L;
-    const bool full = p0 + KT <= lim;  // wave-uniform
-    if (!full) {
-      // zero V of masked keys (stale cache or staging contents may be
-      // non-finite, and 0 * inf would poison the sums)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const int pos = p0 + hf * 16 + g * 4;
-        const unsigned m01 = (pos < lim ? 0xFFFFu : 0u) | (pos + 1 < lim ? 0xFFFF0000u : 0u);
-        const unsigned m23 = (pos + 2 < lim ? 0xFFFFu : 0u) | (pos + 3 < lim ? 0xFFFF0000u : 0u);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          x.v[db][hf].x &= m01;
-          x.v[db][hf].y &= m23;
-        }
-      }
-    }
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) {
-      f32x4 s[2];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int kk = 0; kk < NKK; ++kk) s[kb] = mfma16(x.k[kb][kk], qf[qb][kk], s[kb]);
-      }
-      // s[kb][j]: key p0 + 16 kb + 4 g + j, query 16 qb + c16
-      if (full) {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) s[kb] *= sl2;
-      } else {
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int pos = p0 + kb * 16 + g * 4 + j;
-            s[kb][j] = pos < lim ? s[kb][j] * sl2 : -INFINITY;
-          }
-      }
-      float tmax = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
-      tmax = pair32_max(pair16_max(tmax));
-      const float mn = fmaxf(m[qb], tmax);
-      if (__builtin_amdgcn_ballot_w64(mn > m[qb] + 8.f)) {
-        // m = -inf (nothing seen yet) gives alpha = 0 on zero o and l
-        const float alpha = mn == -INFINITY ? 1.f : exp2f(m[qb] - mn);
-        m[qb] = mn;
-        l[qb] *= alpha;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) o[db][qb] *= alpha;
-      }
-      const float mr = m[qb];
-      uint16_t pb[8];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const float p = mr == -INFINITY ? 0.f : exp2f(s[kb][j] - mr);
-          l[qb] += p;
-          pb[kb * 4 + j] = f2bf_bits(p);
-        }
-      const u32x4 pf = *(const u32x4*)pb;  // keys {4g .. 4g+3} then {16 + 4g ..}
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const u32x4 vf = {x.v[db][0].x, x.v[db][0].y, x.v[db][1].x, x.v[db][1].y};
-        o[db][qb] = mfma16(vf, pf, o[db][qb]);  // O^T(dim 16 db + 4g + j, query)
-      }
-    }
-  };
 
   // tile i sits in slot i % 2. At the top of an iteration tiles i and i + 1
   // are in flight (2 OPS copies): wait for the older one, compute it, and
@@ -273,17 +324,47 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   // copies in flight is the same in every iteration.
   for (int i = 0; i < n; ++i) {
     attn_wait_vmcnt<SM::OPS>();
-    AttnTile<D, QB> x;
-    fetch(i & 1, x);
-    compute(t_lo + i, x);
+    AttnTile<D> x;
+    tile_fetch<D>(smem + (wv * 2 + (i & 1)) * TileLds<D>::TILE, lane, x);
+    const int t = t_lo + i;
+    const bool pre = t < pt;
+    tile_update<D, QB>(x, qf, m, l, o, (pre ? t : t - pt) * KT, pre ? P : L, sl2, g);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     issue(t_lo + (i + 2 < n ? i + 2 : n - 1), i & 1);
   }
   attn_wait_vmcnt<0>();  // the ring is reused for the merge
   __syncthreads();
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    l[qb] = pair32_sum(pair16_sum(l[qb]));
+  for (int qb = 0; qb < QB; ++qb) l[qb] = pair32_sum(pair16_sum(l[qb]));
+
+  // the prefix key ranges of attn_prefix_kernel: range sp is merged by
+  // wavefront sp % 4 (all loads of a range issued together), in range order
+  if (a.S > 0) {
+    const int M = a.nb * L;
+    const int64_t ml_off = (int64_t)a.S * M * a.Hq * D;
+    for (int sp = wv; sp < a.S; sp += 4) {
+      f32x4 oo[QB][NDB];
+      float mo[QB], lo[QB];
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const int row = qb * 16 + c16;
+        const int64_t e = ((int64_t)sp * M + br * L + (row < L ? row : 0)) * a.Hq + h;
+        const float* po = a.part + e * D + g * 4;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) oo[qb][db] = *(const f32x4*)(po + db * 16);
+        mo[qb] = a.part[ml_off + e * 2];
+        lo[qb] = a.part[ml_off + e * 2 + 1];
+      }
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        f32x4 ob[NDB];
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) ob[db] = o[db][qb];
+        merge_state<NDB>(m[qb], l[qb], ob, mo[qb], lo[qb], oo[qb]);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) o[db][qb] = ob[db];
+      }
+    }
   }
 
   // merge the four key ranges: (2, 3) into (0, 1), then 1 into 0
@@ -306,15 +387,15 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   auto take = [&](int slot) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      const float mo = sM[slot][qb * 16 + c16], lo = sL[slot][qb * 16 + c16];
-      const float mn = fmaxf(m[qb], mo);
-      const float fa = mn == -INFINITY ? 0.f : exp2f(m[qb] - mn);
-      const float fb = mn == -INFINITY ? 0.f : exp2f(mo - mn);
-      m[qb] = mn;
-      l[qb] = l[qb] * fa + lo * fb;
+      f32x4 oo[NDB], ob[NDB];
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
-        o[db][qb] = o[db][qb] * fa + *(const f32x4*)&sO[slot][((db * QB + qb) * 64 + lane) * 4] * fb;
+      for (int db = 0; db < NDB; ++db) {
+        oo[db] = *(const f32x4*)&sO[slot][((db * QB + qb) * 64 + lane) * 4];
+        ob[db] = o[db][qb];
+      }
+      merge_state<NDB>(m[qb], l[qb], ob, sM[slot][qb * 16 + c16], sL[slot][qb * 16 + c16], oo);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db][qb] = ob[db];
     }
   };
   if (wv >= 2) put(wv - 2);
@@ -343,8 +424,102 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
+// Shared prefix: one workgroup per (query head h, key range sp, group gr of
+// 64 RB query rows of all branches); wavefront wv owns rows
+// gr 64 RB + 16 RB wv .. (row r = branch * L + position) as RB 16-row blocks. The range's tiles are
+// copied once into a three-slot LDS ring shared by the four wavefronts (a
+// quarter of each tile's copies per wavefront) and computed by all of them.
+// Output: the unnormalised state of every row for this range, O at
+// part[((sp M + r) Hq + h) D ..] and (m, l) at part[S M Hq D + ((sp M + r) Hq + h) 2].
+template <int D, int RB>
+__global__ __launch_bounds__(256, 2) void attn_prefix_kernel(AttnArgs a) {
+  constexpr int NDB = D / 16, NKK = D / 32, RING = 3;
+  constexpr int OPS = TileLds<D>::OPS, OPW = OPS / 4;  // copies per tile and wavefront
+  static_assert(OPS % 4 == 0, "copies per wavefront");
+  __shared__ __attribute__((aligned(1024))) char smem[RING * TileLds<D>::TILE];
+  const int h = blockIdx.x, sp = blockIdx.y, gr = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  const int kvh = h / (a.Hq / a.Hkv);
+  const int L = a.L, P = a.P, M = a.nb * L;
+  const int k_lo = sp * a.KS, k_hi = min(P, k_lo + a.KS);
+  const int n = (k_hi - k_lo + KT - 1) / KT;  // >= 1: the host sizes the ranges
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;
+  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;
+  const uint32_t ring = (uint32_t)(uintptr_t)smem;
+
+  // this wavefront's copies of tile i (keys k_lo + 32 i ..) into slot i % RING;
+  // past the last tile the last one is copied again, so every iteration waits
+  // for the same count
+  auto issue = [&](int i) {
+    const int t = i < n ? i : n - 1;
+    const uint32_t sb = ring + (uint32_t)(i % RING) * TileLds<D>::TILE;
+#pragma unroll
+    for (int c = 0; c < OPW; ++c)
+      tile_copy<D>(wv * OPW + c, kc, vc, a.vld, k_lo + t * KT, P, sb, c16, g);
+  };
+  issue(0);
+  issue(1);
+
+  u32x4 qf[RB][NKK];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = (gr * 4 + wv) * 16 * RB + rb * 16 + c16;
+    const int rr = r < M ? r : 0;
+    const uint16_t* qrow = a.q + (((int64_t)(rr / L) * a.Hq + h) * L + rr % L) * D;
+    const unsigned keep = r < M ? ~0u : 0u;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) qf[rb][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
+  }
+  float m[RB], l[RB];
+  f32x4 o[NDB][RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    m[rb] = M_INIT;
+    l[rb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[db][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // tiles i and i + 1 are in flight at the top of iteration i: wait for this
+  // wavefront's copies of tile i; the barrier then makes every wavefront's
+  // copies visible and retires every read of tile i - 1, whose slot takes i + 2
+  for (int i = 0; i < n; ++i) {
+    attn_wait_vmcnt<OPW>();
+    __syncthreads();
+    issue(i + 2);
+    AttnTile<D> x;
+    tile_fetch<D>(smem + (i % RING) * TileLds<D>::TILE, lane, x);
+    tile_update<D, RB>(x, qf, m, l, o, k_lo + i * KT, k_hi, sl2, g);
+  }
+  attn_wait_vmcnt<0>();  // the repeated copies past the last tile
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int r = (gr * 4 + wv) * 16 * RB + rb * 16 + c16;
+    l[rb] = pair32_sum(pair16_sum(l[rb]));
+    if (r >= M) continue;
+    const int64_t e = ((int64_t)sp * M + r) * a.Hq + h;
+    float* po = a.part + e * D + g * 4;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) *(f32x4*)(po + db * 16) = o[db][rb];
+    if (g == 0) {
+      float* pml = a.part + (int64_t)a.S * M * a.Hq * D + e * 2;
+      pml[0] = m[rb];
+      pml[1] = l[rb];
+    }
+  }
+}
+
 template <int D>
 hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
+  if (a.S > 0) {
+    const dim3 pgrid(a.Hq, a.S, (a.nb * a.L + ATTN_PREFIX_ROWS - 1) / ATTN_PREFIX_ROWS);
+    hipLaunchKernelGGL((attn_prefix_kernel<D, ATTN_PREFIX_ROWS / 64>), pgrid, dim3(256), 0, s, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const dim3 grid(a.Hq, a.nb);
   switch ((a.L + 15) / 16) {
     case 1: hipLaunchKernelGGL((attn_kernel<D, 1>), grid, dim3(256), 0, s, a); break;
@@ -361,6 +536,11 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.L < 1 || a.L > 64 || a.P < 0 || a.Hq % a.Hkv || a.vld % 8 || a.vlds % 8 ||
       a.L > a.vlds || a.P > a.vld)
+    return hipErrorInvalidValue;
+  // shared prefix: every key range non-empty, the ranges cover [0, P), and the
+  // workspace was given
+  if (a.S < 0 || (a.S > 0 && (!a.part || a.KS < KT || a.KS % KT || a.P < 1 ||
+                              (int64_t)(a.S - 1) * a.KS >= a.P || (int64_t)a.S * a.KS < a.P)))
     return hipErrorInvalidValue;
   if (a.d == 128) return launch_d<128>(a, s);
   if (a.d == 64) return launch_d<64>(a, s);

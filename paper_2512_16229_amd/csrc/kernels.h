@@ -102,5 +102,13 @@ struct AttnArgs {
   uint16_t* out;           // packed activations (Mp rows, Hq*d columns)
   int nb, L, P, Hq, Hkv, d, vld, layer, layers, vlds, Mp;
   float scale;
+  // shared-prefix path (S > 0): the prefix runs as S key ranges of KS
+  // positions (a multiple of 32; every range non-empty) for all branches at
+  // once; part is the fp32 workspace: O [S][nb*L][Hq][d], then (m, l)
+  // [S][nb*L][Hq][2]. S = 0: the prefix runs inside the per-branch kernel.
+  int S, KS;
+  float* part;
 };
+// query rows (of all branches) per workgroup of the shared-prefix pass
+constexpr int ATTN_PREFIX_ROWS = 128;
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

@@ -12,13 +12,14 @@ assumption:
     `s_waitcnt vmcnt(N)` all but the N most recent ones have landed; walking
     each kernel in program order with that rule, no instruction other than
     the load itself touches a register whose load may still be in flight;
-  * no gemm kernel uses scratch memory;
+  * no gemm or attention kernel uses scratch memory;
   * the MFMA loop blocks of the GEMM contain no AGPR/VGPR copies (the
     accumulators stay in place).
 The walk follows the text in order, which matches the control flow of these
 kernels: their loads are issued on every path (clamped indices instead of
 branches), so no conditional block holds a load.
 """
+import importlib.util
 import os
 import re
 import shutil
@@ -31,14 +32,24 @@ HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 MEM = re.compile(r"^(global|buffer|flat|scratch)_(load|store|atomic)")
 
 
+def _build_module():
+    # the library's own compile flags (build.py loaded by path: importing the
+    # package would load the library)
+    spec = importlib.util.spec_from_file_location(
+        "lopa_build", os.path.join(ROOT, "paper_2512_16229_amd", "build.py"))
+    b = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(b)
+    return b
+
+
 def _compile(tmp_path_factory, src):
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
+    b = _build_module()
     out = str(tmp_path_factory.mktemp("asm") / (src + ".s"))
-    cmd = [HIPCC, "-O3", "-std=c++17", "--offload-arch=gfx950", "-Xclang", "-target-feature",
-           "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"),
-           "--cuda-device-only", "-S", os.path.join(ROOT, "paper_2512_16229_amd", "csrc", src + ".hip"),
-           "-o", out]
+    flags = [f for f in b.FLAGS if f != "-fPIC"] + b.EXTRA_FLAGS.get(src + ".hip", [])
+    cmd = [HIPCC, *flags, "--cuda-device-only", "-S",
+           os.path.join(ROOT, "paper_2512_16229_amd", "csrc", src + ".hip"), "-o", out]
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     return open(out).read()
@@ -101,17 +112,20 @@ def _inflight_violations(body):
 def test_kernels_found(asm, attn_asm):
     assert len(list(_kernels(asm))) >= 6
     assert len(list(_kernels(attn_asm, "attn_kernel"))) >= 8
+    assert len(list(_kernels(attn_asm, "attn_prefix_kernel"))) >= 2
 
 
 def test_inflight_registers_untouched(asm, attn_asm):
-    for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel")):
+    for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel"),
+                    (attn_asm, "attn_prefix_kernel")):
         for name, body in _kernels(s, kind):
             bad = _inflight_violations(body)
             assert not bad, f"{name}: in-flight registers touched: {bad[:5]}"
 
 
 def test_no_scratch(asm, attn_asm):
-    for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel")):
+    for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel"),
+                    (attn_asm, "attn_prefix_kernel")):
         for name, body in _kernels(s, kind):
             assert "scratch_" not in "\n".join(body), f"{name} spills to scratch"
 
@@ -130,3 +144,23 @@ def test_mfma_loops_keep_accumulators_in_place(asm):
                 copies = [t for t in b if t.startswith(("v_accvgpr_read", "v_accvgpr_write",
                                                         "v_accvgpr_mov"))]
                 assert not copies, f"{name}: {len(copies)} accumulator copies in an MFMA loop"
+
+
+def test_attention_inline_asm_is_memory_only(attn_asm):
+    """The attention kernels' MFMAs are compiler builtins, so the compiler
+    inserts the wait states before their results are read; that holds only
+    for instructions it sees. Its inline assembly is therefore limited to the
+    asynchronous copies and explicit waits (no vector arithmetic that could
+    read an MFMA result too early)."""
+    allowed = re.compile(r"^(s_mov_b32 m0,|global_load_lds_dwordx4|s_waitcnt)")
+    for kind in ("attn_kernel", "attn_prefix_kernel"):
+        for name, body in _kernels(attn_asm, kind):
+            inside = False
+            for line in body:
+                t = line.strip()
+                if t.startswith(";;#ASMSTART"):
+                    inside = True
+                elif t.startswith(";;#ASMEND"):
+                    inside = False
+                elif inside and t and not t.startswith(";"):
+                    assert allowed.match(t), f"{name}: inline asm {t!r}"

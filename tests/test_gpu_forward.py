@@ -73,6 +73,61 @@ def test_verify_forward_parity(cfgname, P, L, k):
             _kv_close(vs, rf["v"][j, layer], f"staging V b{j} l{layer}")
 
 
+# (config, P, L, k, ranges): -1 lets the library choose (these shapes take the
+# shared-prefix path: long prefixes, 4 to 16 branches, one and two 256-row
+# groups, ragged last key range); n >= 1 forces about n key ranges, down to
+# one key in one range and a 5-key last range
+SHARED = [("tiny", 512, 16, 3, -1), ("small", 600, 32, 15, -1), ("small128", 300, 32, 15, -1),
+          ("tiny", 37, 16, 3, 2), ("small128", 1, 8, 2, 1), ("small", 100, 48, 3, 4)]
+
+
+@pytest.mark.parametrize("cfgname,P,L,k,ranges", SHARED)
+def test_shared_prefix_attention(cfgname, P, L, k, ranges):
+    """The shared-prefix attention path (prefix key ranges computed once per
+    query head for all branches, merged per branch) against the oracle, and
+    against the per-(head, branch) path on the same cache."""
+    log(f"shared-prefix attention {cfgname} P={P} L={L} k={k} ranges={ranges}")
+    s = Setup(cfgname, P, L, k)
+    s.gpu_prefill()
+    s.load_oracle_cache()
+    nb, mask = k + 1, s.cfg["mask_id"]
+    s.kv.set_attention_ranges(ranges)
+    S, KS = s.kv.attention_plan(P, nb, L)
+    log(f"  {S} key ranges of {KS}")
+    assert S >= 1 and KS % 32 == 0 and (S - 1) * KS < P <= S * KS
+    if ranges > 0:
+        assert S <= ranges
+    rng = np.random.default_rng(P + 3 * L + k)
+    bt = np.where(rng.random((nb, L)) < 0.7, mask, rng.integers(0, s.cfg["vocab"] - 1, (nb, L)))
+    bt[0] = mask
+    conf, pred = s.gpu_forward(bt)
+    rp = s.pure.forward_block(bt, P, s.cache_p)
+    rf = s.faith.forward_block(bt, P, s.cache_f, keep_hidden=True)
+    e_bf16 = np.max(np.abs(rf["conf"] - rp["conf"]))
+    e_faith = np.max(np.abs(conf - rf["conf"]))
+    decided = vocab_margin(rf["logits"], mask) >= near_tie(e_faith)
+    log(f"  max|dconf| gpu-faithful={e_faith:.2e} faithful-pure={e_bf16:.2e} "
+        f"decided {decided.mean():.2f}")
+    assert e_faith < faithful_bound(e_bf16)
+    # long prefixes on the small random models: the bf16 computation's own
+    # error reaches ~0.05 (faithful oracle vs float64), which widens the
+    # near-tie band; most positions are still decided
+    assert decided.mean() > 0.6
+    assert np.array_equal(pred[decided], rf["pred"][decided])
+    # the per-(head, branch) path on the same inputs
+    s.kv.set_attention_ranges(0)
+    assert s.kv.attention_plan(P, nb, L) == (0, 0)
+    conf0, pred0 = s.gpu_forward(bt)
+    e_path = np.max(np.abs(conf - conf0))
+    e_faith0 = np.max(np.abs(conf0 - rf["conf"]))
+    log(f"  max|dconf| gpu-faithful={e_faith:.2e} (per-branch {e_faith0:.2e}) "
+        f"shared-per_branch={e_path:.2e} faithful-pure={e_bf16:.2e}")
+    assert e_faith0 < faithful_bound(e_bf16)
+    assert e_path < conf_tolerance(e_bf16)
+    decided0 = vocab_margin(rf["logits"], mask) >= near_tie(e_faith0)
+    assert np.array_equal(pred0[decided0], rf["pred"][decided0])
+
+
 @pytest.mark.parametrize("cfgname,P,L,k", [("tiny", 64, 16, 3), ("small", 100, 32, 7),
                                            ("small128", 40, 16, 1)])
 def test_hidden_states_per_layer(cfgname, P, L, k):
@@ -97,14 +152,19 @@ def test_hidden_states_per_layer(cfgname, P, L, k):
             assert np.array_equal(g, r)          # embedding gather is exact
 
 
+# the last two take the shared-prefix attention path (16-row query blocks of
+# the prefix pass that straddle branches)
 @pytest.mark.parametrize("cfgname,P,L,k", [("tiny", 64, 16, 3), ("small", 100, 32, 7),
-                                           ("tiny", 23, 7, 2), ("small", 50, 48, 3)])
+                                           ("tiny", 23, 7, 2), ("small", 50, 48, 3),
+                                           ("tiny", 300, 7, 15), ("small", 400, 24, 7)])
 def test_batch_invariance_and_determinism(cfgname, P, L, k):
     log(f"batch invariance {cfgname} P={P} L={L} k={k}")
     s = Setup(cfgname, P, L, k)
     s.gpu_prefill()
     mask = s.cfg["mask_id"]
     nb = k + 1
+    if P >= 256:
+        assert s.kv.attention_plan(P, nb, L)[0] > 0
     rng = np.random.default_rng(7)
     bt = np.where(rng.random((nb, L)) < 0.7, mask, rng.integers(0, s.cfg["vocab"] - 1, (nb, L)))
     c1, p1 = s.gpu_forward(bt)
