@@ -114,18 +114,20 @@ GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_n
   return best;
 }
 // Attention: the shared-prefix path (attn_prefix_kernel: each prefix tile read
-// once per (query head, 128-row group) for all branches, S key ranges with
-// fp32 partial states merged by the per-branch kernel) when it moves clearly
+// once per (query head, row group) for all branches, S key ranges with fp32
+// partial states merged by the per-branch block kernel) when it moves clearly
 // fewer bytes than the per-(head, branch) path: K/V bytes read plus partial
-// states written and read. S targets two workgroups per CU (the prefix kernel
-// runs two per CU) with ranges of at least four key tiles.
+// states written and read. S targets one wave of workgroups over the CUs
+// (two wavefronts per SIMD) with ranges of at least four key tiles.
 struct AttnPlan {
   int S, KS;
 };
 AttnPlan plan_attention(const lopa_model_cfg& c, int nb, int L, int P, int num_cu) {
   if (P < 256 || nb < 2) return {0, 0};
   const int M = nb * L, G = (M + ATTN_PREFIX_ROWS - 1) / ATTN_PREFIX_ROWS, tiles = (P + 31) / 32;
-  int S = std::min(std::max(1, tiles / 4), std::max(1, 2 * num_cu / (c.heads * G)));
+  // workgroups per CU at two wavefronts per SIMD
+  const int wg_cu = std::max(1, 8 * 32 / ATTN_PREFIX_ROWS);
+  int S = std::min(std::max(1, tiles / 4), std::max(1, wg_cu * num_cu / (c.heads * G)));
   const int KS = 32 * ((tiles + S - 1) / S);
   S = (P + KS - 1) / KS;
   const double kv_row = 2.0 * c.head_dim * 2;  // K and V bytes of one position and head
@@ -144,7 +146,7 @@ AttnPlan fixed_ranges(int S, int P) {
 }
 // the largest number of key ranges plan_attention picks on this device
 int attn_max_ranges(const lopa_model_cfg& c, int num_cu) {
-  return std::max(1, 2 * num_cu / c.heads);
+  return std::max(1, 2 * num_cu / c.heads);  // >= the planner's choice at any ATTN_PREFIX_ROWS >= 128
 }
 
 // bytes of fp32 partial sums the plan writes (QKV always goes through them;

@@ -9,13 +9,14 @@
 //    each, prefix tiles from the cache and block tiles from the branch's
 //    staging) for all L rows, and the four partial softmax states are merged
 //    through LDS. Short prefixes: no state leaves the workgroup.
-//  * attn_prefix_kernel + attn_kernel: the prefix is shared by all branches,
-//    so one workgroup per (query head, key range, 256-row group) streams each
-//    prefix tile of its range once into LDS and computes it for the rows of
-//    every branch (64 rows per wavefront); its unnormalised partial state per
-//    row goes to a workspace. attn_kernel then runs only the block tiles and
-//    merges the partial states of the key ranges. Long prefixes: each prefix
-//    K/V tile is read once per query head instead of once per (head, branch).
+//  * attn_prefix_kernel + attn_block_kernel: the prefix is shared by all
+//    branches, so one workgroup per (query head, key range, 128-row group)
+//    streams each prefix tile of its range once into LDS and computes it for
+//    the rows of every branch (32 rows per wavefront); its unnormalised
+//    partial state per row goes to a workspace. attn_block_kernel then runs
+//    the block tiles per (head, branch) and merges the partial states of the
+//    key ranges. Long prefixes: each prefix K/V tile is read once per (query
+//    head, row group) instead of once per (head, branch).
 // Tiles go global -> LDS by asynchronous copies, then into registers in MFMA
 // operand layout. Scores are formed transposed, S^T = K Q^T, so a lane owns one
 // query column and the probabilities land directly in the operand layout of
@@ -28,6 +29,8 @@
 #include "kernels.h"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace {
 
@@ -125,6 +128,38 @@ __device__ __forceinline__ void tile_copy(int q, const uint16_t* kbase, const ui
   }
 }
 
+// Lane byte offsets of the copies of a tile that lies wholly inside its source
+// (no clamping): k0 / k1 for the K copies of key block 0 / 1, v for the V
+// copies of a source whose V^T rows are vld positions long. (Scalars, not an
+// array: the copy index may be known only at run time, and a dynamically
+// indexed array would live in scratch memory.)
+struct CopyOffsets {
+  uint32_t k0, k1, v;
+};
+template <int D>
+__device__ __forceinline__ CopyOffsets copy_offsets(int64_t vld, int c16, int g) {
+  CopyOffsets c;
+  c.k0 = (uint32_t)((c16 * D + g * 8) * 2);
+  c.k1 = (uint32_t)(((16 + c16) * D + g * 8) * 2);
+  c.v = (uint32_t)((c16 * vld + 8 * g) * 2);
+  return c;
+}
+// tile_copy of a tile with p0 + 32 <= lim: the same copies, addresses from the
+// wave-uniform base and the precomputed lane offsets
+template <int D>
+__device__ __forceinline__ void tile_copy_full(int q, const uint16_t* kbase, const uint16_t* vbase,
+                                               int64_t vld, int p0, uint32_t sb,
+                                               const CopyOffsets& co) {
+  using T = TileLds<D>;
+  if (q < 2 * T::NKK) {
+    const int kb = q / T::NKK, kk = q % T::NKK;
+    attn_dma16(kbase + (int64_t)p0 * D + kk * 32, kb ? co.k1 : co.k0, sb + q * 1024);
+  } else {
+    const int db = q - 2 * T::NKK;
+    attn_dma16(vbase + (int64_t)db * 16 * vld + p0, co.v, sb + q * 1024);
+  }
+}
+
 // LDS slot -> registers (operand layouts)
 template <int D>
 __device__ __forceinline__ void tile_fetch(const char* sb, int lane, AttnTile<D>& x) {
@@ -146,20 +181,21 @@ __device__ __forceinline__ void tile_fetch(const char* sb, int lane, AttnTile<D>
 }
 
 // One key tile (keys p0 .. p0 + 31 of a source of lim positions) for NR blocks
-// of 16 query rows. With s the raw score q.k and sl2 = scale log2(e), the
+// of 16 query rows; ALWAYS_FULL: the caller knows the tile lies wholly inside
+// the source (no masking code). With s the raw score q.k and sl2 = scale log2(e), the
 // probabilities are p = 2^(s sl2 - m) against a reference maximum m (log2
 // units) that trails the running row maximum of s sl2 by at most 8: a row's m,
 // l and o are rescaled only when its maximum has grown past that, so p <= 2^8.
 // o / l and every merge are unchanged by the choice of reference. The maximum
 // is taken over the raw scores (scaling by sl2 > 0 keeps the order and,
 // rounding being monotone, the maximum itself).
-template <int D, int NR>
+template <int D, int NR, bool ALWAYS_FULL>
 __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR][D / 32],
                                             float (&m)[NR], float (&l)[NR],
                                             f32x4 (&o)[D / 16][NR], int p0, int lim, float sl2,
                                             int g) {
   constexpr int NDB = D / 16, NKK = D / 32;
-  const bool full = p0 + KT <= lim;  // wave-uniform
+  const bool full = ALWAYS_FULL || p0 + KT <= lim;  // wave-uniform
   if (!full) {
     // zero V of masked keys (stale cache or staging contents may be
     // non-finite, and 0 * inf would poison the sums); branch-free
@@ -253,9 +289,7 @@ struct AttnSmem {
   static constexpr int OPS = TileLds<D>::OPS;
 };
 
-// Per (query head, branch): the block tiles, and the prefix tiles unless the
-// prefix ran in attn_prefix_kernel (a.S > 0), whose partial states are merged
-// before the four wavefronts' states are.
+// Per (query head, branch): the prefix tiles and the block tiles.
 template <int D, int QB>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   using SM = AttnSmem<D, QB>;
@@ -267,7 +301,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int g = lane >> 4, c16 = lane & 15;
   const int kvh = h / (a.Hq / a.Hkv);
   const int L = a.L, P = a.P;
-  const int pt = a.S > 0 ? 0 : (P + KT - 1) / KT, bt = (L + KT - 1) / KT, T = pt + bt;
+  const int pt = (P + KT - 1) / KT, bt = (L + KT - 1) / KT, T = pt + bt;
   const int t_lo = wv * T / 4, t_hi = (wv + 1) * T / 4;
   const float sl2 = a.scale * 1.4426950408889634f;  // scale * log2(e)
 
@@ -279,14 +313,21 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const uint32_t ring = (uint32_t)(uintptr_t)smem + (uint32_t)(wv * 2) * TileLds<D>::TILE;
 
   // tile t -> this wavefront's ring slot (all OPS copies)
+  const CopyOffsets co_c = copy_offsets<D>(a.vld, c16, g), co_s = copy_offsets<D>(a.vlds, c16, g);
   auto issue = [&](int t, int slot) {
     const bool pre = t < pt;
-    const int p0 = (pre ? t : t - pt) * KT;
+    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
     const uint32_t sb = ring + (uint32_t)slot * TileLds<D>::TILE;
+    if (p0 + KT <= lim) {
 #pragma unroll
-    for (int q = 0; q < SM::OPS; ++q)
-      tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, pre ? P : L, sb,
-                   c16, g);
+      for (int q = 0; q < SM::OPS; ++q)
+        tile_copy_full<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, sb,
+                          pre ? co_c : co_s);
+    } else {
+#pragma unroll
+      for (int q = 0; q < SM::OPS; ++q)
+        tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, lim, sb, c16, g);
+    }
   };
 
   // the first two tiles are in flight while Q is loaded
@@ -328,7 +369,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     tile_fetch<D>(smem + (wv * 2 + (i & 1)) * TileLds<D>::TILE, lane, x);
     const int t = t_lo + i;
     const bool pre = t < pt;
-    tile_update<D, QB>(x, qf, m, l, o, (pre ? t : t - pt) * KT, pre ? P : L, sl2, g);
+    tile_update<D, QB, false>(x, qf, m, l, o, (pre ? t : t - pt) * KT, pre ? P : L, sl2, g);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     issue(t_lo + (i + 2 < n ? i + 2 : n - 1), i & 1);
   }
@@ -336,36 +377,6 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   __syncthreads();
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) l[qb] = pair32_sum(pair16_sum(l[qb]));
-
-  // the prefix key ranges of attn_prefix_kernel: range sp is merged by
-  // wavefront sp % 4 (all loads of a range issued together), in range order
-  if (a.S > 0) {
-    const int M = a.nb * L;
-    const int64_t ml_off = (int64_t)a.S * M * a.Hq * D;
-    for (int sp = wv; sp < a.S; sp += 4) {
-      f32x4 oo[QB][NDB];
-      float mo[QB], lo[QB];
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        const int row = qb * 16 + c16;
-        const int64_t e = ((int64_t)sp * M + br * L + (row < L ? row : 0)) * a.Hq + h;
-        const float* po = a.part + e * D + g * 4;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) oo[qb][db] = *(const f32x4*)(po + db * 16);
-        mo[qb] = a.part[ml_off + e * 2];
-        lo[qb] = a.part[ml_off + e * 2 + 1];
-      }
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        f32x4 ob[NDB];
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) ob[db] = o[db][qb];
-        merge_state<NDB>(m[qb], l[qb], ob, mo[qb], lo[qb], oo[qb]);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) o[db][qb] = ob[db];
-      }
-    }
-  }
 
   // merge the four key ranges: (2, 3) into (0, 1), then 1 into 0
   float(*sO)[SM::MERGE_O] = (float(*)[SM::MERGE_O])smem;
@@ -425,17 +436,18 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 }
 
 // Shared prefix: one workgroup per (query head h, key range sp, group gr of
-// 64 RB query rows of all branches); wavefront wv owns rows
-// gr 64 RB + 16 RB wv .. (row r = branch * L + position) as RB 16-row blocks. The range's tiles are
+// 16 RB NW query rows of all branches); wavefront wv of NW owns rows
+// (gr NW + wv) 16 RB .. (row r = branch * L + position) as RB 16-row blocks. The range's tiles are
 // copied once into a three-slot LDS ring shared by the four wavefronts (a
 // quarter of each tile's copies per wavefront) and computed by all of them.
 // Output: the unnormalised state of every row for this range, O at
 // part[((sp M + r) Hq + h) D ..] and (m, l) at part[S M Hq D + ((sp M + r) Hq + h) 2].
-template <int D, int RB>
-__global__ __launch_bounds__(256, 2) void attn_prefix_kernel(AttnArgs a) {
-  constexpr int NDB = D / 16, NKK = D / 32, RING = 3;
-  constexpr int OPS = TileLds<D>::OPS, OPW = OPS / 4;  // copies per tile and wavefront
-  static_assert(OPS % 4 == 0, "copies per wavefront");
+template <int D, int RB, int NW, int RING>
+__global__ __launch_bounds__(64 * NW, 2) void attn_prefix_kernel(AttnArgs a) {
+  constexpr int NDB = D / 16, NKK = D / 32;
+  constexpr int OPS = TileLds<D>::OPS, OPW = OPS / NW;  // copies per tile and wavefront
+  static_assert(OPS % NW == 0, "copies per wavefront");
+  static_assert(RING >= 3 && (RING - 2) * OPW <= 63, "ring depth");
   __shared__ __attribute__((aligned(1024))) char smem[RING * TileLds<D>::TILE];
   const int h = blockIdx.x, sp = blockIdx.y, gr = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -453,20 +465,26 @@ __global__ __launch_bounds__(256, 2) void attn_prefix_kernel(AttnArgs a) {
   // this wavefront's copies of tile i (keys k_lo + 32 i ..) into slot i % RING;
   // past the last tile the last one is copied again, so every iteration waits
   // for the same count
+  const CopyOffsets co = copy_offsets<D>(a.vld, c16, g);
   auto issue = [&](int i) {
     const int t = i < n ? i : n - 1;
+    const int p0 = k_lo + t * KT;
     const uint32_t sb = ring + (uint32_t)(i % RING) * TileLds<D>::TILE;
+    if (p0 + KT <= P) {
 #pragma unroll
-    for (int c = 0; c < OPW; ++c)
-      tile_copy<D>(wv * OPW + c, kc, vc, a.vld, k_lo + t * KT, P, sb, c16, g);
+      for (int c = 0; c < OPW; ++c) tile_copy_full<D>(wv * OPW + c, kc, vc, a.vld, p0, sb, co);
+    } else {
+#pragma unroll
+      for (int c = 0; c < OPW; ++c) tile_copy<D>(wv * OPW + c, kc, vc, a.vld, p0, P, sb, c16, g);
+    }
   };
-  issue(0);
-  issue(1);
+#pragma unroll
+  for (int i = 0; i < RING - 1; ++i) issue(i);
 
   u32x4 qf[RB][NKK];
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const int r = (gr * 4 + wv) * 16 * RB + rb * 16 + c16;
+    const int r = (gr * NW + wv) * 16 * RB + rb * 16 + c16;
     const int rr = r < M ? r : 0;
     const uint16_t* qrow = a.q + (((int64_t)(rr / L) * a.Hq + h) * L + rr % L) * D;
     const unsigned keep = r < M ? ~0u : 0u;
@@ -483,21 +501,27 @@ __global__ __launch_bounds__(256, 2) void attn_prefix_kernel(AttnArgs a) {
     for (int db = 0; db < NDB; ++db) o[db][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  // tiles i and i + 1 are in flight at the top of iteration i: wait for this
-  // wavefront's copies of tile i; the barrier then makes every wavefront's
-  // copies visible and retires every read of tile i - 1, whose slot takes i + 2
-  for (int i = 0; i < n; ++i) {
-    attn_wait_vmcnt<OPW>();
+  // tiles i .. i + RING - 2 are in flight at the top of iteration i: wait for
+  // this wavefront's copies of tile i; the barrier then makes every
+  // wavefront's copies visible and retires every read of tile i - 1, whose
+  // slot takes tile i + RING - 1
+  // (only the last tile of the last range can be partial: it runs after the
+  // loop, through the masking path)
+  const int n_full = (k_hi - k_lo) / KT;
+  auto step = [&](int i, auto full) {
+    attn_wait_vmcnt<(RING - 2) * OPW>();
     __syncthreads();
-    issue(i + 2);
+    issue(i + RING - 1);
     AttnTile<D> x;
     tile_fetch<D>(smem + (i % RING) * TileLds<D>::TILE, lane, x);
-    tile_update<D, RB>(x, qf, m, l, o, k_lo + i * KT, k_hi, sl2, g);
-  }
+    tile_update<D, RB, decltype(full)::value>(x, qf, m, l, o, k_lo + i * KT, k_hi, sl2, g);
+  };
+  for (int i = 0; i < n_full; ++i) step(i, std::true_type{});
+  if (n_full < n) step(n_full, std::false_type{});
   attn_wait_vmcnt<0>();  // the repeated copies past the last tile
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const int r = (gr * 4 + wv) * 16 * RB + rb * 16 + c16;
+    const int r = (gr * NW + wv) * 16 * RB + rb * 16 + c16;
     l[rb] = pair32_sum(pair16_sum(l[rb]));
     if (r >= M) continue;
     const int64_t e = ((int64_t)sp * M + r) * a.Hq + h;
@@ -512,15 +536,112 @@ __global__ __launch_bounds__(256, 2) void attn_prefix_kernel(AttnArgs a) {
   }
 }
 
+// After attn_prefix_kernel: per (query head, branch), the block tiles (one
+// or two) and the merge of the prefix key ranges. Wavefront wv owns query
+// rows 16 wv .. 16 wv + 15, so no state crosses wavefronts; the block tiles
+// are copied once into LDS (the copies spread over the wavefronts). The
+// partial states of up to four ranges are loaded together, the first four
+// while the tiles are in flight; a row merges its block state and then the
+// ranges in range order.
+template <int D, int QB>
+__global__ __launch_bounds__(64 * QB) void attn_block_kernel(AttnArgs a) {
+  constexpr int NDB = D / 16, NKK = D / 32, OPS = TileLds<D>::OPS, RG = 4;
+  __shared__ __attribute__((aligned(1024))) char smem[2 * TileLds<D>::TILE];
+  const int h = blockIdx.x, br = blockIdx.y;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  const int kvh = h / (a.Hq / a.Hkv);
+  const int L = a.L, bt = (L + KT - 1) / KT, M = a.nb * L;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
+  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
+  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
+  const uint32_t ring = (uint32_t)(uintptr_t)smem;
+  for (int t = 0; t < bt; ++t)
+    for (int q = wv; q < OPS; q += QB)
+      tile_copy<D>(q, ks, vs, a.vlds, t * KT, L, ring + (uint32_t)t * TileLds<D>::TILE, c16, g);
+
+  const int row = wv * 16 + c16;
+  const int rr = row < L ? row : 0;
+  u32x4 qf[1][NKK];
+  {
+    const uint16_t* qrow = a.q + (((int64_t)br * a.Hq + h) * L + rr) * D;
+    const unsigned keep = row < L ? ~0u : 0u;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) qf[0][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
+  }
+  // partial state of range sp for this lane's row
+  const int64_t ml_off = (int64_t)a.S * M * a.Hq * D;
+  f32x4 po[RG][NDB];
+  float pm[RG], pl[RG];
+  auto load_ranges = [&](int sp0) {
+#pragma unroll
+    for (int u = 0; u < RG; ++u) {
+      const int sp = sp0 + u < a.S ? sp0 + u : a.S - 1;
+      const int64_t e = ((int64_t)sp * M + br * L + rr) * a.Hq + h;
+      const float* src = a.part + e * D + g * 4;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) po[u][db] = *(const f32x4*)(src + db * 16);
+      pm[u] = a.part[ml_off + e * 2];
+      pl[u] = a.part[ml_off + e * 2 + 1];
+    }
+  };
+  load_ranges(0);
+  attn_wait_vmcnt<0>();  // the tile copies (and, in order, everything before)
+  __syncthreads();
+
+  float m[1] = {M_INIT}, l[1] = {0.f};
+  f32x4 o[NDB][1];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) o[db][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < bt; ++t) {
+    AttnTile<D> x;
+    tile_fetch<D>(smem + t * TileLds<D>::TILE, lane, x);
+    tile_update<D, 1, false>(x, qf, m, l, o, t * KT, L, sl2, g);
+  }
+  l[0] = pair32_sum(pair16_sum(l[0]));
+  f32x4 ob[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) ob[db] = o[db][0];
+  for (int sp0 = 0; sp0 < a.S; sp0 += RG) {
+    if (sp0 > 0) load_ranges(sp0);
+#pragma unroll
+    for (int u = 0; u < RG; ++u)
+      if (sp0 + u < a.S) merge_state<NDB>(m[0], l[0], ob, pm[u], pl[u], po[u]);
+  }
+  if (row >= L) return;
+  const float inv = 1.0f / l[0];
+  const int r = br * L + row;
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+    uint16_t v4[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v4[j] = f2bf_bits(ob[db][j] * inv);
+    *(uint2*)(a.out + packA_off(r, h * D + db * 16 + g * 4, a.Mp)) = *(const uint2*)v4;
+  }
+}
+
 template <int D>
 hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
   if (a.S > 0) {
     const dim3 pgrid(a.Hq, a.S, (a.nb * a.L + ATTN_PREFIX_ROWS - 1) / ATTN_PREFIX_ROWS);
-    hipLaunchKernelGGL((attn_prefix_kernel<D, ATTN_PREFIX_ROWS / 64>), pgrid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((attn_prefix_kernel<D, 2, ATTN_PREFIX_ROWS / 32, ATTN_PREFIX_RING>), pgrid,
+                       dim3(2 * ATTN_PREFIX_ROWS), 0, s, a);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   const dim3 grid(a.Hq, a.nb);
+  if (a.S > 0) {
+    switch ((a.L + 15) / 16) {
+      case 1: hipLaunchKernelGGL((attn_block_kernel<D, 1>), grid, dim3(64), 0, s, a); break;
+      case 2: hipLaunchKernelGGL((attn_block_kernel<D, 2>), grid, dim3(128), 0, s, a); break;
+      case 3: hipLaunchKernelGGL((attn_block_kernel<D, 3>), grid, dim3(192), 0, s, a); break;
+      case 4: hipLaunchKernelGGL((attn_block_kernel<D, 4>), grid, dim3(256), 0, s, a); break;
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch ((a.L + 15) / 16) {
     case 1: hipLaunchKernelGGL((attn_kernel<D, 1>), grid, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((attn_kernel<D, 2>), grid, dim3(256), 0, s, a); break;

@@ -109,6 +109,9 @@ struct AttnArgs {
   int S, KS;
   float* part;
 };
-// query rows (of all branches) per workgroup of the shared-prefix pass
+// query rows (of all branches) per workgroup of the shared-prefix pass (32
+// per wavefront, two wavefronts per SIMD) and its LDS ring depth in key
+// tiles (all but one in flight)
 constexpr int ATTN_PREFIX_ROWS = 128;
+constexpr int ATTN_PREFIX_RING = 4;
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

@@ -113,11 +113,12 @@ def test_kernels_found(asm, attn_asm):
     assert len(list(_kernels(asm))) >= 6
     assert len(list(_kernels(attn_asm, "attn_kernel"))) >= 8
     assert len(list(_kernels(attn_asm, "attn_prefix_kernel"))) >= 2
+    assert len(list(_kernels(attn_asm, "attn_block_kernel"))) >= 8
 
 
 def test_inflight_registers_untouched(asm, attn_asm):
     for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel"),
-                    (attn_asm, "attn_prefix_kernel")):
+                    (attn_asm, "attn_prefix_kernel"), (attn_asm, "attn_block_kernel")):
         for name, body in _kernels(s, kind):
             bad = _inflight_violations(body)
             assert not bad, f"{name}: in-flight registers touched: {bad[:5]}"
@@ -125,7 +126,7 @@ def test_inflight_registers_untouched(asm, attn_asm):
 
 def test_no_scratch(asm, attn_asm):
     for s, kind in ((asm, "gemm_kernel"), (attn_asm, "attn_kernel"),
-                    (attn_asm, "attn_prefix_kernel")):
+                    (attn_asm, "attn_prefix_kernel"), (attn_asm, "attn_block_kernel")):
         for name, body in _kernels(s, kind):
             assert "scratch_" not in "\n".join(body), f"{name} spills to scratch"
 
@@ -153,7 +154,7 @@ def test_attention_inline_asm_is_memory_only(attn_asm):
     asynchronous copies and explicit waits (no vector arithmetic that could
     read an MFMA result too early)."""
     allowed = re.compile(r"^(s_mov_b32 m0,|global_load_lds_dwordx4|s_waitcnt)")
-    for kind in ("attn_kernel", "attn_prefix_kernel"):
+    for kind in ("attn_kernel", "attn_prefix_kernel", "attn_block_kernel"):
         for name, body in _kernels(attn_asm, kind):
             inside = False
             for line in body:
