@@ -35,6 +35,14 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   float* xr = x + (int64_t)r * H;
   float4 v[NG];
   float ss = 0.f;
+  // the norm weights are loaded first, with the row's inputs, so that no
+  // load waits behind the reduction
+  float4 wt[NG];
+#pragma unroll
+  for (int i = 0; i < NG; ++i) {
+    const int q = tid + 256 * i;
+    wt[i] = ((const float4*)w)[q < nq ? q : nq - 1];
+  }
   if (EMBED) {
     // a token outside [0, vocab) reads row 0 instead of memory past the table
     int tok = tokens[r];
@@ -51,9 +59,13 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   } else {
     // partial sums in split order, then the residual. SC >= 0: the split count
     // is a compile-time constant; SC < 0: S, known at run time.
-    float4 t[NG];
+    float4 t[NG], res[NG];
 #pragma unroll
-    for (int i = 0; i < NG; ++i) t[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int i = 0; i < NG; ++i) {
+      const int q = tid + 256 * i;
+      res[i] = ((const float4*)xr)[q < nq ? q : nq - 1];  // the residual, loaded up front
+      t[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
     const int ns = SC >= 0 ? SC : S;
     for (int sp = 0; sp < ns; ++sp) {
       const float4* pr = (const float4*)(part + ((int64_t)sp * Mp + r) * H);
@@ -68,7 +80,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
     for (int i = 0; i < NG; ++i) {
       const int q = tid + 256 * i;
       const bool ok = q < nq;
-      const float4 u = ((const float4*)xr)[ok ? q : nq - 1];
+      const float4 u = res[i];
       v[i] = make_float4(ok ? u.x + t[i].x : 0.f, ok ? u.y + t[i].y : 0.f,
                          ok ? u.z + t[i].z : 0.f, ok ? u.w + t[i].w : 0.f);
     }
@@ -88,57 +100,65 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   for (int i = 0; i < NG; ++i) {
     const int q = tid + 256 * i;
     if (q < nq) {
-      const float4 wt = ((const float4*)w)[q];
-      const uint32_t lo = (uint32_t)f2bf_bits(v[i].x * inv * wt.x) |
-                          ((uint32_t)f2bf_bits(v[i].y * inv * wt.y) << 16);
-      const uint32_t hi = (uint32_t)f2bf_bits(v[i].z * inv * wt.z) |
-                          ((uint32_t)f2bf_bits(v[i].w * inv * wt.w) << 16);
+      const uint32_t lo = (uint32_t)f2bf_bits(v[i].x * inv * wt[i].x) |
+                          ((uint32_t)f2bf_bits(v[i].y * inv * wt[i].y) << 16);
+      const uint32_t hi = (uint32_t)f2bf_bits(v[i].z * inv * wt[i].z) |
+                          ((uint32_t)f2bf_bits(v[i].w * inv * wt[i].w) << 16);
       *(uint2*)(a + packA_off(r, q * 4, Mp)) = make_uint2(lo, hi);
     }
   }
 }
 
-// One wavefront per row: merge (max, sum, argmax) of all vocabulary tiles.
+// (max, sum, argmax) state of a run of vocabulary tiles: sum of exp(logit -
+// max); the lowest index among equal maxima
+struct LmState {
+  float m, s;
+  int idx;
+};
+__device__ __forceinline__ LmState lm_combine(LmState a, LmState b) {
+  const float nm = fmaxf(a.m, b.m);
+  const float sa = a.m == -INFINITY ? 0.f : a.s * expf(a.m - nm);
+  const float sb = b.m == -INFINITY ? 0.f : b.s * expf(b.m - nm);
+  int ni;
+  if (a.m > b.m) ni = a.idx;
+  else if (b.m > a.m) ni = b.idx;
+  else ni = a.idx < b.idx ? a.idx : b.idx;
+  return {nm, sa + sb, ni};
+}
+
+// One workgroup per row: merge (max, sum, argmax) of all vocabulary tiles.
+// Thread t takes tiles t, t + 256, ... (loads of four tiles in flight); the
+// 256 states are then combined in a fixed tree (wavefront shuffles, then the
+// four wavefronts in order), the same for every row.
 __global__ __launch_bounds__(256) void lm_merge_kernel(const float* __restrict__ pm,
                                                        const float* __restrict__ ps,
                                                        const int32_t* __restrict__ pi, int M,
                                                        int tiles, float* __restrict__ conf,
                                                        int32_t* __restrict__ pred) {
-  const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= M) return;
-  float m = -INFINITY, s = 0.f;
-  int idx = 0x7fffffff;
-  for (int t = lane; t < tiles; t += 64) {
-    const float tm = pm[(int64_t)r * tiles + t], ts = ps[(int64_t)r * tiles + t];
-    const int ti = pi[(int64_t)r * tiles + t];
+  __shared__ LmState red[4];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int r = blockIdx.x;
+  LmState st{-INFINITY, 0.f, 0x7fffffff};
+  const float* rm = pm + (int64_t)r * tiles;
+  const float* rs = ps + (int64_t)r * tiles;
+  const int32_t* ri = pi + (int64_t)r * tiles;
+#pragma unroll 4
+  for (int t = tid; t < tiles; t += 256) {
+    const float tm = rm[t], ts = rs[t];
+    const int ti = ri[t];
     if (tm == -INFINITY) continue;
-    if (tm > m) {
-      s = s * expf(m - tm) + ts;
-      m = tm;
-      idx = ti;
-    } else {
-      s += ts * expf(tm - m);
-      if (tm == m && ti < idx) idx = ti;
-    }
+    st = lm_combine(st, {tm, ts, ti});
   }
   for (int o = 1; o < 64; o <<= 1) {
-    const float om = __shfl_xor(m, o), os = __shfl_xor(s, o);
-    const int oi = __shfl_xor(idx, o);
-    const float nm = fmaxf(m, om);
-    const float a = (m == -INFINITY) ? 0.f : s * expf(m - nm);
-    const float b = (om == -INFINITY) ? 0.f : os * expf(om - nm);
-    int ni;
-    if (m > om) ni = idx;
-    else if (om > m) ni = oi;
-    else ni = idx < oi ? idx : oi;
-    m = nm;
-    s = a + b;
-    idx = ni;
+    const LmState ot{__shfl_xor(st.m, o), __shfl_xor(st.s, o), __shfl_xor(st.idx, o)};
+    st = lm_combine(st, ot);
   }
-  if (lane == 0) {
-    conf[r] = 1.0f / s;
-    pred[r] = (idx == 0x7fffffff) ? 0 : idx;  // all logits non-finite: report token 0
+  if (lane == 0) red[wv] = st;
+  __syncthreads();
+  if (tid == 0) {
+    st = lm_combine(lm_combine(red[0], red[1]), lm_combine(red[2], red[3]));
+    conf[r] = 1.0f / st.s;
+    pred[r] = (st.idx == 0x7fffffff) ? 0 : st.idx;  // all logits non-finite: report token 0
   }
 }
 
@@ -243,8 +263,7 @@ hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, i
 
 hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, int M, int tiles,
                            float* conf, int32_t* pred, hipStream_t s) {
-  hipLaunchKernelGGL(lm_merge_kernel, dim3((M + 3) / 4), dim3(256), 0, s, pm, ps, pi, M, tiles,
-                     conf, pred);
+  hipLaunchKernelGGL(lm_merge_kernel, dim3(M), dim3(256), 0, s, pm, ps, pi, M, tiles, conf, pred);
   return hipGetLastError();
 }
 

@@ -182,6 +182,15 @@ __global__ __launch_bounds__(256) void commit_kernel(
     const uint4* s4 = (const uint4*)src;
     uint4* d4 = (uint4*)(dst + (int64_t)P * d);
     for (int e = threadIdx.x; e < L * d / 8; e += blockDim.x) d4[e] = s4[e];
+  } else if (L <= 256) {
+    // V^T rows: dimension dim holds its L positions contiguously. With lp the
+    // power of two >= L, thread t copies position t % lp of dimensions
+    // t / lp, t / lp + 256 / lp, ... (shifts and masks, no division)
+    const int lg = 32 - __builtin_clz(L - 1 > 0 ? L - 1 : 1) - (L == 1 ? 1 : 0);
+    const int i = threadIdx.x & ((1 << lg) - 1);
+    if (i < L)
+      for (int dim = threadIdx.x >> lg; dim < d; dim += 256 >> lg)
+        dst[(int64_t)dim * vld + P + i] = src[(int64_t)dim * vlds + i];
   } else {
     for (int e = threadIdx.x; e < L * d; e += blockDim.x) {
       const int dim = e / L, i = e % L;
