@@ -408,6 +408,20 @@ def main():
     per_step_ms = {kd: t / args.steps for kd, (t, n) in prof.items()}
     log("per-step ms by kind: " + ", ".join(f"{kd} {v:.3f}" for kd, v in per_step_ms.items()))
 
+    # the box's own copy bandwidth (device-to-device copy of 1 GiB, read + write
+    # bytes over the event time), the reference a measured roofline is read against
+    src = torch.empty(1 << 29, dtype=torch.int16, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * src.numel() * 2 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+
     gu_bytes = gateup_launch_bytes(cfg, M)
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
     sb = step_bytes(cfg, P, L, nb)
@@ -431,7 +445,9 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(os.path.join(ROOT, "profiles",
                                                               "gemm_swiglu_dream7b_hbm_traffic.md")),
-                     "bytes_per_launch": gu_bytes, "avg_launch_ms": round(gu_ms, 4)},
+                     "bytes_per_launch": gu_bytes, "avg_launch_ms": round(gu_ms, 4),
+                     "copy_gbs_measured": round(copy_gbs, 1),
+                     "frac_of_measured_copy": round(achieved / copy_gbs, 4)},
         "step_roofline": {"hbm_bytes": sb, "flops": sf,
                           "hbm_frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "mfma_frac": round(sf / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)},
