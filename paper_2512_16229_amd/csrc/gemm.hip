@@ -157,37 +157,47 @@ __device__ __forceinline__ void resid_epilogue(const GemmArgs& a, f32x4 (&acc)[4
 // down-projection operand. The SwiGLU GEMM accumulates the transposed tile
 // (weights as the MFMA's first operand), so acc[mb][nb][j] holds row
 // row0 + 16 mb + c16, column 16 (tile NB + nb) + 4 g + j: a lane's four
-// outputs of a block are four consecutive columns of one row, stored as one
-// 8-byte write (the packed operand keeps 8 consecutive columns of a row in one
-// 16-byte lane slot).
+// outputs of a block are four consecutive columns of one row. The packed
+// operand keeps 8 consecutive columns of a row in one 16-byte lane slot, so
+// lanes l and l ^ 16 (column groups 4g and 4(g ^ 1) of the same row) trade
+// halves with one permlane swap per dword: afterwards the even lane holds the
+// slot of row block mb, the odd lane the slot of row block mb + 1, and each
+// writes 16 bytes.
 template <int NB>
 __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
                                                 int row0, int lane) {
   constexpr int PAIRS = NB / 2;
   const int g = lane >> 4, c16 = lane & 15;
   const int Nout = a.N >> 1;
+  auto swiglu4 = [&](int mb, int p, uint32_t (&hv)[2]) {
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb) {
-    const int r = row0 + mb * 16 + c16;
+    for (int jj = 0; jj < 2; ++jj) {
+      float h2[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int j = 2 * jj + u;
+        const float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
+        // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
+        // 1 ulp each, far below the bf16 rounding of the result)
+        const float ex = __builtin_amdgcn_exp2f(-gt * 1.4426950408889634f);
+        h2[u] = gt * __builtin_amdgcn_rcpf(1.0f + ex) * up;
+      }
+      hv[jj] = (uint32_t)f2bf_bits(h2[0]) | ((uint32_t)f2bf_bits(h2[1]) << 16);
+    }
+  };
+#pragma unroll
+  for (int mp = 0; mp < 2; ++mp) {
+    const int r = row0 + (2 * mp + (g & 1)) * 16 + c16;
 #pragma unroll
     for (int p = 0; p < PAIRS; ++p) {
-      uint32_t hv[2];
-#pragma unroll
-      for (int jj = 0; jj < 2; ++jj) {
-        float h2[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int j = 2 * jj + u;
-          const float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
-          // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
-          // 1 ulp each, far below the bf16 rounding of the result)
-          const float ex = __builtin_amdgcn_exp2f(-gt * 1.4426950408889634f);
-          h2[u] = gt * __builtin_amdgcn_rcpf(1.0f + ex) * up;
-        }
-        hv[jj] = (uint32_t)f2bf_bits(h2[0]) | ((uint32_t)f2bf_bits(h2[1]) << 16);
-      }
-      const int col = (tile * PAIRS + p) * 16 + g * 4;
-      if (r < a.M && col < Nout) *(uint2*)(a.a_out + packA_off(r, col, a.Mp)) = make_uint2(hv[0], hv[1]);
+      uint32_t h0[2], h1[2];
+      swiglu4(2 * mp, p, h0);
+      swiglu4(2 * mp + 1, p, h1);
+      const auto w0 = __builtin_amdgcn_permlane16_swap(h0[0], h1[0], false, false);
+      const auto w1 = __builtin_amdgcn_permlane16_swap(h0[1], h1[1], false, false);
+      const int col = (tile * PAIRS + p) * 16 + (g >> 1) * 8;
+      if (r < a.M && col < Nout)
+        *(uint4*)(a.a_out + packA_off(r, col, a.Mp)) = make_uint4(w0[0], w1[0], w0[1], w1[1]);
     }
   }
 }
