@@ -263,9 +263,14 @@ def decode(model, prompt, gen_len: int, L: int, k: int, tau: float, max_len=None
 #       forward, as a single block does.
 def decode_window(model: OracleModel, prompt, gen_len: int, L: int, k: int, tau: float,
                   tau_add: float, tau_act: float, w_max: int, metric: int = METRIC_MEAN,
-                  window: int = 4, eta: float = 0.25, trace=None, max_len=None):
+                  window: int = 4, eta: float = 0.25, trace=None, max_len=None,
+                  block_causal: bool = False):
     """Generate gen_len tokens (gen_len / L blocks) with a sliding window of up
-    to w_max active blocks. Returns tokens, iterations, forwards, tpf, cache."""
+    to w_max active blocks. Returns tokens, iterations, forwards, tpf, cache.
+    block_causal: the window's blocks attend block-causally (a block sees the
+    prefix, the earlier window blocks and itself; Sec. 3.4, LoPA-Dist-Ascend)
+    instead of with full attention inside the window."""
+    cblk = L if block_causal else 0
     mask_id = model.cfg["mask_id"]
     prompt = np.asarray(prompt, dtype=np.int64)
     cache = KVCache(model.cfg, max_len or (len(prompt) + gen_len))
@@ -292,7 +297,7 @@ def decode_window(model: OracleModel, prompt, gen_len: int, L: int, k: int, tau:
     while committed < n_blocks:
         if not active:
             append_block()
-            o = model.forward_block(tokens[None], P, cache)
+            o = model.forward_block(tokens[None], P, cache, causal_blk=cblk)
             conf, pred = o["conf"][0].copy(), o["pred"][0].copy()
             covered[:] = [True] * len(covered)
             forwards += 1
@@ -301,7 +306,7 @@ def decode_window(model: OracleModel, prompt, gen_len: int, L: int, k: int, tau:
         n_el = L * next((i for i, a in enumerate(active) if not a), len(active))
         state_in = (tokens.copy(), conf.copy(), pred.copy())
         bt, fill_pos, valid, n_valid = build_branches(tokens, conf, pred, mask_id, tau, k, n_el)
-        o = model.forward_block(bt[:n_valid], P, cache)
+        o = model.forward_block(bt[:n_valid], P, cache, causal_blk=cblk)
         nb, Lw = k + 1, len(tokens)
         conf_b = np.zeros((nb, Lw))
         pred_b = np.zeros((nb, Lw), dtype=np.int64)

@@ -127,12 +127,15 @@ class OracleModel:
         return bf16_round(a) if self.mode == "faithful" else a
 
     # ------------------------------------------------------------------
-    def attention(self, q, k_blk, v_blk, kp, vp):
+    def attention(self, q, k_blk, v_blk, kp, vp, causal_blk: int = 0):
         """Softmax attention of the block rows of each branch.
 
         q: [nb, Hq, L, d]; k_blk, v_blk: [nb, Hkv, L, d] (the branch's own block);
         kp, vp: [Hkv, P, d] (shared committed prefix). Every row sees all P prefix
-        keys and all L keys of its own branch; nothing of other branches.
+        keys and all L keys of its own branch (causal_blk = 0); nothing of other
+        branches. causal_blk = c > 0 (the block-wise causal mask of LoPA-Dist's
+        Ascend system, Sec. 3.4): the L rows are consecutive sub-blocks of c, and
+        a row of sub-block b sees the prefix and the keys of sub-blocks <= b only.
         Returns o: [nb, Hq, L, d]."""
         cfg = self.cfg
         nb, Hq, L, d = q.shape
@@ -143,6 +146,9 @@ class OracleModel:
             g = h // group
             s_pre = np.einsum("bld,pd->blp", q[:, h], kp[g]) * scale           # [nb, L, P]
             s_blk = np.einsum("bld,bmd->blm", q[:, h], k_blk[:, g]) * scale    # [nb, L, L]
+            if causal_blk:
+                sub = np.arange(L) // causal_blk
+                s_blk = np.where(sub[None, :, None] >= sub[None, None, :], s_blk, -np.inf)
             s = np.concatenate([s_pre, s_blk], axis=-1)
             e = np.exp(s - s.max(axis=-1, keepdims=True))
             den = e.sum(axis=-1, keepdims=True)
@@ -154,14 +160,15 @@ class OracleModel:
         return out
 
     def forward_block(self, tokens, prefix_len: int, cache: KVCache, keep_hidden: bool = False,
-                      n_layers=None):
+                      n_layers=None, causal_blk: int = 0):
         """One batched forward of nb branches of the active block.
 
         tokens: int [nb, L] (block rows at positions prefix_len .. prefix_len+L-1).
         Returns dict: conf [nb, L] (float64), pred [nb, L] (int64), k / v
         [nb, layers, Hkv, L, d] (post-RoPE block keys / values), and, if asked,
         'hidden' [nb, L, H] (final-normed rows) and 'logits'. With n_layers set,
-        returns only {'x': residual stream after that many layers}."""
+        returns only {'x': residual stream after that many layers}. causal_blk:
+        the attention mask inside the block (see attention)."""
         cfg = self.cfg
         tokens = np.asarray(tokens, dtype=np.int64)
         nb, L = tokens.shape
@@ -187,7 +194,7 @@ class OracleModel:
             k = self._store(apply_rope(k, ang))
             v = self._store(v)
             ks[:, li], vs[:, li] = k, v
-            o = self.attention(q, k, v, cache.k[li, :, :P], cache.v[li, :, :P])
+            o = self.attention(q, k, v, cache.k[li, :, :P], cache.v[li, :, :P], causal_blk)
             o = self._store(o.transpose(0, 2, 1, 3).reshape(nb, L, Hq * d))
             x = x + o @ w["wo"].T
             h2 = self._store(rms_norm(x, w["ln2"], cfg["rms_eps"]))

@@ -219,3 +219,52 @@ def test_window_invariants(w_max, tau_add, tau_act):
             assert np.array_equal(res["cache"].k[:, :, P:P + c * L], it["k"][w][:, :, :c * L])
         P += c * L
     assert P == 32 + gen
+
+
+# ----------------------------- block-causal window (Sec. 3.4, LoPA-Dist-Ascend)
+def test_block_causal_rows_match_block_forwards(tiny):
+    """With the block-wise causal mask, the rows of window sub-block 0 are the
+    forward of sub-block 0 alone, and the rows of sub-block 1 are the forward of
+    sub-block 1 alone after sub-block 0's K/V were written to the cache at its
+    positions (the pre-written K/V are final: no later block changes them).
+    With a sub-block as long as the window the mask is no mask at all."""
+    cfg, m, cache, P = tiny
+    mask, L = cfg["mask_id"], 8
+    rng = np.random.default_rng(11)
+    bt = np.where(rng.random((3, 2 * L)) < 0.5, mask, rng.integers(0, cfg["vocab"] - 1, (3, 2 * L)))
+    full = m.forward_block(bt, P, cache, causal_blk=L)
+    first = m.forward_block(bt[:, :L], P, cache)
+    np.testing.assert_allclose(full["conf"][:, :L], first["conf"], rtol=0, atol=1e-12)
+    assert np.array_equal(full["pred"][:, :L], first["pred"])
+    np.testing.assert_allclose(full["k"][..., :L, :], first["k"], rtol=0, atol=1e-10)
+    np.testing.assert_allclose(full["v"][..., :L, :], first["v"], rtol=0, atol=1e-10)
+    for j in range(3):
+        c = cache.copy()
+        c.commit(P, first["k"][j], first["v"][j])
+        second = m.forward_block(bt[j:j + 1, L:], P + L, c)
+        np.testing.assert_allclose(full["conf"][j, L:], second["conf"][0], rtol=0, atol=1e-12)
+        assert np.array_equal(full["pred"][j, L:], second["pred"][0])
+        np.testing.assert_allclose(full["k"][j][..., L:, :], second["k"][0], rtol=0, atol=1e-10)
+    nomask = m.forward_block(bt, P, cache)
+    same = m.forward_block(bt, P, cache, causal_blk=2 * L)
+    assert np.array_equal(nomask["conf"], same["conf"]) and np.array_equal(nomask["k"], same["k"])
+    # and the mask does change rows of sub-block 0 when later rows may be seen
+    assert np.max(np.abs(nomask["conf"][:, :L] - full["conf"][:, :L])) > 0
+
+
+@pytest.mark.parametrize("w_max,tau_add,tau_act", [(2, 0.1, 0.5), (3, 0.0, 0.3)])
+def test_block_causal_window_cache_is_prefill_of_output(w_max, tau_add, tau_act):
+    """Single-phase consistency: with block-causal attention in the window, the
+    K/V a block leaves in the cache depend only on the prefix and the block's
+    own final tokens, so the cache after the decode equals a block-causal
+    prefill of prompt + generated tokens (prompt a whole number of blocks)."""
+    cfg = synth.config("tiny")
+    m = OracleModel(cfg, synth.model_weights(cfg), "faithful")
+    mask, L, gen = cfg["mask_id"], 16, 64
+    prompt = synth.prompt(cfg, 32).numpy()
+    res = lopa.decode_window(m, prompt, gen, L, 3, 0.9, tau_add, tau_act, w_max, block_causal=True)
+    assert len(res["tokens"]) == gen and not np.any(res["tokens"] == mask)
+    ref = KVCache(cfg, 32 + gen)
+    lopa.prefill(m, ref, np.concatenate([prompt, res["tokens"]]), L)
+    np.testing.assert_allclose(res["cache"].k, ref.k, rtol=0, atol=1e-9)
+    np.testing.assert_allclose(res["cache"].v, ref.v, rtol=0, atol=1e-9)
