@@ -265,13 +265,15 @@ def e2e_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7, tau=0.
 
 
 def e2e_window_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7, tau=0.9,
-                      tau_add=0.1, tau_act=0.95, w_max=2):
+                      tau_add=0.1, tau_act=0.95, w_max=2, block_causal=False):
     """End-to-end decode with the multi-block window (Sec. 3.3, integration with
     D2F): up to w_max active blocks explored as one window, the D2F gates at the
-    appendix's GSM8K setting (tau_add 0.1, tau_act 0.95, tau_conf 0.9)."""
+    appendix's GSM8K setting (tau_add 0.1, tau_act 0.95, tau_conf 0.9);
+    block_causal: the Ascend system's block-wise causal mask inside the window
+    (Sec. 3.4) instead of full attention."""
     import torch
     kv = lp.KV(model, prompt_len + gen, k + 1, L * w_max)
-    dec = lp.WindowDecoder(model, kv, L, k, tau, tau_add, tau_act, w_max)
+    dec = lp.WindowDecoder(model, kv, L, k, tau, tau_add, tau_act, w_max, block_causal=block_causal)
     prompt = synth.prompt(cfg, prompt_len, device="cuda")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -280,7 +282,8 @@ def e2e_window_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7,
     t = time.perf_counter() - t0
     return {"workload": (f"{cfg['name']} shape, {prompt_len}-token uniform-random prompt (prefill "
                          f"included), {gen} generated tokens, window of up to {w_max} blocks of {L}, "
-                         f"k={k}, tau {tau}, tau_add {tau_add}, tau_act {tau_act}"),
+                         f"k={k}, tau {tau}, tau_add {tau_add}, tau_act {tau_act}"
+                         + (", block-causal attention inside the window" if block_causal else "")),
             "tokens_per_s": round(gen / t, 1), "tokens_per_forward": round(out["tpf"], 3),
             "forwards": out["forwards"], "iterations": out["iterations"], "seconds": round(t, 4)}
 
@@ -464,6 +467,12 @@ def main():
             log(f"end-to-end window decode in {time.perf_counter() - t0:.1f}s: "
                 f"{result['e2e_window_decode']['tokens_per_s']} tok/s, "
                 f"TPF {result['e2e_window_decode']['tokens_per_forward']}")
+            t0 = time.perf_counter()
+            result["e2e_window_decode_block_causal"] = e2e_window_decode(
+                lp, synth, model, cfg, L=L, k=k, tau=tau, block_causal=True)
+            log(f"end-to-end block-causal window decode in {time.perf_counter() - t0:.1f}s: "
+                f"{result['e2e_window_decode_block_causal']['tokens_per_s']} tok/s, "
+                f"TPF {result['e2e_window_decode_block_causal']['tokens_per_forward']}")
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         try:

@@ -269,6 +269,19 @@ int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer,
  * lopa_kv_attention_plan reports the (n_ranges, range_len) a verify forward of
  * this shape would use; host only, nothing is launched. */
 int lopa_kv_set_attention_ranges(lopa_kv* kv, int32_t n_ranges);
+
+/* Attention mask inside the active block (window) of later verify forwards.
+ * sub_block = 0 (the default): full attention among the block's L rows
+ * (Sec. 3.3). sub_block = c > 0, a multiple of 16: the block-wise causal mask
+ * of the paper's Ascend system (Sec. 3.4): the L rows are consecutive
+ * sub-blocks of c rows (the window's blocks) and a row of sub-block b attends
+ * to the committed prefix and to the rows of sub-blocks 0..b of its own
+ * branch. A block's K/V then never depend on later blocks, so the K/V a
+ * completed leading block leaves in the cache (lopa_commit_kv_rows) are final
+ * without a separate winner commit protocol. A verify forward with L > c needs
+ * L % c == 0 (LOPA_ESHAPE otherwise); L <= c is unmasked. sub_block negative or
+ * not a multiple of 16: LOPA_EINVAL. Host only; applies to later calls. */
+int lopa_kv_set_block_causal(lopa_kv* kv, int32_t sub_block);
 int lopa_kv_attention_plan(const lopa_kv* kv, int32_t prefix_len, int32_t n_branches, int32_t L,
                            int32_t* n_ranges, int32_t* range_len);
 

@@ -116,6 +116,11 @@ class KV:
         n >= 1: shared prefix cut into about n key ranges."""
         _check(lib.lopa_kv_set_attention_ranges(self.handle, n_ranges))
 
+    def set_block_causal(self, sub_block: int):
+        """0: full attention inside the block; c > 0 (multiple of 16): rows of
+        sub-block b see the prefix and sub-blocks 0..b of their branch."""
+        _check(lib.lopa_kv_set_block_causal(self.handle, sub_block))
+
     def attention_plan(self, prefix_len: int, n_branches: int, L: int):
         """(n_ranges, range_len) of a verify forward of this shape; (0, 0) is
         the per-(head, branch) path."""

@@ -44,6 +44,7 @@ EXPORTS = ["lopa_model_create", "lopa_model_destroy", "lopa_kv_create", "lopa_kv
            "lopa_branch_confidence_select", "lopa_branch_confidence_select_metric", "lopa_commit_kv",
            "lopa_commit_kv_rows", "lopa_kv_read", "lopa_kv_write",
            "lopa_kv_read_staging", "lopa_debug_hidden", "lopa_kv_set_attention_ranges",
+           "lopa_kv_set_block_causal",
            "lopa_kv_attention_plan", "lopa_kv_profile",
            "lopa_kv_profile_read"]
 METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
@@ -76,6 +77,7 @@ def _load():
         "lopa_kv_read_staging": (C.c_int, [P, I32, I32, P, P, P]),
         "lopa_debug_hidden": (C.c_int, [P, P, I32, P, I32, I32, I32, P, P]),
         "lopa_kv_set_attention_ranges": (C.c_int, [P, I32]),
+        "lopa_kv_set_block_causal": (C.c_int, [P, I32]),
         "lopa_kv_attention_plan": (C.c_int, [P, I32, I32, I32, C.POINTER(C.c_int32),
                                              C.POINTER(C.c_int32)]),
         "lopa_kv_profile": (C.c_int, [P, I32]),

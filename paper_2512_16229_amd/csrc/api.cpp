@@ -191,6 +191,7 @@ struct lopa_kv {
   float* attn_part = nullptr;   // shared-prefix attention partial states
   size_t attn_part_bytes = 0;
   int attn_ranges = -1;         // lopa_kv_set_attention_ranges: -1 automatic
+  int causal_blk = 0;           // lopa_kv_set_block_causal: 0 full attention in the block
   float* pm = nullptr;
   float* ps = nullptr;
   int32_t* pi = nullptr;
@@ -576,6 +577,8 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     at.KS = ap.KS;
     at.part = kv->attn_part;
   }
+  // a block of one sub-block (or less) needs no mask
+  at.cblk = kv->causal_blk && L > kv->causal_blk ? kv->causal_blk : 0;
   const int n_layers = stop_layer >= 0 ? std::min(stop_layer, c.layers) : c.layers;
   for (int l = 0; l < n_layers; ++l) {
     const LayerPack& p = m->layers[l];
@@ -644,6 +647,9 @@ static int check_verify(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   if (prefix_len < 0) return fail(LOPA_EINVAL, "prefix_len < 0");
   if ((int64_t)prefix_len + L > kv->max_len)
     return fail(LOPA_ECAPACITY, "prefix_len %d + L %d > max_len %d", prefix_len, L, kv->max_len);
+  if (kv->causal_blk && L > kv->causal_blk && L % kv->causal_blk)
+    return fail(LOPA_ESHAPE, "L %d is not a multiple of the block-causal sub-block %d", L,
+                kv->causal_blk);
   return LOPA_OK;
 }
 
@@ -775,6 +781,14 @@ int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer, void*
   uint16_t* sv = kv->staging + (((size_t)branch * c.layers + layer) * 2 + 1) * Hkv * head;
   HIP_TRY(launch_kv_rows(sk, sv, (int64_t)head, kv->vlds, Hkv, d, 0, L, (uint16_t*)k_dst,
                          (uint16_t*)v_dst, 0, (hipStream_t)stream));
+  return LOPA_OK;
+}
+
+int lopa_kv_set_block_causal(lopa_kv* kv, int32_t sub_block) {
+  if (!kv) return fail(LOPA_EINVAL, "null pointer argument");
+  if (sub_block < 0 || sub_block % 16)
+    return fail(LOPA_EINVAL, "sub_block %d is not 0 or a positive multiple of 16", sub_block);
+  kv->causal_blk = sub_block;
   return LOPA_OK;
 }
 

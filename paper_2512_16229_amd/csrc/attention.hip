@@ -193,7 +193,7 @@ template <int D, int NR, bool ALWAYS_FULL>
 __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR][D / 32],
                                             float (&m)[NR], float (&l)[NR],
                                             f32x4 (&o)[D / 16][NR], int p0, int lim, float sl2,
-                                            int g) {
+                                            int g, int cblk = 0, int row0 = 0) {
   constexpr int NDB = D / 16, NKK = D / 32;
   const bool full = ALWAYS_FULL || p0 + KT <= lim;  // wave-uniform
   if (!full) {
@@ -213,6 +213,13 @@ __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR
   }
 #pragma unroll
   for (int qb = 0; qb < NR; ++qb) {
+    // block-causal mask (cblk > 0, a multiple of 16): rows row0 + 16 qb .. lie
+    // in one sub-block and see the keys of the sub-blocks up to their own
+    int lq = lim;
+    if (cblk) {
+      lq = min(lim, ((row0 + qb * 16) / cblk + 1) * cblk);
+      if (p0 >= lq) continue;  // no key of this tile is visible to these rows
+    }
     f32x4 s[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -221,13 +228,13 @@ __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR
       for (int kk = 0; kk < NKK; ++kk) s[kb] = mfma16(x.k[kb][kk], qf[qb][kk], s[kb]);
     }
     // s[kb][j]: key p0 + 16 kb + 4 g + j, query 16 qb + c16
-    if (!full) {
+    if (!full || p0 + KT > lq) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int pos = p0 + kb * 16 + g * 4 + j;
-          s[kb][j] = pos < lim ? s[kb][j] : -INFINITY;
+          s[kb][j] = pos < lq ? s[kb][j] : -INFINITY;
         }
     }
     float tmax = max2(max3(s[0][0], s[0][1], s[0][2]),
@@ -369,7 +376,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     tile_fetch<D>(smem + (wv * 2 + (i & 1)) * TileLds<D>::TILE, lane, x);
     const int t = t_lo + i;
     const bool pre = t < pt;
-    tile_update<D, QB, false>(x, qf, m, l, o, (pre ? t : t - pt) * KT, pre ? P : L, sl2, g);
+    tile_update<D, QB, false>(x, qf, m, l, o, (pre ? t : t - pt) * KT, pre ? P : L, sl2, g,
+                              pre ? 0 : a.cblk, 0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     issue(t_lo + (i + 2 < n ? i + 2 : n - 1), i & 1);
   }
@@ -598,7 +606,7 @@ __global__ __launch_bounds__(64 * QB) void attn_block_kernel(AttnArgs a) {
   for (int t = 0; t < bt; ++t) {
     AttnTile<D> x;
     tile_fetch<D>(smem + t * TileLds<D>::TILE, lane, x);
-    tile_update<D, 1, false>(x, qf, m, l, o, t * KT, L, sl2, g);
+    tile_update<D, 1, false>(x, qf, m, l, o, t * KT, L, sl2, g, a.cblk, wv * 16);
   }
   l[0] = pair32_sum(pair16_sum(l[0]));
   f32x4 ob[NDB];
@@ -658,6 +666,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.L < 1 || a.L > 64 || a.P < 0 || a.Hq % a.Hkv || a.vld % 8 || a.vlds % 8 ||
       a.L > a.vlds || a.P > a.vld)
     return hipErrorInvalidValue;
+  if (a.cblk < 0 || (a.cblk > 0 && (a.cblk % 16 || a.L % a.cblk))) return hipErrorInvalidValue;
   // shared prefix: every key range non-empty, the ranges cover [0, P), and the
   // workspace was given
   if (a.S < 0 || (a.S > 0 && (!a.part || a.KS < KT || a.KS % KT || a.P < 1 ||

@@ -108,6 +108,10 @@ struct AttnArgs {
   // [S][nb*L][Hq][2]. S = 0: the prefix runs inside the per-branch kernel.
   int S, KS;
   float* part;
+  // block-causal mask inside the block (cblk > 0, a multiple of 16 dividing L):
+  // a row of sub-block r / cblk sees the prefix and the block keys of the
+  // sub-blocks up to its own. 0: full attention inside the block.
+  int cblk;
 };
 // query rows (of all branches) per workgroup of the shared-prefix pass (32
 // per wavefront, two wavefronts per SIMD) and its LDS ring depth in key

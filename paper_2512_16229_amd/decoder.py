@@ -141,8 +141,11 @@ class WindowDecoder:
 
     def __init__(self, model: Model, kv: KV, L: int, k: int, tau: float, tau_add: float,
                  tau_act: float, w_max: int, metric: int = METRIC_MEAN, window: int = 4,
-                 eta: float = 0.25):
+                 eta: float = 0.25, block_causal: bool = False):
         self.model, self.kv, self.L, self.k = model, kv, L, k
+        # block_causal: the window's blocks attend block-causally (Sec. 3.4,
+        # the Ascend system's mask) instead of with full attention
+        self.block_causal = bool(block_causal)
         self.tau, self.tau_add, self.tau_act, self.w_max = float(tau), float(tau_add), float(tau_act), w_max
         self.metric, self.window, self.eta = int(metric), int(window), float(eta)
         self.mask_id = model.cfg["mask_id"]
@@ -169,6 +172,7 @@ class WindowDecoder:
 
     def decode(self, prompt: torch.Tensor, gen_len: int, trace=None) -> dict:
         L, k, nb, mask = self.L, self.k, self.k + 1, self.mask_id
+        self.kv.set_block_causal(L if self.block_causal else 0)
         P = Decoder(self.model, self.kv, L, 0, self.tau).prefill(prompt)
         n_blocks = gen_len // L
         active, covered, out = [], [], []

@@ -170,13 +170,28 @@ def test_window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, g
     committed cache rows): lopa_build_branches_window bit-exact, the verify
     forward over the whole window within the faithful tolerance, the selection,
     and lopa_commit_kv_rows of the blocks that leave the window."""
-    log(f"window teacher-forced {cfgname} P={P} L={L} k={k} w_max={w_max} tau_add={tau_add} tau_act={tau_act}")
+    _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, False)
+
+
+@pytest.mark.parametrize("cfgname,P,L,k,tau,tau_add,tau_act,w_max,gen", WINDOW_CASES)
+def test_window_teacher_forced_block_causal(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen):
+    """The same replay with the block-wise causal mask inside the window (the
+    Ascend system's protocol, Sec. 3.4)."""
+    _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, True)
+
+
+def _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, block_causal):
+    log(f"window teacher-forced {cfgname} P={P} L={L} k={k} w_max={w_max} tau_add={tau_add} "
+        f"tau_act={tau_act} block_causal={block_causal}")
     s = Setup(cfgname, 0, L * w_max, k, max_len=P + gen)
     lp, mask, nb = s.lp, s.cfg["mask_id"], k + 1
+    cblk = L if block_causal else 0
+    s.kv.set_block_causal(cblk)
     tau32 = f32(tau)
     prompt = synth.prompt(s.cfg, P).numpy()
     otrace = []
-    res = lopa.decode_window(s.faith, prompt, gen, L, k, tau32, tau_add, tau_act, w_max, trace=otrace)
+    res = lopa.decode_window(s.faith, prompt, gen, L, k, tau32, tau_add, tau_act, w_max, trace=otrace,
+                             block_causal=block_causal)
     assert len(res["tokens"]) == gen and not np.any(res["tokens"] == mask)
     cache = res["cache"]
     checked = windows = 0
@@ -205,7 +220,8 @@ def test_window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, g
         gp = pred_b.view(nb, Lw).cpu().numpy()[:n_valid]
         eps = np.max(np.abs(gc - it["conf"][:n_valid]))
         # the case's own bf16 sensitivity: the pure oracle on the same inputs
-        e_bf16 = np.max(np.abs(it["conf"][:n_valid] - s.pure.forward_block(obt[:n_valid], P_t, cache)["conf"]))
+        e_bf16 = np.max(np.abs(it["conf"][:n_valid] - s.pure.forward_block(obt[:n_valid], P_t, cache,
+                                                                            causal_blk=cblk)["conf"]))
         assert eps < faithful_bound(e_bf16)
         scores = torch.empty(nb, dtype=F32, device="cuda")
         win = torch.empty(1, dtype=I32, device="cuda")
@@ -232,15 +248,17 @@ def test_window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, g
     assert checked >= 1 and windows >= 1
 
 
+@pytest.mark.parametrize("block_causal", [False, True])
 @pytest.mark.parametrize("cfgname,P,L,k,tau,tau_add,tau_act,w_max,gen", WINDOW_CASES[:2])
-def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen):
+def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, block_causal):
     """The GPU WindowDecoder end to end: a filled, committed sequence, and the
     oracle's trajectory until a decision the oracle calls a near-tie."""
-    log(f"window free-running {cfgname} P={P} L={L} k={k} w_max={w_max}")
+    log(f"window free-running {cfgname} P={P} L={L} k={k} w_max={w_max} block_causal={block_causal}")
     s = Setup(cfgname, 0, L * w_max, k, max_len=P + gen)
     mask = s.cfg["mask_id"]
     prompt = synth.prompt(s.cfg, P)
-    dec = s.lp.WindowDecoder(s.model, s.kv, L, k, tau, tau_add, tau_act, w_max)
+    dec = s.lp.WindowDecoder(s.model, s.kv, L, k, tau, tau_add, tau_act, w_max,
+                             block_causal=block_causal)
     gtrace = []
     out = dec.decode(prompt, gen, gtrace)
     g_tokens = out["tokens"].numpy()
@@ -248,7 +266,7 @@ def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_
     assert out["forwards"] >= out["iterations"] >= gen // (L * w_max)
     otrace = []
     res = lopa.decode_window(s.faith, prompt.numpy(), gen, L, k, f32(tau), tau_add, tau_act, w_max,
-                             trace=otrace)
+                             trace=otrace, block_causal=block_causal)
     for t, (g, o) in enumerate(zip(gtrace, otrace)):
         ow = o["branch_tokens"][o["winner"]]
         if not np.array_equal(g["tokens"].numpy(), ow):

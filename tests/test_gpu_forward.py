@@ -180,3 +180,43 @@ def test_batch_invariance_and_determinism(cfgname, P, L, k):
     one = np.stack([bt[2]] + [bt[2]] * (nb - 1))
     co, po = s.gpu_forward(one)
     assert np.array_equal(co[0], c1[2]) and np.array_equal(po[0], p1[2])
+
+
+# (config, P, L, k, sub-block, attention ranges): the block-causal mask inside
+# the block (Sec. 3.4, the Ascend system's mask) on both attention paths; 16-row
+# sub-blocks make a 32-key tile partly visible to a row block
+CAUSAL = [("small", 100, 64, 3, 32, 0), ("small", 300, 64, 3, 32, 2), ("tiny", 40, 48, 2, 16, 0),
+          ("tiny", 272, 48, 5, 16, -1), ("small128", 64, 64, 1, 16, 1)]
+
+
+@pytest.mark.parametrize("cfgname,P,L,k,cblk,ranges", CAUSAL)
+def test_block_causal_forward(cfgname, P, L, k, cblk, ranges):
+    log(f"block-causal forward {cfgname} P={P} L={L} k={k} sub-block {cblk} ranges {ranges}")
+    s = Setup(cfgname, P, L, k)
+    s.gpu_prefill()
+    s.load_oracle_cache()
+    nb, mask = k + 1, s.cfg["mask_id"]
+    s.kv.set_attention_ranges(ranges)
+    s.kv.set_block_causal(cblk)
+    rng = np.random.default_rng(P + L + cblk)
+    bt = np.where(rng.random((nb, L)) < 0.6, mask, rng.integers(0, s.cfg["vocab"] - 1, (nb, L)))
+    conf, pred = s.gpu_forward(bt)
+    rf = s.faith.forward_block(bt, P, s.cache_f, keep_hidden=True, causal_blk=cblk)
+    rp = s.pure.forward_block(bt, P, s.cache_p, causal_blk=cblk)
+    e_bf16 = np.max(np.abs(rf["conf"] - rp["conf"]))
+    e_faith = np.max(np.abs(conf - rf["conf"]))
+    decided = vocab_margin(rf["logits"], mask) >= near_tie(e_faith)
+    log(f"  max|dconf| gpu-faithful={e_faith:.2e} faithful-pure={e_bf16:.2e} decided {decided.mean():.2f}")
+    assert e_faith < faithful_bound(e_bf16)
+    assert decided.mean() > 0.6
+    assert np.array_equal(pred[decided], rf["pred"][decided])
+    # the mask matters: the unmasked oracle differs by more than the tolerance
+    # somewhere in the first sub-block
+    full = s.faith.forward_block(bt, P, s.cache_f)
+    assert np.max(np.abs(full["conf"][:, :cblk] - rf["conf"][:, :cblk])) > 0
+    # staged K / V of the last sub-block, and a block of one sub-block is unmasked
+    for layer in range(s.cfg["layers"]):
+        ks, vs = s.kv.read_staging(nb - 1, layer, L)
+        _kv_close(ks, rf["k"][nb - 1, layer], f"staging K l{layer}")
+        _kv_close(vs, rf["v"][nb - 1, layer], f"staging V l{layer}")
+    s.kv.set_block_causal(0)
