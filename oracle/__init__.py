@@ -11,10 +11,13 @@ Plain, slow, obviously correct numpy, float64 throughout:
   * lopa.py   - Eq. 1 threshold fill, anchor + lookahead branches (Alg. 1 steps
                 1-2), Eq. 2 branch confidence and selection (Alg. 1 step 3),
                 logit reuse (Sec. 3.2) and the decode loop.
+  * fp8.py    - E4M3 rounding and per-row / per-channel scaling for the FP8 MLP
+                mode of the forward.
 
-Two precision modes of the forward (see model.py): "pure" (float64 from the
-given weights) and "faithful" (float64 arithmetic with bf16 round-to-nearest-even
-at the points where a bf16 implementation stores values). Integer decisions are
+Precision modes of the forward (see model.py): "pure" (float64 from the
+given weights), "faithful" (float64 arithmetic with bf16 round-to-nearest-even
+at the points where a bf16 implementation stores values) and "fp8" (faithful
+with the MLP projections in W8A8 E4M3). Integer decisions are
 compared against "faithful", confidences against "pure".
 
 Parity status per function: every function here is pinned by tests under
@@ -24,3 +27,4 @@ which need trained weights and datasets that are not available.
 """
 from .model import OracleModel, KVCache, bf16_round  # noqa: F401
 from . import lopa  # noqa: F401
+from . import fp8  # noqa: F401

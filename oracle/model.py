@@ -32,10 +32,16 @@ Precision modes:
     v after bias/RoPE, and the softmax numerators exp(s - rowmax) that multiply
     V (the row max is the global max over the row's keys; the denominator is
     the sum of the unrounded numerators).
+  * "fp8": "faithful", except that the MLP projections run in FP8 (W8A8,
+    oracle/fp8.py): gate / up / down weights quantised per output channel, the
+    normed input of gate/up quantised per row from its unrounded value, the
+    SwiGLU output (stored bf16) quantised per row before the down projection.
 """
 from __future__ import annotations
 
 import numpy as np
+
+from .fp8 import fp8_matmul, quantize_rows
 
 
 def bf16_round(x) -> np.ndarray:
@@ -111,10 +117,10 @@ class KVCache:
 
 class OracleModel:
     def __init__(self, cfg: dict, weights: dict, mode: str = "pure"):
-        if mode not in ("pure", "faithful"):
+        if mode not in ("pure", "faithful", "fp8"):
             raise ValueError(mode)
         self.cfg, self.mode = cfg, mode
-        r = bf16_round if mode == "faithful" else (lambda a: a)
+        r = bf16_round if mode in ("faithful", "fp8") else (lambda a: a)
         self.embed = r(_np(weights["embed"]))
         self.lm_head = r(_np(weights["lm_head"]))
         self.final_norm = _np(weights["final_norm"])
@@ -122,9 +128,13 @@ class OracleModel:
         for lw in weights["layers"]:
             self.layers.append({k: (r(_np(v)) if k not in ("ln1", "ln2") else _np(v))
                                 for k, v in lw.items()})
+        if mode == "fp8":
+            for w in self.layers:
+                for key in ("w_gate", "w_up", "w_down"):
+                    w[key + "_q"], w[key + "_s"] = quantize_rows(w[key])
 
     def _store(self, a: np.ndarray) -> np.ndarray:
-        return bf16_round(a) if self.mode == "faithful" else a
+        return bf16_round(a) if self.mode in ("faithful", "fp8") else a
 
     # ------------------------------------------------------------------
     def attention(self, q, k_blk, v_blk, kp, vp, causal_blk: int = 0):
@@ -197,9 +207,15 @@ class OracleModel:
             o = self.attention(q, k, v, cache.k[li, :, :P], cache.v[li, :, :P], causal_blk)
             o = self._store(o.transpose(0, 2, 1, 3).reshape(nb, L, Hq * d))
             x = x + o @ w["wo"].T
-            h2 = self._store(rms_norm(x, w["ln2"], cfg["rms_eps"]))
-            a = self._store(silu(h2 @ w["w_gate"].T) * (h2 @ w["w_up"].T))
-            x = x + a @ w["w_down"].T
+            if self.mode == "fp8":
+                h2 = rms_norm(x, w["ln2"], cfg["rms_eps"])
+                a = self._store(silu(fp8_matmul(h2, w["w_gate_q"], w["w_gate_s"]))
+                                * fp8_matmul(h2, w["w_up_q"], w["w_up_s"]))
+                x = x + fp8_matmul(a, w["w_down_q"], w["w_down_s"])
+            else:
+                h2 = self._store(rms_norm(x, w["ln2"], cfg["rms_eps"]))
+                a = self._store(silu(h2 @ w["w_gate"].T) * (h2 @ w["w_up"].T))
+                x = x + a @ w["w_down"].T
         if n_layers is not None:
             return {"x": x}
         hf = self._store(rms_norm(x, self.final_norm, cfg["rms_eps"]))
