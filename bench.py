@@ -288,6 +288,58 @@ def e2e_window_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7,
             "forwards": out["forwards"], "iterations": out["iterations"], "seconds": round(t, 4)}
 
 
+def fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, steps, warmup):
+    """The same verify step (the block's first iteration, replayed) with the MLP
+    projections in W8A8 E4M3: a second model from the same weights; ms/step,
+    branch-tokens/s and per-kind times."""
+    import torch
+    nb, dev = k + 1, "cuda"
+    model = lp.Model(cfg, w, precision="fp8_mlp")
+    kv = lp.KV(model, P + L, nb, L)
+    dec = lp.Decoder(model, kv, L, k, tau)
+    assert dec.prefill(synth.prompt(cfg, P, device=dev)) == P
+    dec.init_block(P)
+    i32 = dict(dtype=torch.int32, device=dev)
+    tokens, conf, pred = dec.tokens.clone(), dec.conf.clone(), dec.pred.clone()
+    bt, fp = torch.empty(nb * L, **i32), torch.empty(nb, **i32)
+    va, nv = torch.empty(nb, dtype=torch.uint8, device=dev), torch.empty(1, **i32)
+    cb, pb = torch.empty(nb * L, dtype=torch.float32, device=dev), torch.empty(nb * L, **i32)
+    sc, win = torch.empty(nb, dtype=torch.float32, device=dev), torch.empty(1, **i32)
+    nt, nc = torch.empty(L, **i32), torch.empty(L, dtype=torch.float32, device=dev)
+    npd, nu, off = torch.empty(L, **i32), torch.empty(1, **i32), torch.empty(1, **i32)
+    mask = cfg["mask_id"]
+
+    def step():
+        lp.lopa_build_branches(tokens, conf, pred, L, mask, tau, k, bt, fp, va, nv)
+        lp.lopa_verify_forward(model, kv, P, bt, nb, L, cb, pb)
+        lp.lopa_branch_confidence_select(bt, cb, pb, va, nb, L, mask, sc, win, nt, nc, npd, nu)
+        lp.lopa_commit_kv(kv, win, P, L, off)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    kv.profile(lp.PROF_KINDS)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    prof = kv.profile_read()
+    kv.profile(())
+    out = {"workload": "the headline step with gate / up / down in W8A8 E4M3 (per-channel weight "
+                       "and per-row activation scales); attention, QKV / O and the LM head bf16",
+           "ms_per_step": round(ms, 4), "branch_tokens_per_s": round(nb * L / (ms * 1e-3), 1),
+           "kernel_ms_per_step": {kd: round(t / steps, 4) for kd, (t, n) in prof.items()}}
+    del dec, kv, model
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -301,6 +353,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=4)
     ap.add_argument("--no-e2e", action="store_true", help="skip the end-to-end decode run")
+    ap.add_argument("--precision", default="bf16", choices=["bf16", "fp8_mlp"],
+                    help="projection precision of the timed model (the headline is bf16; "
+                         "fp8_mlp: gate / up / down in W8A8 E4M3)")
+    ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 MLP step figures")
     ap.add_argument("--attn-ranges", type=int, default=-1,
                     help="attention path of the timed steps: -1 library choice, 0 per-(head, "
                          "branch), n >= 1 shared prefix in about n key ranges")
@@ -344,8 +400,8 @@ def main():
     torch.cuda.synchronize()
     log(f"weights generated on the GPU in {time.perf_counter() - t0:.1f}s")
     t0 = time.perf_counter()
-    model = lp.Model(cfg, w)
-    log(f"model repacked in {time.perf_counter() - t0:.1f}s")
+    model = lp.Model(cfg, w, precision=args.precision)
+    log(f"model repacked in {time.perf_counter() - t0:.1f}s ({args.precision})")
     kv = lp.KV(model, P + L, nb, L)
     dec = lp.Decoder(model, kv, L, k, tau)
     t0 = time.perf_counter()
@@ -436,7 +492,7 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic",
+        "dtype": "bf16" if args.precision == "bf16" else "bf16 + fp8(e4m3) MLP", "data": "synthetic",
         "config": {"workload": (f"LoPA verify step, {args.config} shape ({cfg['layers']}L H{cfg['hidden']} "
                                 f"{cfg['heads']}q/{cfg['kv_heads']}kv d{cfg['head_dim']} F{cfg['ffn']} "
                                 f"V{cfg['vocab']}), random bf16 weights, prefix {P}, block {L}, "
@@ -473,6 +529,12 @@ def main():
             log(f"end-to-end block-causal window decode in {time.perf_counter() - t0:.1f}s: "
                 f"{result['e2e_window_decode_block_causal']['tokens_per_s']} tok/s, "
                 f"TPF {result['e2e_window_decode_block_causal']['tokens_per_forward']}")
+    if args.precision == "bf16" and not args.no_fp8:
+        t0 = time.perf_counter()
+        result["fp8_mlp_step"] = fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, args.steps,
+                                                  args.warmup)
+        log(f"FP8 MLP step in {time.perf_counter() - t0:.1f}s: "
+            f"{result['fp8_mlp_step']['ms_per_step']} ms/step")
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         try:

@@ -109,6 +109,22 @@ typedef struct lopa_kv lopa_kv;
  * weights on `stream` and wait for that to finish. *out receives the handle. */
 int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w,
                       void* stream, lopa_model** out);
+
+/* Precision of the projections of a model (lopa_model_create_ex).
+ * LOPA_PRECISION_BF16: every weight and GEMM operand bf16 (lopa_model_create).
+ * LOPA_PRECISION_FP8_MLP: the three MLP projections (gate, up, down: three
+ * quarters of a layer's weight bytes at the Dream-7B shape) in W8A8 FP8, the
+ * paper's Ascend system's weight / activation quantisation (Sec. 3.4) carried
+ * to the MI355X matrix cores: E4M3 values (no infinities, largest 448, round
+ * to nearest even, saturating) with one fp32 scale per weight output channel
+ * (max |w| / 448 of the row) and one per activation row (max |a| / 448 of the
+ * row, computed where the row is produced: the RMSNorm for gate/up, a
+ * requantisation of the bf16 SwiGLU output for down); the products are summed
+ * in fp32 and the scales applied after the sum. Attention, QKV / O and the LM
+ * head stay bf16. The caller's weights are still bf16. */
+enum { LOPA_PRECISION_BF16 = 0, LOPA_PRECISION_FP8_MLP = 1 };
+int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* weights,
+                         int32_t precision, void* stream, lopa_model** out);
 void lopa_model_destroy(lopa_model* m);
 
 /* Static KV cache of max_len positions for one sequence (Sec. 3.4: a

@@ -20,7 +20,7 @@ import torch
 
 from ._abi import (EXPORTS, LIB_PATH, LOPA_ECAPACITY, LOPA_EHIP, LOPA_EINVAL, LOPA_ENOMEM,  # noqa: F401
                    LOPA_ESHAPE, LOPA_OK, MAX_BLOCK, MAX_ROWS, METRIC_LOWEST_SEGMENT, METRIC_MEAN,
-                   METRIC_WINDOW_MIN, PROF_KINDS, LopaError, lib,
+                   METRIC_WINDOW_MIN, PRECISIONS, PROF_KINDS, LopaError, lib,
                    lopa_layer_weights, lopa_model_cfg, lopa_weight_ptrs)
 
 
@@ -53,7 +53,11 @@ def _stream(stream):
 class Model:
     """Repacked model weights on the device (lopa_model)."""
 
-    def __init__(self, cfg: dict, weights: dict, stream=None):
+    def __init__(self, cfg: dict, weights: dict, stream=None, precision: str = "bf16"):
+        """precision: "bf16", or "fp8_mlp" (gate / up / down in W8A8 E4M3 with
+        per-channel weight and per-row activation scales)."""
+        if precision not in PRECISIONS:
+            raise ValueError(f"precision {precision!r} not in {sorted(PRECISIONS)}")
         c = lopa_model_cfg(cfg["layers"], cfg["hidden"], cfg["heads"], cfg["kv_heads"],
                            cfg["head_dim"], cfg["ffn"], cfg["vocab"], cfg["mask_id"],
                            cfg["rms_eps"], cfg["rope_theta"], 1 if cfg["qkv_bias"] else 0)
@@ -71,8 +75,9 @@ class Model:
                              _ptr(weights["final_norm"], bf, "final_norm"),
                              _ptr(weights["lm_head"], bf, "lm_head"))
         h = C.c_void_p()
-        _check(lib.lopa_model_create(C.byref(c), C.byref(w), _stream(stream), C.byref(h)))
-        self.handle, self.cfg = h, dict(cfg)
+        _check(lib.lopa_model_create_ex(C.byref(c), C.byref(w), PRECISIONS[precision],
+                                        _stream(stream), C.byref(h)))
+        self.handle, self.cfg, self.precision = h, dict(cfg), precision
 
     def close(self):
         if getattr(self, "handle", None) and lib is not None:

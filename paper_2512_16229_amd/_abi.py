@@ -38,7 +38,7 @@ class lopa_weight_ptrs(C.Structure):
                 ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
 
 
-EXPORTS = ["lopa_model_create", "lopa_model_destroy", "lopa_kv_create", "lopa_kv_destroy",
+EXPORTS = ["lopa_model_create", "lopa_model_create_ex", "lopa_model_destroy", "lopa_kv_create", "lopa_kv_destroy",
            "lopa_strerror", "lopa_last_error", "lopa_build_branches", "lopa_build_branches_window",
            "lopa_verify_forward",
            "lopa_branch_confidence_select", "lopa_branch_confidence_select_metric", "lopa_commit_kv",
@@ -48,6 +48,7 @@ EXPORTS = ["lopa_model_create", "lopa_model_destroy", "lopa_kv_create", "lopa_kv
            "lopa_kv_attention_plan", "lopa_kv_profile",
            "lopa_kv_profile_read"]
 METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
+PRECISIONS = {"bf16": 0, "fp8_mlp": 1}
 PROF_KINDS = ["qkv", "attn", "oproj", "gateup", "down", "lmhead", "norm", "merge"]
 
 
@@ -58,6 +59,8 @@ def _load():
     P, I32, F32 = C.c_void_p, C.c_int32, C.c_float
     sig = {
         "lopa_model_create": (C.c_int, [C.POINTER(lopa_model_cfg), C.POINTER(lopa_weight_ptrs), P,
+                                        C.POINTER(C.c_void_p)]),
+        "lopa_model_create_ex": (C.c_int, [C.POINTER(lopa_model_cfg), C.POINTER(lopa_weight_ptrs), I32, P,
                                         C.POINTER(C.c_void_p)]),
         "lopa_model_destroy": (None, [P]),
         "lopa_kv_create": (C.c_int, [P, I32, I32, I32, C.POINTER(C.c_void_p)]),

@@ -56,8 +56,14 @@ int dalloc(DevBuf& b, size_t bytes, std::vector<void*>& owned) {
 struct LayerPack {
   uint16_t* qkv;   // blk_qkv blocks, K = H
   uint16_t* o;     // blk_h blocks, K = Hq * d
-  uint16_t* gu;    // blk_gu blocks (gate / up pairs), K = H
-  uint16_t* down;  // blk_h blocks, K = round256(F)
+  uint16_t* gu;    // blk_gu blocks (gate / up pairs), K = H (bf16 models)
+  uint16_t* down;  // blk_h blocks, K = round256(F) (bf16 models)
+  // FP8 MLP models: E4M3 weights (K = round512(H), round512(F)) and the scale
+  // of every packed column
+  uint8_t* gu8 = nullptr;
+  uint8_t* down8 = nullptr;
+  float* sw_gu = nullptr;
+  float* sw_down = nullptr;
   float* bias;     // [Nqkv] or null
   float* ln1;
   float* ln2;
@@ -66,6 +72,7 @@ struct LayerPack {
 // rows of the packed activation buffers: whole 256-row tiles
 int padded_rows(int M) { return 256 * ((M + 255) / 256); }
 int round256(int k) { return 256 * ((k + 255) / 256); }
+int round512(int k) { return 512 * ((k + 511) / 512); }
 int round_up(int x, int m) { return m * ((x + m - 1) / m); }
 
 // Decomposition of one GEMM (see gemm.hip): tile width nb (16-column blocks)
@@ -166,6 +173,8 @@ struct lopa_model {
   int blk_qkv = 0, blk_h = 0, blk_gu = 0, blk_lm = 0;  // packed 16-column blocks
   int nb_qkv = 0, nb_o = 0, nb_down = 0, nb_lm = 0;     // tile widths of the packed weights
   int tiles_lm = 0;                                     // LM-head column tiles
+  int fp8 = 0;                                          // LOPA_PRECISION_FP8_MLP
+  int nb_down8 = 0;                                     // FP8 down-projection tile width
   std::vector<LayerPack> layers;
   uint16_t* embed = nullptr;
   uint16_t* lm = nullptr;
@@ -186,6 +195,12 @@ struct lopa_kv {
   float* x = nullptr;           // [mp_max][H]
   uint16_t* abuf = nullptr;     // packed [mp_max][H]
   uint16_t* fbuf = nullptr;     // packed [mp_max][round256(F)], padding columns zero
+  // FP8 MLP models: the FP8 operands of gate/up and down (padding columns zero)
+  // and their per-row scales
+  uint8_t* a8_gu = nullptr;     // packed [mp_max][round512(H)] E4M3
+  uint8_t* a8_dn = nullptr;     // packed [mp_max][round512(F)] E4M3
+  float* sa_gu = nullptr;
+  float* sa_dn = nullptr;
   uint16_t* qbuf = nullptr;     // [max_branches][Hq][max_block][d]
   float* partials = nullptr;
   float* attn_part = nullptr;   // shared-prefix attention partial states
@@ -247,7 +262,8 @@ StepPlans step_plans(const lopa_model* m, int MT) {
   p.qkv = plan_gemm(EPI_QKV, m->blk_qkv, c.hidden / 64, MT, m->num_cu, m->nb_qkv);
   p.o = plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu, m->nb_o);
   p.gu = plan_gemm(EPI_SWIGLU, m->blk_gu, c.hidden / 64, MT, m->num_cu, 10);
-  p.down = plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu, m->nb_down);
+  p.down = m->fp8 ? plan_gemm(EPI_RESID, m->blk_h, round512(c.ffn) / 128, MT, m->num_cu, m->nb_down8)
+                  : plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu, m->nb_down);
   p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, c.hidden / 64, MT, m->num_cu, m->nb_lm);
   return p;
 }
@@ -291,7 +307,14 @@ static int check_cfg(const lopa_model_cfg* c) {
 
 int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void* stream,
                       lopa_model** out) {
+  return lopa_model_create_ex(cfg, w, LOPA_PRECISION_BF16, stream, out);
+}
+
+int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, int32_t precision,
+                         void* stream, lopa_model** out) {
   if (!out) return fail(LOPA_EINVAL, "out is null");
+  if (precision != LOPA_PRECISION_BF16 && precision != LOPA_PRECISION_FP8_MLP)
+    return fail(LOPA_EINVAL, "unknown precision %d", precision);
   *out = nullptr;
   int rc = check_cfg(cfg);
   if (rc) return rc;
@@ -345,6 +368,8 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
   m->nb_qkv = plan_gemm(EPI_QKV, m->blk_qkv, H / 64, 1, m->num_cu, 0).nb;
   m->nb_o = plan_gemm(EPI_RESID, m->blk_h, c.heads * d / 64, 1, m->num_cu, 0).nb;
   m->nb_down = plan_gemm(EPI_RESID, m->blk_h, round256(F) / 64, 1, m->num_cu, 0).nb;
+  m->fp8 = precision == LOPA_PRECISION_FP8_MLP;
+  m->nb_down8 = plan_gemm(EPI_RESID, m->blk_h, round512(F) / 128, 1, m->num_cu, 0).nb;
   auto alloc16 = [&](uint16_t** p, size_t elems) -> int {
     DevBuf b;
     int r = dalloc(b, elems * 2, m->owned);
@@ -358,16 +383,34 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
     return r;
   };
   const int FP = round256(F);  // down projection K, zero-padded
+  const int KPH8 = round512(H), KPF8 = round512(F);  // FP8 MLP K, zero-padded
   // elements of a packed weight: blocks x K x 16
   auto wsize = [](int blocks, int K) { return (size_t)blocks * K * 16; };
+  auto alloc8 = [&](uint8_t** p, size_t bytes) -> int {
+    DevBuf b;
+    int r = dalloc(b, bytes, m->owned);
+    *p = (uint8_t*)b.p;
+    return r;
+  };
+  // FP8: per source row scaling pairs (gate, up: F rows; down: H rows)
+  float *inv_g = nullptr, *sc_g = nullptr, *inv_u = nullptr, *sc_u = nullptr, *inv_d = nullptr,
+        *sc_d = nullptr;
+  if (m->fp8 && ((rc = allocf(&inv_g, F)) || (rc = allocf(&sc_g, F)) || (rc = allocf(&inv_u, F)) ||
+                 (rc = allocf(&sc_u, F)) || (rc = allocf(&inv_d, H)) || (rc = allocf(&sc_d, H))))
+    return bail(rc);
   m->layers.resize(c.layers);
   for (int l = 0; l < c.layers; ++l) {
     const lopa_layer_weights& lw = w->layers[l];
     LayerPack& p = m->layers[l];
+    p.gu = p.down = nullptr;
     if ((rc = alloc16(&p.qkv, wsize(m->blk_qkv, H))) ||
         (rc = alloc16(&p.o, wsize(m->blk_h, c.heads * d))) ||
-        (rc = alloc16(&p.gu, wsize(m->blk_gu, H))) ||
-        (rc = alloc16(&p.down, wsize(m->blk_h, FP))) ||
+        (!m->fp8 && (rc = alloc16(&p.gu, wsize(m->blk_gu, H)))) ||
+        (!m->fp8 && (rc = alloc16(&p.down, wsize(m->blk_h, FP)))) ||
+        (m->fp8 && (rc = alloc8(&p.gu8, wsize(m->blk_gu, KPH8)))) ||
+        (m->fp8 && (rc = alloc8(&p.down8, wsize(m->blk_h, KPF8)))) ||
+        (m->fp8 && (rc = allocf(&p.sw_gu, (size_t)m->blk_gu * 16))) ||
+        (m->fp8 && (rc = allocf(&p.sw_down, (size_t)m->blk_h * 16))) ||
         (rc = allocf(&p.ln1, H)) || (rc = allocf(&p.ln2, H)))
       return bail(rc);
     p.bias = nullptr;
@@ -380,10 +423,22 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
                            m->blk_qkv, m->nb_qkv, 0, p.qkv, s)) != hipSuccess ||
         (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
                            c.heads * d, m->blk_h, m->nb_o, 0, p.o, s)) != hipSuccess ||
-        (e = launch_repack((const uint16_t*)lw.w_gate, F, (const uint16_t*)lw.w_up, F, nullptr,
-                           0, H, H, m->blk_gu, 10, 1, p.gu, s)) != hipSuccess ||
-        (e = launch_repack((const uint16_t*)lw.w_down, H, nullptr, 0, nullptr, 0, F, FP,
-                           m->blk_h, m->nb_down, 0, p.down, s)) != hipSuccess ||
+        (!m->fp8 &&
+         (e = launch_repack((const uint16_t*)lw.w_gate, F, (const uint16_t*)lw.w_up, F, nullptr,
+                            0, H, H, m->blk_gu, 10, 1, p.gu, s)) != hipSuccess) ||
+        (!m->fp8 &&
+         (e = launch_repack((const uint16_t*)lw.w_down, H, nullptr, 0, nullptr, 0, F, FP,
+                            m->blk_h, m->nb_down, 0, p.down, s)) != hipSuccess) ||
+        (m->fp8 &&
+         ((e = launch_rowscale((const uint16_t*)lw.w_gate, F, H, inv_g, sc_g, s)) != hipSuccess ||
+          (e = launch_rowscale((const uint16_t*)lw.w_up, F, H, inv_u, sc_u, s)) != hipSuccess ||
+          (e = launch_rowscale((const uint16_t*)lw.w_down, H, F, inv_d, sc_d, s)) != hipSuccess ||
+          (e = launch_repack8((const uint16_t*)lw.w_gate, inv_g, sc_g, F,
+                              (const uint16_t*)lw.w_up, inv_u, sc_u, F, H, KPH8, m->blk_gu, 10, 1,
+                              p.gu8, p.sw_gu, s)) != hipSuccess ||
+          (e = launch_repack8((const uint16_t*)lw.w_down, inv_d, sc_d, H, nullptr, nullptr,
+                              nullptr, 0, F, KPF8, m->blk_h, m->nb_down8, 0, p.down8, p.sw_down,
+                              s)) != hipSuccess)) ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln1, p.ln1, H, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln2, p.ln2, H, s)) != hipSuccess)
       return bail(fail(LOPA_EHIP, "layer %d repack: %s", l, hipGetErrorString(e)));
@@ -460,6 +515,12 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   KV_ALLOC(x, float*, rows * H * 4);
   KV_ALLOC(abuf, uint16_t*, rows * H * 2);
   KV_ALLOC(fbuf, uint16_t*, rows * FP * 2);
+  if (m->fp8) {
+    KV_ALLOC(a8_gu, uint8_t*, rows * round512(H));
+    KV_ALLOC(a8_dn, uint8_t*, rows * round512(F));
+    KV_ALLOC(sa_gu, float*, rows * 4);
+    KV_ALLOC(sa_dn, float*, rows * 4);
+  }
   KV_ALLOC(qbuf, uint16_t*, (size_t)max_branches * c.heads * max_block * d * 2);
   KV_ALLOC(partials, float*, part_b);
   kv->attn_part_bytes = (size_t)attn_max_ranges(c, m->num_cu) * max_branches * max_block *
@@ -482,6 +543,8 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   if ((e = hipMemcpy(kv->rope, tab.data(), tab.size() * 4, hipMemcpyHostToDevice)) ||
       (e = hipMemset(kv->cache, 0, cache_e * 2)) || (e = hipMemset(kv->staging, 0, stag_e * 2)) ||
       (e = hipMemset(kv->abuf, 0, rows * H * 2)) || (e = hipMemset(kv->fbuf, 0, rows * FP * 2)) ||
+      (m->fp8 && ((e = hipMemset(kv->a8_gu, 0, rows * round512(H))) ||
+                  (e = hipMemset(kv->a8_dn, 0, rows * round512(F))))) ||
       (e = hipDeviceSynchronize()))
     return bail(fail(LOPA_EHIP, "kv create: %s", hipGetErrorString(e)));
   *out = kv;
@@ -544,6 +607,8 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.W = W;
     g.N = N;
     g.KC = K / 64;
+    g.f8 = 0;
+    g.sa = g.sw = nullptr;
     g.nb = p.nb;
     g.tiles = p.tiles;
     g.splits = p.splits;
@@ -604,14 +669,45 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.x = kv->x;
     { ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
       HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, c.heads * d, plan.o)); }
-    { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-      HIP_TRY(launch_resnorm(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
-                             c.rms_eps, M, Mp, H, kv->x, kv->abuf, s)); }
     g.a_out = kv->fbuf;
-    { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
-      HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, H, plan.gu)); }
-    { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
-      HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, round256(F), plan.down)); }
+    if (m->fp8) {
+      // FP8 MLP: the normed rows straight to E4M3 with their scales, gate/up,
+      // the SwiGLU output (bf16) requantised per row, down
+      { ProfScope ps_(kv, LOPA_PROF_NORM, s);
+        HIP_TRY(launch_resnorm8(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
+                                c.rms_eps, M, Mp, H, kv->x, kv->a8_gu, kv->sa_gu, s)); }
+      auto gemm8 = [&](int epi, const uint8_t* A, const uint8_t* W, int N, int KP,
+                       const float* sa, const float* sw, const GemmPlan& pl) {
+        g.A = (const uint16_t*)A;
+        g.W = (const uint16_t*)W;
+        g.N = N;
+        g.KC = KP / 128;
+        g.f8 = 1;
+        g.sa = sa;
+        g.sw = sw;
+        g.nb = pl.nb;
+        g.tiles = pl.tiles;
+        g.splits = pl.splits;
+        g.gcols = pl.tiles * pl.splits;
+        return launch_gemm(epi, g, s);
+      };
+      { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
+        HIP_TRY(gemm8(EPI_SWIGLU, kv->a8_gu, p.gu8, 2 * F, round512(H), kv->sa_gu, p.sw_gu,
+                      plan.gu)); }
+      { ProfScope ps_(kv, LOPA_PROF_NORM, s);
+        HIP_TRY(launch_quant_rows8(kv->fbuf, F, M, Mp, kv->a8_dn, kv->sa_dn, s)); }
+      { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
+        HIP_TRY(gemm8(EPI_RESID, kv->a8_dn, p.down8, H, round512(F), kv->sa_dn, p.sw_down,
+                      plan.down)); }
+    } else {
+      { ProfScope ps_(kv, LOPA_PROF_NORM, s);
+        HIP_TRY(launch_resnorm(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
+                               c.rms_eps, M, Mp, H, kv->x, kv->abuf, s)); }
+      { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
+        HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, H, plan.gu)); }
+      { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
+        HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, round256(F), plan.down)); }
+    }
     const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
       HIP_TRY(launch_resnorm(kv->partials, plan.down.splits > 1 ? plan.down.splits : 0, next_w,

@@ -124,6 +124,17 @@ __device__ __forceinline__ void pin_landed(u32x4& v) { asm volatile("" : "+v"(v)
 __device__ __forceinline__ void mfma_acc(f32x4& c, const u32x4& a, const u32x4& b) {
   asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(c) : "v"(a), "v"(b));
 }
+// FP8 (E4M3 x E4M3) form: one 16x16x128 MFMA over 32 bytes per lane of each
+// operand, unit scales (E8M0 127 = 2^0; the real scales are applied in the
+// epilogue). A lane's byte b of A and byte b of B meet in the same product, so
+// any placement of K inside the 32 bytes works as long as A and W use the same.
+__device__ __forceinline__ void mfma_acc_f8(f32x4& c, const u32x8& a, const u32x8& b) {
+  asm volatile("v_mfma_scale_f32_16x16x128_f8f6f4 %0, %1, %2, %0, %3, %3 op_sel_hi:[0,0,0]"
+               : "+a"(c) : "v"(a), "v"(b), "v"(127));
+}
+__device__ __forceinline__ u32x8 cat8(const u32x4& lo, const u32x4& hi) {
+  return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+}
 __device__ __forceinline__ void mfma_settle() {
   asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
@@ -132,6 +143,25 @@ __device__ __forceinline__ void mfma_settle() {
 // acc[mb][nb][j]: row row0 + 16 mb + 4 g + j, column 16 (tile NB + nb) + c16
 // of this wavefront (g = lane / 16, c16 = lane % 16); the SwiGLU GEMM holds
 // the transposed tile (see swiglu_epilogue).
+
+// FP8: the accumulated products times the row's and the column's scales
+// (acc[mb][nb][j]: row row0 + 16 mb + 4 g + j, packed column 16 (tile NB + nb) + c16)
+template <int NB>
+__device__ __forceinline__ void f8_scale(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
+                                         int row0, int lane) {
+  const int g = lane >> 4, c16 = lane & 15;
+  float swc[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) swc[nb] = a.sw[(tile * NB + nb) * 16 + c16];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float sr = a.sa[row0 + mb * 16 + g * 4 + j];
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) acc[mb][nb][j] = acc[mb][nb][j] * sr * swc[nb];
+    }
+}
 
 template <int NB>
 __device__ __forceinline__ void resid_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
@@ -163,20 +193,26 @@ __device__ __forceinline__ void resid_epilogue(const GemmArgs& a, f32x4 (&acc)[4
 // halves with one permlane swap per dword: afterwards the even lane holds the
 // slot of row block mb, the odd lane the slot of row block mb + 1, and each
 // writes 16 bytes.
-template <int NB>
+template <int NB, bool F8>
 __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[4][NB], int tile,
                                                 int row0, int lane) {
   constexpr int PAIRS = NB / 2;
   const int g = lane >> 4, c16 = lane & 15;
   const int Nout = a.N >> 1;
   auto swiglu4 = [&](int mb, int p, uint32_t (&hv)[2]) {
+    // FP8: scales of the row (this lane's) and of the gate / up columns
+    const float sr = F8 ? a.sa[row0 + mb * 16 + c16] : 1.f;
 #pragma unroll
     for (int jj = 0; jj < 2; ++jj) {
       float h2[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int j = 2 * jj + u;
-        const float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
+        float gt = acc[mb][2 * p][j], up = acc[mb][2 * p + 1][j];
+        if constexpr (F8) {
+          gt = gt * sr * a.sw[(tile * NB + 2 * p) * 16 + 4 * g + j];
+          up = up * sr * a.sw[(tile * NB + 2 * p + 1) * 16 + 4 * g + j];
+        }
         // silu(g) = g / (1 + e^-g) with the hardware exp2 and reciprocal (about
         // 1 ulp each, far below the bf16 rounding of the result)
         const float ex = __builtin_amdgcn_exp2f(-gt * 1.4426950408889634f);
@@ -346,9 +382,59 @@ constexpr int BPF = 4;
     cs = cs + 2 >= RING ? cs + 2 - RING : cs + 2;                                        \
   }
 
-template <int EPI, int NB>
+// FP8 form of GEMM_PAIR: a weight unit (block, k-half) covers 64 values of K
+// (16 per lane), and the units are read in (block, half) order, so both halves
+// of a block are in registers together; each block then takes one 16x16x128 MFMA per
+// row block with both activation halves as its first operand. The activation
+// set of an iteration is read until its last block, so both halves are
+// reissued at the end of the iteration (the weight copies as in GEMM_PAIR).
+#define GEMM_PAIR_F8(s0, s1)                                                             \
+  {                                                                                      \
+    wait_vmcnt<2 * OPS>();                                                               \
+    lds_barrier();                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < 8; ++i_) {                                   \
+      pin_landed(s0[i_]);                                                                \
+      pin_landed(s1[i_]);                                                                \
+    }                                                                                    \
+    const u32x4* wl0_ = (const u32x4*)(smem + cs * SM::CHUNK);                           \
+    const int c1_ = cs + 1 == RING ? 0 : cs + 1;                                         \
+    const u32x4* wl1_ = (const u32x4*)(smem + c1_ * SM::CHUNK);                          \
+    const int is0_ = cs >= 2 ? cs - 2 : cs + RING - 2;                                   \
+    const int is1_ = is0_ + 1 == RING ? 0 : is0_ + 1;                                    \
+    u32x4 bf_[4 * NB];                                                                   \
+    _Pragma("unroll") for (int f_ = 0; f_ < BPF; ++f_) bf_[f_] = wl0_[f_ * 64 + lane];    \
+    __builtin_amdgcn_sched_barrier(0);                                                   \
+    _Pragma("unroll") for (int f_ = 0; f_ < 4 * NB; ++f_) {                              \
+      const int e_ = f_ / (2 * NB), g_ = f_ % (2 * NB); /* iteration, unit */           \
+      if (f_ + BPF < 4 * NB) {                                                           \
+        const int fn_ = f_ + BPF, gn_ = fn_ % (2 * NB);                                  \
+        bf_[fn_] = (fn_ < 2 * NB ? wl0_ : wl1_)[gn_ * 64 + lane];                        \
+      }                                                                                  \
+      if (g_ & 1) {                                                                      \
+        const u32x8 b8_ = cat8(bf_[f_ - 1], bf_[f_]);                                    \
+        _Pragma("unroll") for (int mb_ = 0; mb_ < 4; ++mb_) {                            \
+          const u32x8 a8_ = cat8((e_ ? s1 : s0)[mb_], (e_ ? s1 : s0)[4 + mb_]);          \
+          if constexpr (EPI == EPI_SWIGLU)                                               \
+            mfma_acc_f8(acc[mb_][g_ >> 1], b8_, a8_);                                    \
+          else                                                                           \
+            mfma_acc_f8(acc[mb_][g_ >> 1], a8_, b8_);                                    \
+        }                                                                                \
+      }                                                                                  \
+      if (g_ >= 1 && g_ <= NB / 2) GEMM_ISSUE_W(g_ - 1, e_ ? is1_ : is0_);               \
+      if (g_ == 2 * NB - 1) {                                                            \
+        GEMM_ISSUE_A((e_ ? s1 : s0), 0);                                                 \
+        GEMM_ISSUE_A((e_ ? s1 : s0), 1);                                                 \
+        GEMM_ADVANCE_LOAD();                                                             \
+      }                                                                                  \
+      __builtin_amdgcn_sched_barrier(0);                                                 \
+    }                                                                                    \
+    cs = cs + 2 >= RING ? cs + 2 - RING : cs + 2;                                        \
+  }
+
+template <int EPI, int NB, bool F8>
 __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_kernel(GemmArgs a) {
   using SM = GemmSmem<EPI, NB>;
+  static_assert(!F8 || EPI == EPI_SWIGLU || EPI == EPI_RESID, "FP8 epilogues");
   constexpr int OPS = 8 + NB / 2;  // vector memory operations per wavefront per iteration
   static_assert(NB % 2 == 0 && 3 * OPS <= 63, "tile width");
   static_assert(RING == 6 && LEAD == 4, "pair schedule");
@@ -404,18 +490,24 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
       for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
     mfma_settle();
     for (int qq = 0; qq < nq; ++qq) {
-      GEMM_PAIR(a0, a1);
-      GEMM_PAIR(a2, a3);
+      if constexpr (F8) {
+        GEMM_PAIR_F8(a0, a1);
+        GEMM_PAIR_F8(a2, a3);
+      } else {
+        GEMM_PAIR(a0, a1);
+        GEMM_PAIR(a2, a3);
+      }
     }
     GEMM_DRAIN();
     mfma_settle();
+    if constexpr (F8 && EPI == EPI_RESID) f8_scale<NB>(a, acc, t_lo, row0, lane);
     if (EPI != EPI_QKV && a.splits == 1) {
       if constexpr (EPI == EPI_LMHEAD) {
         lds_barrier();  // the ring becomes the reduction area (every copy has landed)
         lm_epilogue<NB>(a, acc, t_lo, row0, lane, (float*)smem + wv * 64 * 16 * 3);
       }
       if constexpr (EPI == EPI_RESID) resid_epilogue<NB>(a, acc, t_lo, row0, lane);
-      if constexpr (EPI == EPI_SWIGLU) swiglu_epilogue<NB>(a, acc, t_lo, row0, lane);
+      if constexpr (EPI == EPI_SWIGLU) swiglu_epilogue<NB, F8>(a, acc, t_lo, row0, lane);
     } else if constexpr (EPI == EPI_RESID) {
       // row-major partial sums [split][Mp][N], added by the following RMSNorm
       const int g = lane >> 4, c16 = lane & 15;
@@ -518,10 +610,10 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
   }
 }
 
-template <int EPI, int NB>
+template <int EPI, int NB, bool F8 = false>
 hipError_t launch_nb(const GemmArgs& a, hipStream_t s) {
   const int grid = a.mtiles * a.gcols;
-  hipLaunchKernelGGL((gemm_kernel<EPI, NB>), dim3(grid), dim3(GEMM_THREADS), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<EPI, NB, F8>), dim3(grid), dim3(GEMM_THREADS), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if constexpr (EPI == EPI_QKV) {
@@ -556,6 +648,15 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
       a.gcols < 1 || a.Mp != 256 * a.mtiles)
     return hipErrorInvalidValue;
   if (a.gcols != a.tiles * a.splits) return hipErrorInvalidValue;
+  if (a.f8) {
+    if (!a.sa || !a.sw) return hipErrorInvalidValue;
+    switch (epi * 16 + a.nb) {
+      case EPI_RESID * 16 + 4: return launch_nb<EPI_RESID, 4, true>(a, s);
+      case EPI_RESID * 16 + 8: return launch_nb<EPI_RESID, 8, true>(a, s);
+      case EPI_SWIGLU * 16 + 10: return launch_nb<EPI_SWIGLU, 10, true>(a, s);
+    }
+    return hipErrorInvalidValue;
+  }
   switch (epi * 16 + a.nb) {
     case EPI_QKV * 16 + 4: return launch_nb<EPI_QKV, 4>(a, s);
     case EPI_QKV * 16 + 8: return launch_nb<EPI_QKV, 8>(a, s);

@@ -53,6 +53,20 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
 // then a[r] = pack(rmsnorm(x[r]) * w), for r < M. H % 256 == 0.
 hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, int M, int Mp,
                           int H, float* x, uint16_t* a, hipStream_t s);
+// FP8 (E4M3, per-row scale) forms: launch_resnorm with the normed row written
+// as the packed FP8 operand a8 and its scale sa[r]; the packed bf16 operand a
+// (K columns) requantised to FP8; per-row scaling pairs of a bf16 weight
+// [rows][K]; the FP8 weight repack (see gemm.hip; KP % 512 == 0)
+hipError_t launch_resnorm8(const float* part, int S, const float* w, float eps, int M, int Mp,
+                           int H, float* x, uint8_t* a8, float* sa, hipStream_t s);
+hipError_t launch_quant_rows8(const uint16_t* a, int K, int M, int Mp, uint8_t* a8, float* sa,
+                              hipStream_t s);
+hipError_t launch_rowscale(const uint16_t* w, int rows, int K, float* inv, float* scale,
+                           hipStream_t s);
+hipError_t launch_repack8(const uint16_t* s0, const float* inv0, const float* sc0, int r0,
+                          const uint16_t* s1, const float* inv1, const float* sc1, int r1, int K,
+                          int KP, int blocks, int nb, int pairs, uint8_t* dst, float* sw,
+                          hipStream_t s);
 // merge per-tile softmax partials into conf / pred
 hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, int M,
                            int tiles, float* conf, int32_t* pred, hipStream_t s);
@@ -88,6 +102,13 @@ struct GemmArgs {
   float* ps;           // [M][tiles] sum of exp(l - max)
   int32_t* pi;         // [M][tiles] argmax
   int vocab, mask_id;
+  // FP8 operands (f8 != 0; EPI_SWIGLU and EPI_RESID): A and W hold E4M3 bytes in
+  // the same fragment layout (a 16-byte lane slot holds 16 values of K instead
+  // of 8), KC counts 128-wide k-chunks, and the epilogue scales the fp32 sum
+  // of products by sa[row] * sw[packed column]
+  int f8;
+  const float* sa;     // [Mp] per-row activation scales
+  const float* sw;     // [blocks * 16] per-column weight scales, packed column order
 };
 // bytes of LDS of gemm_kernel<epi, nb> (-1: not instantiated)
 int gemm_smem_bytes(int epi, int nb);

@@ -20,15 +20,41 @@
 // select: no load sits under a branch, so all of them can be in flight
 // together.
 constexpr int CPT = 8;  // 4-column groups per thread at most
-template <bool EMBED, int SC, int NG>
+
+// E4M3 (no infinities, max 448) of x, round to nearest even, saturating:
+// subnormals (|x| < 2^-6) are multiples of 2^-9, and a normal value of binade
+// 2^E has 3 fraction bits, so its code is rint(|x| 2^(3 - E)) - 8 + (E + 7) 8
+// (a mantissa that rounds up to 16 carries into the exponent by itself).
+__device__ __forceinline__ uint32_t f32_to_e4m3(float x) {
+  const uint32_t sign = (__float_as_uint(x) >> 24) & 0x80u;
+  const float ax = fminf(fabsf(x), 448.f);
+  if (ax < 0.015625f) return sign | (uint32_t)rintf(ax * 512.f);
+  const int E = (int)((__float_as_uint(ax) >> 23) & 0xffu) - 127;
+  return sign | (uint32_t)(((E + 7) << 3) + (int)rintf(ldexpf(ax, 3 - E)) - 8);
+}
+// byte offset of (row r, column c) in the packed FP8 operand: 64-column blocks
+// of 16-row blocks, lane (r % 16) + 16 ((c % 64) / 16) holding 16 consecutive
+// columns (the bf16 layout with twice the columns per lane slot)
+__device__ __forceinline__ int64_t packA8_off(int r, int c, int Mp) {
+  return ((int64_t)((c >> 6) * (Mp >> 4) + (r >> 4)) * 64 + (r & 15) + 16 * ((c & 63) >> 4)) * 16 +
+         (c & 15);
+}
+// the per-row scaling of the FP8 operand: inverse 448 / max|v|, scale max|v| / 448
+__device__ __forceinline__ float e4m3_inv(float amax) { return amax > 0.f ? __fdiv_rn(448.f, amax) : 0.f; }
+__device__ __forceinline__ float e4m3_scale(float amax) { return amax > 0.f ? __fdiv_rn(amax, 448.f) : 0.f; }
+
+template <bool EMBED, int SC, int NG, bool A8>
 __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict__ tokens,
                                                       const uint16_t* __restrict__ embed,
                                                       int vocab, const float* __restrict__ part,
                                                       int S, const float* __restrict__ w,
                                                       float eps, int M, int Mp, int H,
                                                       float* __restrict__ x,
-                                                      uint16_t* __restrict__ a) {
+                                                      uint16_t* __restrict__ a,
+                                                      uint8_t* __restrict__ a8,
+                                                      float* __restrict__ sa) {
   __shared__ float red[4];
+  __shared__ float redm[4];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int r = blockIdx.x;
   const int nq = H >> 2;
@@ -96,17 +122,164 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   __syncthreads();
   const float tot = red[0] + red[1] + red[2] + red[3];
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+  if constexpr (A8) {
+    // FP8 operand: the normed row, its largest magnitude (lanes, then
+    // wavefronts 0..3), then E4M3 of each value times 448 / max
+    float4 y[NG];
+    float mx = 0.f;
 #pragma unroll
-  for (int i = 0; i < NG; ++i) {
-    const int q = tid + 256 * i;
-    if (q < nq) {
-      const uint32_t lo = (uint32_t)f2bf_bits(v[i].x * inv * wt[i].x) |
-                          ((uint32_t)f2bf_bits(v[i].y * inv * wt[i].y) << 16);
-      const uint32_t hi = (uint32_t)f2bf_bits(v[i].z * inv * wt[i].z) |
-                          ((uint32_t)f2bf_bits(v[i].w * inv * wt[i].w) << 16);
-      *(uint2*)(a + packA_off(r, q * 4, Mp)) = make_uint2(lo, hi);
+    for (int i = 0; i < NG; ++i) {
+      const int q = tid + 256 * i;
+      y[i] = make_float4(v[i].x * inv * wt[i].x, v[i].y * inv * wt[i].y, v[i].z * inv * wt[i].z,
+                         v[i].w * inv * wt[i].w);
+      if (q < nq)
+        mx = fmaxf(mx, fmaxf(fmaxf(fabsf(y[i].x), fabsf(y[i].y)), fmaxf(fabsf(y[i].z), fabsf(y[i].w))));
+    }
+    mx = wave_max(mx);
+    if (lane == 0) redm[wv] = mx;
+    __syncthreads();
+    mx = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+    const float si = e4m3_inv(mx);
+#pragma unroll
+    for (int i = 0; i < NG; ++i) {
+      const int q = tid + 256 * i;
+      if (q < nq) {
+        const uint32_t b = f32_to_e4m3(y[i].x * si) | (f32_to_e4m3(y[i].y * si) << 8) |
+                           (f32_to_e4m3(y[i].z * si) << 16) | (f32_to_e4m3(y[i].w * si) << 24);
+        *(uint32_t*)(a8 + packA8_off(r, q * 4, Mp)) = b;
+      }
+    }
+    if (tid == 0) sa[r] = e4m3_scale(mx);
+  } else {
+#pragma unroll
+    for (int i = 0; i < NG; ++i) {
+      const int q = tid + 256 * i;
+      if (q < nq) {
+        const uint32_t lo = (uint32_t)f2bf_bits(v[i].x * inv * wt[i].x) |
+                            ((uint32_t)f2bf_bits(v[i].y * inv * wt[i].y) << 16);
+        const uint32_t hi = (uint32_t)f2bf_bits(v[i].z * inv * wt[i].z) |
+                            ((uint32_t)f2bf_bits(v[i].w * inv * wt[i].w) << 16);
+        *(uint2*)(a + packA_off(r, q * 4, Mp)) = make_uint2(lo, hi);
+      }
     }
   }
+}
+
+// FP8 operand of a projection from the packed bf16 one (the SwiGLU output):
+// one workgroup per row r < M; thread t takes the 8-column groups t + 256 i
+// (16 bytes each, kept in registers), the row's largest magnitude (lanes, then
+// wavefronts 0..3), then E4M3 of each value times 448 / max into the FP8
+// layout, and the row's scale.
+constexpr int Q8_GROUPS = 12;  // 8-column groups per thread at most (K <= 24576)
+__global__ __launch_bounds__(256) void quant_rows8_kernel(const uint16_t* __restrict__ a, int K,
+                                                          int Mp, uint8_t* __restrict__ a8,
+                                                          float* __restrict__ sa) {
+  __shared__ float redm[4];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int r = blockIdx.x;
+  const int ng = K >> 3;
+  uint4 raw[Q8_GROUPS];
+#pragma unroll
+  for (int i = 0; i < Q8_GROUPS; ++i) {
+    const int gi = tid + 256 * i;
+    raw[i] = *(const uint4*)(a + packA_off(r, 8 * (gi < ng ? gi : ng - 1), Mp));
+  }
+  auto val = [](uint32_t u, int hi) { return bf2f_bits(hi ? u >> 16 : u & 0xffff); };
+  float mx = 0.f;
+#pragma unroll
+  for (int i = 0; i < Q8_GROUPS; ++i) {
+    if (tid + 256 * i >= ng) continue;
+    const uint32_t w4[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(val(w4[e >> 1], e & 1)));
+  }
+  mx = wave_max(mx);
+  if (lane == 0) redm[wv] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+  const float si = e4m3_inv(mx);
+#pragma unroll
+  for (int i = 0; i < Q8_GROUPS; ++i) {
+    const int gi = tid + 256 * i;
+    if (gi >= ng) continue;
+    const uint32_t w4[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+    uint32_t b[2] = {0u, 0u};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) b[e >> 2] |= f32_to_e4m3(val(w4[e >> 1], e & 1) * si) << (8 * (e & 3));
+    *(uint2*)(a8 + packA8_off(r, 8 * gi, Mp)) = make_uint2(b[0], b[1]);
+  }
+  if (tid == 0) sa[r] = e4m3_scale(mx);
+}
+
+// Per source row of a bf16 weight [rows][K]: the FP8 scaling pair
+// (inv = 448 / max|w|, scale = max|w| / 448). One workgroup per row.
+__global__ __launch_bounds__(256) void rowscale_kernel(const uint16_t* __restrict__ w, int K,
+                                                       float* __restrict__ inv,
+                                                       float* __restrict__ scale) {
+  __shared__ float redm[4];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const uint16_t* wr = w + (int64_t)blockIdx.x * K;
+  float mx = 0.f;
+  for (int k = tid; k < K; k += 256) mx = fmaxf(mx, fabsf(bf2f_bits(wr[k])));
+  mx = wave_max(mx);
+  if (lane == 0) redm[wv] = mx;
+  __syncthreads();
+  if (tid == 0) {
+    mx = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+    inv[blockIdx.x] = e4m3_inv(mx);
+    scale[blockIdx.x] = e4m3_scale(mx);
+  }
+}
+
+// FP8 weight repack: the layout of repack_kernel with 16 E4M3 values (16
+// bytes) per lane slot, i.e. unit (block, kk) of k-chunk kc holds columns
+// kc 128 + kk 64 + 16 (lane / 16) .. + 15; the values are the bf16 weights
+// times their row's inverse scale. sw gets the scale of every packed column
+// (0 for padding columns). One or two sources (pairs: alternating blocks).
+__global__ __launch_bounds__(256) void repack8_kernel(const uint16_t* __restrict__ s0,
+                                                      const float* __restrict__ inv0,
+                                                      const float* __restrict__ sc0, int r0,
+                                                      const uint16_t* __restrict__ s1,
+                                                      const float* __restrict__ inv1,
+                                                      const float* __restrict__ sc1, int r1,
+                                                      int K, int KC, int NB, int64_t total,
+                                                      int pairs, uint8_t* __restrict__ dst,
+                                                      float* __restrict__ sw) {
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= total) return;
+  const int lane = (int)(gid & 63);
+  int64_t u = gid >> 6;
+  const int kk = (int)(u & 1);
+  u >>= 1;
+  const int nbi = (int)(u % NB);
+  u /= NB;
+  const int kc = (int)(u % KC);
+  const int blk = (int)(u / KC) * NB + nbi;
+  const int k0 = kc * 128 + kk * 64 + (lane >> 4) * 16;
+  const uint16_t* src = nullptr;
+  float si = 0.f, sc = 0.f;
+  int row = 0;
+  if (pairs) {
+    row = (blk >> 1) * 16 + (lane & 15);
+    if (!(blk & 1)) { if (row < r0) { src = s0; si = inv0[row]; sc = sc0[row]; } }
+    else { if (row < r1) { src = s1; si = inv1[row]; sc = sc1[row]; } }
+  } else {
+    row = blk * 16 + (lane & 15);
+    if (row < r0) { src = s0; si = inv0[row]; sc = sc0[row]; }
+  }
+  uint32_t b[4] = {0u, 0u, 0u, 0u};
+  if (src && k0 < K) {
+    const uint4 h0 = *(const uint4*)(src + (int64_t)row * K + k0);
+    const uint4 h1 = *(const uint4*)(src + (int64_t)row * K + k0 + 8);
+    const uint32_t w8[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float v = bf2f_bits((e & 1) ? w8[e >> 1] >> 16 : w8[e >> 1] & 0xffff);
+      b[e >> 2] |= f32_to_e4m3(v * si) << (8 * (e & 3));
+    }
+  }
+  *(uint4*)(dst + gid * 16) = make_uint4(b[0], b[1], b[2], b[3]);
+  if (kc == 0 && kk == 0 && (lane >> 4) == 0) sw[blk * 16 + (lane & 15)] = src ? sc : 0.f;
 }
 
 // (max, sum, argmax) state of a run of vocabulary tiles: sum of exp(logit -
@@ -214,8 +387,8 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
                              uint16_t* a, hipStream_t s) {
   if (H % 256 || H > 1024 * CPT) return hipErrorInvalidValue;
 #define EMBEDNORM(NG)                                                                     \
-  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG>), dim3(M), dim3(256), 0, s, tokens, embed, \
-                     vocab, nullptr, 0, w, eps, M, Mp, H, x, a)
+  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, false>), dim3(M), dim3(256), 0, s, tokens,   \
+                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, a, nullptr, nullptr)
   switch (resnorm_groups(H)) {
     case 1: EMBEDNORM(1); break;
     case 2: EMBEDNORM(2); break;
@@ -227,12 +400,12 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
 }
 
 namespace {
-template <int NG>
+template <int NG, bool A8>
 void resnorm_ng(const float* part, int S, const float* w, float eps, int M, int Mp, int H,
-                float* x, uint16_t* a, hipStream_t s) {
+                float* x, uint16_t* a, uint8_t* a8, float* sa, hipStream_t s) {
 #define RESNORM(SC)                                                                         \
-  hipLaunchKernelGGL((resnorm_kernel<false, SC, NG>), dim3(M), dim3(256), 0, s, nullptr,     \
-                     nullptr, 0, part, S, w, eps, M, Mp, H, x, a)
+  hipLaunchKernelGGL((resnorm_kernel<false, SC, NG, A8>), dim3(M), dim3(256), 0, s, nullptr, \
+                     nullptr, 0, part, S, w, eps, M, Mp, H, x, a, a8, sa)
   switch (S) {
     case 0: RESNORM(0); break;
     case 2: RESNORM(2); break;
@@ -253,11 +426,48 @@ hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, i
                           int H, float* x, uint16_t* a, hipStream_t s) {
   if (H % 256 || H > 1024 * CPT || S < 0) return hipErrorInvalidValue;
   switch (resnorm_groups(H)) {
-    case 1: resnorm_ng<1>(part, S, w, eps, M, Mp, H, x, a, s); break;
-    case 2: resnorm_ng<2>(part, S, w, eps, M, Mp, H, x, a, s); break;
-    case 4: resnorm_ng<4>(part, S, w, eps, M, Mp, H, x, a, s); break;
-    default: resnorm_ng<8>(part, S, w, eps, M, Mp, H, x, a, s); break;
+    case 1: resnorm_ng<1, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
+    case 2: resnorm_ng<2, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
+    case 4: resnorm_ng<4, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
+    default: resnorm_ng<8, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_resnorm8(const float* part, int S, const float* w, float eps, int M, int Mp,
+                           int H, float* x, uint8_t* a8, float* sa, hipStream_t s) {
+  if (H % 256 || H > 1024 * CPT || S < 0 || !a8 || !sa) return hipErrorInvalidValue;
+  switch (resnorm_groups(H)) {
+    case 1: resnorm_ng<1, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
+    case 2: resnorm_ng<2, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
+    case 4: resnorm_ng<4, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
+    default: resnorm_ng<8, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_quant_rows8(const uint16_t* a, int K, int M, int Mp, uint8_t* a8, float* sa,
+                              hipStream_t s) {
+  if (K % 64 || K > 8 * 256 * Q8_GROUPS || M < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(quant_rows8_kernel, dim3(M), dim3(256), 0, s, a, K, Mp, a8, sa);
+  return hipGetLastError();
+}
+
+hipError_t launch_rowscale(const uint16_t* w, int rows, int K, float* inv, float* scale,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(rowscale_kernel, dim3(rows), dim3(256), 0, s, w, K, inv, scale);
+  return hipGetLastError();
+}
+
+hipError_t launch_repack8(const uint16_t* s0, const float* inv0, const float* sc0, int r0,
+                          const uint16_t* s1, const float* inv1, const float* sc1, int r1, int K,
+                          int KP, int blocks, int nb, int pairs, uint8_t* dst, float* sw,
+                          hipStream_t s) {
+  if (KP % 512 || KP < K || K % 16 || nb < 1 || blocks % nb) return hipErrorInvalidValue;
+  const int KC = KP / 128;
+  const int64_t total = (int64_t)blocks * KC * 2 * 64;
+  hipLaunchKernelGGL(repack8_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, s0,
+                     inv0, sc0, r0, s1, inv1, sc1, r1, K, KC, nb, total, pairs, dst, sw);
   return hipGetLastError();
 }
 

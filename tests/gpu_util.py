@@ -62,18 +62,21 @@ def f32(x: float) -> float:
 class Setup:
     """Same seeded model + prompt on both sides, each side prefilled by itself."""
 
-    def __init__(self, cfgname: str, P: int, L: int, k: int, max_len=None, **over):
+    def __init__(self, cfgname: str, P: int, L: int, k: int, max_len=None, precision="bf16",
+                 **over):
+        """precision "fp8_mlp": the GPU model's MLP in FP8, and self.faith the
+        oracle's FP8 mode (the same quantisation points)."""
         import paper_2512_16229_amd as lp
         self.lp = lp
         self.cfg = synth.config(cfgname, **over)
         self.w = synth.model_weights(self.cfg)
         self.P, self.L, self.k = P, L, k
         self.max_len = max_len or (P + 2 * L)
-        self.model = lp.Model(self.cfg, to_dev_bf16(self.w))
+        self.model = lp.Model(self.cfg, to_dev_bf16(self.w), precision=precision)
         self.kv = lp.KV(self.model, self.max_len, k + 1, L)
         self.prompt = synth.prompt(self.cfg, P)
         self.pure = OracleModel(self.cfg, self.w, "pure")
-        self.faith = OracleModel(self.cfg, self.w, "faithful")
+        self.faith = OracleModel(self.cfg, self.w, "fp8" if precision == "fp8_mlp" else "faithful")
         self.cache_p = KVCache(self.cfg, self.max_len)
         self.cache_f = KVCache(self.cfg, self.max_len)
         if P:
