@@ -201,6 +201,7 @@ struct lopa_kv {
   uint8_t* a8_dn = nullptr;     // packed [mp_max][round512(F)] E4M3
   float* sa_gu = nullptr;
   float* sa_dn = nullptr;
+  uint32_t* rowmax_dn = nullptr;  // per-row max |SwiGLU output| (float bits)
   uint16_t* qbuf = nullptr;     // [max_branches][Hq][max_block][d]
   float* partials = nullptr;
   float* attn_part = nullptr;   // shared-prefix attention partial states
@@ -520,6 +521,7 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
     KV_ALLOC(a8_dn, uint8_t*, rows * round512(F));
     KV_ALLOC(sa_gu, float*, rows * 4);
     KV_ALLOC(sa_dn, float*, rows * 4);
+    KV_ALLOC(rowmax_dn, uint32_t*, rows * 4);
   }
   KV_ALLOC(qbuf, uint16_t*, (size_t)max_branches * c.heads * max_block * d * 2);
   KV_ALLOC(partials, float*, part_b);
@@ -675,7 +677,8 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
       // the SwiGLU output (bf16) requantised per row, down
       { ProfScope ps_(kv, LOPA_PROF_NORM, s);
         HIP_TRY(launch_resnorm8(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
-                                c.rms_eps, M, Mp, H, kv->x, kv->a8_gu, kv->sa_gu, s)); }
+                                c.rms_eps, M, Mp, H, kv->x, kv->a8_gu, kv->sa_gu, kv->rowmax_dn,
+                                s)); }
       auto gemm8 = [&](int epi, const uint8_t* A, const uint8_t* W, int N, int KP,
                        const float* sa, const float* sw, const GemmPlan& pl) {
         g.A = (const uint16_t*)A;
@@ -685,6 +688,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
         g.f8 = 1;
         g.sa = sa;
         g.sw = sw;
+        g.rowmax = kv->rowmax_dn;
         g.nb = pl.nb;
         g.tiles = pl.tiles;
         g.splits = pl.splits;
@@ -695,7 +699,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
         HIP_TRY(gemm8(EPI_SWIGLU, kv->a8_gu, p.gu8, 2 * F, round512(H), kv->sa_gu, p.sw_gu,
                       plan.gu)); }
       { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-        HIP_TRY(launch_quant_rows8(kv->fbuf, F, M, Mp, kv->a8_dn, kv->sa_dn, s)); }
+        HIP_TRY(launch_quant_rows8(kv->fbuf, F, M, Mp, kv->rowmax_dn, kv->a8_dn, kv->sa_dn, s)); }
       { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
         HIP_TRY(gemm8(EPI_RESID, kv->a8_dn, p.down8, H, round512(F), kv->sa_dn, p.sw_down,
                       plan.down)); }

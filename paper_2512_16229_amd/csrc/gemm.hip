@@ -199,6 +199,7 @@ __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[
   constexpr int PAIRS = NB / 2;
   const int g = lane >> 4, c16 = lane & 15;
   const int Nout = a.N >> 1;
+  float mxr[4] = {0.f, 0.f, 0.f, 0.f};  // FP8: largest |output| of each row block's row
   auto swiglu4 = [&](int mb, int p, uint32_t (&hv)[2]) {
     // FP8: scales of the row (this lane's) and of the gate / up columns
     const float sr = F8 ? a.sa[row0 + mb * 16 + c16] : 1.f;
@@ -219,6 +220,8 @@ __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[
         h2[u] = gt * __builtin_amdgcn_rcpf(1.0f + ex) * up;
       }
       hv[jj] = (uint32_t)f2bf_bits(h2[0]) | ((uint32_t)f2bf_bits(h2[1]) << 16);
+      if constexpr (F8)
+        mxr[mb] = fmaxf(mxr[mb], fmaxf(fabsf(bf2f_bits(hv[jj] & 0xffffu)), fabsf(bf2f_bits(hv[jj] >> 16))));
     }
   };
 #pragma unroll
@@ -234,6 +237,18 @@ __device__ __forceinline__ void swiglu_epilogue(const GemmArgs& a, f32x4 (&acc)[
       const int col = (tile * PAIRS + p) * 16 + (g >> 1) * 8;
       if (r < a.M && col < Nout)
         *(uint4*)(a.a_out + packA_off(r, col, a.Mp)) = make_uint4(w0[0], w1[0], w0[1], w1[1]);
+    }
+  }
+  if constexpr (F8) {
+    // the row maxima of this tile's outputs (the stored bf16 values) into the
+    // per-row maximum over all tiles: the lanes c16 + 16 g hold the same row;
+    // an unsigned maximum of the bits orders non-negative floats exactly
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      float m = fmaxf(mxr[mb], __shfl_xor(mxr[mb], 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+      const int r = row0 + mb * 16 + c16;
+      if (g == 0 && r < a.M) atomicMax(a.rowmax + r, __float_as_uint(m));
     }
   }
 }

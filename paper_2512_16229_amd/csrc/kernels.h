@@ -58,9 +58,10 @@ hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, i
 // (K columns) requantised to FP8; per-row scaling pairs of a bf16 weight
 // [rows][K]; the FP8 weight repack (see gemm.hip; KP % 512 == 0)
 hipError_t launch_resnorm8(const float* part, int S, const float* w, float eps, int M, int Mp,
-                           int H, float* x, uint8_t* a8, float* sa, hipStream_t s);
-hipError_t launch_quant_rows8(const uint16_t* a, int K, int M, int Mp, uint8_t* a8, float* sa,
-                              hipStream_t s);
+                           int H, float* x, uint8_t* a8, float* sa, uint32_t* rowmax_zero,
+                           hipStream_t s);
+hipError_t launch_quant_rows8(const uint16_t* a, int K, int M, int Mp, const uint32_t* rowmax,
+                              uint8_t* a8, float* sa, hipStream_t s);
 hipError_t launch_rowscale(const uint16_t* w, int rows, int K, float* inv, float* scale,
                            hipStream_t s);
 hipError_t launch_repack8(const uint16_t* s0, const float* inv0, const float* sc0, int r0,
@@ -109,6 +110,8 @@ struct GemmArgs {
   int f8;
   const float* sa;     // [Mp] per-row activation scales
   const float* sw;     // [blocks * 16] per-column weight scales, packed column order
+  uint32_t* rowmax;    // FP8 EPI_SWIGLU: atomic maximum of |output| (float bits) per row,
+                       // zeroed beforehand (the requantisation's row scale)
 };
 // bytes of LDS of gemm_kernel<epi, nb> (-1: not instantiated)
 int gemm_smem_bytes(int epi, int nb);

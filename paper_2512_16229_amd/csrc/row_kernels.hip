@@ -52,7 +52,8 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
                                                       float* __restrict__ x,
                                                       uint16_t* __restrict__ a,
                                                       uint8_t* __restrict__ a8,
-                                                      float* __restrict__ sa) {
+                                                      float* __restrict__ sa,
+                                                      uint32_t* __restrict__ rowmax_zero) {
   __shared__ float red[4];
   __shared__ float redm[4];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -149,7 +150,10 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
         *(uint32_t*)(a8 + packA8_off(r, q * 4, Mp)) = b;
       }
     }
-    if (tid == 0) sa[r] = e4m3_scale(mx);
+    if (tid == 0) {
+      sa[r] = e4m3_scale(mx);
+      if (rowmax_zero) rowmax_zero[r] = 0u;  // for the SwiGLU GEMM's row maxima
+    }
   } else {
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
@@ -165,50 +169,33 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   }
 }
 
-// FP8 operand of a projection from the packed bf16 one (the SwiGLU output):
-// one workgroup per row r < M; thread t takes the 8-column groups t + 256 i
-// (16 bytes each, kept in registers), the row's largest magnitude (lanes, then
-// wavefronts 0..3), then E4M3 of each value times 448 / max into the FP8
-// layout, and the row's scale.
-constexpr int Q8_GROUPS = 12;  // 8-column groups per thread at most (K <= 24576)
-__global__ __launch_bounds__(256) void quant_rows8_kernel(const uint16_t* __restrict__ a, int K,
-                                                          int Mp, uint8_t* __restrict__ a8,
+// FP8 operand of a projection from the packed bf16 one (the SwiGLU output),
+// whose per-row maximum magnitude the producing GEMM has already reduced
+// (rowmax, float bits): one thread per 16-byte lane slot of the bf16 layout
+// (8 columns of one row), E4M3 of each value times 448 / max into the FP8
+// layout; the thread holding columns 0..7 writes the row's scale.
+__global__ __launch_bounds__(256) void quant_rows8_kernel(const uint16_t* __restrict__ a, int KB,
+                                                          int M, int Mp, int RBm,
+                                                          const uint32_t* __restrict__ rowmax,
+                                                          uint8_t* __restrict__ a8,
                                                           float* __restrict__ sa) {
-  __shared__ float redm[4];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int r = blockIdx.x;
-  const int ng = K >> 3;
-  uint4 raw[Q8_GROUPS];
-#pragma unroll
-  for (int i = 0; i < Q8_GROUPS; ++i) {
-    const int gi = tid + 256 * i;
-    raw[i] = *(const uint4*)(a + packA_off(r, 8 * (gi < ng ? gi : ng - 1), Mp));
-  }
-  auto val = [](uint32_t u, int hi) { return bf2f_bits(hi ? u >> 16 : u & 0xffff); };
-  float mx = 0.f;
-#pragma unroll
-  for (int i = 0; i < Q8_GROUPS; ++i) {
-    if (tid + 256 * i >= ng) continue;
-    const uint32_t w4[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) mx = fmaxf(mx, fabsf(val(w4[e >> 1], e & 1)));
-  }
-  mx = wave_max(mx);
-  if (lane == 0) redm[wv] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int lane = (int)(gid & 63);
+  const int64_t frag = gid >> 6;  // (kb, rb) over the row blocks that hold rows < M
+  const int rb = (int)(frag % RBm), kb = (int)(frag / RBm);
+  const int r = rb * 16 + (lane & 15), g = lane >> 4;
+  if (kb >= KB || r >= M) return;
+  const uint4 raw = *(const uint4*)(a + ((int64_t)(kb * (Mp >> 4) + rb) * 64 + lane) * 8);
+  const float mx = __uint_as_float(rowmax[r]);
   const float si = e4m3_inv(mx);
+  const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+  uint32_t b[2] = {0u, 0u};
 #pragma unroll
-  for (int i = 0; i < Q8_GROUPS; ++i) {
-    const int gi = tid + 256 * i;
-    if (gi >= ng) continue;
-    const uint32_t w4[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
-    uint32_t b[2] = {0u, 0u};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) b[e >> 2] |= f32_to_e4m3(val(w4[e >> 1], e & 1) * si) << (8 * (e & 3));
-    *(uint2*)(a8 + packA8_off(r, 8 * gi, Mp)) = make_uint2(b[0], b[1]);
-  }
-  if (tid == 0) sa[r] = e4m3_scale(mx);
+  for (int e = 0; e < 8; ++e)
+    b[e >> 2] |= f32_to_e4m3(bf2f_bits((e & 1) ? w4[e >> 1] >> 16 : w4[e >> 1] & 0xffff) * si)
+                 << (8 * (e & 3));
+  *(uint2*)(a8 + packA8_off(r, kb * 32 + g * 8, Mp)) = make_uint2(b[0], b[1]);
+  if (kb == 0 && g == 0) sa[r] = e4m3_scale(mx);
 }
 
 // Per source row of a bf16 weight [rows][K]: the FP8 scaling pair
@@ -388,7 +375,7 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
   if (H % 256 || H > 1024 * CPT) return hipErrorInvalidValue;
 #define EMBEDNORM(NG)                                                                     \
   hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, false>), dim3(M), dim3(256), 0, s, tokens,   \
-                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, a, nullptr, nullptr)
+                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr)
   switch (resnorm_groups(H)) {
     case 1: EMBEDNORM(1); break;
     case 2: EMBEDNORM(2); break;
@@ -402,10 +389,10 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
 namespace {
 template <int NG, bool A8>
 void resnorm_ng(const float* part, int S, const float* w, float eps, int M, int Mp, int H,
-                float* x, uint16_t* a, uint8_t* a8, float* sa, hipStream_t s) {
+                float* x, uint16_t* a, uint8_t* a8, float* sa, uint32_t* rz, hipStream_t s) {
 #define RESNORM(SC)                                                                         \
   hipLaunchKernelGGL((resnorm_kernel<false, SC, NG, A8>), dim3(M), dim3(256), 0, s, nullptr, \
-                     nullptr, 0, part, S, w, eps, M, Mp, H, x, a, a8, sa)
+                     nullptr, 0, part, S, w, eps, M, Mp, H, x, a, a8, sa, rz)
   switch (S) {
     case 0: RESNORM(0); break;
     case 2: RESNORM(2); break;
@@ -426,30 +413,33 @@ hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, i
                           int H, float* x, uint16_t* a, hipStream_t s) {
   if (H % 256 || H > 1024 * CPT || S < 0) return hipErrorInvalidValue;
   switch (resnorm_groups(H)) {
-    case 1: resnorm_ng<1, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
-    case 2: resnorm_ng<2, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
-    case 4: resnorm_ng<4, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
-    default: resnorm_ng<8, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, s); break;
+    case 1: resnorm_ng<1, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
+    case 2: resnorm_ng<2, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
+    case 4: resnorm_ng<4, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
+    default: resnorm_ng<8, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_resnorm8(const float* part, int S, const float* w, float eps, int M, int Mp,
-                           int H, float* x, uint8_t* a8, float* sa, hipStream_t s) {
+                           int H, float* x, uint8_t* a8, float* sa, uint32_t* rz, hipStream_t s) {
   if (H % 256 || H > 1024 * CPT || S < 0 || !a8 || !sa) return hipErrorInvalidValue;
   switch (resnorm_groups(H)) {
-    case 1: resnorm_ng<1, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
-    case 2: resnorm_ng<2, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
-    case 4: resnorm_ng<4, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
-    default: resnorm_ng<8, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, s); break;
+    case 1: resnorm_ng<1, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
+    case 2: resnorm_ng<2, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
+    case 4: resnorm_ng<4, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
+    default: resnorm_ng<8, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_quant_rows8(const uint16_t* a, int K, int M, int Mp, uint8_t* a8, float* sa,
-                              hipStream_t s) {
-  if (K % 64 || K > 8 * 256 * Q8_GROUPS || M < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(quant_rows8_kernel, dim3(M), dim3(256), 0, s, a, K, Mp, a8, sa);
+hipError_t launch_quant_rows8(const uint16_t* a, int K, int M, int Mp, const uint32_t* rowmax,
+                              uint8_t* a8, float* sa, hipStream_t s) {
+  if (K % 64 || M < 1 || M > Mp || !rowmax) return hipErrorInvalidValue;
+  const int KB = K / 32, RBm = (M + 15) / 16;
+  const int64_t threads = (int64_t)KB * RBm * 64;
+  hipLaunchKernelGGL(quant_rows8_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
+                     a, KB, M, Mp, RBm, rowmax, a8, sa);
   return hipGetLastError();
 }
 
