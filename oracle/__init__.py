@@ -16,8 +16,8 @@ Plain, slow, obviously correct numpy, float64 throughout:
 
 Precision modes of the forward (see model.py): "pure" (float64 from the
 given weights), "faithful" (float64 arithmetic with bf16 round-to-nearest-even
-at the points where a bf16 implementation stores values) and "fp8" (faithful
-with the MLP projections in W8A8 E4M3). Integer decisions are
+at the points where a bf16 implementation stores values), "fp8_mlp" (faithful
+with the MLP projections in W8A8 E4M3) and "fp8" (also QKV and the LM head). Integer decisions are
 compared against "faithful", confidences against "pure".
 
 Parity status per function: every function here is pinned by tests under

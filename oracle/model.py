@@ -32,10 +32,13 @@ Precision modes:
     v after bias/RoPE, and the softmax numerators exp(s - rowmax) that multiply
     V (the row max is the global max over the row's keys; the denominator is
     the sum of the unrounded numerators).
-  * "fp8": "faithful", except that the MLP projections run in FP8 (W8A8,
+  * "fp8_mlp": "faithful", except that the MLP projections run in FP8 (W8A8,
     oracle/fp8.py): gate / up / down weights quantised per output channel, the
     normed input of gate/up quantised per row from its unrounded value, the
     SwiGLU output (stored bf16) quantised per row before the down projection.
+  * "fp8": "fp8_mlp", and the QKV projection and the LM head in FP8 as well
+    (their weights per output channel, their normed inputs per row from the
+    unrounded values); the output projection stays bf16.
 """
 from __future__ import annotations
 
@@ -117,10 +120,12 @@ class KVCache:
 
 class OracleModel:
     def __init__(self, cfg: dict, weights: dict, mode: str = "pure"):
-        if mode not in ("pure", "faithful", "fp8"):
+        if mode not in ("pure", "faithful", "fp8_mlp", "fp8"):
             raise ValueError(mode)
         self.cfg, self.mode = cfg, mode
-        r = bf16_round if mode in ("faithful", "fp8") else (lambda a: a)
+        self.fp8_mlp = mode in ("fp8_mlp", "fp8")
+        self.fp8_qkv_lm = mode == "fp8"
+        r = bf16_round if mode != "pure" else (lambda a: a)
         self.embed = r(_np(weights["embed"]))
         self.lm_head = r(_np(weights["lm_head"]))
         self.final_norm = _np(weights["final_norm"])
@@ -128,13 +133,16 @@ class OracleModel:
         for lw in weights["layers"]:
             self.layers.append({k: (r(_np(v)) if k not in ("ln1", "ln2") else _np(v))
                                 for k, v in lw.items()})
-        if mode == "fp8":
-            for w in self.layers:
-                for key in ("w_gate", "w_up", "w_down"):
-                    w[key + "_q"], w[key + "_s"] = quantize_rows(w[key])
+        quantized = (("w_gate", "w_up", "w_down") if self.fp8_mlp else ()) + \
+            (("wq", "wk", "wv") if self.fp8_qkv_lm else ())
+        for w in self.layers:
+            for key in quantized:
+                w[key + "_q"], w[key + "_s"] = quantize_rows(w[key])
+        if self.fp8_qkv_lm:
+            self.lm_head_q, self.lm_head_s = quantize_rows(self.lm_head)
 
     def _store(self, a: np.ndarray) -> np.ndarray:
-        return bf16_round(a) if self.mode in ("faithful", "fp8") else a
+        return bf16_round(a) if self.mode != "pure" else a
 
     # ------------------------------------------------------------------
     def attention(self, q, k_blk, v_blk, kp, vp, causal_blk: int = 0):
@@ -191,10 +199,16 @@ class OracleModel:
         for li, w in enumerate(self.layers):
             if n_layers is not None and li == n_layers:
                 return {"x": x}
-            h = self._store(rms_norm(x, w["ln1"], cfg["rms_eps"]))
-            q = h @ w["wq"].T
-            k = h @ w["wk"].T
-            v = h @ w["wv"].T
+            if self.fp8_qkv_lm:
+                h = rms_norm(x, w["ln1"], cfg["rms_eps"])
+                q = fp8_matmul(h, w["wq_q"], w["wq_s"])
+                k = fp8_matmul(h, w["wk_q"], w["wk_s"])
+                v = fp8_matmul(h, w["wv_q"], w["wv_s"])
+            else:
+                h = self._store(rms_norm(x, w["ln1"], cfg["rms_eps"]))
+                q = h @ w["wq"].T
+                k = h @ w["wk"].T
+                v = h @ w["wv"].T
             if cfg["qkv_bias"]:
                 q, k, v = q + w["bq"], k + w["bk"], v + w["bv"]
             q = q.reshape(nb, L, Hq, d).transpose(0, 2, 1, 3)
@@ -207,7 +221,7 @@ class OracleModel:
             o = self.attention(q, k, v, cache.k[li, :, :P], cache.v[li, :, :P], causal_blk)
             o = self._store(o.transpose(0, 2, 1, 3).reshape(nb, L, Hq * d))
             x = x + o @ w["wo"].T
-            if self.mode == "fp8":
+            if self.fp8_mlp:
                 h2 = rms_norm(x, w["ln2"], cfg["rms_eps"])
                 a = self._store(silu(fp8_matmul(h2, w["w_gate_q"], w["w_gate_s"]))
                                 * fp8_matmul(h2, w["w_up_q"], w["w_up_s"]))
@@ -218,8 +232,12 @@ class OracleModel:
                 x = x + a @ w["w_down"].T
         if n_layers is not None:
             return {"x": x}
-        hf = self._store(rms_norm(x, self.final_norm, cfg["rms_eps"]))
-        logits = hf @ self.lm_head.T                                    # [nb, L, V]
+        if self.fp8_qkv_lm:
+            hf = rms_norm(x, self.final_norm, cfg["rms_eps"])
+            logits = fp8_matmul(hf, self.lm_head_q, self.lm_head_s)    # [nb, L, V]
+        else:
+            hf = self._store(rms_norm(x, self.final_norm, cfg["rms_eps"]))
+            logits = hf @ self.lm_head.T                                # [nb, L, V]
         conf, pred = confidence(logits, cfg["mask_id"])
         out = {"conf": conf, "pred": pred, "k": ks, "v": vs}
         if keep_hidden:

@@ -64,8 +64,9 @@ class Setup:
 
     def __init__(self, cfgname: str, P: int, L: int, k: int, max_len=None, precision="bf16",
                  **over):
-        """precision "fp8_mlp": the GPU model's MLP in FP8, and self.faith the
-        oracle's FP8 mode (the same quantisation points)."""
+        """precision "fp8_mlp" / "fp8": the GPU model's MLP (and QKV and LM head)
+        in FP8, and self.faith the oracle's mode of the same name (the same
+        quantisation points)."""
         import paper_2512_16229_amd as lp
         self.lp = lp
         self.cfg = synth.config(cfgname, **over)
@@ -76,7 +77,7 @@ class Setup:
         self.kv = lp.KV(self.model, self.max_len, k + 1, L)
         self.prompt = synth.prompt(self.cfg, P)
         self.pure = OracleModel(self.cfg, self.w, "pure")
-        self.faith = OracleModel(self.cfg, self.w, "fp8" if precision == "fp8_mlp" else "faithful")
+        self.faith = OracleModel(self.cfg, self.w, "faithful" if precision == "bf16" else precision)
         self.cache_p = KVCache(self.cfg, self.max_len)
         self.cache_f = KVCache(self.cfg, self.max_len)
         if P:

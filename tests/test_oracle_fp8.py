@@ -101,7 +101,7 @@ def test_fp8_mode_forward():
     cfg = synth.config("tiny")
     w = synth.model_weights(cfg)
     f = OracleModel(cfg, w, "faithful")
-    q = OracleModel(cfg, w, "fp8")
+    q = OracleModel(cfg, w, "fp8_mlp")
     layer = q.layers[0]
     for key in ("w_gate", "w_up", "w_down"):
         assert np.all(np.abs(layer[key + "_q"]) <= E4M3_MAX)
@@ -122,6 +122,31 @@ def test_fp8_mode_forward():
 @pytest.mark.parametrize("k", [0, 3])
 def test_fp8_mode_decodes(k):
     cfg = synth.config("tiny")
-    q = OracleModel(cfg, synth.model_weights(cfg), "fp8")
+    q = OracleModel(cfg, synth.model_weights(cfg), "fp8_mlp")
     res = lopa.decode(q, synth.prompt(cfg, 32).numpy(), 32, 16, k, 0.9)
+    assert len(res["tokens"]) == 32 and not np.any(res["tokens"] == cfg["mask_id"])
+
+
+def test_fp8_full_mode_quantizes_qkv_and_lm_head():
+    """The "fp8" mode adds the QKV projection and the LM head: their weights
+    dequantise to the bf16 weights within the E4M3 step, the LM head's logits
+    are the quantised product of the final-normed rows, and the output
+    projection keeps its bf16 weights."""
+    cfg = synth.config("tiny")
+    w = synth.model_weights(cfg)
+    f = OracleModel(cfg, w, "faithful")
+    q = OracleModel(cfg, w, "fp8")
+    for key in ("wq", "wk", "wv"):
+        l0, f0 = q.layers[0], f.layers[0]
+        err = np.abs(l0[key + "_q"] * l0[key + "_s"][:, None] - f0[key])
+        assert np.all(err <= 2.0 ** -4 * np.abs(f0[key]) + 2.0 ** -10 * l0[key + "_s"][:, None] * 1.0001)
+    assert "wo_q" not in q.layers[0]
+    err = np.abs(q.lm_head_q * q.lm_head_s[:, None] - f.lm_head)
+    assert np.all(err <= 2.0 ** -4 * np.abs(f.lm_head) + 2.0 ** -10 * q.lm_head_s[:, None] * 1.0001)
+    cache = KVCache(cfg, 48)
+    bt = np.full((2, 16), cfg["mask_id"])
+    out = q.forward_block(bt, 0, cache, keep_hidden=True)
+    np.testing.assert_allclose(out["logits"], fp8_matmul(out["hidden"], q.lm_head_q, q.lm_head_s),
+                               rtol=0, atol=1e-12)
+    res = lopa.decode(q, synth.prompt(cfg, 32).numpy(), 32, 16, 3, 0.9)
     assert len(res["tokens"]) == 32 and not np.any(res["tokens"] == cfg["mask_id"])
