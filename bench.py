@@ -288,13 +288,14 @@ def e2e_window_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7,
             "forwards": out["forwards"], "iterations": out["iterations"], "seconds": round(t, 4)}
 
 
-def fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, steps, warmup):
-    """The same verify step (the block's first iteration, replayed) with the MLP
-    projections in W8A8 E4M3: a second model from the same weights; ms/step,
+def fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, steps, warmup, precision):
+    """The same verify step (the block's first iteration, replayed) with the
+    projections of `precision` in W8A8 E4M3 ("fp8_mlp": gate / up / down; "fp8":
+    also QKV and the LM head): a second model from the same weights; ms/step,
     branch-tokens/s and per-kind times."""
     import torch
     nb, dev = k + 1, "cuda"
-    model = lp.Model(cfg, w, precision="fp8_mlp")
+    model = lp.Model(cfg, w, precision=precision)
     kv = lp.KV(model, P + L, nb, L)
     dec = lp.Decoder(model, kv, L, k, tau)
     assert dec.prefill(synth.prompt(cfg, P, device=dev)) == P
@@ -331,8 +332,12 @@ def fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, steps, warmup):
     torch.cuda.synchronize()
     prof = kv.profile_read()
     kv.profile(())
-    out = {"workload": "the headline step with gate / up / down in W8A8 E4M3 (per-channel weight "
-                       "and per-row activation scales); attention, QKV / O and the LM head bf16",
+    what = ("gate / up / down" if precision == "fp8_mlp"
+            else "QKV, gate / up / down and the LM head")
+    rest = ("attention, QKV / O and the LM head bf16" if precision == "fp8_mlp"
+            else "attention and the output projection bf16")
+    out = {"workload": f"the headline step with {what} in W8A8 E4M3 (per-channel weight "
+                       f"and per-row activation scales); {rest}",
            "ms_per_step": round(ms, 4), "branch_tokens_per_s": round(nb * L / (ms * 1e-3), 1),
            "kernel_ms_per_step": {kd: round(t / steps, 4) for kd, (t, n) in prof.items()}}
     del dec, kv, model
@@ -353,10 +358,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=4)
     ap.add_argument("--no-e2e", action="store_true", help="skip the end-to-end decode run")
-    ap.add_argument("--precision", default="bf16", choices=["bf16", "fp8_mlp"],
+    ap.add_argument("--precision", default="bf16", choices=["bf16", "fp8_mlp", "fp8"],
                     help="projection precision of the timed model (the headline is bf16; "
-                         "fp8_mlp: gate / up / down in W8A8 E4M3)")
-    ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 MLP step figures")
+                         "fp8_mlp: gate / up / down in W8A8 E4M3; fp8: also QKV and the LM head)")
+    ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 step figures")
     ap.add_argument("--attn-ranges", type=int, default=-1,
                     help="attention path of the timed steps: -1 library choice, 0 per-(head, "
                          "branch), n >= 1 shared prefix in about n key ranges")
@@ -492,7 +497,8 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16" if args.precision == "bf16" else "bf16 + fp8(e4m3) MLP", "data": "synthetic",
+        "dtype": {"bf16": "bf16", "fp8_mlp": "bf16 + fp8(e4m3) MLP",
+                  "fp8": "bf16 + fp8(e4m3) QKV/MLP/LM head"}[args.precision], "data": "synthetic",
         "config": {"workload": (f"LoPA verify step, {args.config} shape ({cfg['layers']}L H{cfg['hidden']} "
                                 f"{cfg['heads']}q/{cfg['kv_heads']}kv d{cfg['head_dim']} F{cfg['ffn']} "
                                 f"V{cfg['vocab']}), random bf16 weights, prefix {P}, block {L}, "
@@ -530,11 +536,13 @@ def main():
                 f"{result['e2e_window_decode_block_causal']['tokens_per_s']} tok/s, "
                 f"TPF {result['e2e_window_decode_block_causal']['tokens_per_forward']}")
     if args.precision == "bf16" and not args.no_fp8:
-        t0 = time.perf_counter()
-        result["fp8_mlp_step"] = fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, args.steps,
-                                                  args.warmup)
-        log(f"FP8 MLP step in {time.perf_counter() - t0:.1f}s: "
-            f"{result['fp8_mlp_step']['ms_per_step']} ms/step")
+        for prec in ("fp8_mlp", "fp8"):
+            t0 = time.perf_counter()
+            key = prec + "_step"
+            result[key] = fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, args.steps,
+                                           args.warmup, prec)
+            log(f"{prec} step in {time.perf_counter() - t0:.1f}s: "
+                f"{result[key]['ms_per_step']} ms/step")
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         try:

@@ -48,7 +48,7 @@ EXPORTS = ["lopa_model_create", "lopa_model_create_ex", "lopa_model_destroy", "l
            "lopa_kv_attention_plan", "lopa_kv_profile",
            "lopa_kv_profile_read"]
 METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
-PRECISIONS = {"bf16": 0, "fp8_mlp": 1}
+PRECISIONS = {"bf16": 0, "fp8_mlp": 1, "fp8": 2}
 PROF_KINDS = ["qkv", "attn", "oproj", "gateup", "down", "lmhead", "norm", "merge"]
 
 

@@ -54,7 +54,7 @@ int dalloc(DevBuf& b, size_t bytes, std::vector<void*>& owned) {
 
 // Packed weights: [blocks of 16 output features][K / 64][2][64][8] bf16.
 struct LayerPack {
-  uint16_t* qkv;   // blk_qkv blocks, K = H
+  uint16_t* qkv;   // blk_qkv blocks, K = H (models with a bf16 QKV projection)
   uint16_t* o;     // blk_h blocks, K = Hq * d
   uint16_t* gu;    // blk_gu blocks (gate / up pairs), K = H (bf16 models)
   uint16_t* down;  // blk_h blocks, K = round256(F) (bf16 models)
@@ -64,6 +64,9 @@ struct LayerPack {
   uint8_t* down8 = nullptr;
   float* sw_gu = nullptr;
   float* sw_down = nullptr;
+  // FP8 models: E4M3 QKV weights (K = round512(H)) and their column scales
+  uint8_t* qkv8 = nullptr;
+  float* sw_qkv = nullptr;
   float* bias;     // [Nqkv] or null
   float* ln1;
   float* ln2;
@@ -173,11 +176,14 @@ struct lopa_model {
   int blk_qkv = 0, blk_h = 0, blk_gu = 0, blk_lm = 0;  // packed 16-column blocks
   int nb_qkv = 0, nb_o = 0, nb_down = 0, nb_lm = 0;     // tile widths of the packed weights
   int tiles_lm = 0;                                     // LM-head column tiles
-  int fp8 = 0;                                          // LOPA_PRECISION_FP8_MLP
+  int fp8 = 0;       // FP8 MLP (LOPA_PRECISION_FP8_MLP and LOPA_PRECISION_FP8)
+  int fp8_qkv_lm = 0;  // FP8 QKV projection and LM head too (LOPA_PRECISION_FP8)
   int nb_down8 = 0;                                     // FP8 down-projection tile width
   std::vector<LayerPack> layers;
   uint16_t* embed = nullptr;
-  uint16_t* lm = nullptr;
+  uint16_t* lm = nullptr;   // bf16 LM head (when not FP8)
+  uint8_t* lm8 = nullptr;   // FP8 LM head, K = round512(H), and its column scales
+  float* sw_lm = nullptr;
   float* final_norm = nullptr;
   std::vector<void*> owned;
   ~lopa_model() {
@@ -195,8 +201,9 @@ struct lopa_kv {
   float* x = nullptr;           // [mp_max][H]
   uint16_t* abuf = nullptr;     // packed [mp_max][H]
   uint16_t* fbuf = nullptr;     // packed [mp_max][round256(F)], padding columns zero
-  // FP8 MLP models: the FP8 operands of gate/up and down (padding columns zero)
-  // and their per-row scales
+  // FP8 models: the FP8 operands of gate/up and down (padding columns zero)
+  // and their per-row scales; a8_gu / sa_gu also carry the normed rows into
+  // the QKV projection and the LM head of LOPA_PRECISION_FP8 models
   uint8_t* a8_gu = nullptr;     // packed [mp_max][round512(H)] E4M3
   uint8_t* a8_dn = nullptr;     // packed [mp_max][round512(F)] E4M3
   float* sa_gu = nullptr;
@@ -260,12 +267,13 @@ struct StepPlans {
 StepPlans step_plans(const lopa_model* m, int MT) {
   const lopa_model_cfg& c = m->cfg;
   StepPlans p;
-  p.qkv = plan_gemm(EPI_QKV, m->blk_qkv, c.hidden / 64, MT, m->num_cu, m->nb_qkv);
+  const int kch = m->fp8_qkv_lm ? round512(c.hidden) / 128 : c.hidden / 64;
+  p.qkv = plan_gemm(EPI_QKV, m->blk_qkv, kch, MT, m->num_cu, m->nb_qkv);
   p.o = plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu, m->nb_o);
   p.gu = plan_gemm(EPI_SWIGLU, m->blk_gu, c.hidden / 64, MT, m->num_cu, 10);
   p.down = m->fp8 ? plan_gemm(EPI_RESID, m->blk_h, round512(c.ffn) / 128, MT, m->num_cu, m->nb_down8)
                   : plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu, m->nb_down);
-  p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, c.hidden / 64, MT, m->num_cu, m->nb_lm);
+  p.lm = plan_gemm(EPI_LMHEAD, m->blk_lm, kch, MT, m->num_cu, m->nb_lm);
   return p;
 }
 }  // namespace
@@ -314,7 +322,8 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, void
 int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, int32_t precision,
                          void* stream, lopa_model** out) {
   if (!out) return fail(LOPA_EINVAL, "out is null");
-  if (precision != LOPA_PRECISION_BF16 && precision != LOPA_PRECISION_FP8_MLP)
+  if (precision != LOPA_PRECISION_BF16 && precision != LOPA_PRECISION_FP8_MLP &&
+      precision != LOPA_PRECISION_FP8)
     return fail(LOPA_EINVAL, "unknown precision %d", precision);
   *out = nullptr;
   int rc = check_cfg(cfg);
@@ -369,7 +378,8 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
   m->nb_qkv = plan_gemm(EPI_QKV, m->blk_qkv, H / 64, 1, m->num_cu, 0).nb;
   m->nb_o = plan_gemm(EPI_RESID, m->blk_h, c.heads * d / 64, 1, m->num_cu, 0).nb;
   m->nb_down = plan_gemm(EPI_RESID, m->blk_h, round256(F) / 64, 1, m->num_cu, 0).nb;
-  m->fp8 = precision == LOPA_PRECISION_FP8_MLP;
+  m->fp8 = precision == LOPA_PRECISION_FP8_MLP || precision == LOPA_PRECISION_FP8;
+  m->fp8_qkv_lm = precision == LOPA_PRECISION_FP8;
   m->nb_down8 = plan_gemm(EPI_RESID, m->blk_h, round512(F) / 128, 1, m->num_cu, 0).nb;
   auto alloc16 = [&](uint16_t** p, size_t elems) -> int {
     DevBuf b;
@@ -393,18 +403,25 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
     *p = (uint8_t*)b.p;
     return r;
   };
-  // FP8: per source row scaling pairs (gate, up: F rows; down: H rows)
+  // FP8: per source row scaling pairs (gate, up: F rows; down: H rows; q, k,
+  // v: n_qkv rows; LM head: V rows)
   float *inv_g = nullptr, *sc_g = nullptr, *inv_u = nullptr, *sc_u = nullptr, *inv_d = nullptr,
-        *sc_d = nullptr;
+        *sc_d = nullptr, *inv_q = nullptr, *sc_q = nullptr;
   if (m->fp8 && ((rc = allocf(&inv_g, F)) || (rc = allocf(&sc_g, F)) || (rc = allocf(&inv_u, F)) ||
                  (rc = allocf(&sc_u, F)) || (rc = allocf(&inv_d, H)) || (rc = allocf(&sc_d, H))))
     return bail(rc);
+  if (m->fp8_qkv_lm &&
+      ((rc = allocf(&inv_q, std::max(m->n_qkv, V))) || (rc = allocf(&sc_q, std::max(m->n_qkv, V)))))
+    return bail(rc);
+  const int nq = c.heads * d, nk = c.kv_heads * d;
   m->layers.resize(c.layers);
   for (int l = 0; l < c.layers; ++l) {
     const lopa_layer_weights& lw = w->layers[l];
     LayerPack& p = m->layers[l];
-    p.gu = p.down = nullptr;
-    if ((rc = alloc16(&p.qkv, wsize(m->blk_qkv, H))) ||
+    p.gu = p.down = p.qkv = nullptr;
+    if ((!m->fp8_qkv_lm && (rc = alloc16(&p.qkv, wsize(m->blk_qkv, H)))) ||
+        (m->fp8_qkv_lm && (rc = alloc8(&p.qkv8, wsize(m->blk_qkv, KPH8)))) ||
+        (m->fp8_qkv_lm && (rc = allocf(&p.sw_qkv, (size_t)m->blk_qkv * 16))) ||
         (rc = alloc16(&p.o, wsize(m->blk_h, c.heads * d))) ||
         (!m->fp8 && (rc = alloc16(&p.gu, wsize(m->blk_gu, H)))) ||
         (!m->fp8 && (rc = alloc16(&p.down, wsize(m->blk_h, FP)))) ||
@@ -420,8 +437,16 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
     const uint16_t* wk = (const uint16_t*)lw.wk;
     const uint16_t* wv = (const uint16_t*)lw.wv;
     hipError_t e;
-    if ((e = launch_repack(wq, c.heads * d, wk, c.kv_heads * d, wv, c.kv_heads * d, H, H,
-                           m->blk_qkv, m->nb_qkv, 0, p.qkv, s)) != hipSuccess ||
+    if ((!m->fp8_qkv_lm &&
+         (e = launch_repack(wq, nq, wk, nk, wv, nk, H, H, m->blk_qkv, m->nb_qkv, 0, p.qkv, s)) !=
+             hipSuccess) ||
+        (m->fp8_qkv_lm &&
+         ((e = launch_rowscale(wq, nq, H, inv_q, sc_q, s)) != hipSuccess ||
+          (e = launch_rowscale(wk, nk, H, inv_q + nq, sc_q + nq, s)) != hipSuccess ||
+          (e = launch_rowscale(wv, nk, H, inv_q + nq + nk, sc_q + nq + nk, s)) != hipSuccess ||
+          (e = launch_repack8(wq, inv_q, sc_q, nq, wk, inv_q + nq, sc_q + nq, nk, wv,
+                              inv_q + nq + nk, sc_q + nq + nk, nk, H, KPH8, m->blk_qkv,
+                              m->nb_qkv, 0, p.qkv8, p.sw_qkv, s)) != hipSuccess)) ||
         (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
                            c.heads * d, m->blk_h, m->nb_o, 0, p.o, s)) != hipSuccess ||
         (!m->fp8 &&
@@ -435,11 +460,11 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
           (e = launch_rowscale((const uint16_t*)lw.w_up, F, H, inv_u, sc_u, s)) != hipSuccess ||
           (e = launch_rowscale((const uint16_t*)lw.w_down, H, F, inv_d, sc_d, s)) != hipSuccess ||
           (e = launch_repack8((const uint16_t*)lw.w_gate, inv_g, sc_g, F,
-                              (const uint16_t*)lw.w_up, inv_u, sc_u, F, H, KPH8, m->blk_gu, 10, 1,
-                              p.gu8, p.sw_gu, s)) != hipSuccess ||
+                              (const uint16_t*)lw.w_up, inv_u, sc_u, F, nullptr, nullptr, nullptr,
+                              0, H, KPH8, m->blk_gu, 10, 1, p.gu8, p.sw_gu, s)) != hipSuccess ||
           (e = launch_repack8((const uint16_t*)lw.w_down, inv_d, sc_d, H, nullptr, nullptr,
-                              nullptr, 0, F, KPF8, m->blk_h, m->nb_down8, 0, p.down8, p.sw_down,
-                              s)) != hipSuccess)) ||
+                              nullptr, 0, nullptr, nullptr, nullptr, 0, F, KPF8, m->blk_h,
+                              m->nb_down8, 0, p.down8, p.sw_down, s)) != hipSuccess)) ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln1, p.ln1, H, s)) != hipSuccess ||
         (e = launch_bf16_to_f32((const uint16_t*)lw.ln2, p.ln2, H, s)) != hipSuccess)
       return bail(fail(LOPA_EHIP, "layer %d repack: %s", l, hipGetErrorString(e)));
@@ -453,13 +478,20 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
     }
   }
   if ((rc = alloc16(&m->embed, (size_t)V * H)) ||
-      (rc = alloc16(&m->lm, wsize(m->blk_lm, H))) ||
+      (!m->fp8_qkv_lm && (rc = alloc16(&m->lm, wsize(m->blk_lm, H)))) ||
+      (m->fp8_qkv_lm && (rc = alloc8(&m->lm8, wsize(m->blk_lm, KPH8)))) ||
+      (m->fp8_qkv_lm && (rc = allocf(&m->sw_lm, (size_t)m->blk_lm * 16))) ||
       (rc = allocf(&m->final_norm, H)))
     return bail(rc);
   hipError_t e;
+  const uint16_t* lmw = (const uint16_t*)w->lm_head;
   if ((e = hipMemcpyAsync(m->embed, w->embed, (size_t)V * H * 2, hipMemcpyDeviceToDevice, s)) ||
-      (e = launch_repack((const uint16_t*)w->lm_head, V, nullptr, 0, nullptr, 0, H, H,
-                         m->blk_lm, m->nb_lm, 0, m->lm, s)) ||
+      (!m->fp8_qkv_lm && (e = launch_repack(lmw, V, nullptr, 0, nullptr, 0, H, H, m->blk_lm,
+                                            m->nb_lm, 0, m->lm, s))) ||
+      (m->fp8_qkv_lm &&
+       ((e = launch_rowscale(lmw, V, H, inv_q, sc_q, s)) ||
+        (e = launch_repack8(lmw, inv_q, sc_q, V, nullptr, nullptr, nullptr, 0, nullptr, nullptr,
+                            nullptr, 0, H, KPH8, m->blk_lm, m->nb_lm, 0, m->lm8, m->sw_lm, s)))) ||
       (e = launch_bf16_to_f32((const uint16_t*)w->final_norm, m->final_norm, H, s)) ||
       (e = hipStreamSynchronize(s)))
     return bail(fail(LOPA_EHIP, "model create: %s", hipGetErrorString(e)));
@@ -546,7 +578,9 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
       (e = hipMemset(kv->cache, 0, cache_e * 2)) || (e = hipMemset(kv->staging, 0, stag_e * 2)) ||
       (e = hipMemset(kv->abuf, 0, rows * H * 2)) || (e = hipMemset(kv->fbuf, 0, rows * FP * 2)) ||
       (m->fp8 && ((e = hipMemset(kv->a8_gu, 0, rows * round512(H))) ||
-                  (e = hipMemset(kv->a8_dn, 0, rows * round512(F))))) ||
+                  (e = hipMemset(kv->a8_dn, 0, rows * round512(F))) ||
+                  (e = hipMemset(kv->sa_gu, 0, rows * 4)) ||
+                  (e = hipMemset(kv->sa_dn, 0, rows * 4)))) ||
       (e = hipDeviceSynchronize()))
     return bail(fail(LOPA_EHIP, "kv create: %s", hipGetErrorString(e)));
   *out = kv;
@@ -617,10 +651,32 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.gcols = p.tiles * p.splits;
     return launch_gemm(epi, g, s);
   };
+  // FP8 operands: A, W E4M3 with K = KP (a multiple of 512), row / column scales
+  auto gemm8 = [&](int epi, const uint8_t* A, const uint8_t* W, int N, int KP, const float* sa,
+                   const float* sw, const GemmPlan& pl) {
+    g.A = (const uint16_t*)A;
+    g.W = (const uint16_t*)W;
+    g.N = N;
+    g.KC = KP / 128;
+    g.f8 = 1;
+    g.sa = sa;
+    g.sw = sw;
+    g.rowmax = kv->rowmax_dn;
+    g.nb = pl.nb;
+    g.tiles = pl.tiles;
+    g.splits = pl.splits;
+    g.gcols = pl.tiles * pl.splits;
+    return launch_gemm(epi, g, s);
+  };
+  const bool f8x = m->fp8_qkv_lm;  // the normed rows go to the QKV / LM head in E4M3
 
   { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-  HIP_TRY(launch_embed_norm(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M, Mp, H, kv->x,
-                            kv->abuf, s)); }
+    if (f8x)
+      HIP_TRY(launch_embed_norm8(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M,
+                                 Mp, H, kv->x, kv->a8_gu, kv->sa_gu, s));
+    else
+      HIP_TRY(launch_embed_norm(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M,
+                                Mp, H, kv->x, kv->abuf, s)); }
   AttnArgs at{};
   at.q = kv->qbuf;
   at.staging = kv->staging;
@@ -662,7 +718,11 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.vlds = kv->vlds;
     g.P = prefix_len;
     { ProfScope ps_(kv, LOPA_PROF_QKV, s);
-      HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, H, plan.qkv)); }
+      if (f8x)
+        HIP_TRY(gemm8(EPI_QKV, kv->a8_gu, p.qkv8, m->n_qkv, round512(H), kv->sa_gu, p.sw_qkv,
+                      plan.qkv));
+      else
+        HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, H, plan.qkv)); }
     at.layer = l;
     at.kcache = kv->cache + ((size_t)l * 2 + 0) * c.kv_heads * d * kv->vld;
     at.vcache = kv->cache + ((size_t)l * 2 + 1) * c.kv_heads * d * kv->vld;
@@ -679,22 +739,6 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
         HIP_TRY(launch_resnorm8(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
                                 c.rms_eps, M, Mp, H, kv->x, kv->a8_gu, kv->sa_gu, kv->rowmax_dn,
                                 s)); }
-      auto gemm8 = [&](int epi, const uint8_t* A, const uint8_t* W, int N, int KP,
-                       const float* sa, const float* sw, const GemmPlan& pl) {
-        g.A = (const uint16_t*)A;
-        g.W = (const uint16_t*)W;
-        g.N = N;
-        g.KC = KP / 128;
-        g.f8 = 1;
-        g.sa = sa;
-        g.sw = sw;
-        g.rowmax = kv->rowmax_dn;
-        g.nb = pl.nb;
-        g.tiles = pl.tiles;
-        g.splits = pl.splits;
-        g.gcols = pl.tiles * pl.splits;
-        return launch_gemm(epi, g, s);
-      };
       { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
         HIP_TRY(gemm8(EPI_SWIGLU, kv->a8_gu, p.gu8, 2 * F, round512(H), kv->sa_gu, p.sw_gu,
                       plan.gu)); }
@@ -713,9 +757,14 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
         HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, round256(F), plan.down)); }
     }
     const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
+    const int dsplits = plan.down.splits > 1 ? plan.down.splits : 0;
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-      HIP_TRY(launch_resnorm(kv->partials, plan.down.splits > 1 ? plan.down.splits : 0, next_w,
-                             c.rms_eps, M, Mp, H, kv->x, kv->abuf, s)); }
+      if (f8x)
+        HIP_TRY(launch_resnorm8(kv->partials, dsplits, next_w, c.rms_eps, M, Mp, H, kv->x,
+                                kv->a8_gu, kv->sa_gu, nullptr, s));
+      else
+        HIP_TRY(launch_resnorm(kv->partials, dsplits, next_w, c.rms_eps, M, Mp, H, kv->x,
+                               kv->abuf, s)); }
   }
   if (stop_layer >= 0) {
     HIP_TRY(hipMemcpyAsync(x_out, kv->x, (size_t)M * H * 4, hipMemcpyDeviceToDevice, s));
@@ -727,7 +776,11 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   g.vocab = c.vocab;
   g.mask_id = c.mask_id;
   { ProfScope ps_(kv, LOPA_PROF_LMHEAD, s);
-    HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, c.vocab, H, plan.lm)); }
+    if (f8x)
+      HIP_TRY(gemm8(EPI_LMHEAD, kv->a8_gu, m->lm8, c.vocab, round512(H), kv->sa_gu, m->sw_lm,
+                    plan.lm));
+    else
+      HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, c.vocab, H, plan.lm)); }
   { ProfScope ps_(kv, LOPA_PROF_MERGE, s);
     HIP_TRY(launch_lm_merge(kv->pm, kv->ps, kv->pi, M, m->tiles_lm, conf, pred, s)); }
   kv->last_nb = n_branches;

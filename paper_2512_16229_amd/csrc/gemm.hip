@@ -449,7 +449,8 @@ constexpr int BPF = 4;
 template <int EPI, int NB, bool F8>
 __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_kernel(GemmArgs a) {
   using SM = GemmSmem<EPI, NB>;
-  static_assert(!F8 || EPI == EPI_SWIGLU || EPI == EPI_RESID, "FP8 epilogues");
+  // FP8: the epilogues of RESID and LMHEAD take scaled sums (f8_scale), SWIGLU
+  // scales inside its epilogue, QKV in the fix-up (its partial sums are raw)
   constexpr int OPS = 8 + NB / 2;  // vector memory operations per wavefront per iteration
   static_assert(NB % 2 == 0 && 3 * OPS <= 63, "tile width");
   static_assert(RING == 6 && LEAD == 4, "pair schedule");
@@ -515,7 +516,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
     }
     GEMM_DRAIN();
     mfma_settle();
-    if constexpr (F8 && EPI == EPI_RESID) f8_scale<NB>(a, acc, t_lo, row0, lane);
+    if constexpr (F8 && (EPI == EPI_RESID || EPI == EPI_LMHEAD)) f8_scale<NB>(a, acc, t_lo, row0, lane);
     if (EPI != EPI_QKV && a.splits == 1) {
       if constexpr (EPI == EPI_LMHEAD) {
         lds_barrier();  // the ring becomes the reduction area (every copy has landed)
@@ -588,10 +589,18 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
     const int base = sect == 0 ? 0 : (sect == 1 ? qcols : qcols + kcols);
     const int head = (n - base) / D, dim = (n - base) % D;
     if (sect < 2 && dim >= HD) return;  // written with its rotation partner
-    const f32x4 v1 = sum(tile, nb);
+    f32x4 v1 = sum(tile, nb);
     f32x4 v2 = {0.f, 0.f, 0.f, 0.f};
     const int n2 = n + HD;
     if (sect < 2) v2 = sum((n2 >> 4) / NB, (n2 >> 4) % NB);
+    if (a.f8) {  // FP8 operands: the sums of products times the row and column scales
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float sr = r0 + j < a.M ? a.sa[r0 + j] : 0.f;
+        v1[j] = v1[j] * sr * a.sw[n];
+        if (sect < 2) v2[j] = v2[j] * sr * a.sw[n2];
+      }
+    }
     const float b1 = a.bias ? a.bias[n] : 0.f;
     const float b2 = (a.bias && sect < 2) ? a.bias[n2] : 0.f;
 #pragma unroll
@@ -664,11 +673,15 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
     return hipErrorInvalidValue;
   if (a.gcols != a.tiles * a.splits) return hipErrorInvalidValue;
   if (a.f8) {
-    if (!a.sa || !a.sw) return hipErrorInvalidValue;
+    if (!a.sa || !a.sw || (epi == EPI_SWIGLU && !a.rowmax)) return hipErrorInvalidValue;
     switch (epi * 16 + a.nb) {
+      case EPI_QKV * 16 + 4: return launch_nb<EPI_QKV, 4, true>(a, s);
+      case EPI_QKV * 16 + 8: return launch_nb<EPI_QKV, 8, true>(a, s);
       case EPI_RESID * 16 + 4: return launch_nb<EPI_RESID, 4, true>(a, s);
       case EPI_RESID * 16 + 8: return launch_nb<EPI_RESID, 8, true>(a, s);
       case EPI_SWIGLU * 16 + 10: return launch_nb<EPI_SWIGLU, 10, true>(a, s);
+      case EPI_LMHEAD * 16 + 8: return launch_nb<EPI_LMHEAD, 8, true>(a, s);
+      case EPI_LMHEAD * 16 + 10: return launch_nb<EPI_LMHEAD, 10, true>(a, s);
     }
     return hipErrorInvalidValue;
   }

@@ -65,9 +65,13 @@ hipError_t launch_quant_rows8(const uint16_t* a, int K, int M, int Mp, const uin
 hipError_t launch_rowscale(const uint16_t* w, int rows, int K, float* inv, float* scale,
                            hipStream_t s);
 hipError_t launch_repack8(const uint16_t* s0, const float* inv0, const float* sc0, int r0,
-                          const uint16_t* s1, const float* inv1, const float* sc1, int r1, int K,
+                          const uint16_t* s1, const float* inv1, const float* sc1, int r1,
+                          const uint16_t* s2, const float* inv2, const float* sc2, int r2, int K,
                           int KP, int blocks, int nb, int pairs, uint8_t* dst, float* sw,
                           hipStream_t s);
+hipError_t launch_embed_norm8(const int32_t* tokens, const uint16_t* embed, int vocab,
+                              const float* w, float eps, int M, int Mp, int H, float* x,
+                              uint8_t* a8, float* sa, hipStream_t s);
 // merge per-tile softmax partials into conf / pred
 hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, int M,
                            int tiles, float* conf, int32_t* pred, hipStream_t s);
@@ -103,7 +107,7 @@ struct GemmArgs {
   float* ps;           // [M][tiles] sum of exp(l - max)
   int32_t* pi;         // [M][tiles] argmax
   int vocab, mask_id;
-  // FP8 operands (f8 != 0; EPI_SWIGLU and EPI_RESID): A and W hold E4M3 bytes in
+  // FP8 operands (f8 != 0; any epilogue): A and W hold E4M3 bytes in
   // the same fragment layout (a 16-byte lane slot holds 16 values of K instead
   // of 8), KC counts 128-wide k-chunks, and the epilogue scales the fp32 sum
   // of products by sa[row] * sw[packed column]

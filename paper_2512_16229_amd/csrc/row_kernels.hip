@@ -222,13 +222,17 @@ __global__ __launch_bounds__(256) void rowscale_kernel(const uint16_t* __restric
 // bytes) per lane slot, i.e. unit (block, kk) of k-chunk kc holds columns
 // kc 128 + kk 64 + 16 (lane / 16) .. + 15; the values are the bf16 weights
 // times their row's inverse scale. sw gets the scale of every packed column
-// (0 for padding columns). One or two sources (pairs: alternating blocks).
+// (0 for padding columns). Up to three sources: concatenated rows, or (pairs)
+// alternating blocks of the first two.
 __global__ __launch_bounds__(256) void repack8_kernel(const uint16_t* __restrict__ s0,
                                                       const float* __restrict__ inv0,
                                                       const float* __restrict__ sc0, int r0,
                                                       const uint16_t* __restrict__ s1,
                                                       const float* __restrict__ inv1,
                                                       const float* __restrict__ sc1, int r1,
+                                                      const uint16_t* __restrict__ s2,
+                                                      const float* __restrict__ inv2,
+                                                      const float* __restrict__ sc2, int r2,
                                                       int K, int KC, int NB, int64_t total,
                                                       int pairs, uint8_t* __restrict__ dst,
                                                       float* __restrict__ sw) {
@@ -251,8 +255,10 @@ __global__ __launch_bounds__(256) void repack8_kernel(const uint16_t* __restrict
     if (!(blk & 1)) { if (row < r0) { src = s0; si = inv0[row]; sc = sc0[row]; } }
     else { if (row < r1) { src = s1; si = inv1[row]; sc = sc1[row]; } }
   } else {
-    row = blk * 16 + (lane & 15);
-    if (row < r0) { src = s0; si = inv0[row]; sc = sc0[row]; }
+    const int n = blk * 16 + (lane & 15);
+    if (n < r0) { src = s0; row = n; si = inv0[row]; sc = sc0[row]; }
+    else if (n < r0 + r1) { src = s1; row = n - r0; si = inv1[row]; sc = sc1[row]; }
+    else if (n < r0 + r1 + r2) { src = s2; row = n - r0 - r1; si = inv2[row]; sc = sc2[row]; }
   }
   uint32_t b[4] = {0u, 0u, 0u, 0u};
   if (src && k0 < K) {
@@ -386,6 +392,23 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
   return hipGetLastError();
 }
 
+hipError_t launch_embed_norm8(const int32_t* tokens, const uint16_t* embed, int vocab,
+                              const float* w, float eps, int M, int Mp, int H, float* x,
+                              uint8_t* a8, float* sa, hipStream_t s) {
+  if (H % 256 || H > 1024 * CPT || !a8 || !sa) return hipErrorInvalidValue;
+#define EMBEDNORM8(NG)                                                                    \
+  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, true>), dim3(M), dim3(256), 0, s, tokens,  \
+                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, nullptr, a8, sa, nullptr)
+  switch (resnorm_groups(H)) {
+    case 1: EMBEDNORM8(1); break;
+    case 2: EMBEDNORM8(2); break;
+    case 4: EMBEDNORM8(4); break;
+    default: EMBEDNORM8(8); break;
+  }
+#undef EMBEDNORM8
+  return hipGetLastError();
+}
+
 namespace {
 template <int NG, bool A8>
 void resnorm_ng(const float* part, int S, const float* w, float eps, int M, int Mp, int H,
@@ -450,14 +473,16 @@ hipError_t launch_rowscale(const uint16_t* w, int rows, int K, float* inv, float
 }
 
 hipError_t launch_repack8(const uint16_t* s0, const float* inv0, const float* sc0, int r0,
-                          const uint16_t* s1, const float* inv1, const float* sc1, int r1, int K,
+                          const uint16_t* s1, const float* inv1, const float* sc1, int r1,
+                          const uint16_t* s2, const float* inv2, const float* sc2, int r2, int K,
                           int KP, int blocks, int nb, int pairs, uint8_t* dst, float* sw,
                           hipStream_t s) {
   if (KP % 512 || KP < K || K % 16 || nb < 1 || blocks % nb) return hipErrorInvalidValue;
   const int KC = KP / 128;
   const int64_t total = (int64_t)blocks * KC * 2 * 64;
   hipLaunchKernelGGL(repack8_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, s0,
-                     inv0, sc0, r0, s1, inv1, sc1, r1, K, KC, nb, total, pairs, dst, sw);
+                     inv0, sc0, r0, s1, inv1, sc1, r1, s2, inv2, sc2, r2, K, KC, nb, total, pairs,
+                     dst, sw);
   return hipGetLastError();
 }
 

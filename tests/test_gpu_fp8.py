@@ -1,6 +1,7 @@
-"""GPU parity of the FP8 MLP model mode (lopa_model_create_ex with
-LOPA_PRECISION_FP8_MLP: gate / up / down in W8A8 E4M3) against the oracle's
-FP8 mode, which quantises at the same points with the same rules.
+"""GPU parity of the FP8 model modes (lopa_model_create_ex with
+LOPA_PRECISION_FP8_MLP: gate / up / down in W8A8 E4M3; LOPA_PRECISION_FP8:
+also the QKV projection and the LM head) against the oracle's FP8 modes, which
+quantise at the same points with the same rules.
 
 Teacher-forced prefix (the oracle's cache rows), then: confidences within the
 case's own tolerance (2e-2, or a few times the oracle's own sensitivity to
@@ -13,6 +14,8 @@ import pytest
 import torch
 
 from gpu_util import Setup, conf_tolerance, log, near_tie, vocab_margin
+from oracle.fp8 import E4M3_MAX, e4m3_round, fp8_matmul
+from oracle.model import confidence, rms_norm
 
 pytestmark = pytest.mark.gpu
 
@@ -20,6 +23,7 @@ pytestmark = pytest.mark.gpu
 # attention path (P = 300, 16 branches)
 CASES = [("tiny", 64, 16, 3), ("small", 100, 32, 7), ("small128", 40, 16, 2), ("tiny", 23, 7, 2),
          ("small", 300, 32, 15)]
+PRECS = ["fp8_mlp", "fp8"]
 
 
 def _tokens(s, nb, L, seed):
@@ -43,10 +47,11 @@ def _sensitivity(s, bt, P, base_conf, seed=0):
     return float(np.max(np.abs(s.faith.forward_block(bt, P, c2)["conf"] - base_conf)))
 
 
+@pytest.mark.parametrize("prec", PRECS)
 @pytest.mark.parametrize("cfgname,P,L,k", CASES)
-def test_fp8_forward_parity(cfgname, P, L, k):
-    log(f"fp8 forward {cfgname} P={P} L={L} k={k}")
-    s = Setup(cfgname, P, L, k, precision="fp8_mlp")
+def test_fp8_forward_parity(cfgname, P, L, k, prec):
+    log(f"{prec} forward {cfgname} P={P} L={L} k={k}")
+    s = Setup(cfgname, P, L, k, precision=prec)
     s.load_oracle_cache()
     nb, mask = k + 1, s.cfg["mask_id"]
     bt = _tokens(s, nb, L, P + L + k)
@@ -64,18 +69,45 @@ def test_fp8_forward_parity(cfgname, P, L, k):
     assert not np.any(pred == mask)
 
 
+def _tie_free_tokens(s, n, seed):
+    """n tokens whose first-layer RMSNorm rows have no value at an E4M3 tie.
+    With bf16 embeddings and unit norm weights, 448 x_i / max|x| is often
+    exactly halfway between two E4M3 values; each side's float32 roundings
+    then pick either neighbour, both correct readings of the rule, and one
+    such code moves its row by about a percent. Rows without ties have one
+    correct code sequence."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for t in rng.permutation(s.cfg["vocab"] - 1):
+        if t == s.cfg["mask_id"]:
+            continue
+        h = rms_norm(s.faith.embed[t][None], s.faith.layers[0]["ln1"], s.cfg["rms_eps"])[0]
+        v = np.abs(h) * (E4M3_MAX / np.max(np.abs(h)))
+        if np.array_equal(e4m3_round(v * (1 - 1e-6)), e4m3_round(v * (1 + 1e-6))):
+            out.append(t)
+            if len(out) == n:
+                return np.array(out)
+    raise AssertionError("not enough tie-free tokens")
+
+
+@pytest.mark.parametrize("prec", PRECS)
 @pytest.mark.parametrize("cfgname", ["tiny", "small", "small128"])
-def test_fp8_first_layer_single_key(cfgname):
+def test_fp8_first_layer_single_key(cfgname, prec):
     """No prefix and one-row blocks: every row attends to itself only, so the
-    bf16 parts agree with the oracle to float32 rounding and the first layer's
-    residual stream isolates the FP8 MLP (weight repack, per-row scales of the
-    RMSNorm output, FP8 GEMMs, SwiGLU, requantisation, down projection). The
-    bound covers the rare whole-code changes that bf16 rounding-order
-    differences of the SwiGLU output cause in its requantisation; a wrong
-    layout or scale would be off by order one."""
-    s = Setup(cfgname, 0, 1, 7, precision="fp8_mlp")
+    first layer's residual stream isolates the FP8 projections (weight repack,
+    per-row scales of the RMSNorm outputs, FP8 GEMMs, the QKV fix-up's
+    scaling, SwiGLU, requantisation, down projection); a wrong layout or scale
+    would be off by order one. fp8_mlp: the bf16 parts agree with the oracle to
+    float32 rounding, and the bound covers the rare whole-code changes that
+    bf16 rounding-order differences of the SwiGLU output cause in its
+    requantisation. fp8: V comes from float32 sums of the FP8 QKV and differs
+    from the oracle's by bf16 steps in a few elements (checked on its own in
+    test_fp8_qkv_staging); those move the RMSNorm row by about 1e-4, which
+    flips about one gate/up operand code in every other row, each moving its
+    row's MLP output by about a percent, hence the wider bound."""
+    s = Setup(cfgname, 0, 1, 7, precision=prec)
     nb = 8
-    bt = np.random.default_rng(1).integers(0, s.cfg["vocab"] - 1, (nb, 1))
+    bt = _tie_free_tokens(s, nb, 1).reshape(nb, 1)
     btd = torch.tensor(bt, dtype=torch.int32, device="cuda").reshape(-1)
     x = torch.empty(nb * s.cfg["hidden"], dtype=torch.float32, device="cuda")
     s.lp.lopa_debug_hidden(s.model, s.kv, 0, btd, nb, 1, 1, x)
@@ -83,15 +115,78 @@ def test_fp8_first_layer_single_key(cfgname):
     g = x.view(nb, 1, -1).cpu().numpy().astype(np.float64)
     r = s.faith.forward_block(bt, 0, s.cache_f, n_layers=1)["x"]
     rel = np.linalg.norm(g - r) / np.linalg.norm(r)
-    log(f"fp8 first layer, single key, {cfgname}: rel-L2 {rel:.2e}")
-    assert rel < 2e-3
+    log(f"{prec} first layer, single key, {cfgname}: rel-L2 {rel:.2e}")
+    assert rel < (2e-3 if prec == "fp8_mlp" else 1e-2)
 
 
+@pytest.mark.parametrize("cfgname", ["tiny", "small", "small128"])
+def test_fp8_qkv_staging(cfgname):
+    """LOPA_PRECISION_FP8: the first layer's K and V (the FP8 QKV GEMM, its
+    per-column and per-row scales applied in the fix-up, bias, RoPE) against
+    the oracle's, from token rows without E4M3 ties: every element within two
+    bf16 steps of the oracle's bf16 value (float32 against float64 sums of the
+    same exact products), and the relative L2 error at the bf16 level."""
+    L, nb = 16, 4
+    s = Setup(cfgname, 0, L, nb - 1, precision="fp8")
+    bt = _tie_free_tokens(s, nb * L, 2).reshape(nb, L)
+    s.gpu_forward(bt)
+    rf = s.faith.forward_block(bt, 0, s.cache_f)
+    worst = 0.0
+    for j in range(nb):
+        ks, vs = s.kv.read_staging(j, 0, L)
+        for g, r in ((ks, rf["k"][j, 0]), (vs, rf["v"][j, 0])):
+            g = g.float().cpu().numpy().astype(np.float64)
+            # a bf16 step at the value, with a floor for values that are small
+            # by cancellation (the float32 sums' error scales with the terms)
+            mag = np.maximum(np.abs(r), 2.0 ** -8 * np.max(np.abs(r)))
+            step = 2.0 ** (np.floor(np.log2(mag)) - 7)
+            ratio = np.abs(g - r) / step
+            i = np.unravel_index(np.argmax(ratio), ratio.shape)
+            assert ratio[i] <= 2, f"branch {j}: {g[i]} vs {r[i]} at {i}"
+            worst = max(worst, np.linalg.norm(g - r) / np.linalg.norm(r))
+    log(f"fp8 QKV staging {cfgname}: worst rel-L2 {worst:.2e}")
+    assert worst < 2e-3
+
+
+@pytest.mark.parametrize("cfgname,P,L,k", [("tiny", 64, 16, 3), ("small", 100, 32, 7)])
+def test_fp8_lm_head_from_gpu_hidden(cfgname, P, L, k):
+    """LOPA_PRECISION_FP8: the final RMSNorm, the FP8 LM head and the
+    confidences, isolated: the oracle takes the GPU's own residual stream after
+    the last layer (lopa_debug_hidden) through its final norm, per-row E4M3
+    quantisation and quantised product; the confidences agree to float32
+    accumulation accuracy and the predictions wherever the top two logits are
+    not within that accuracy."""
+    s = Setup(cfgname, P, L, k, precision="fp8")
+    s.load_oracle_cache()
+    nb = k + 1
+    bt = _tokens(s, nb, L, 4)
+    conf, pred = s.gpu_forward(bt)
+    btd = torch.tensor(bt, dtype=torch.int32, device="cuda").reshape(-1)
+    x = torch.empty(nb * L * s.cfg["hidden"], dtype=torch.float32, device="cuda")
+    s.lp.lopa_debug_hidden(s.model, s.kv, P, btd, nb, L, s.cfg["layers"], x)
+    torch.cuda.synchronize()
+    xg = x.view(nb, L, -1).cpu().numpy().astype(np.float64)
+    o = s.faith
+    hf = rms_norm(xg, o.final_norm, s.cfg["rms_eps"])
+    logits = fp8_matmul(hf, o.lm_head_q, o.lm_head_s)
+    rc, rp = confidence(logits, s.cfg["mask_id"])
+    # rows with a value within float32 distance of an E4M3 tie may take either code
+    v = np.abs(hf) * (E4M3_MAX / np.max(np.abs(hf), axis=-1, keepdims=True))
+    clear = np.all(e4m3_round(v * (1 - 1e-5)) == e4m3_round(v * (1 + 1e-5)), axis=-1)
+    e = np.max(np.abs(conf - rc)[clear])
+    decided = (vocab_margin(logits, s.cfg["mask_id"]) >= 1e-3) & clear
+    log(f"fp8 LM head from the GPU's hidden rows {cfgname}: max|dconf| {e:.2e}, "
+        f"rows without ties {clear.mean():.2f}, decided {decided.mean():.2f}")
+    assert clear.mean() > 0.8 and e < 2e-4
+    assert decided.mean() > 0.7 and np.array_equal(pred[decided], rp[decided])
+
+
+@pytest.mark.parametrize("prec", PRECS)
 @pytest.mark.parametrize("cfgname,P,L,k", [("tiny", 64, 16, 3), ("small", 50, 48, 3)])
-def test_fp8_batch_invariance(cfgname, P, L, k):
+def test_fp8_batch_invariance(cfgname, P, L, k, prec):
     """Per-row activation scales keep rows independent: identical branches give
     identical bits, permuted branches permuted bits, repeats the same bits."""
-    s = Setup(cfgname, P, L, k, precision="fp8_mlp")
+    s = Setup(cfgname, P, L, k, precision=prec)
     s.load_oracle_cache()
     nb = k + 1
     bt = _tokens(s, nb, L, 9)
@@ -105,17 +200,18 @@ def test_fp8_batch_invariance(cfgname, P, L, k):
     assert np.array_equal(cp, c1[perm]) and np.array_equal(pp, p1[perm])
 
 
-def test_fp8_decode_block():
+@pytest.mark.parametrize("prec", PRECS)
+def test_fp8_decode_block(prec):
     """The FP8 model through the decode loop: the block fills within L
     iterations and nothing stays masked (the oracle's FP8 trajectory is logged
     beside it)."""
     from oracle import lopa
-    s = Setup("tiny", 64, 16, 3, precision="fp8_mlp")
+    s = Setup("tiny", 64, 16, 3, precision=prec)
     dec = s.gpu_prefill()
     s.load_oracle_cache()
     iters = dec.decode_block(64)
     toks = dec.tokens.cpu().numpy()
     assert 1 <= iters <= 16 and not np.any(toks == s.cfg["mask_id"])
     otoks, oiters, _ = lopa.decode_block(s.faith, s.cache_f.copy(), 64, 16, 3, np.float32(0.9))
-    log(f"  fp8 decode: {iters} iterations (oracle {oiters}), "
+    log(f"  {prec} decode: {iters} iterations (oracle {oiters}), "
         f"{int(np.sum(toks == otoks))}/16 tokens equal")
