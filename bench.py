@@ -26,13 +26,15 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 MFMA_BF16_PEAK_TFS = 2500.0  # dense bf16
 
 
-def step_bytes(cfg, P, L, nb):
+def step_bytes(cfg, P, L, nb, precision="bf16"):
     """Algorithmic HBM bytes of one verify step (weights once, prefix K/V once,
-    staging written, commit copy)."""
+    staging written, commit copy); FP8 modes: one byte per quantised weight."""
     H, F, V, d = cfg["hidden"], cfg["ffn"], cfg["vocab"], cfg["head_dim"]
     Hq, Hkv, Ly = cfg["heads"], cfg["kv_heads"], cfg["layers"]
-    layer_w = (H * (Hq + 2 * Hkv) * d + Hq * d * H + 2 * F * H + F * H) * 2
-    w = Ly * layer_w + V * H * 2
+    bq = 1 if precision == "fp8" else 2       # QKV and LM head
+    bm = 1 if precision != "bf16" else 2      # gate / up / down
+    layer_w = H * (Hq + 2 * Hkv) * d * bq + Hq * d * H * 2 + 3 * F * H * bm
+    w = Ly * layer_w + V * H * bq
     kv_prefix = Ly * 2 * Hkv * P * d * 2
     staging = nb * Ly * 2 * Hkv * L * d * 2
     commit = 2 * Ly * 2 * Hkv * L * d * 2
@@ -48,11 +50,15 @@ def step_flops(cfg, P, L, nb):
     return gemm + attn
 
 
-def gateup_launch_bytes(cfg, M):
+def gateup_launch_bytes(cfg, M, precision="bf16"):
     """Algorithmic bytes of one gate/up + SwiGLU launch: its weights, the
-    normalised activations read once, the SwiGLU output written once."""
+    normalised activations read once, the SwiGLU output (bf16) written once.
+    FP8 modes: one byte per weight and activation value, plus the per-channel
+    and per-row fp32 scales and the row maxima written for the requantisation."""
     H, F = cfg["hidden"], cfg["ffn"]
-    return 2 * F * H * 2 + M * H * 2 + M * F * 2
+    if precision == "bf16":
+        return 2 * F * H * 2 + M * H * 2 + M * F * 2
+    return 2 * F * H + M * H + M * F * 2 + 2 * F * 4 + M * 4 + M * 4
 
 
 def gemm_source_sha():
@@ -486,9 +492,9 @@ def main():
     copy_gbs = 5 * 2 * src.numel() * 2 / (e0.elapsed_time(e1) * 1e-3) / 1e9
     del src, dst
 
-    gu_bytes = gateup_launch_bytes(cfg, M)
+    gu_bytes = gateup_launch_bytes(cfg, M, args.precision)
     achieved = gu_bytes / (gu_ms * 1e-3) / 1e9
-    sb = step_bytes(cfg, P, L, nb)
+    sb = step_bytes(cfg, P, L, nb, args.precision)
     sf = step_flops(cfg, P, L, nb)
     result = {
         "metric": "LoPA verify-step ms & branch-tokens/s (7B shape, k=7); % HBM/MFMA roofline",
@@ -509,7 +515,8 @@ def main():
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic(os.path.join(ROOT, "profiles",
-                                                              "gemm_swiglu_dream7b_hbm_traffic.md")),
+                                                              "gemm_swiglu_dream7b_hbm_traffic.md"))
+                     if args.precision == "bf16" else None,
                      "bytes_per_launch": gu_bytes, "avg_launch_ms": round(gu_ms, 4),
                      "copy_gbs_measured": round(copy_gbs, 1),
                      "frac_of_measured_copy": round(achieved / copy_gbs, 4)},
