@@ -104,6 +104,22 @@ def test_model_create_null_weights(lp):
     assert lp.lib.lopa_model_create(C.byref(cfg), C.byref(w), None, C.byref(h)) == -1
 
 
+@pytest.mark.parametrize("precision", [-1, 3, 7])
+def test_model_create_unknown_precision(lp, precision):
+    """lopa_model_create_ex rejects a precision outside {BF16, FP8_MLP, FP8}
+    before any HIP call; the known ones pass that check and stop at the null
+    weight pointers."""
+    cfg = lp.lopa_model_cfg(2, 256, 4, 2, 64, 704, 1024, 1023, 1e-6, 1e4, 1)
+    h = C.c_void_p()
+    w = lp.lopa_weight_ptrs()
+    rc = lp.lib.lopa_model_create_ex(C.byref(cfg), C.byref(w), precision, None, C.byref(h))
+    assert rc == -1 and "precision" in lp.lib.lopa_last_error().decode()
+    assert not h.value
+    for known in lp.PRECISIONS.values():
+        rc = lp.lib.lopa_model_create_ex(C.byref(cfg), C.byref(w), known, None, C.byref(h))
+        assert rc == -1 and "weight pointer" in lp.lib.lopa_last_error().decode()
+
+
 def test_kv_create_validation(lp):
     h = C.c_void_p()
     assert lp.lib.lopa_kv_create(None, 128, 8, 32, C.byref(h)) == -1
