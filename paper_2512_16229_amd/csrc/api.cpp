@@ -249,7 +249,11 @@ struct ProfScope {
     if (!(kv->prof_mask & (1 << kind))) return;
     if (kv->ev_used == kv->ev_pool.size()) {
       lopa_kv::Ev e{kind, nullptr, nullptr};
-      if (hipEventCreate(&e.a) != hipSuccess || hipEventCreate(&e.b) != hipSuccess) return;
+      // timing only: no system-scope fence (its cache write-back would be
+      // timed with the launch and slow the work after it)
+      if (hipEventCreateWithFlags(&e.a, hipEventDisableSystemFence) != hipSuccess ||
+          hipEventCreateWithFlags(&e.b, hipEventDisableSystemFence) != hipSuccess)
+        return;
       kv->ev_pool.push_back(e);
     }
     ev = &kv->ev_pool[kv->ev_used++];
