@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -647,6 +648,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.W = W;
     g.N = N;
     g.KC = K / 64;
+    g.rot = epi == EPI_SWIGLU || epi == EPI_RESID;
     g.f8 = 0;
     g.sa = g.sw = nullptr;
     g.nb = p.nb;
@@ -662,6 +664,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.W = (const uint16_t*)W;
     g.N = N;
     g.KC = KP / 128;
+    g.rot = epi == EPI_SWIGLU || epi == EPI_RESID;
     g.f8 = 1;
     g.sa = sa;
     g.sw = sw;

@@ -323,9 +323,10 @@ __device__ __forceinline__ void lm_epilogue(const GemmArgs& a, f32x4 (&acc)[4][N
 // slot `slot` (NB / 2 copies of 1 KiB per wavefront). Weight layout
 // [tile][KC][NB][2][64 lanes][8]: the chunk of iteration (tile, kc) is one
 // contiguous run, and so is a tile's whole k-range. The addresses advance by
-// one k-chunk per issued iteration (a_next, w_next); past the last k-chunk the
-// last one is issued again (an L2 hit), which keeps every wait count and the
-// loop branch-free.
+// one k-chunk per issued iteration (a_next, w_next), from kc0 to the end of the
+// range and then from its start (rotation, GemmArgs::rot); after the last of
+// the range's iterations the last chunk is issued again (an L2 hit), which keeps
+// every wait count constant and the loop branch-free.
 #define GEMM_ISSUE_A(set, half)                                                          \
   load_frag4(set[4 * (half) + 0], set[4 * (half) + 1], set[4 * (half) + 2],              \
              set[4 * (half) + 3], a_next + (half) * a_half, voff)
@@ -334,10 +335,17 @@ __device__ __forceinline__ void lm_epilogue(const GemmArgs& a, f32x4 (&acc)[4][N
             lds_wave + (uint32_t)(slot) * (uint32_t)SM::CHUNK + (uint32_t)(r) * 4096u)
 #define GEMM_ADVANCE_LOAD()                                                              \
   {                                                                                      \
-    if (lk + 1 < kc_end) {                                                               \
-      ++lk;                                                                              \
-      a_next += a_kstep;                                                                 \
-      w_next += SM::CHUNK;                                                               \
+    if (li + 1 < n_it) {                                                                 \
+      ++li;                                                                              \
+      if (lk + 1 < kc_end) {                                                             \
+        ++lk;                                                                            \
+        a_next += a_kstep;                                                               \
+        w_next += SM::CHUNK;                                                             \
+      } else {                                                                           \
+        lk = kc_beg;                                                                     \
+        a_next -= (int64_t)(n_it - 1) * a_kstep;                                         \
+        w_next -= (int64_t)(n_it - 1) * SM::CHUNK;                                       \
+      }                                                                                  \
     }                                                                                    \
   }
 #define GEMM_ISSUE(set, slot)                                                            \
@@ -484,12 +492,15 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   // activation fragment (kb, rb) at A + ((kb RB) + rb) KiB: k-chunk kc, half h
   // of this wavefront's first row block -> a_next + h a_half
   const int64_t a_half = (int64_t)RB * 1024, a_kstep = 2 * a_half;
-  const char* a_next = (const char*)a.A + ((int64_t)2 * kc_beg * RB + rb0) * 1024;
+  const int n_it = kc_end - kc_beg;  // iterations of this workgroup
+  const int kc0 = kc_beg + (a.rot ? 4 * (t_lo % nq) : 0);  // first k-chunk
+  const char* a_next = (const char*)a.A + ((int64_t)2 * kc0 * RB + rb0) * 1024;
   // weight chunk (tile, kc) at W + (tile KC + kc) CHUNK; its 1 KiB unit u (block
   // u / 2, k-half u % 2) at + u KiB; wavefront wv copies units 4 r + wv
-  const char* w_next = (const char*)a.W + ((int64_t)t_lo * KC + kc_beg) * SM::CHUNK + wv * 1024;
+  const char* w_next = (const char*)a.W + ((int64_t)t_lo * KC + kc0) * SM::CHUNK + wv * 1024;
   const uint32_t lds_wave = sW_base + (uint32_t)wv * 1024u;
-  int lk = kc_beg;  // k-chunk of the next iteration to issue
+  int lk = kc0;  // k-chunk of the next iteration to issue
+  int li = 0;    // iterations issued before it
 
   f32x4 acc[4][NB];
   u32x4 a0[8], a1[8], a2[8], a3[8];

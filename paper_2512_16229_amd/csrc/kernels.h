@@ -112,6 +112,11 @@ struct GemmArgs {
   // of 8), KC counts 128-wide k-chunks, and the epilogue scales the fp32 sum
   // of products by sa[row] * sw[packed column]
   int f8;
+  // rot != 0: each workgroup starts its k-range at chunk 4 (column tile mod
+  // quads) and wraps, so the workgroups of an XCD, which otherwise advance in
+  // step, read different slices of the shared activation operand at a time
+  // (spread over the L2 channels); the sums of a column stay in one fixed order
+  int rot;
   const float* sa;     // [Mp] per-row activation scales
   const float* sw;     // [blocks * 16] per-column weight scales, packed column order
   uint32_t* rowmax;    // FP8 EPI_SWIGLU: atomic maximum of |output| (float bits) per row,
