@@ -337,11 +337,15 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     }
   };
 
-  // the first two tiles are in flight while Q is loaded
+  // the first two tiles are in flight while Q is loaded. The query heads of
+  // one KV head start at different tiles of the range (and wrap), so that
+  // their workgroups do not request the same K/V lines at the same moment.
   const int n = t_hi - t_lo;
+  const int rot = n > 0 ? (h % (a.Hq / a.Hkv)) % n : 0;
+  auto tile_of = [&](int i) { const int r = i + rot; return t_lo + (r < n ? r : r - n); };
   if (n > 0) {
-    issue(t_lo, 0);
-    issue(t_lo + (n > 1 ? 1 : 0), 1);
+    issue(tile_of(0), 0);
+    issue(tile_of(n > 1 ? 1 : 0), 1);
   }
 
   // Q^T operand: query column 16 qb + c16, dims 32 kk + 8 g .. +8
@@ -374,12 +378,12 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     attn_wait_vmcnt<SM::OPS>();
     AttnTile<D> x;
     tile_fetch<D>(smem + (wv * 2 + (i & 1)) * TileLds<D>::TILE, lane, x);
-    const int t = t_lo + i;
+    const int t = tile_of(i);
     const bool pre = t < pt;
     tile_update<D, QB, false>(x, qf, m, l, o, (pre ? t : t - pt) * KT, pre ? P : L, sl2, g,
                               pre ? 0 : a.cblk, 0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    issue(t_lo + (i + 2 < n ? i + 2 : n - 1), i & 1);
+    issue(tile_of(i + 2 < n ? i + 2 : n - 1), i & 1);
   }
   attn_wait_vmcnt<0>();  // the ring is reused for the merge
   __syncthreads();
