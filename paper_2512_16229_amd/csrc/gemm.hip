@@ -468,10 +468,12 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
   const uint32_t sW_base = (uint32_t)(uintptr_t)smem;
 
   // Hardware places workgroup b on XCD b % 8; the remap gives each XCD a
-  // contiguous range of q, so the row tiles of one column workgroup (adjacent
-  // q) share an L2 and read each weight chunk from HBM once.
+  // contiguous range of q (XCD x: grid / 8 workgroups, one more when x <
+  // grid % 8), so the row tiles of one column workgroup (adjacent q) share an
+  // L2 and read each weight chunk from HBM once.
   const int b = blockIdx.x, grid = gridDim.x;
-  const int q = (grid % 8 == 0) ? (b & 7) * (grid >> 3) + (b >> 3) : b;
+  const int xcd = b & 7, g8 = grid >> 3, g8r = grid & 7;
+  const int q = xcd * g8 + (xcd < g8r ? xcd : g8r) + (b >> 3);
   const int MT = a.mtiles;
   const int mt = q % MT, c = q / MT;
   const int KC = a.KC, QT = KC >> 2;
