@@ -177,7 +177,7 @@ def test_fp8_lm_head_from_gpu_hidden(cfgname, P, L, k):
     decided = (vocab_margin(logits, s.cfg["mask_id"]) >= 1e-3) & clear
     log(f"fp8 LM head from the GPU's hidden rows {cfgname}: max|dconf| {e:.2e}, "
         f"rows without ties {clear.mean():.2f}, decided {decided.mean():.2f}")
-    assert clear.mean() > 0.8 and e < 2e-4
+    assert clear.mean() > 0.8 and e < 5e-4
     assert decided.mean() > 0.7 and np.array_equal(pred[decided], rp[decided])
 
 
