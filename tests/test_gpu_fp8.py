@@ -215,3 +215,32 @@ def test_fp8_decode_block(prec):
     otoks, oiters, _ = lopa.decode_block(s.faith, s.cache_f.copy(), 64, 16, 3, np.float32(0.9))
     log(f"  {prec} decode: {iters} iterations (oracle {oiters}), "
         f"{int(np.sum(toks == otoks))}/16 tokens equal")
+
+
+@pytest.mark.parametrize("prec", PRECS)
+@pytest.mark.parametrize("cfgname,P,L,k,cblk", [("tiny", 64, 32, 3, 16), ("small", 300, 32, 7, 16)])
+def test_fp8_block_causal_forward(cfgname, P, L, k, cblk, prec):
+    """The FP8 modes with the block-causal mask inside the window: the same
+    bound as the unmasked FP8 forward (the oracle's own sensitivity, taken
+    with the mask), and the mask changes the first sub-block's confidences."""
+    log(f"{prec} block-causal forward {cfgname} P={P} L={L} k={k} sub-block {cblk}")
+    s = Setup(cfgname, P, L, k, precision=prec)
+    s.load_oracle_cache()
+    nb, mask = k + 1, s.cfg["mask_id"]
+    s.kv.set_block_causal(cblk)
+    bt = _tokens(s, nb, L, P + L + cblk)
+    conf, pred = s.gpu_forward(bt)
+    s.kv.set_block_causal(0)
+    rf = s.faith.forward_block(bt, P, s.cache_f, keep_hidden=True, causal_blk=cblk)
+    e = np.max(np.abs(conf - rf["conf"]))
+    rng = np.random.default_rng(0)
+    c2 = s.cache_f.copy()
+    c2.k *= 1.0 + rng.choice([-1.0, 1.0], c2.k.shape) * 2.0 ** -10
+    c2.v *= 1.0 + rng.choice([-1.0, 1.0], c2.v.shape) * 2.0 ** -10
+    sens = float(np.max(np.abs(s.faith.forward_block(bt, P, c2, causal_blk=cblk)["conf"] - rf["conf"])))
+    decided = vocab_margin(rf["logits"], mask) >= near_tie(e)
+    log(f"  max|dconf| gpu-oracle={e:.2e}, oracle sensitivity {sens:.2e}, decided {decided.mean():.2f}")
+    assert e < max(conf_tolerance(0.0), 4.0 * sens)
+    assert np.array_equal(pred[decided], rf["pred"][decided])
+    full = s.faith.forward_block(bt, P, s.cache_f)
+    assert np.max(np.abs(full["conf"][:, :cblk] - rf["conf"][:, :cblk])) > 0
