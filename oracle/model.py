@@ -119,33 +119,66 @@ class KVCache:
 
 
 class OracleModel:
-    def __init__(self, cfg: dict, weights: dict, mode: str = "pure"):
+    def __init__(self, cfg: dict, weights: dict, mode: str = "pure", keep_layers=True,
+                 share=None, bf16_weights: bool = False):
+        """weights["layers"] may be any sequence of layer dicts (a lazy one for
+        the full-size shapes); each layer is converted on first use and kept
+        when keep_layers is True, or the keep_layers most recently used ones
+        when it is an int. share: a bf16-mode model built from the same
+        bf16-valued weights whose converted layers this one reuses (the same
+        float64 values: rounding a bf16 value to bf16 changes nothing).
+        bf16_weights: the caller's weights hold bf16 values already, so the
+        non-pure modes skip rounding them (the identity on such values)."""
         if mode not in ("pure", "faithful", "fp8_mlp", "fp8"):
             raise ValueError(mode)
         self.cfg, self.mode = cfg, mode
         self.fp8_mlp = mode in ("fp8_mlp", "fp8")
         self.fp8_qkv_lm = mode == "fp8"
-        r = bf16_round if mode != "pure" else (lambda a: a)
+        r = bf16_round if (mode != "pure" and not bf16_weights) else (lambda a: a)
+        self._r = r
         self.embed = r(_np(weights["embed"]))
         self.lm_head = r(_np(weights["lm_head"]))
         self.final_norm = _np(weights["final_norm"])
-        self.layers = []
-        for lw in weights["layers"]:
-            self.layers.append({k: (r(_np(v)) if k not in ("ln1", "ln2") else _np(v))
-                                for k, v in lw.items()})
-        quantized = (("w_gate", "w_up", "w_down") if self.fp8_mlp else ()) + \
-            (("wq", "wk", "wv") if self.fp8_qkv_lm else ())
-        for w in self.layers:
-            for key in quantized:
-                w[key + "_q"], w[key + "_s"] = quantize_rows(w[key])
+        self._raw_layers = weights["layers"]
+        self._keep = keep_layers
+        self._layers = {}
+        if share is not None:
+            if self.fp8_mlp or share.fp8_mlp:
+                raise ValueError("only bf16-mode models share converted layers")
+            self._layers = share._layers
         if self.fp8_qkv_lm:
             self.lm_head_q, self.lm_head_s = quantize_rows(self.lm_head)
+
+    @property
+    def layers(self) -> list:
+        """All layers, converted (and kept when keep_layers is true)."""
+        return [self.layer(i) for i in range(self.cfg["layers"])]
+
+    def layer(self, li: int) -> dict:
+        """Layer li's weights as the forward uses them (rounded to bf16 in the
+        non-pure modes, plus the E4M3 codes and scales of the quantised ones)."""
+        if li in self._layers:
+            w = self._layers.pop(li)
+            self._layers[li] = w          # most recently used last
+            return w
+        lw = self._raw_layers[li]
+        w = {k: (self._r(_np(v)) if k not in ("ln1", "ln2") else _np(v)) for k, v in lw.items()}
+        quantized = (("w_gate", "w_up", "w_down") if self.fp8_mlp else ()) + \
+            (("wq", "wk", "wv") if self.fp8_qkv_lm else ())
+        for key in quantized:
+            w[key + "_q"], w[key + "_s"] = quantize_rows(w[key])
+        if self._keep is True or (self._keep and not isinstance(self._keep, bool)):
+            self._layers[li] = w
+            if not isinstance(self._keep, bool):
+                while len(self._layers) > self._keep:
+                    self._layers.pop(next(iter(self._layers)))
+        return w
 
     def _store(self, a: np.ndarray) -> np.ndarray:
         return bf16_round(a) if self.mode != "pure" else a
 
     # ------------------------------------------------------------------
-    def attention(self, q, k_blk, v_blk, kp, vp, causal_blk: int = 0):
+    def attention(self, q, k_blk, v_blk, kp, vp, causal_blk: int = 0, trace=None):
         """Softmax attention of the block rows of each branch.
 
         q: [nb, Hq, L, d]; k_blk, v_blk: [nb, Hkv, L, d] (the branch's own block);
@@ -171,6 +204,8 @@ class OracleModel:
             e = np.exp(s - s.max(axis=-1, keepdims=True))
             den = e.sum(axis=-1, keepdims=True)
             num = self._store(e)
+            if trace is not None:
+                trace(num)
             P = kp.shape[1]
             o = (np.einsum("blp,pd->bld", num[..., :P], vp[g])
                  + np.einsum("blm,bmd->bld", num[..., P:], v_blk[:, g]))
@@ -178,27 +213,38 @@ class OracleModel:
         return out
 
     def forward_block(self, tokens, prefix_len: int, cache: KVCache, keep_hidden: bool = False,
-                      n_layers=None, causal_blk: int = 0):
+                      n_layers=None, causal_blk: int = 0, x_in=None, first_layer: int = 0,
+                      trace=None):
         """One batched forward of nb branches of the active block.
 
         tokens: int [nb, L] (block rows at positions prefix_len .. prefix_len+L-1).
         Returns dict: conf [nb, L] (float64), pred [nb, L] (int64), k / v
-        [nb, layers, Hkv, L, d] (post-RoPE block keys / values), and, if asked,
-        'hidden' [nb, L, H] (final-normed rows) and 'logits'. With n_layers set,
-        returns only {'x': residual stream after that many layers}. causal_blk:
-        the attention mask inside the block (see attention)."""
+        [nb, layers, Hkv, L, d] (post-RoPE block keys / values; layers before
+        first_layer are left zero), and, if asked, 'hidden' [nb, L, H]
+        (final-normed rows) and 'logits'. With n_layers set, returns only
+        {'x': residual stream after that many layers, 'k', 'v'}. causal_blk:
+        the attention mask inside the block (see attention).
+        x_in / first_layer: start from the given residual stream [nb, L, H]
+        before layer first_layer instead of the embeddings (a layer-by-layer
+        comparison feeds each layer the other side's input).
+        trace: a list that receives (name, layer, value) for every value the
+        non-pure modes round to bf16 (the GEMM inputs h, o, h2, a and the
+        final hf; q, k, v after bias / RoPE; the softmax numerators p) and for
+        the residual stream x after each layer (never rounded)."""
         cfg = self.cfg
         tokens = np.asarray(tokens, dtype=np.int64)
         nb, L = tokens.shape
         H, Hq, Hkv, d = cfg["hidden"], cfg["heads"], cfg["kv_heads"], cfg["head_dim"]
         P = int(prefix_len)
         ang = rope_angles(np.arange(P, P + L), d, cfg["rope_theta"])
-        x = self.embed[tokens]                                          # [nb, L, H]
-        ks = np.empty((nb, cfg["layers"], Hkv, L, d))
-        vs = np.empty_like(ks)
-        for li, w in enumerate(self.layers):
-            if n_layers is not None and li == n_layers:
-                return {"x": x}
+        x = self.embed[tokens] if x_in is None else np.array(x_in, dtype=np.float64)  # [nb, L, H]
+        ks = np.zeros((nb, cfg["layers"], Hkv, L, d))
+        vs = np.zeros_like(ks)
+        last = cfg["layers"] if n_layers is None else n_layers
+        tr = (lambda name, li, v: trace.append((name, li, v))) if trace is not None else \
+            (lambda name, li, v: None)
+        for li in range(first_layer, last):
+            w = self.layer(li)
             if self.fp8_qkv_lm:
                 h = rms_norm(x, w["ln1"], cfg["rms_eps"])
                 q = fp8_matmul(h, w["wq_q"], w["wq_s"])
@@ -206,6 +252,7 @@ class OracleModel:
                 v = fp8_matmul(h, w["wv_q"], w["wv_s"])
             else:
                 h = self._store(rms_norm(x, w["ln1"], cfg["rms_eps"]))
+                tr("h", li, h)
                 q = h @ w["wq"].T
                 k = h @ w["wk"].T
                 v = h @ w["wv"].T
@@ -217,9 +264,14 @@ class OracleModel:
             q = self._store(apply_rope(q, ang))
             k = self._store(apply_rope(k, ang))
             v = self._store(v)
+            tr("q", li, q)
+            tr("k", li, k)
+            tr("v", li, v)
             ks[:, li], vs[:, li] = k, v
-            o = self.attention(q, k, v, cache.k[li, :, :P], cache.v[li, :, :P], causal_blk)
+            o = self.attention(q, k, v, cache.k[li, :, :P], cache.v[li, :, :P], causal_blk,
+                               trace=(lambda p_, li=li: tr("p", li, p_)))
             o = self._store(o.transpose(0, 2, 1, 3).reshape(nb, L, Hq * d))
+            tr("o", li, o)
             x = x + o @ w["wo"].T
             if self.fp8_mlp:
                 h2 = rms_norm(x, w["ln2"], cfg["rms_eps"])
@@ -228,21 +280,35 @@ class OracleModel:
                 x = x + fp8_matmul(a, w["w_down_q"], w["w_down_s"])
             else:
                 h2 = self._store(rms_norm(x, w["ln2"], cfg["rms_eps"]))
+                tr("h2", li, h2)
                 a = self._store(silu(h2 @ w["w_gate"].T) * (h2 @ w["w_up"].T))
                 x = x + a @ w["w_down"].T
+            tr("a", li, a)
+            tr("x", li, x)
         if n_layers is not None:
-            return {"x": x}
+            return {"x": x, "k": ks, "v": vs}
+        out = self.lm_from_residual(x, trace=trace)
+        res = {"conf": out["conf"], "pred": out["pred"], "k": ks, "v": vs}
+        if keep_hidden:
+            res["hidden"], res["logits"] = out["hidden"], out["logits"]
+        return res
+
+    def lm_from_residual(self, x, trace=None) -> dict:
+        """Final RMSNorm, LM head and Conf / candidate (Sec. 3.1) of residual
+        rows x [..., H]: {'conf', 'pred', 'hidden' (the LM head's input),
+        'logits'}."""
+        cfg = self.cfg
+        x = np.asarray(x, dtype=np.float64)
         if self.fp8_qkv_lm:
             hf = rms_norm(x, self.final_norm, cfg["rms_eps"])
-            logits = fp8_matmul(hf, self.lm_head_q, self.lm_head_s)    # [nb, L, V]
+            logits = fp8_matmul(hf, self.lm_head_q, self.lm_head_s)
         else:
             hf = self._store(rms_norm(x, self.final_norm, cfg["rms_eps"]))
-            logits = hf @ self.lm_head.T                                # [nb, L, V]
+            if trace is not None:
+                trace.append(("hf", cfg["layers"], hf))
+            logits = hf @ self.lm_head.T
         conf, pred = confidence(logits, cfg["mask_id"])
-        out = {"conf": conf, "pred": pred, "k": ks, "v": vs}
-        if keep_hidden:
-            out["hidden"], out["logits"] = hf, logits
-        return out
+        return {"conf": conf, "pred": pred, "hidden": hf, "logits": logits}
 
 
 def confidence(logits: np.ndarray, mask_id: int):

@@ -170,3 +170,101 @@ def test_faithful_close_to_pure():
     assert np.max(np.abs(cf.k[:, :, :32] - cp.k[:, :, :32])) < 0.05 * np.max(np.abs(cp.k))
     # faithful stores bf16 values
     assert np.array_equal(bf16_round(cf.k[:, :, :32]), cf.k[:, :, :32])
+
+
+# ----------------------------------------------- bf16 rounding points (R16)
+# The faithful mode rounds to bf16 exactly where a bf16 implementation stores
+# a value: the input of every projection (h, o, h2, a and the final hf), q, k
+# and v after bias / RoPE, and the softmax numerators p that multiply V (taken
+# against the global row maximum). The residual stream x, the scores, the
+# softmax sums and the logits stay unrounded.
+ROUNDED = ("h", "q", "k", "v", "p", "o", "h2", "a")
+
+
+def _trace(mode, P=24, L=16, nb=3, seed=5):
+    cfg, w = _tiny()
+    w = synth.to_bf16_values(w)
+    m = OracleModel(cfg, w, mode)
+    cache = KVCache(cfg, P + L)
+    lopa.prefill(m, cache, synth.prompt(cfg, P).numpy(), L)
+    rng = np.random.default_rng(seed)
+    bt = np.where(rng.random((nb, L)) < 0.6, cfg["mask_id"], rng.integers(0, cfg["vocab"] - 1, (nb, L)))
+    tr = []
+    out = m.forward_block(bt, P, cache, trace=tr, keep_hidden=True)
+    return cfg, tr, out
+
+
+def _is_bf16(v):
+    return np.array_equal(bf16_round(v), v)
+
+
+def test_faithful_rounds_exactly_the_r16_points():
+    cfg, tr, out = _trace("faithful")
+    names = {}
+    for name, li, v in tr:
+        names.setdefault(name, set()).add(li)
+        if name in ROUNDED or name == "hf":
+            assert _is_bf16(v), f"{name} of layer {li} is not a bf16 value"
+        elif name == "x":
+            assert not _is_bf16(v), f"residual stream of layer {li} was rounded"
+    layers = set(range(cfg["layers"]))
+    for name in ROUNDED + ("x",):
+        assert names.get(name) == layers, f"{name} not traced in every layer"
+    assert names["hf"] == {cfg["layers"]}
+    # the numerators are taken against the global row maximum: each row's
+    # largest numerator is exactly exp(0) = 1
+    for name, li, v in tr:
+        if name == "p":
+            assert np.array_equal(v.max(axis=-1), np.ones(v.shape[:-1]))
+    # the logits are not rounded
+    assert not _is_bf16(out["logits"])
+
+
+def test_pure_rounds_nothing():
+    """The same trace in the pure mode has no bf16 values at those points, so a
+    rounding dropped from the faithful mode shows up in the test above."""
+    cfg, tr, _ = _trace("pure")
+    for name, li, v in tr:
+        if name in ROUNDED + ("hf", "x") and name != "p":
+            assert not _is_bf16(v), f"{name} of layer {li} is bf16 in the pure mode"
+        if name == "p":
+            off = v[v < 1.0]
+            assert not _is_bf16(off)
+
+
+def test_each_rounding_point_changes_the_result():
+    """Dropping any single rounding point of the faithful mode changes its
+    output (so every point is live, not only present in the trace)."""
+    cfg, w = _tiny()
+    w = synth.to_bf16_values(w)
+    P, L = 24, 16
+    base = OracleModel(cfg, w, "faithful")
+    cache = KVCache(cfg, P + L)
+    lopa.prefill(base, cache, synth.prompt(cfg, P).numpy(), L)
+    bt = np.full((2, L), cfg["mask_id"])
+    ref = base.forward_block(bt, P, cache, keep_hidden=True)
+    for skip in ROUNDED + ("hf",):
+        # every rounding goes through _store, in the order h, q, k, v, the
+        # numerators of each head, o, h2, a per layer, then hf: count the calls
+        # to check that order, then skip the one point under test
+        m = OracleModel(cfg, w, "faithful")
+        orig = m._store
+        order = []
+
+        def store(a, orig=orig, order=order):
+            order.append(a.shape)
+            return orig(a)
+        m._store = store
+        m.forward_block(bt, P, cache)
+        heads = cfg["heads"]
+        per_layer = ["h", "q", "k", "v"] + ["p"] * heads + ["o", "h2", "a"]
+        seq = per_layer * cfg["layers"] + ["hf"]
+        assert len(seq) == len(order)
+        m2 = OracleModel(cfg, w, "faithful")
+        it = iter(seq)
+
+        def store2(a, it=it, skip=skip, orig=m2._store):
+            return a if next(it) == skip else orig(a)
+        m2._store = store2
+        got = m2.forward_block(bt, P, cache, keep_hidden=True)
+        assert not np.array_equal(got["logits"], ref["logits"]), f"dropping {skip} changes nothing"
