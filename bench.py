@@ -368,9 +368,6 @@ def main():
                     help="projection precision of the timed model (the headline is bf16; "
                          "fp8_mlp: gate / up / down in W8A8 E4M3; fp8: also QKV and the LM head)")
     ap.add_argument("--no-fp8", action="store_true", help="skip the FP8 step figures")
-    ap.add_argument("--attn-ranges", type=int, default=-1,
-                    help="attention path of the timed steps: -1 library choice, 0 per-(head, "
-                         "branch), n >= 1 shared prefix in about n key ranges")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy 5 times (HBM counter calibration)")
     ap.add_argument("--hbm-counters", action="store_true",
@@ -420,10 +417,6 @@ def main():
     dec.init_block(P)
     torch.cuda.synchronize()
     log(f"prefill of {P} positions + initial forward in {time.perf_counter() - t0:.1f}s")
-    kv.set_attention_ranges(args.attn_ranges)
-    attn_plan = kv.attention_plan(P, nb, L)
-    log(f"attention: {attn_plan[0]} shared-prefix key ranges of {attn_plan[1]}"
-        if attn_plan[0] else "attention: per-(head, branch) path")
 
     i32 = dict(dtype=torch.int32, device=dev)
     tokens, conf, pred = dec.tokens.clone(), dec.conf.clone(), dec.pred.clone()
@@ -509,8 +502,7 @@ def main():
                                 f"{cfg['heads']}q/{cfg['kv_heads']}kv d{cfg['head_dim']} F{cfg['ffn']} "
                                 f"V{cfg['vocab']}), random bf16 weights, prefix {P}, block {L}, "
                                 f"k={k} ({nb} branches, {M} rows), tau {tau}"),
-                   "prefix": P, "block": L, "k": k, "rows": M,
-                   "attn_key_ranges": attn_plan[0]},
+                   "prefix": P, "block": L, "k": k, "rows": M},
         "roofline": {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (gemm_kernel<EPI_SWIGLU>)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),

@@ -135,8 +135,14 @@ void lopa_model_destroy(lopa_model* m);
 /* Static KV cache of max_len positions for one sequence (Sec. 3.4: a
  * pre-allocated static cache instead of dynamic objects), plus K/V staging for
  * max_branches branches of a block of up to max_block positions, plus the
- * verify workspace. Cache layout (bf16): K [layers][kv_heads][max_len][head_dim],
- * V likewise. Zero-initialised. */
+ * verify workspace. Cache layout (bf16, library-owned; read and write rows
+ * through lopa_kv_read / lopa_kv_write, which use [kv_heads][len][head_dim]
+ * whatever the internal layout): per layer and KV head, K as
+ * [max_len rounded up to 8][head_dim] (position-major) and V transposed as
+ * [head_dim][max_len rounded up to 8] (8 consecutive positions of one
+ * dimension are one aligned 16-byte run, the attention kernel's copy unit);
+ * layers outermost, then K / V, then KV heads. The per-branch staging has the
+ * same two layouts with max_block. Zero-initialised. */
 int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches,
                    int32_t max_block, lopa_kv** out);
 void lopa_kv_destroy(lopa_kv* kv);
@@ -273,24 +279,6 @@ int lopa_kv_write(lopa_kv* kv, int32_t layer, int32_t start, int32_t len,
 int lopa_kv_read_staging(const lopa_kv* kv, int32_t branch, int32_t layer,
                          void* k_dst, void* v_dst, void* stream);
 
-/* Attention path of lopa_verify_forward (Sec. 3.3: every branch attends to the
- * same committed prefix). With a long prefix and several branches the prefix
- * part runs once per query head for all branches: the prefix is cut into
- * n_ranges key ranges of range_len positions (a multiple of 32; the last may
- * be shorter), each range's unnormalised softmax state is written per row to a
- * workspace owned by the cache, and the per-branch block attention merges them
- * in range order. n_ranges = 0 is the per-(head, branch) path, which streams
- * the prefix once per branch. The two paths agree up to floating-point
- * rounding order.
- * lopa_kv_set_attention_ranges chooses the path for later calls: -1 (the
- * default) lets the library pick from the shapes, 0 forces the per-branch
- * path, n >= 1 forces about n ranges (fewer if the prefix has fewer 32-key
- * tiles; the per-branch path for an empty prefix). n above the device's limit
- * (max(1, floor(2 compute units / heads))) is LOPA_EINVAL.
- * lopa_kv_attention_plan reports the (n_ranges, range_len) a verify forward of
- * this shape would use; host only, nothing is launched. */
-int lopa_kv_set_attention_ranges(lopa_kv* kv, int32_t n_ranges);
-
 /* Attention mask inside the active block (window) of later verify forwards.
  * sub_block = 0 (the default): full attention among the block's L rows
  * (Sec. 3.3). sub_block = c > 0, a multiple of 16: the block-wise causal mask
@@ -303,8 +291,6 @@ int lopa_kv_set_attention_ranges(lopa_kv* kv, int32_t n_ranges);
  * L % c == 0 (LOPA_ESHAPE otherwise); L <= c is unmasked. sub_block negative or
  * not a multiple of 16: LOPA_EINVAL. Host only; applies to later calls. */
 int lopa_kv_set_block_causal(lopa_kv* kv, int32_t sub_block);
-int lopa_kv_attention_plan(const lopa_kv* kv, int32_t prefix_len, int32_t n_branches, int32_t L,
-                           int32_t* n_ranges, int32_t* range_len);
 
 /* Launch timing of lopa_verify_forward with HIP events on the call's stream.
  * kinds_mask selects which launches get an event pair (bit i = kind i below);

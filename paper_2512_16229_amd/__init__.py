@@ -116,23 +116,10 @@ class KV:
         _check(lib.lopa_kv_read_staging(self.handle, branch, layer, _ptr(k), _ptr(v), _stream(stream)))
         return k, v
 
-    def set_attention_ranges(self, n_ranges: int):
-        """-1: the library picks the attention path; 0: per-(head, branch);
-        n >= 1: shared prefix cut into about n key ranges."""
-        _check(lib.lopa_kv_set_attention_ranges(self.handle, n_ranges))
-
     def set_block_causal(self, sub_block: int):
         """0: full attention inside the block; c > 0 (multiple of 16): rows of
         sub-block b see the prefix and sub-blocks 0..b of their branch."""
         _check(lib.lopa_kv_set_block_causal(self.handle, sub_block))
-
-    def attention_plan(self, prefix_len: int, n_branches: int, L: int):
-        """(n_ranges, range_len) of a verify forward of this shape; (0, 0) is
-        the per-(head, branch) path."""
-        s, ks = C.c_int32(), C.c_int32()
-        _check(lib.lopa_kv_attention_plan(self.handle, prefix_len, n_branches, L, C.byref(s),
-                                          C.byref(ks)))
-        return s.value, ks.value
 
     def profile(self, kinds=()):
         """Time launches of the given kinds (names from PROF_KINDS) with HIP events."""

@@ -43,9 +43,8 @@ EXPORTS = ["lopa_model_create", "lopa_model_create_ex", "lopa_model_destroy", "l
            "lopa_verify_forward",
            "lopa_branch_confidence_select", "lopa_branch_confidence_select_metric", "lopa_commit_kv",
            "lopa_commit_kv_rows", "lopa_kv_read", "lopa_kv_write",
-           "lopa_kv_read_staging", "lopa_debug_hidden", "lopa_kv_set_attention_ranges",
-           "lopa_kv_set_block_causal",
-           "lopa_kv_attention_plan", "lopa_kv_profile",
+           "lopa_kv_read_staging", "lopa_debug_hidden",
+           "lopa_kv_set_block_causal", "lopa_kv_profile",
            "lopa_kv_profile_read"]
 METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
 PRECISIONS = {"bf16": 0, "fp8_mlp": 1, "fp8": 2}
@@ -79,10 +78,7 @@ def _load():
         "lopa_kv_write": (C.c_int, [P, I32, I32, I32, P, P, P]),
         "lopa_kv_read_staging": (C.c_int, [P, I32, I32, P, P, P]),
         "lopa_debug_hidden": (C.c_int, [P, P, I32, P, I32, I32, I32, P, P]),
-        "lopa_kv_set_attention_ranges": (C.c_int, [P, I32]),
         "lopa_kv_set_block_causal": (C.c_int, [P, I32]),
-        "lopa_kv_attention_plan": (C.c_int, [P, I32, I32, I32, C.POINTER(C.c_int32),
-                                             C.POINTER(C.c_int32)]),
         "lopa_kv_profile": (C.c_int, [P, I32]),
         "lopa_kv_profile_read": (C.c_int, [P, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
     }

@@ -124,42 +124,6 @@ GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_n
   }
   return best;
 }
-// Attention: the shared-prefix path (attn_prefix_kernel: each prefix tile read
-// once per (query head, row group) for all branches, S key ranges with fp32
-// partial states merged by the per-branch block kernel) when it moves clearly
-// fewer bytes than the per-(head, branch) path: K/V bytes read plus partial
-// states written and read. S targets one wave of workgroups over the CUs
-// (two wavefronts per SIMD) with ranges of at least four key tiles.
-struct AttnPlan {
-  int S, KS;
-};
-AttnPlan plan_attention(const lopa_model_cfg& c, int nb, int L, int P, int num_cu) {
-  if (P < 256 || nb < 2) return {0, 0};
-  const int M = nb * L, G = (M + ATTN_PREFIX_ROWS - 1) / ATTN_PREFIX_ROWS, tiles = (P + 31) / 32;
-  // workgroups per CU at two wavefronts per SIMD
-  const int wg_cu = std::max(1, 8 * 32 / ATTN_PREFIX_ROWS);
-  int S = std::min(std::max(1, tiles / 4), std::max(1, wg_cu * num_cu / (c.heads * G)));
-  const int KS = 32 * ((tiles + S - 1) / S);
-  S = (P + KS - 1) / KS;
-  const double kv_row = 2.0 * c.head_dim * 2;  // K and V bytes of one position and head
-  const double per_branch = (double)c.heads * nb * P * kv_row;
-  const double shared =
-      (double)c.heads * G * P * kv_row + 2.0 * S * M * c.heads * (c.head_dim + 2) * 4.0;
-  if (shared >= 0.75 * per_branch) return {0, 0};
-  return {S, KS};
-}
-// a fixed number of key ranges (0: the per-(head, branch) path)
-AttnPlan fixed_ranges(int S, int P) {
-  if (S <= 0 || P < 1) return {0, 0};
-  const int tiles = (P + 31) / 32;
-  const int KS = 32 * ((tiles + std::min(S, tiles) - 1) / std::min(S, tiles));
-  return {(P + KS - 1) / KS, KS};
-}
-// the largest number of key ranges plan_attention picks on this device
-int attn_max_ranges(const lopa_model_cfg& c, int num_cu) {
-  return std::max(1, 2 * num_cu / c.heads);  // >= the planner's choice at any ATTN_PREFIX_ROWS >= 128
-}
-
 // bytes of fp32 partial sums the plan writes (QKV always goes through them;
 // the residual projections store [splits][Mp][N] row-major)
 size_t plan_partial_bytes(int epi, const GemmPlan& p, int MT) {
@@ -212,9 +176,6 @@ struct lopa_kv {
   uint32_t* rowmax_dn = nullptr;  // per-row max |SwiGLU output| (float bits)
   uint16_t* qbuf = nullptr;     // [max_branches][Hq][max_block][d]
   float* partials = nullptr;
-  float* attn_part = nullptr;   // shared-prefix attention partial states
-  size_t attn_part_bytes = 0;
-  int attn_ranges = -1;         // lopa_kv_set_attention_ranges: -1 automatic
   int causal_blk = 0;           // lopa_kv_set_block_causal: 0 full attention in the block
   float* pm = nullptr;
   float* ps = nullptr;
@@ -562,9 +523,6 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   }
   KV_ALLOC(qbuf, uint16_t*, (size_t)max_branches * c.heads * max_block * d * 2);
   KV_ALLOC(partials, float*, part_b);
-  kv->attn_part_bytes = (size_t)attn_max_ranges(c, m->num_cu) * max_branches * max_block *
-                        c.heads * (d + 2) * 4;
-  KV_ALLOC(attn_part, float*, kv->attn_part_bytes);
   KV_ALLOC(pm, float*, rows * m->tiles_lm * 4);
   KV_ALLOC(ps, float*, rows * m->tiles_lm * 4);
   KV_ALLOC(pi, int32_t*, rows * m->tiles_lm * 4);
@@ -621,11 +579,6 @@ int lopa_build_branches(const int32_t* tokens, const float* conf, const int32_t*
 
 // The verify forward; with stop_layer >= 0 it stops after that many layers and
 // copies the fp32 residual stream to x_out instead of producing conf / pred.
-static AttnPlan kv_attention_plan(const lopa_kv* kv, int P, int nb, int L) {
-  return kv->attn_ranges < 0 ? plan_attention(kv->m->cfg, nb, L, P, kv->m->num_cu)
-                             : fixed_ranges(kv->attn_ranges, P);
-}
-
 static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
                        const int32_t* branch_tokens, int32_t n_branches, int32_t L, float* conf,
                        int32_t* pred, void* stream, int stop_layer, float* x_out) {
@@ -699,14 +652,6 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   at.vlds = kv->vlds;
   at.Mp = Mp;
   at.scale = 1.0f / std::sqrt((float)d);
-  {
-    const AttnPlan ap = kv_attention_plan(kv, prefix_len, n_branches, L);
-    if ((size_t)ap.S * n_branches * L * c.heads * (d + 2) * 4 > kv->attn_part_bytes)
-      return fail(LOPA_ESHAPE, "attention workspace too small for %d key ranges", ap.S);
-    at.S = ap.S;
-    at.KS = ap.KS;
-    at.part = kv->attn_part;
-  }
   // a block of one sub-block (or less) needs no mask
   at.cblk = kv->causal_blk && L > kv->causal_blk ? kv->causal_blk : 0;
   const int n_layers = stop_layer >= 0 ? std::min(stop_layer, c.layers) : c.layers;
@@ -949,26 +894,6 @@ int lopa_kv_set_block_causal(lopa_kv* kv, int32_t sub_block) {
   if (sub_block < 0 || sub_block % 16)
     return fail(LOPA_EINVAL, "sub_block %d is not 0 or a positive multiple of 16", sub_block);
   kv->causal_blk = sub_block;
-  return LOPA_OK;
-}
-
-int lopa_kv_set_attention_ranges(lopa_kv* kv, int32_t n_ranges) {
-  if (!kv) return fail(LOPA_EINVAL, "null pointer argument");
-  const int mx = attn_max_ranges(kv->m->cfg, kv->m->num_cu);
-  if (n_ranges < -1 || n_ranges > mx)
-    return fail(LOPA_EINVAL, "n_ranges %d outside [-1, %d]", n_ranges, mx);
-  kv->attn_ranges = n_ranges;
-  return LOPA_OK;
-}
-
-int lopa_kv_attention_plan(const lopa_kv* kv, int32_t prefix_len, int32_t n_branches, int32_t L,
-                           int32_t* n_ranges, int32_t* range_len) {
-  if (!kv || !n_ranges || !range_len) return fail(LOPA_EINVAL, "null pointer argument");
-  if (prefix_len < 0 || n_branches < 1 || L < 1)
-    return fail(LOPA_EINVAL, "prefix_len, n_branches or L out of range");
-  const AttnPlan ap = kv_attention_plan(kv, prefix_len, n_branches, L);
-  *n_ranges = ap.S;
-  *range_len = ap.KS;
   return LOPA_OK;
 }
 

@@ -3,20 +3,15 @@
 // all L rows of its own branch (full attention inside the block); branches
 // never see each other. Grouped-query: query head h reads KV head h / (Hq/Hkv).
 //
-// Two paths, chosen by the host from the prefix length:
-//  * attn_kernel alone: one workgroup per (query head, branch) with four
-//    wavefronts; each wavefront takes a quarter of the key tiles (32 keys
-//    each, prefix tiles from the cache and block tiles from the branch's
-//    staging) for all L rows, and the four partial softmax states are merged
-//    through LDS. Short prefixes: no state leaves the workgroup.
-//  * attn_prefix_kernel + attn_block_kernel: the prefix is shared by all
-//    branches, so one workgroup per (query head, key range, 128-row group)
-//    streams each prefix tile of its range once into LDS and computes it for
-//    the rows of every branch (32 rows per wavefront); its unnormalised
-//    partial state per row goes to a workspace. attn_block_kernel then runs
-//    the block tiles per (head, branch) and merges the partial states of the
-//    key ranges. Long prefixes: each prefix K/V tile is read once per (query
-//    head, row group) instead of once per (head, branch).
+// One workgroup per (query head, branch) with four wavefronts; each wavefront
+// takes a quarter of the key tiles (32 keys each, prefix tiles from the cache
+// and block tiles from the branch's staging) for all L rows. The prefix K/V
+// are read from HBM once per KV head per layer (the workgroups of a KV head
+// find them in L2). The softmax takes two passes over the tiles: pass 1 forms
+// the scores and each row's largest score (over the four wavefronts, through
+// LDS); pass 2 forms them again (the same instructions, the same bits) and
+// rounds each probability to bf16 against that exact maximum before it meets
+// V, so no state is rescaled and the four partial states add up.
 // Tiles go global -> LDS by asynchronous copies, then into registers in MFMA
 // operand layout. Scores are formed transposed, S^T = K Q^T, so a lane owns one
 // query column and the probabilities land directly in the operand layout of
@@ -84,9 +79,6 @@ __device__ __forceinline__ float pair32_sum(float x) {
 // range: such probabilities are < 2^-126 of the row maximum and flush to 0)
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Reference maximum before any key: finite, so that 2^(m_old - m_new) and
-// s * scale - m stay defined (a row's first finite score always moves m).
-constexpr float M_INIT = -1e30f;
 
 template <int N>
 __device__ __forceinline__ void attn_wait_vmcnt() {
@@ -180,18 +172,15 @@ __device__ __forceinline__ void tile_fetch(const char* sb, int lane, AttnTile<D>
   }
 }
 
-// One key tile (keys p0 .. p0 + 31 of a source of lim positions) for NR blocks
-// of 16 query rows; ALWAYS_FULL: the caller knows the tile lies wholly inside
-// the source (no masking code). With s the raw score q.k and sl2 = scale log2(e), the
-// probabilities are p = 2^(s sl2 - m) against a reference maximum m (log2
-// units) that trails the running row maximum of s sl2 by at most 8: a row's m,
-// l and o are rescaled only when its maximum has grown past that, so p <= 2^8.
-// o / l and every merge are unchanged by the choice of reference. The maximum
-// is taken over the raw scores (scaling by sl2 > 0 keeps the order and,
-// rounding being monotone, the maximum itself).
+// Pass 2 of one key tile (keys p0 .. p0 + 31 of a source of lim positions) for
+// NR blocks of 16 query rows; ALWAYS_FULL: the caller knows the tile lies
+// wholly inside the source (no masking code). With s the raw score q.k and
+// sl2 = scale log2(e), p = 2^(s sl2 - m) against the row's exact maximum m
+// (log2 units, from pass 1), so p <= 1 and no state is ever rescaled; l sums
+// the unrounded p, and V meets p rounded to bf16.
 template <int D, int NR, bool ALWAYS_FULL>
 __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR][D / 32],
-                                            float (&m)[NR], float (&l)[NR],
+                                            const float (&m)[NR], float (&l)[NR],
                                             f32x4 (&o)[D / 16][NR], int p0, int lim, float sl2,
                                             int g, int cblk = 0, int row0 = 0) {
   constexpr int NDB = D / 16, NKK = D / 32;
@@ -237,21 +226,6 @@ __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR
           s[kb][j] = pos < lq ? s[kb][j] : -INFINITY;
         }
     }
-    float tmax = max2(max3(s[0][0], s[0][1], s[0][2]),
-                      max3(max3(s[0][3], s[1][0], s[1][1]), s[1][2], s[1][3]));
-    tmax = pair32_max(pair16_max(tmax));
-    const float mn = max2(m[qb], tmax * sl2);
-    const bool grow = mn > m[qb] + 8.f;
-    if (__builtin_amdgcn_ballot_w64(grow)) {
-      // only the rows that need it move their reference (the others scale by
-      // exactly 1), so a row's arithmetic never depends on the other rows of
-      // the wavefront; from M_INIT alpha is 0 on zero o and l
-      const float alpha = grow ? fast_exp2(m[qb] - mn) : 1.f;
-      m[qb] = grow ? mn : m[qb];
-      l[qb] *= alpha;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db][qb] *= alpha;
-    }
     const float nm = -m[qb];
     uint16_t pb[8];
 #pragma unroll
@@ -271,19 +245,46 @@ __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR
   }
 }
 
-// merge another softmax state (mo, lo, oo) into (m, l, o): both brought to the
-// larger reference maximum, then summed (a state that saw no key has m =
-// M_INIT and zero l, o: it scales to 0 against any real maximum)
-template <int NDB>
-__device__ __forceinline__ void merge_state(float& m, float& l, f32x4 (&o)[NDB], float mo,
-                                            float lo, const f32x4 (&oo)[NDB]) {
-  const float mn = max2(m, mo);
-  const float fa = fast_exp2(m - mn);
-  const float fb = fast_exp2(mo - mn);
-  m = mn;
-  l = l * fa + lo * fb;
+// Pass 1 of the two-pass softmax: the largest raw score q.k of each query
+// column over the keys of one tile (K fragments read from the LDS slot sb),
+// with the same masking as tile_update; mraw keeps the running maximum.
+template <int D, int NR>
+__device__ __forceinline__ void tile_max(const char* sb, int lane, const u32x4 (&qf)[NR][D / 32],
+                                         float (&mraw)[NR], int p0, int lim, int g, int cblk,
+                                         int row0) {
+  constexpr int NKK = D / 32;
+  u32x4 kf[2][NKK];
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) o[db] = o[db] * fa + oo[db] * fb;
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+      kf[kb][kk] = *(const u32x4*)(sb + ((kb * NKK + kk) * 64 + lane) * 16);
+#pragma unroll
+  for (int qb = 0; qb < NR; ++qb) {
+    int lq = lim;
+    if (cblk) {
+      lq = min(lim, ((row0 + qb * 16) / cblk + 1) * cblk);
+      if (p0 >= lq) continue;
+    }
+    f32x4 s[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk) s[kb] = mfma16(kf[kb][kk], qf[qb][kk], s[kb]);
+    }
+    if (p0 + KT > lq) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int pos = p0 + kb * 16 + g * 4 + j;
+          s[kb][j] = pos < lq ? s[kb][j] : -INFINITY;
+        }
+    }
+    mraw[qb] = max2(mraw[qb], max2(max3(s[0][0], s[0][1], s[0][2]),
+                                   max3(max3(s[0][3], s[1][0], s[1][1]), s[1][2], s[1][3])));
+  }
 }
 
 template <int D, int QB>
@@ -291,7 +292,7 @@ struct AttnSmem {
   static constexpr int NDB = D / 16;
   static constexpr int RING = 4 * 2 * TileLds<D>::TILE;  // four wavefronts x two slots
   static constexpr int MERGE_O = NDB * QB * 64 * 4;      // floats of one merge slot
-  static constexpr int MERGE = (2 * MERGE_O + 4 * QB * 16) * 4;
+  static constexpr int MERGE = (2 * MERGE_O + 2 * QB * 16) * 4;
   static constexpr int BYTES = RING > MERGE ? RING : MERGE;
   static constexpr int OPS = TileLds<D>::OPS;
 };
@@ -337,6 +338,23 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     }
   };
 
+  // K copies of tile t only (pass 1)
+  auto issue_k = [&](int t, int slot) {
+    const bool pre = t < pt;
+    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
+    const uint32_t sb = ring + (uint32_t)slot * TileLds<D>::TILE;
+    if (p0 + KT <= lim) {
+#pragma unroll
+      for (int q = 0; q < 2 * NKK; ++q)
+        tile_copy_full<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, sb,
+                          pre ? co_c : co_s);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 2 * NKK; ++q)
+        tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, lim, sb, c16, g);
+    }
+  };
+
   // the first two tiles are in flight while Q is loaded. The query heads of
   // one KV head start at different tiles of the range (and wrap), so that
   // their workgroups do not request the same K/V lines at the same moment.
@@ -344,8 +362,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int rot = n > 0 ? (h % (a.Hq / a.Hkv)) % n : 0;
   auto tile_of = [&](int i) { const int r = i + rot; return t_lo + (r < n ? r : r - n); };
   if (n > 0) {
-    issue(tile_of(0), 0);
-    issue(tile_of(n > 1 ? 1 : 0), 1);
+    issue_k(tile_of(0), 0);
+    issue_k(tile_of(n > 1 ? 1 : 0), 1);
   }
 
   // Q^T operand: query column 16 qb + c16, dims 32 kk + 8 g .. +8
@@ -359,14 +377,44 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int kk = 0; kk < NKK; ++kk) qf[qb][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
   }
 
+  // Pass 1: each row's largest score over this wavefront's tiles (K only,
+  // the same ring and order), then over the four wavefronts: the exact row
+  // maximum, against which pass 2 rounds every probability.
+  float mraw[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) mraw[qb] = -INFINITY;
+  for (int i = 0; i < n; ++i) {
+    attn_wait_vmcnt<2 * NKK>();
+    const int t = tile_of(i);
+    const bool pre = t < pt;
+    tile_max<D, QB>(smem + (wv * 2 + (i & 1)) * TileLds<D>::TILE, lane, qf, mraw,
+                    (pre ? t : t - pt) * KT, pre ? P : L, g, pre ? 0 : a.cblk, 0);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    issue_k(tile_of(i + 2 < n ? i + 2 : n - 1), i & 1);
+  }
+  attn_wait_vmcnt<0>();
+  __shared__ float s_max[4][QB * 16];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    mraw[qb] = pair32_max(pair16_max(mraw[qb]));
+    if (g == 0) s_max[wv][qb * 16 + c16] = mraw[qb];
+  }
+  __syncthreads();
   float m[QB], l[QB];  // reference max (log2 units) and this lane's partial sum
   f32x4 o[NDB][QB];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    m[qb] = M_INIT;
+    const float mx = max2(max2(s_max[0][qb * 16 + c16], s_max[1][qb * 16 + c16]),
+                          max2(s_max[2][qb * 16 + c16], s_max[3][qb * 16 + c16]));
+    m[qb] = mx * sl2;  // every probability 2^(s sl2 - m) <= 1: never rescaled
     l[qb] = 0.f;
 #pragma unroll
     for (int db = 0; db < NDB; ++db) o[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // Pass 2: the first two tiles again, K and V
+  if (n > 0) {
+    issue(tile_of(0), 0);
+    issue(tile_of(n > 1 ? 1 : 0), 1);
   }
 
   // tile i sits in slot i % 2. At the top of an iteration tiles i and i + 1
@@ -390,10 +438,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) l[qb] = pair32_sum(pair16_sum(l[qb]));
 
-  // merge the four key ranges: (2, 3) into (0, 1), then 1 into 0
+  // the four key ranges share the reference maximum: their states add up,
+  // (2, 3) into (0, 1), then 1 into 0 (a fixed order)
   float(*sO)[SM::MERGE_O] = (float(*)[SM::MERGE_O])smem;
-  float(*sM)[QB * 16] = (float(*)[QB * 16])(smem + 2 * SM::MERGE_O * 4);
-  float(*sL)[QB * 16] = (float(*)[QB * 16])(smem + 2 * SM::MERGE_O * 4 + 2 * QB * 16 * 4);
+  float(*sL)[QB * 16] = (float(*)[QB * 16])(smem + 2 * SM::MERGE_O * 4);
   auto put = [&](int slot) {
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
@@ -402,23 +450,15 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
         *(f32x4*)&sO[slot][((db * QB + qb) * 64 + lane) * 4] = o[db][qb];
     if (g == 0)
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        sM[slot][qb * 16 + c16] = m[qb];
-        sL[slot][qb * 16 + c16] = l[qb];
-      }
+      for (int qb = 0; qb < QB; ++qb) sL[slot][qb * 16 + c16] = l[qb];
   };
   auto take = [&](int slot) {
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
-      f32x4 oo[NDB], ob[NDB];
+      l[qb] += sL[slot][qb * 16 + c16];
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        oo[db] = *(const f32x4*)&sO[slot][((db * QB + qb) * 64 + lane) * 4];
-        ob[db] = o[db][qb];
-      }
-      merge_state<NDB>(m[qb], l[qb], ob, sM[slot][qb * 16 + c16], sL[slot][qb * 16 + c16], oo);
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db][qb] = ob[db];
+      for (int db = 0; db < NDB; ++db)
+        o[db][qb] += *(const f32x4*)&sO[slot][((db * QB + qb) * 64 + lane) * 4];
     }
   };
   if (wv >= 2) put(wv - 2);
@@ -447,213 +487,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
-// Shared prefix: one workgroup per (query head h, key range sp, group gr of
-// 16 RB NW query rows of all branches); wavefront wv of NW owns rows
-// (gr NW + wv) 16 RB .. (row r = branch * L + position) as RB 16-row blocks. The range's tiles are
-// copied once into a three-slot LDS ring shared by the four wavefronts (a
-// quarter of each tile's copies per wavefront) and computed by all of them.
-// Output: the unnormalised state of every row for this range, O at
-// part[((sp M + r) Hq + h) D ..] and (m, l) at part[S M Hq D + ((sp M + r) Hq + h) 2].
-template <int D, int RB, int NW, int RING>
-__global__ __launch_bounds__(64 * NW, 2) void attn_prefix_kernel(AttnArgs a) {
-  constexpr int NDB = D / 16, NKK = D / 32;
-  constexpr int OPS = TileLds<D>::OPS, OPW = OPS / NW;  // copies per tile and wavefront
-  static_assert(OPS % NW == 0, "copies per wavefront");
-  static_assert(RING >= 3 && (RING - 2) * OPW <= 63, "ring depth");
-  __shared__ __attribute__((aligned(1024))) char smem[RING * TileLds<D>::TILE];
-  const int h = blockIdx.x, sp = blockIdx.y, gr = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int g = lane >> 4, c16 = lane & 15;
-  const int kvh = h / (a.Hq / a.Hkv);
-  const int L = a.L, P = a.P, M = a.nb * L;
-  const int k_lo = sp * a.KS, k_hi = min(P, k_lo + a.KS);
-  const int n = (k_hi - k_lo + KT - 1) / KT;  // >= 1: the host sizes the ranges
-  const float sl2 = a.scale * 1.4426950408889634f;
-  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;
-  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;
-  const uint32_t ring = (uint32_t)(uintptr_t)smem;
-
-  // this wavefront's copies of tile i (keys k_lo + 32 i ..) into slot i % RING;
-  // past the last tile the last one is copied again, so every iteration waits
-  // for the same count
-  const CopyOffsets co = copy_offsets<D>(a.vld, c16, g);
-  auto issue = [&](int i) {
-    const int t = i < n ? i : n - 1;
-    const int p0 = k_lo + t * KT;
-    const uint32_t sb = ring + (uint32_t)(i % RING) * TileLds<D>::TILE;
-    if (p0 + KT <= P) {
-#pragma unroll
-      for (int c = 0; c < OPW; ++c) tile_copy_full<D>(wv * OPW + c, kc, vc, a.vld, p0, sb, co);
-    } else {
-#pragma unroll
-      for (int c = 0; c < OPW; ++c) tile_copy<D>(wv * OPW + c, kc, vc, a.vld, p0, P, sb, c16, g);
-    }
-  };
-#pragma unroll
-  for (int i = 0; i < RING - 1; ++i) issue(i);
-
-  u32x4 qf[RB][NKK];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int r = (gr * NW + wv) * 16 * RB + rb * 16 + c16;
-    const int rr = r < M ? r : 0;
-    const uint16_t* qrow = a.q + (((int64_t)(rr / L) * a.Hq + h) * L + rr % L) * D;
-    const unsigned keep = r < M ? ~0u : 0u;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) qf[rb][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
-  }
-  float m[RB], l[RB];
-  f32x4 o[NDB][RB];
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    m[rb] = M_INIT;
-    l[rb] = 0.f;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) o[db][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  // tiles i .. i + RING - 2 are in flight at the top of iteration i: wait for
-  // this wavefront's copies of tile i; the barrier then makes every
-  // wavefront's copies visible and retires every read of tile i - 1, whose
-  // slot takes tile i + RING - 1
-  // (only the last tile of the last range can be partial: it runs after the
-  // loop, through the masking path)
-  const int n_full = (k_hi - k_lo) / KT;
-  auto step = [&](int i, auto full) {
-    attn_wait_vmcnt<(RING - 2) * OPW>();
-    __syncthreads();
-    issue(i + RING - 1);
-    AttnTile<D> x;
-    tile_fetch<D>(smem + (i % RING) * TileLds<D>::TILE, lane, x);
-    tile_update<D, RB, decltype(full)::value>(x, qf, m, l, o, k_lo + i * KT, k_hi, sl2, g);
-  };
-  for (int i = 0; i < n_full; ++i) step(i, std::true_type{});
-  if (n_full < n) step(n_full, std::false_type{});
-  attn_wait_vmcnt<0>();  // the repeated copies past the last tile
-#pragma unroll
-  for (int rb = 0; rb < RB; ++rb) {
-    const int r = (gr * NW + wv) * 16 * RB + rb * 16 + c16;
-    l[rb] = pair32_sum(pair16_sum(l[rb]));
-    if (r >= M) continue;
-    const int64_t e = ((int64_t)sp * M + r) * a.Hq + h;
-    float* po = a.part + e * D + g * 4;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) *(f32x4*)(po + db * 16) = o[db][rb];
-    if (g == 0) {
-      float* pml = a.part + (int64_t)a.S * M * a.Hq * D + e * 2;
-      pml[0] = m[rb];
-      pml[1] = l[rb];
-    }
-  }
-}
-
-// After attn_prefix_kernel: per (query head, branch), the block tiles (one
-// or two) and the merge of the prefix key ranges. Wavefront wv owns query
-// rows 16 wv .. 16 wv + 15, so no state crosses wavefronts; the block tiles
-// are copied once into LDS (the copies spread over the wavefronts). The
-// partial states of up to four ranges are loaded together, the first four
-// while the tiles are in flight; a row merges its block state and then the
-// ranges in range order.
-template <int D, int QB>
-__global__ __launch_bounds__(64 * QB) void attn_block_kernel(AttnArgs a) {
-  constexpr int NDB = D / 16, NKK = D / 32, OPS = TileLds<D>::OPS, RG = 4;
-  __shared__ __attribute__((aligned(1024))) char smem[2 * TileLds<D>::TILE];
-  const int h = blockIdx.x, br = blockIdx.y;
-  const int lane = threadIdx.x & 63;
-  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int g = lane >> 4, c16 = lane & 15;
-  const int kvh = h / (a.Hq / a.Hkv);
-  const int L = a.L, bt = (L + KT - 1) / KT, M = a.nb * L;
-  const float sl2 = a.scale * 1.4426950408889634f;
-  const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
-  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
-  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
-  const uint32_t ring = (uint32_t)(uintptr_t)smem;
-  for (int t = 0; t < bt; ++t)
-    for (int q = wv; q < OPS; q += QB)
-      tile_copy<D>(q, ks, vs, a.vlds, t * KT, L, ring + (uint32_t)t * TileLds<D>::TILE, c16, g);
-
-  const int row = wv * 16 + c16;
-  const int rr = row < L ? row : 0;
-  u32x4 qf[1][NKK];
-  {
-    const uint16_t* qrow = a.q + (((int64_t)br * a.Hq + h) * L + rr) * D;
-    const unsigned keep = row < L ? ~0u : 0u;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) qf[0][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
-  }
-  // partial state of range sp for this lane's row
-  const int64_t ml_off = (int64_t)a.S * M * a.Hq * D;
-  f32x4 po[RG][NDB];
-  float pm[RG], pl[RG];
-  auto load_ranges = [&](int sp0) {
-#pragma unroll
-    for (int u = 0; u < RG; ++u) {
-      const int sp = sp0 + u < a.S ? sp0 + u : a.S - 1;
-      const int64_t e = ((int64_t)sp * M + br * L + rr) * a.Hq + h;
-      const float* src = a.part + e * D + g * 4;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) po[u][db] = *(const f32x4*)(src + db * 16);
-      pm[u] = a.part[ml_off + e * 2];
-      pl[u] = a.part[ml_off + e * 2 + 1];
-    }
-  };
-  load_ranges(0);
-  attn_wait_vmcnt<0>();  // the tile copies (and, in order, everything before)
-  __syncthreads();
-
-  float m[1] = {M_INIT}, l[1] = {0.f};
-  f32x4 o[NDB][1];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) o[db][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int t = 0; t < bt; ++t) {
-    AttnTile<D> x;
-    tile_fetch<D>(smem + t * TileLds<D>::TILE, lane, x);
-    tile_update<D, 1, false>(x, qf, m, l, o, t * KT, L, sl2, g, a.cblk, wv * 16);
-  }
-  l[0] = pair32_sum(pair16_sum(l[0]));
-  f32x4 ob[NDB];
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) ob[db] = o[db][0];
-  for (int sp0 = 0; sp0 < a.S; sp0 += RG) {
-    if (sp0 > 0) load_ranges(sp0);
-#pragma unroll
-    for (int u = 0; u < RG; ++u)
-      if (sp0 + u < a.S) merge_state<NDB>(m[0], l[0], ob, pm[u], pl[u], po[u]);
-  }
-  if (row >= L) return;
-  const float inv = 1.0f / l[0];
-  const int r = br * L + row;
-#pragma unroll
-  for (int db = 0; db < NDB; ++db) {
-    uint16_t v4[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) v4[j] = f2bf_bits(ob[db][j] * inv);
-    *(uint2*)(a.out + packA_off(r, h * D + db * 16 + g * 4, a.Mp)) = *(const uint2*)v4;
-  }
-}
-
 template <int D>
 hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
-  if (a.S > 0) {
-    const dim3 pgrid(a.Hq, a.S, (a.nb * a.L + ATTN_PREFIX_ROWS - 1) / ATTN_PREFIX_ROWS);
-    hipLaunchKernelGGL((attn_prefix_kernel<D, 2, ATTN_PREFIX_ROWS / 32, ATTN_PREFIX_RING>), pgrid,
-                       dim3(2 * ATTN_PREFIX_ROWS), 0, s, a);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
   const dim3 grid(a.Hq, a.nb);
-  if (a.S > 0) {
-    switch ((a.L + 15) / 16) {
-      case 1: hipLaunchKernelGGL((attn_block_kernel<D, 1>), grid, dim3(64), 0, s, a); break;
-      case 2: hipLaunchKernelGGL((attn_block_kernel<D, 2>), grid, dim3(128), 0, s, a); break;
-      case 3: hipLaunchKernelGGL((attn_block_kernel<D, 3>), grid, dim3(192), 0, s, a); break;
-      case 4: hipLaunchKernelGGL((attn_block_kernel<D, 4>), grid, dim3(256), 0, s, a); break;
-      default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
-  }
   switch ((a.L + 15) / 16) {
     case 1: hipLaunchKernelGGL((attn_kernel<D, 1>), grid, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((attn_kernel<D, 2>), grid, dim3(256), 0, s, a); break;
@@ -671,11 +507,6 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
       a.L > a.vlds || a.P > a.vld)
     return hipErrorInvalidValue;
   if (a.cblk < 0 || (a.cblk > 0 && (a.cblk % 16 || a.L % a.cblk))) return hipErrorInvalidValue;
-  // shared prefix: every key range non-empty, the ranges cover [0, P), and the
-  // workspace was given
-  if (a.S < 0 || (a.S > 0 && (!a.part || a.KS < KT || a.KS % KT || a.P < 1 ||
-                              (int64_t)(a.S - 1) * a.KS >= a.P || (int64_t)a.S * a.KS < a.P)))
-    return hipErrorInvalidValue;
   if (a.d == 128) return launch_d<128>(a, s);
   if (a.d == 64) return launch_d<64>(a, s);
   return hipErrorInvalidValue;

@@ -135,20 +135,9 @@ struct AttnArgs {
   uint16_t* out;           // packed activations (Mp rows, Hq*d columns)
   int nb, L, P, Hq, Hkv, d, vld, layer, layers, vlds, Mp;
   float scale;
-  // shared-prefix path (S > 0): the prefix runs as S key ranges of KS
-  // positions (a multiple of 32; every range non-empty) for all branches at
-  // once; part is the fp32 workspace: O [S][nb*L][Hq][d], then (m, l)
-  // [S][nb*L][Hq][2]. S = 0: the prefix runs inside the per-branch kernel.
-  int S, KS;
-  float* part;
   // block-causal mask inside the block (cblk > 0, a multiple of 16 dividing L):
   // a row of sub-block r / cblk sees the prefix and the block keys of the
   // sub-blocks up to its own. 0: full attention inside the block.
   int cblk;
 };
-// query rows (of all branches) per workgroup of the shared-prefix pass (32
-// per wavefront, two wavefronts per SIMD) and its LDS ring depth in key
-// tiles (all but one in flight)
-constexpr int ATTN_PREFIX_ROWS = 128;
-constexpr int ATTN_PREFIX_RING = 4;
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

@@ -93,14 +93,17 @@ class Decoder:
         self.forwards += 1
 
     def decode_block(self, P: int, trace=None) -> int:
-        """Run iterations until the winner has no unfilled position; returns the count."""
+        """Run iterations until the winner has no unfilled position; returns the count.
+        trace: a list that receives each iteration's snapshot and the state
+        (tokens, conf, pred) the iteration started from (host copies)."""
         self.init_block(P)
         it = 0
         while True:
+            state = (self.tokens.cpu(), self.conf.cpu(), self.pred.cpu()) if trace is not None else None
             self.step(P)
             it += 1
             if trace is not None:
-                trace.append(self.snapshot())
+                trace.append(dict(self.snapshot(), state=state))
             if int(self.next_unfilled.item()) == 0:
                 return it
             if it > self.L:
@@ -204,6 +207,8 @@ class WindowDecoder:
                 append_block()
             Lw = len(active) * L
             n_el = L * next((i for i, a in enumerate(active) if not a), len(active))
+            state = ((self.tokens[:Lw].cpu(), self.conf[:Lw].cpu(), self.pred[:Lw].cpu())
+                     if trace is not None else None)
             lopa_build_branches_window(self.tokens[:Lw], self.conf[:Lw], self.pred[:Lw], Lw, n_el,
                                        mask, self.tau, k, self.bt[:nb * Lw], self.fill_pos,
                                        self.valid, self.n_valid)
@@ -234,7 +239,11 @@ class WindowDecoder:
             if trace is not None:
                 trace.append(dict(prefix_len=P, n_eligible=n_el, winner=int(self.winner.item()),
                                   tokens=host.clone(), committed_blocks=c,
-                                  scores=self.scores.cpu()))
+                                  scores=self.scores.cpu(), state=state,
+                                  branch_tokens=self.bt[:nb * Lw].view(nb, Lw).cpu(),
+                                  valid=self.valid.cpu(), n_valid=int(self.n_valid.item()),
+                                  conf=self.conf_b[:nb * Lw].view(nb, Lw).cpu(),
+                                  pred=self.pred_b[:nb * Lw].view(nb, Lw).cpu()))
             if c:
                 lopa_commit_kv_rows(self.kv, self.winner, P, Lw, c * L, self.append_offset)
                 out.append(host[:c * L].clone())

@@ -4,26 +4,52 @@ configuration bench.py times (every plan and kernel of the step at that size):
   * Dream-7B, prefix 2048, k = 15 (16 branches x 32 rows: two row tiles);
   * LLaDA-8B (MHA, no biases), prefix 1024, k = 7.
 
-The oracle cannot run 28-32 float64 layers at these sizes in seconds, so outputs
-are sampled where it can compute them one by one:
-  * the residual stream after the first layer for every row (one float64
-    layer, the prefix K/V of that layer taken from the GPU's own cache);
-  * Conf / candidate token of sampled rows from the GPU's final residual stream:
-    final RMSNorm + the full-vocabulary LM head + softmax in float64 (Sec. 3.1).
-The LM head is spread (N(0, 8/sqrt(H))) so that confidences are informative."""
+One whole LoPA iteration (Alg. 1) at each shape, all layers, every row:
+  * the block's initial forward (all positions masked) gives the state; its
+    confidences / candidates against the oracle's LM head on its final rows;
+  * lopa_build_branches on that state against the oracle's Eq. 1 / top-k on
+    the same confidences (bit-exact);
+  * lopa_verify_forward of all k+1 branches against the float64 oracle with
+    the fixed tolerances of gpu_util.check_forward: every layer fed the GPU's
+    own input residual stream (rel-L2 vs the bf16-faithful layer), confidences
+    within 2e-2 of the pure oracle end to end, and the oracle's LM head +
+    softmax on the GPU's own final rows (confidence within 1e-3, candidate
+    tokens equal where the top-2 margin is >= 1e-3);
+  * lopa_branch_confidence_select against Eq. 2 on the GPU's confidences;
+  * lopa_commit_kv: the cache rows equal the winner's staged K/V bit for bit.
+The prefix K/V are the GPU's own block-causal prefill, read back and handed to
+the oracle (teacher-forced prefix). The oracle streams the weights layer by
+layer from the GPU's bf16 tensors. The LM head is spread (N(0, 5/sqrt(H)): logit std 5)
+so that confidences are informative."""
+import types
+
 import numpy as np
 import pytest
 import torch
 
 import synth
-from gpu_util import conf_tolerance, faithful_bound, log, near_tie, vocab_margin
-from oracle import KVCache, OracleModel
-from oracle.model import bf16_round, confidence, rms_norm
+from gpu_util import (NEAR_TIE, check_forward, conf_tol, f32, gpu_residual, log, score_margin,
+                      tf_lm_check)
+from oracle import KVCache, OracleModel, lopa
 
 pytestmark = pytest.mark.gpu
 
 L = 32
+TAU = 0.9
 CASES = [("dream7b_spread", 512, 7), ("dream7b_spread", 2048, 15), ("llada8b_spread", 1024, 7)]
+
+
+class _Layers:
+    """The oracle's view of the GPU's bf16 layer weights, one layer at a time."""
+
+    def __init__(self, w):
+        self.w = w
+
+    def __len__(self):
+        return len(self.w["layers"])
+
+    def __getitem__(self, i):
+        return {k: v.float().cpu() for k, v in self.w["layers"][i].items()}
 
 
 @pytest.fixture(scope="module", params=CASES, ids=lambda c: f"{c[0]}-P{c[1]}-k{c[2]}")
@@ -35,75 +61,74 @@ def big(request):
     w = synth.model_weights(cfg, device="cuda", dtype=torch.bfloat16)
     model = lp.Model(cfg, w)
     kv = lp.KV(model, P + L, K + 1, L)
-    dec = lp.Decoder(model, kv, L, K, 0.9)
+    dec = lp.Decoder(model, kv, L, K, TAU)
     assert dec.prefill(synth.prompt(cfg, P, device="cuda")) == P
-    rng = np.random.default_rng(11)
-    mask = cfg["mask_id"]
-    bt = np.where(rng.random((K + 1, L)) < 0.7, mask, rng.integers(0, cfg["vocab"] - 1, (K + 1, L)))
-    bt[0] = mask
     torch.cuda.synchronize()
-    yield dict(lp=lp, cfg=cfg, w=w, model=model, kv=kv, bt=bt, P=P)
-    del dec, kv, model, w
+    host = {"embed": w["embed"].float().cpu(), "layers": _Layers(w),
+            "final_norm": w["final_norm"].float().cpu(), "lm_head": w["lm_head"].float().cpu()}
+    cache = KVCache(cfg, P + L)
+    for layer in range(cfg["layers"]):
+        kg, vg = kv.read(layer, 0, P)
+        cache.k[layer, :, :P] = kg.float().cpu().numpy()
+        cache.v[layer, :, :P] = vg.float().cpu().numpy()
+    s = types.SimpleNamespace(lp=lp, cfg=cfg, model=model, kv=kv, P=P, L=L, k=K, dec=dec,
+                              cache_f=cache)
+    # one converted layer at a time, shared by both modes (bf16-valued weights)
+    s.faith = OracleModel(cfg, host, "faithful", keep_layers=1, bf16_weights=True)
+    s.pure = OracleModel(cfg, host, "pure", keep_layers=1, share=s.faith,
+                         bf16_weights=True)
+    yield s
+    del s, dec, kv, model, w, host
     torch.cuda.empty_cache()
 
 
-def _hidden(big, n_layers):
-    lp, cfg, bt, P = big["lp"], big["cfg"], big["bt"], big["P"]
-    nb = bt.shape[0]
-    x = torch.empty(nb * L * cfg["hidden"], dtype=torch.float32, device="cuda")
-    btd = torch.tensor(bt, dtype=torch.int32, device="cuda").reshape(-1)
-    lp.lopa_debug_hidden(big["model"], big["kv"], P, btd, nb, L, n_layers, x)
-    torch.cuda.synchronize()
-    return x.view(nb, L, -1).cpu().numpy().astype(np.float64)
-
-
-def test_first_layer_all_rows(big):
-    cfg, w, bt, P = big["cfg"], big["w"], big["bt"], big["P"]
-    log(f"  layer 0, {bt.size} rows, prefix {P}")
-    g = _hidden(big, 1)
-    cfg1 = dict(cfg, layers=1)
-    host = {"embed": w["embed"].float().cpu(),
-            "layers": [{k: v.float().cpu() for k, v in w["layers"][0].items()}],
-            "final_norm": w["final_norm"].float().cpu(),
-            "lm_head": w["lm_head"][:1].float().cpu()}        # not reached with n_layers=1
-    faith = OracleModel(cfg1, host, "faithful")
-    del host
-    cache = KVCache(cfg1, P + L)
-    kg, vg = big["kv"].read(0, 0, P)                          # the GPU's prefix, layer 0 (bf16)
-    cache.k[0, :, :P] = kg.float().cpu().numpy()
-    cache.v[0, :, :P] = vg.float().cpu().numpy()
-    r = faith.forward_block(bt, P, cache, n_layers=1)["x"]
-    rel = np.linalg.norm(g - r) / np.linalg.norm(r)
-    log(f"  residual stream after layer 0: rel-L2 {rel:.2e}")
-    assert rel < 1e-2
-
-
-def test_lm_head_sampled_rows(big):
-    lp, cfg, w, bt, P = big["lp"], big["cfg"], big["w"], big["bt"], big["P"]
-    log("  LM head + Conf on sampled rows, full vocabulary")
-    nb = bt.shape[0]
-    conf_g = torch.empty(nb * L, dtype=torch.float32, device="cuda")
-    pred_g = torch.empty(nb * L, dtype=torch.int32, device="cuda")
-    btd = torch.tensor(bt, dtype=torch.int32, device="cuda").reshape(-1)
-    lp.lopa_verify_forward(big["model"], big["kv"], P, btd, nb, L, conf_g, pred_g)
-    torch.cuda.synchronize()
-    conf_g = conf_g.cpu().numpy().astype(np.float64)
-    pred_g = pred_g.cpu().numpy()
-    x = _hidden(big, cfg["layers"]).reshape(nb * L, -1)
-    rows = np.random.default_rng(3).choice(nb * L, 24, replace=False)
-    lm = w["lm_head"].float().cpu().numpy().astype(np.float64)   # bf16 values
-    fn = w["final_norm"].float().cpu().numpy().astype(np.float64)
-    h = rms_norm(x[rows], fn, cfg["rms_eps"])
-    lg_pure = h @ lm.T
-    lg_faith = bf16_round(h) @ lm.T                              # the LM head's operand is bf16
-    cp, _ = confidence(lg_pure, cfg["mask_id"])
-    cf, pf = confidence(lg_faith, cfg["mask_id"])
-    e_bf16 = np.max(np.abs(cf - cp))
-    e = np.max(np.abs(conf_g[rows] - cf))
-    log(f"  max|dconf| gpu-faithful {e:.2e}, gpu-pure {np.max(np.abs(conf_g[rows] - cp)):.2e}, "
-        f"faithful-pure {e_bf16:.2e}; conf range {cf.min():.3f}..{cf.max():.3f}")
-    assert e < faithful_bound(e_bf16)
-    assert np.max(np.abs(conf_g[rows] - cp)) < conf_tolerance(e_bf16)
-    decided = vocab_margin(lg_faith, cfg["mask_id"]) >= near_tie(e)
-    assert decided.mean() > 0.8
-    assert np.array_equal(pred_g[rows][decided], pf[decided])
+def test_lopa_iteration_full_depth(big):
+    s = big
+    lp, cfg, P, K = s.lp, s.cfg, s.P, s.k
+    mask, nb = cfg["mask_id"], K + 1
+    dec = s.dec
+    # the block's initial forward: the state of the first iteration
+    dec.init_block(P)
+    tokens = dec.tokens.cpu().numpy()
+    conf0 = dec.conf.cpu().numpy().astype(np.float64)
+    pred0 = dec.pred.cpu().numpy()
+    log(f"  initial forward: conf {conf0.min():.3f}..{conf0.max():.3f}")
+    tf_lm_check(s, gpu_residual(s, tokens[None], cfg["layers"]), conf0[None], pred0[None],
+                "initial forward")
+    # Eq. 1 + lookahead branches (Alg. 1 steps 1-2) on that state
+    lp.lopa_build_branches(dec.tokens, dec.conf, dec.pred, L, mask, TAU, K, dec.branch_tokens,
+                           dec.fill_pos, dec.valid, dec.n_valid)
+    bt = dec.branch_tokens.view(nb, L).cpu().numpy()
+    rbt, rfp, rva, rnv = lopa.build_branches(tokens, conf0, pred0, mask, f32(TAU), K)
+    assert np.array_equal(bt, rbt) and np.array_equal(dec.valid.cpu().numpy(), rva)
+    assert int(dec.n_valid.item()) == rnv
+    # the verify forward of all branches (Alg. 1 step 3), every layer
+    lp.lopa_verify_forward(s.model, s.kv, P, dec.branch_tokens, nb, L, dec.conf_b, dec.pred_b)
+    gc = dec.conf_b.view(nb, L).cpu().numpy().astype(np.float64)
+    gp = dec.pred_b.view(nb, L).cpu().numpy()
+    log(f"  verify forward: {nb * L} rows, conf {gc.min():.3f}..{gc.max():.3f}")
+    st = check_forward(s, rbt, gc, gp, layers=True, e2e_faithful=True, label="verify forward")
+    # Eq. 2 on the GPU's confidences, and vs the pure oracle's scores
+    outs = (dec.scores, dec.winner, dec.next_tokens, dec.next_conf, dec.next_pred,
+            dec.next_unfilled)
+    lp.lopa_branch_confidence_select(dec.branch_tokens, dec.conf_b, dec.pred_b, dec.valid, nb, L,
+                                     mask, *outs)
+    gs = dec.scores.cpu().numpy().astype(np.float64)
+    ts, tw = lopa.select(rbt, gc, rva, mask)
+    ps, _ = lopa.select(rbt, st["pure"]["conf"], rva, mask)
+    fin = np.isfinite(ts)
+    assert np.max(np.abs(gs[fin] - ts[fin]), initial=0) <= 1e-5
+    assert np.max(np.abs(gs[fin] - ps[fin]), initial=0) <= conf_tol(s.cfg)
+    w = int(dec.winner.item())
+    if score_margin(ts) >= NEAR_TIE:
+        assert np.array_equal(rbt[w], rbt[tw])
+    assert np.array_equal(dec.next_tokens.cpu().numpy(), rbt[w])
+    assert np.array_equal(dec.next_conf.cpu().numpy(), dec.conf_b.view(nb, L)[w].cpu().numpy())
+    # commit the winner's K/V (Sec. 3.4): the cache rows equal its staging
+    lp.lopa_commit_kv(s.kv, dec.winner, P, L, dec.append_offset)
+    assert int(dec.append_offset.item()) == P
+    for layer in (0, cfg["layers"] // 2, cfg["layers"] - 1):
+        kc, vc = s.kv.read(layer, P, L)
+        ks, vs = s.kv.read_staging(w, layer, L)
+        assert torch.equal(kc, ks) and torch.equal(vc, vs)
+    log(f"  winner {w}, score margin {score_margin(ts):.2e}")

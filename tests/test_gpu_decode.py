@@ -3,17 +3,20 @@
 Teacher-forced: every iteration the GPU gets the oracle's state (block
 tokens, confidences, candidates and the committed K/V cache) and the four
 C-ABI calls are compared one by one. Free-running: the GPU decodes a block on
-its own and its trajectory must equal the oracle's until a decision whose
-oracle margin is a near-tie, where either outcome is correct. Near-tie margins
-are 1e-3 or twice the measured GPU-vs-oracle confidence gap (gpu_util.near_tie)."""
+its own; at every iteration each of its decisions is checked against the
+oracle's decision on the GPU's own inputs (Eq. 1 and the lookahead branches
+from the GPU's state, the forward against the oracle forward of the same
+branches, Eq. 2 and the winner from the GPU's confidences), so the whole
+trajectory is a LoPA trajectory of the GPU's forward. The tolerances are the
+fixed ones of gpu_util; a near-tie is a decision whose oracle margin is below
+1e-3."""
 import numpy as np
 import pytest
 import torch
 
 import synth
-from gpu_util import (FAITHFUL_TOL, Setup, build_margin, conf_tolerance, f32, faithful_bound, log,
-                      near_tie,
-                      score_margin, vocab_margin)
+from gpu_util import (NEAR_TIE, conf_tol, Setup, check_forward, f32, log,
+                      score_margin)
 from oracle import lopa
 
 pytestmark = pytest.mark.gpu
@@ -26,7 +29,7 @@ def _d(a, dt):
 
 
 @pytest.mark.parametrize("cfgname,P,L,k,tau", [("tiny", 64, 16, 3, 0.9), ("tiny", 64, 16, 7, 0.5),
-                                               ("small", 100, 32, 7, 0.9)])
+                                               ("small", 100, 32, 7, 0.9), ("tiny", 40, 16, 3, 0.999)])
 def test_teacher_forced_iterations(cfgname, P, L, k, tau):
     log(f"teacher-forced {cfgname} P={P} L={L} k={k} tau={tau}")
     s = Setup(cfgname, P, L, k)
@@ -50,20 +53,15 @@ def test_teacher_forced_iterations(cfgname, P, L, k, tau):
         assert np.array_equal(bt.view(nb, L).cpu().numpy(), rbt)
         assert np.array_equal(va.cpu().numpy(), rva) and int(nv.item()) == rnv
         # verify the oracle's branches
-        out_f = s.faith.forward_block(rbt, P, s.cache_f, keep_hidden=True)
-        out_p = s.pure.forward_block(rbt, P, s.cache_p)
         conf_b = torch.empty(nb * L, dtype=F32, device="cuda")
         pred_b = torch.empty(nb * L, dtype=I32, device="cuda")
         lp.lopa_verify_forward(s.model, s.kv, P, _d(rbt.ravel(), I32), nb, L, conf_b, pred_b)
         gc = conf_b.view(nb, L).cpu().numpy().astype(np.float64)
         gp = pred_b.view(nb, L).cpu().numpy()
-        eps = np.max(np.abs(gc - out_f["conf"]))
-        e_bf16 = np.max(np.abs(out_f["conf"] - out_p["conf"]))
-        assert eps < faithful_bound(e_bf16)
-        assert np.max(np.abs(gc - out_p["conf"])) < conf_tolerance(e_bf16)
-        dec = vocab_margin(out_f["logits"], mask) >= near_tie(eps)
-        assert np.array_equal(gp[dec], out_f["pred"][dec])
-        # select on the GPU's verification outputs
+        st = check_forward(s, rbt, gc, gp, label=f"iteration {steps}")
+        # select on the GPU's verification outputs: the oracle's Eq. 2 on the
+        # same confidences decides the winner; the scores also within the
+        # end-to-end tolerance of the pure oracle's
         scores = torch.empty(nb, dtype=F32, device="cuda")
         win = torch.empty(1, dtype=I32, device="cuda")
         nt = torch.empty(L, dtype=I32, device="cuda")
@@ -72,15 +70,18 @@ def test_teacher_forced_iterations(cfgname, P, L, k, tau):
         nu = torch.empty(1, dtype=I32, device="cuda")
         lp.lopa_branch_confidence_select(_d(rbt.ravel(), I32), conf_b, pred_b, _d(rva, U8), nb, L,
                                          mask, scores, win, nt, ncf, npd, nu)
-        rs, rw = lopa.select(rbt, out_f["conf"], rva, mask)
         gs = scores.cpu().numpy().astype(np.float64)
-        fin = np.isfinite(rs)
-        s_eps = np.max(np.abs(gs[fin] - rs[fin]), initial=0)
-        assert s_eps < faithful_bound(e_bf16)
+        ts, tw = lopa.select(rbt, gc, rva, mask)
+        ps, _ = lopa.select(rbt, st["pure"]["conf"], rva, mask)
+        fin = np.isfinite(ts)
+        assert np.array_equal(np.isfinite(gs), fin) and np.array_equal(gs[~fin], ts[~fin])
+        assert np.max(np.abs(gs[fin] - ts[fin]), initial=0) <= 1e-5
+        assert np.max(np.abs(gs[fin] - ps[fin]), initial=0) <= conf_tol(s.cfg)
         w = int(win.item())
-        if score_margin(rs) >= near_tie(s_eps):
-            assert np.array_equal(rbt[w], rbt[rw])
+        if score_margin(ts) >= NEAR_TIE:
+            assert np.array_equal(rbt[w], rbt[tw])
             checked += 1
+        rw = lopa.select(rbt, st["faith"]["conf"], rva, mask)[1]
         # commit the oracle's winner and compare the written rows (and re-sync the
         # GPU prefix to the oracle's, as the next iteration is teacher-forced too)
         off = torch.empty(1, dtype=I32, device="cuda")
@@ -88,7 +89,7 @@ def test_teacher_forced_iterations(cfgname, P, L, k, tau):
         assert int(off.item()) == P
         for layer in range(s.cfg["layers"]):
             kk, vv = s.kv.read(layer, P, L)
-            ref = out_f["k"][rw, layer]
+            ref = st["faith"]["k"][rw, layer]
             assert np.max(np.abs(kk.float().cpu().numpy() - ref)) <= 0.05 * max(1.0, np.abs(ref).max())
         state, _ = lopa.lopa_step(s.faith, s.cache_f, P, state, k, tau32)
         s.load_oracle_cache(P + L)
@@ -106,49 +107,66 @@ def _first_divergence(gtrace, otrace):
     return None
 
 
-@pytest.mark.parametrize("cfgname,P,L,k,tau,metric", [
-    ("tiny", 64, 16, 3, 0.9, (0, 4, 0.25)), ("tiny", 32, 16, 0, 0.9, (0, 4, 0.25)),
-    ("small", 100, 32, 7, 0.9, (0, 4, 0.25)), ("small128", 40, 16, 2, 0.7, (0, 4, 0.25)),
-    ("tiny", 64, 16, 3, 0.9, (1, 4, 0.25)), ("tiny", 64, 16, 5, 0.9, (2, 4, 0.25))])
-def test_free_running_block(cfgname, P, L, k, tau, metric):
+# (config, P, L, k, tau, (metric, window, eta), fewest iterations): tau 0.999
+# makes the blocks take many iterations (one or two fills each)
+FREE = [("tiny", 64, 16, 3, 0.9, (0, 4, 0.25), 1), ("tiny", 32, 16, 0, 0.9, (0, 4, 0.25), 1),
+        ("small", 100, 32, 7, 0.9, (0, 4, 0.25), 1), ("small128", 40, 16, 2, 0.7, (0, 4, 0.25), 1),
+        ("tiny", 64, 16, 3, 0.9, (1, 4, 0.25), 1), ("tiny", 64, 16, 5, 0.9, (2, 4, 0.25), 1),
+        ("tiny", 48, 16, 3, 0.999, (0, 4, 0.25), 4), ("small", 64, 32, 7, 0.999, (0, 4, 0.25), 4),
+        ("tiny", 48, 16, 2, 0.999, (1, 3, 0.25), 4)]
+
+
+@pytest.mark.parametrize("cfgname,P,L,k,tau,metric,min_iters", FREE)
+def test_free_running_block(cfgname, P, L, k, tau, metric, min_iters):
     """metric = (branch confidence, window, eta): Eq. 2, or the window minimum /
-    lowest-segment alternatives."""
+    lowest-segment alternatives. The GPU decodes the block on its own (prefix
+    K/V teacher-forced, so the oracle forward of each iteration sees the same
+    prefix); every iteration is then replayed decision by decision."""
     log(f"free-running {cfgname} P={P} L={L} k={k} tau={tau} metric={metric}")
     s = Setup(cfgname, P, L, k)
     dec = s.gpu_prefill(tau)
+    s.load_oracle_cache()
     dec.metric, dec.window, dec.eta = metric[0], metric[1], metric[2]
     gtrace = []
     g_iters = dec.decode_block(P, gtrace)
-    otrace = []
-    o_tokens, o_iters, _ = lopa.decode_block(s.faith, s.cache_f.copy(), P, L, k, f32(tau), otrace,
-                                             metric[0], metric[1], f32(metric[2]))
+    mask, nb, tau32 = s.cfg["mask_id"], k + 1, f32(tau)
     g_tokens = dec.tokens.cpu().numpy()
+    assert not np.any(g_tokens == mask) and len(gtrace) == g_iters >= min_iters
+    excused = 0
+    for t, g in enumerate(gtrace):
+        tokens, conf, pred = (v.numpy() for v in g["state"])
+        # Eq. 1 + lookahead branches from the GPU's own state (fp32 conf)
+        rbt, rfp, rva, rnv = lopa.build_branches(tokens, conf.astype(np.float64), pred, mask, tau32, k)
+        gbt = g["branch_tokens"].numpy()
+        assert np.array_equal(gbt, rbt), f"iteration {t}: branches differ"
+        assert np.array_equal(g["valid"].numpy(), rva) and g["n_valid"] == rnv
+        # the verify forward of these branches against the oracle's
+        gc = g["conf"].numpy().astype(np.float64)
+        gp = g["pred"].numpy()
+        st = check_forward(s, rbt, gc, gp, layers=t == 0, label=f"iteration {t}")
+        # selection from the GPU's confidences; scores also vs the pure oracle's
+        ts, tw = lopa.select(rbt, gc, rva, mask, metric[0], metric[1], f32(metric[2]))
+        ps, _ = lopa.select(rbt, st["pure"]["conf"], rva, mask, metric[0], metric[1], f32(metric[2]))
+        gs = g["scores"].numpy().astype(np.float64)
+        fin = np.isfinite(ts)
+        assert np.array_equal(np.isfinite(gs), fin) and np.array_equal(gs[~fin], ts[~fin])
+        assert np.max(np.abs(gs[fin] - ts[fin]), initial=0) <= 1e-5
+        assert np.max(np.abs(gs[fin] - ps[fin]), initial=0) <= conf_tol(s.cfg)
+        if score_margin(ts) >= NEAR_TIE:
+            assert np.array_equal(rbt[g["winner"]], rbt[tw]), f"iteration {t}: winner differs"
+        else:
+            excused += 1
+        # the next state is the winner's row
+        assert np.array_equal(g["tokens"].numpy(), rbt[g["winner"]])
+    # the oracle's own trajectory (its own forwards): reported, not asserted --
+    # two bf16 computations take different branches where a margin is within
+    # their confidence difference
+    otrace = []
+    o_tokens, o_iters, _ = lopa.decode_block(s.faith, s.cache_f.copy(), P, L, k, tau32, otrace,
+                                             metric[0], metric[1], f32(metric[2]))
     t = _first_divergence(gtrace, otrace)
-    mask = s.cfg["mask_id"]
-    if t is None:
-        assert np.array_equal(g_tokens, o_tokens) and g_iters == o_iters
-        log(f"  identical trajectory, {g_iters} iterations")
-        return
-    # a divergence is allowed only at a near-tie of the oracle's decisions at that iteration
-    o = otrace[t]
-    prev = otrace[t - 1] if t else None
-    if prev is None:
-        st = lopa.init_block(s.faith, s.cache_f, P, L)
-    else:
-        w = prev["winner"]
-        st = (prev["branch_tokens"][w], prev["conf"][w], prev["pred"][w])
-    bm = build_margin(st[0], st[1], mask, f32(tau), k)
-    sm = score_margin(o["scores"])
-    log(f"  diverged at iteration {t}: build margin {bm:.2e}, score margin {sm:.2e}")
-    # no per-step gap can be measured once trajectories run free: use the widest
-    # bound the teacher-forced tests allow
-    tie = near_tie(2 * FAITHFUL_TOL)
-    assert min(bm, sm) < tie or _pred_near_tie(s, st, P, L, tie)
-
-
-def _pred_near_tie(s, state, P, L, tie):
-    out = s.faith.forward_block(state[0][None], P, s.cache_f, keep_hidden=True)
-    return bool(np.any(vocab_margin(out["logits"], s.cfg["mask_id"]) < tie))
+    log(f"  {g_iters} iterations, {excused} winner near-ties; oracle's own trajectory: "
+        + ("identical" if t is None and np.array_equal(g_tokens, o_tokens) else f"diverges at iteration {t}"))
 
 
 # ---------------------------------------------- multi-block window (R27-R30)
@@ -208,21 +226,17 @@ def _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, 
         lp.lopa_build_branches_window(_d(tokens, I32), _d(conf32, F32), _d(pred, I32), Lw, n_el, mask,
                                       tau, k, bt, fp, va, nv)
         rbt, rfp, rva, rnv = lopa.build_branches(tokens, conf32.astype(np.float64), pred, mask, tau32, k, n_el)
-        if build_margin(tokens, conf32, mask, tau32, k, n_el) >= near_tie(0.0):
-            assert np.array_equal(bt.view(nb, Lw).cpu().numpy(), rbt)
-            assert np.array_equal(va.cpu().numpy(), rva) and int(nv.item()) == rnv
+        assert np.array_equal(bt.view(nb, Lw).cpu().numpy(), rbt)
+        assert np.array_equal(va.cpu().numpy(), rva) and int(nv.item()) == rnv
         # the oracle's branches through the GPU forward over the whole window
         obt, n_valid = it["branch_tokens"], it["n_valid"]
         conf_b = torch.empty(nb * Lw, dtype=F32, device="cuda")
         pred_b = torch.empty(nb * Lw, dtype=I32, device="cuda")
         lp.lopa_verify_forward(s.model, s.kv, P_t, _d(obt.ravel(), I32), nb, Lw, conf_b, pred_b)
-        gc = conf_b.view(nb, Lw).cpu().numpy().astype(np.float64)[:n_valid]
-        gp = pred_b.view(nb, Lw).cpu().numpy()[:n_valid]
-        eps = np.max(np.abs(gc - it["conf"][:n_valid]))
-        # the case's own bf16 sensitivity: the pure oracle on the same inputs
-        e_bf16 = np.max(np.abs(it["conf"][:n_valid] - s.pure.forward_block(obt[:n_valid], P_t, cache,
-                                                                            causal_blk=cblk)["conf"]))
-        assert eps < faithful_bound(e_bf16)
+        gc = conf_b.view(nb, Lw).cpu().numpy().astype(np.float64)
+        gp = pred_b.view(nb, Lw).cpu().numpy()
+        check_forward(s, obt, gc, gp, P=P_t, cache_f=cache, causal_blk=cblk,
+                      layers=Lw > L, label=f"window {Lw} rows, prefix {P_t}")
         scores = torch.empty(nb, dtype=F32, device="cuda")
         win = torch.empty(1, dtype=I32, device="cuda")
         nt = torch.empty(Lw, dtype=I32, device="cuda")
@@ -231,9 +245,9 @@ def _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, 
         nu = torch.empty(1, dtype=I32, device="cuda")
         lp.lopa_branch_confidence_select(_d(obt.ravel(), I32), conf_b, pred_b, _d(it["valid"], U8), nb,
                                          Lw, mask, scores, win, nt, ncf, npd, nu)
-        rs = it["scores"]
-        if score_margin(rs) >= near_tie(eps):
-            assert np.array_equal(obt[int(win.item())], obt[it["winner"]])
+        ts, tw = lopa.select(obt, gc, it["valid"], mask)
+        if score_margin(ts) >= NEAR_TIE:
+            assert np.array_equal(obt[int(win.item())], obt[tw])
             checked += 1
         c = it["committed_blocks"]
         if c:
@@ -264,17 +278,37 @@ def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_
     g_tokens = out["tokens"].numpy()
     assert len(g_tokens) == gen and not np.any(g_tokens == mask)
     assert out["forwards"] >= out["iterations"] >= gen // (L * w_max)
+    # replay every iteration's decisions on the GPU's own inputs: the window
+    # state it started from, its forward against the oracle forward of the
+    # same branches over the GPU's own committed prefix (rows [0, P) never
+    # change once committed), and the selection from its confidences
+    from oracle import KVCache
+    cache = KVCache(s.cfg, P + gen)
+    end = P + gen
+    for layer in range(s.cfg["layers"]):
+        kk, vv = s.kv.read(layer, 0, end)
+        cache.k[layer, :, :end] = kk.float().cpu().numpy()
+        cache.v[layer, :, :end] = vv.float().cpu().numpy()
+    cblk = L if block_causal else 0
+    excused = 0
+    for t, g in enumerate(gtrace):
+        tokens, conf, pred = (v.numpy() for v in g["state"])
+        rbt, rfp, rva, rnv = lopa.build_branches(tokens, conf.astype(np.float64), pred, mask, f32(tau), k,
+                                                 g["n_eligible"])
+        assert np.array_equal(g["branch_tokens"].numpy(), rbt), f"iteration {t}: branches differ"
+        assert np.array_equal(g["valid"].numpy(), rva) and g["n_valid"] == rnv
+        gc = g["conf"].numpy().astype(np.float64)
+        check_forward(s, rbt, gc, g["pred"].numpy(), P=g["prefix_len"], cache_f=cache,
+                      causal_blk=cblk, layers=False, label=f"iteration {t}")
+        ts, tw = lopa.select(rbt, gc, rva, mask)
+        if score_margin(ts) >= NEAR_TIE:
+            assert g["winner"] == tw or np.array_equal(rbt[g["winner"]], rbt[tw])
+        else:
+            excused += 1
+        assert np.array_equal(g["tokens"].numpy(), rbt[g["winner"]])
     otrace = []
     res = lopa.decode_window(s.faith, prompt.numpy(), gen, L, k, f32(tau), tau_add, tau_act, w_max,
                              trace=otrace, block_causal=block_causal)
-    for t, (g, o) in enumerate(zip(gtrace, otrace)):
-        ow = o["branch_tokens"][o["winner"]]
-        if not np.array_equal(g["tokens"].numpy(), ow):
-            tokens, conf, pred = o["state"]
-            bm = build_margin(tokens, conf, mask, f32(tau), k, o["n_eligible"])
-            sm = score_margin(o["scores"])
-            log(f"  diverged at iteration {t}: build margin {bm:.2e}, score margin {sm:.2e}")
-            assert min(bm, sm) < near_tie(2 * FAITHFUL_TOL)
-            return
-    assert np.array_equal(g_tokens, res["tokens"]) and out["forwards"] == res["forwards"]
-    log(f"  identical trajectory: {out['iterations']} iterations, {out['forwards']} forwards, TPF {out['tpf']:.2f}")
+    same = np.array_equal(g_tokens, res["tokens"])
+    log(f"  {out['iterations']} iterations, {out['forwards']} forwards, TPF {out['tpf']:.2f}; "
+        f"{excused} winner near-ties; oracle's own trajectory {'identical' if same else 'differs'}")
