@@ -322,6 +322,27 @@ int lopa_debug_hidden(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
                       const int32_t* branch_tokens, int32_t n_branches, int32_t L,
                       int32_t n_layers, float* x_out, void* stream);
 
+/* For callers that cannot allocate device memory where they run the step
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): lopa_verify_forward with the same arguments, outputs and errors,
+ * whose working memory (residual stream, packed GEMM operands, queries,
+ * split-K partial sums, LM-head statistics; the KV cache and staging stay in
+ * kv) lives in one device array compiled into the library, of
+ * LOPA_NOALLOC_MAX_BYTES per GPU, held by every GPU the library runs on until
+ * the process ends. The call allocates nothing and frees nothing; it enqueues
+ * a small fill kernel that zeroes the operands' padding columns, then the
+ * forward. A shape whose working memory exceeds LOPA_NOALLOC_MAX_BYTES
+ * (64 MiB: 256 rows of the Dream-7B or LLaDA-8B shape fit, 512 do not) is
+ * LOPA_ESHAPE before anything is enqueued; the current device must be the
+ * model's (LOPA_EINVAL). Every call on a GPU shares that GPU's array: calls
+ * that overlap on one GPU (other streams or threads) race and give undefined
+ * results; calls ordered on one stream do not. The first call on a device
+ * looks up the array's address there (not inside a capture). */
+#define LOPA_NOALLOC_MAX_BYTES (64ull << 20)
+int lopa_verify_forward_noalloc(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                                const int32_t* branch_tokens, int32_t n_branches, int32_t L,
+                                float* conf, int32_t* pred, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

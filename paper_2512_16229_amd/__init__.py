@@ -175,6 +175,14 @@ def lopa_verify_forward(model: Model, kv: KV, prefix_len, branch_tokens, n_branc
                                    _stream(stream)))
 
 
+def lopa_verify_forward_noalloc(model: Model, kv: KV, prefix_len, branch_tokens, n_branches, L,
+                                conf, pred, stream=None):
+    _check(lib.lopa_verify_forward_noalloc(model.handle, kv.handle, prefix_len,
+                                           _ptr(branch_tokens, I32, "branch_tokens"), n_branches,
+                                           L, _ptr(conf, F32, "conf"), _ptr(pred, I32, "pred"),
+                                           _stream(stream)))
+
+
 def lopa_branch_confidence_select(branch_tokens, conf, pred, valid, n_branches, L, mask_id, scores,
                                   winner, next_tokens, next_conf, next_pred, next_unfilled,
                                   stream=None):

@@ -45,7 +45,7 @@ EXPORTS = ["lopa_model_create", "lopa_model_create_ex", "lopa_model_destroy", "l
            "lopa_commit_kv_rows", "lopa_kv_read", "lopa_kv_write",
            "lopa_kv_read_staging", "lopa_debug_hidden",
            "lopa_kv_set_block_causal", "lopa_kv_profile",
-           "lopa_kv_profile_read"]
+           "lopa_kv_profile_read", "lopa_verify_forward_noalloc"]
 METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
 PRECISIONS = {"bf16": 0, "fp8_mlp": 1, "fp8": 2}
 PROF_KINDS = ["qkv", "attn", "oproj", "gateup", "down", "lmhead", "norm", "merge"]
@@ -81,6 +81,7 @@ def _load():
         "lopa_kv_set_block_causal": (C.c_int, [P, I32]),
         "lopa_kv_profile": (C.c_int, [P, I32]),
         "lopa_kv_profile_read": (C.c_int, [P, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
+        "lopa_verify_forward_noalloc": (C.c_int, [P, P, I32, P, I32, I32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

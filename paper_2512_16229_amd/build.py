@@ -14,7 +14,8 @@ OUT = os.path.join(HERE, "liblopa.so")
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"
 ARCH = os.environ.get("LOPA_ARCH", "gfx950")
 
-SOURCES = ["api.cpp", "step_kernels.hip", "row_kernels.hip", "gemm.hip", "attention.hip"]
+SOURCES = ["api.cpp", "step_kernels.hip", "row_kernels.hip", "gemm.hip", "attention.hip",
+           "noalloc.hip"]
 # attention: scores are never NaN, and without NaN semantics the maximum of
 # scores needs no quieting of its operands
 EXTRA_FLAGS = {"attention.hip": ["-fno-honor-nans"]}

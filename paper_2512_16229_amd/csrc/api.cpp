@@ -15,6 +15,7 @@
 
 #include "../../include/lopa.h"
 #include "kernels.h"
+#include "verify.h"
 
 namespace {
 
@@ -581,7 +582,8 @@ int lopa_build_branches(const int32_t* tokens, const float* conf, const int32_t*
 // copies the fp32 residual stream to x_out instead of producing conf / pred.
 static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
                        const int32_t* branch_tokens, int32_t n_branches, int32_t L, float* conf,
-                       int32_t* pred, void* stream, int stop_layer, float* x_out) {
+                       int32_t* pred, void* stream, int stop_layer, float* x_out,
+                       const VerifyWs& ws) {
   const lopa_model_cfg& c = m->cfg;
   hipStream_t s = (hipStream_t)stream;
   const int M = n_branches * L;
@@ -594,7 +596,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   g.M = M;
   g.Mp = Mp;
   g.mtiles = MT;
-  g.partials = kv->partials;
+  g.partials = ws.partials;
   auto gemm = [&](int epi, const uint16_t* A, const uint16_t* W, int N, int K,
                   const GemmPlan& p) {
     g.A = A;
@@ -621,7 +623,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.f8 = 1;
     g.sa = sa;
     g.sw = sw;
-    g.rowmax = kv->rowmax_dn;
+    g.rowmax = ws.rowmax_dn;
     g.nb = pl.nb;
     g.tiles = pl.tiles;
     g.splits = pl.splits;
@@ -633,14 +635,14 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   { ProfScope ps_(kv, LOPA_PROF_NORM, s);
     if (f8x)
       HIP_TRY(launch_embed_norm8(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M,
-                                 Mp, H, kv->x, kv->a8_gu, kv->sa_gu, s));
+                                 Mp, H, ws.x, ws.a8_gu, ws.sa_gu, s));
     else
       HIP_TRY(launch_embed_norm(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M,
-                                Mp, H, kv->x, kv->abuf, s)); }
+                                Mp, H, ws.x, ws.abuf, s)); }
   AttnArgs at{};
-  at.q = kv->qbuf;
+  at.q = ws.qbuf;
   at.staging = kv->staging;
-  at.out = kv->abuf;
+  at.out = ws.abuf;
   at.nb = n_branches;
   at.L = L;
   at.P = prefix_len;
@@ -659,7 +661,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     const LayerPack& p = m->layers[l];
     g.bias = p.bias;
     g.rope = kv->rope;
-    g.q_out = kv->qbuf;
+    g.q_out = ws.qbuf;
     g.staging = kv->staging;
     g.layer = l;
     g.layers = c.layers;
@@ -671,70 +673,70 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     g.P = prefix_len;
     { ProfScope ps_(kv, LOPA_PROF_QKV, s);
       if (f8x)
-        HIP_TRY(gemm8(EPI_QKV, kv->a8_gu, p.qkv8, m->n_qkv, round512(H), kv->sa_gu, p.sw_qkv,
+        HIP_TRY(gemm8(EPI_QKV, ws.a8_gu, p.qkv8, m->n_qkv, round512(H), ws.sa_gu, p.sw_qkv,
                       plan.qkv));
       else
-        HIP_TRY(gemm(EPI_QKV, kv->abuf, p.qkv, m->n_qkv, H, plan.qkv)); }
+        HIP_TRY(gemm(EPI_QKV, ws.abuf, p.qkv, m->n_qkv, H, plan.qkv)); }
     at.layer = l;
     at.kcache = kv->cache + ((size_t)l * 2 + 0) * c.kv_heads * d * kv->vld;
     at.vcache = kv->cache + ((size_t)l * 2 + 1) * c.kv_heads * d * kv->vld;
     { ProfScope ps_(kv, LOPA_PROF_ATTN, s);
       HIP_TRY(launch_attention(at, s)); }
-    g.x = kv->x;
+    g.x = ws.x;
     { ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
-      HIP_TRY(gemm(EPI_RESID, kv->abuf, p.o, H, c.heads * d, plan.o)); }
-    g.a_out = kv->fbuf;
+      HIP_TRY(gemm(EPI_RESID, ws.abuf, p.o, H, c.heads * d, plan.o)); }
+    g.a_out = ws.fbuf;
     if (m->fp8) {
       // FP8 MLP: the normed rows straight to E4M3 with their scales, gate/up,
       // the SwiGLU output (bf16) requantised per row, down
       { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-        HIP_TRY(launch_resnorm8(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
-                                c.rms_eps, M, Mp, H, kv->x, kv->a8_gu, kv->sa_gu, kv->rowmax_dn,
+        HIP_TRY(launch_resnorm8(ws.partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
+                                c.rms_eps, M, Mp, H, ws.x, ws.a8_gu, ws.sa_gu, ws.rowmax_dn,
                                 s)); }
       { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
-        HIP_TRY(gemm8(EPI_SWIGLU, kv->a8_gu, p.gu8, 2 * F, round512(H), kv->sa_gu, p.sw_gu,
+        HIP_TRY(gemm8(EPI_SWIGLU, ws.a8_gu, p.gu8, 2 * F, round512(H), ws.sa_gu, p.sw_gu,
                       plan.gu)); }
       { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-        HIP_TRY(launch_quant_rows8(kv->fbuf, F, M, Mp, kv->rowmax_dn, kv->a8_dn, kv->sa_dn, s)); }
+        HIP_TRY(launch_quant_rows8(ws.fbuf, F, M, Mp, ws.rowmax_dn, ws.a8_dn, ws.sa_dn, s)); }
       { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
-        HIP_TRY(gemm8(EPI_RESID, kv->a8_dn, p.down8, H, round512(F), kv->sa_dn, p.sw_down,
+        HIP_TRY(gemm8(EPI_RESID, ws.a8_dn, p.down8, H, round512(F), ws.sa_dn, p.sw_down,
                       plan.down)); }
     } else {
       { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-        HIP_TRY(launch_resnorm(kv->partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
-                               c.rms_eps, M, Mp, H, kv->x, kv->abuf, s)); }
+        HIP_TRY(launch_resnorm(ws.partials, plan.o.splits > 1 ? plan.o.splits : 0, p.ln2,
+                               c.rms_eps, M, Mp, H, ws.x, ws.abuf, s)); }
       { ProfScope ps_(kv, LOPA_PROF_GATEUP, s);
-        HIP_TRY(gemm(EPI_SWIGLU, kv->abuf, p.gu, 2 * F, H, plan.gu)); }
+        HIP_TRY(gemm(EPI_SWIGLU, ws.abuf, p.gu, 2 * F, H, plan.gu)); }
       { ProfScope ps_(kv, LOPA_PROF_DOWN, s);
-        HIP_TRY(gemm(EPI_RESID, kv->fbuf, p.down, H, round256(F), plan.down)); }
+        HIP_TRY(gemm(EPI_RESID, ws.fbuf, p.down, H, round256(F), plan.down)); }
     }
     const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
     const int dsplits = plan.down.splits > 1 ? plan.down.splits : 0;
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
       if (f8x)
-        HIP_TRY(launch_resnorm8(kv->partials, dsplits, next_w, c.rms_eps, M, Mp, H, kv->x,
-                                kv->a8_gu, kv->sa_gu, nullptr, s));
+        HIP_TRY(launch_resnorm8(ws.partials, dsplits, next_w, c.rms_eps, M, Mp, H, ws.x,
+                                ws.a8_gu, ws.sa_gu, nullptr, s));
       else
-        HIP_TRY(launch_resnorm(kv->partials, dsplits, next_w, c.rms_eps, M, Mp, H, kv->x,
-                               kv->abuf, s)); }
+        HIP_TRY(launch_resnorm(ws.partials, dsplits, next_w, c.rms_eps, M, Mp, H, ws.x,
+                               ws.abuf, s)); }
   }
   if (stop_layer >= 0) {
-    HIP_TRY(hipMemcpyAsync(x_out, kv->x, (size_t)M * H * 4, hipMemcpyDeviceToDevice, s));
+    HIP_TRY(hipMemcpyAsync(x_out, ws.x, (size_t)M * H * 4, hipMemcpyDeviceToDevice, s));
     return LOPA_OK;
   }
-  g.pm = kv->pm;
-  g.ps = kv->ps;
-  g.pi = kv->pi;
+  g.pm = ws.pm;
+  g.ps = ws.ps;
+  g.pi = ws.pi;
   g.vocab = c.vocab;
   g.mask_id = c.mask_id;
   { ProfScope ps_(kv, LOPA_PROF_LMHEAD, s);
     if (f8x)
-      HIP_TRY(gemm8(EPI_LMHEAD, kv->a8_gu, m->lm8, c.vocab, round512(H), kv->sa_gu, m->sw_lm,
+      HIP_TRY(gemm8(EPI_LMHEAD, ws.a8_gu, m->lm8, c.vocab, round512(H), ws.sa_gu, m->sw_lm,
                     plan.lm));
     else
-      HIP_TRY(gemm(EPI_LMHEAD, kv->abuf, m->lm, c.vocab, H, plan.lm)); }
+      HIP_TRY(gemm(EPI_LMHEAD, ws.abuf, m->lm, c.vocab, H, plan.lm)); }
   { ProfScope ps_(kv, LOPA_PROF_MERGE, s);
-    HIP_TRY(launch_lm_merge(kv->pm, kv->ps, kv->pi, M, m->tiles_lm, conf, pred, s)); }
+    HIP_TRY(launch_lm_merge(ws.pm, ws.ps, ws.pi, M, m->tiles_lm, conf, pred, s)); }
   kv->last_nb = n_branches;
   kv->last_L = L;
   kv->last_P = prefix_len;
@@ -758,14 +760,32 @@ static int check_verify(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   return LOPA_OK;
 }
 
+// the working buffers the KV handle owns (allocated by lopa_kv_create)
+static VerifyWs kv_ws(const lopa_kv* kv) {
+  VerifyWs w;
+  w.x = kv->x;
+  w.abuf = kv->abuf;
+  w.fbuf = kv->fbuf;
+  w.qbuf = kv->qbuf;
+  w.partials = kv->partials;
+  w.pm = kv->pm;
+  w.ps = kv->ps;
+  w.pi = kv->pi;
+  w.a8_gu = kv->a8_gu;
+  w.a8_dn = kv->a8_dn;
+  w.sa_gu = kv->sa_gu;
+  w.sa_dn = kv->sa_dn;
+  w.rowmax_dn = kv->rowmax_dn;
+  return w;
+}
+
 int lopa_verify_forward(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
                         const int32_t* branch_tokens, int32_t n_branches, int32_t L, float* conf,
                         int32_t* pred, void* stream) {
-  if (!conf || !pred) return fail(LOPA_EINVAL, "null pointer argument");
-  int rc = check_verify(m, kv, prefix_len, branch_tokens, n_branches, L);
+  int rc = verify_check(m, kv, prefix_len, branch_tokens, n_branches, L, conf, pred);
   if (rc) return rc;
   return verify_impl(m, kv, prefix_len, branch_tokens, n_branches, L, conf, pred, stream, -1,
-                     nullptr);
+                     nullptr, kv_ws(kv));
 }
 
 int lopa_debug_hidden(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
@@ -776,7 +796,7 @@ int lopa_debug_hidden(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   if (rc) return rc;
   if (n_layers < 0 || n_layers > m->cfg.layers) return fail(LOPA_EINVAL, "n_layers out of range");
   return verify_impl(m, kv, prefix_len, branch_tokens, n_branches, L, nullptr, nullptr, stream,
-                     n_layers, x_out);
+                     n_layers, x_out, kv_ws(kv));
 }
 
 int lopa_branch_confidence_select_metric(const int32_t* branch_tokens, const float* conf,
@@ -925,3 +945,112 @@ int lopa_kv_profile_read(lopa_kv* kv, double* total_ms, int64_t* launches) {
 }
 
 }  // extern "C"
+
+// ------------------------------------------------- workspace (internal)
+int model_device(const lopa_model* m) { return m->device; }
+
+int lopa_fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int verify_check(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                 const int32_t* branch_tokens, int32_t n_branches, int32_t L, float* conf,
+                 int32_t* pred) {
+  if (!conf || !pred) return fail(LOPA_EINVAL, "null pointer argument");
+  return check_verify(m, kv, prefix_len, branch_tokens, n_branches, L);
+}
+
+int verify_with_ws(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
+                   const int32_t* branch_tokens, int32_t n_branches, int32_t L, float* conf,
+                   int32_t* pred, void* stream, const VerifyWs& ws) {
+  return verify_impl(m, kv, prefix_len, branch_tokens, n_branches, L, conf, pred, stream, -1,
+                     nullptr, ws);
+}
+
+namespace {
+// the regions of a VerifyWs for nb x L rows, in carving order (bytes, each
+// rounded up to 256): x, abuf, fbuf, qbuf, partials, pm, ps, pi, then the FP8
+// operands of FP8 models
+struct WsLayout {
+  size_t sz[13] = {};
+};
+WsLayout ws_layout(const lopa_model* m, int32_t nb, int32_t L) {
+  const lopa_model_cfg& c = m->cfg;
+  const size_t rows = (size_t)padded_rows(nb * L);
+  const int MT = (int)(rows / 256);
+  const StepPlans p = step_plans(m, MT);
+  WsLayout w;
+  w.sz[0] = rows * c.hidden * 4;
+  w.sz[1] = rows * c.hidden * 2;
+  w.sz[2] = rows * round256(c.ffn) * 2;
+  w.sz[3] = (size_t)nb * c.heads * L * c.head_dim * 2;
+  w.sz[4] = std::max({(size_t)16, plan_partial_bytes(EPI_QKV, p.qkv, MT),
+                      plan_partial_bytes(EPI_RESID, p.o, MT), plan_partial_bytes(EPI_RESID, p.down, MT)});
+  w.sz[5] = w.sz[6] = w.sz[7] = rows * m->tiles_lm * 4;
+  if (m->fp8) {
+    w.sz[8] = rows * round512(c.hidden);
+    w.sz[9] = rows * round512(c.ffn);
+    w.sz[10] = w.sz[11] = w.sz[12] = rows * 4;
+  }
+  for (size_t& v : w.sz) v = (v + 255) / 256 * 256;
+  return w;
+}
+}  // namespace
+
+size_t verify_ws_bytes(const lopa_model* m, int32_t n_branches, int32_t L) {
+  size_t t = 0;
+  for (size_t v : ws_layout(m, n_branches, L).sz) t += v;
+  return t;
+}
+
+VerifyWs verify_ws_carve(const lopa_model* m, int32_t n_branches, int32_t L, char* base) {
+  const WsLayout w = ws_layout(m, n_branches, L);
+  char* r[13];
+  for (int i = 0; i < 13; ++i) {
+    r[i] = base;
+    base += w.sz[i];
+  }
+  VerifyWs ws;
+  ws.x = (float*)r[0];
+  ws.abuf = (uint16_t*)r[1];
+  ws.fbuf = (uint16_t*)r[2];
+  ws.qbuf = (uint16_t*)r[3];
+  ws.partials = (float*)r[4];
+  ws.pm = (float*)r[5];
+  ws.ps = (float*)r[6];
+  ws.pi = (int32_t*)r[7];
+  if (m->fp8) {
+    ws.a8_gu = (uint8_t*)r[8];
+    ws.a8_dn = (uint8_t*)r[9];
+    ws.sa_gu = (float*)r[10];
+    ws.sa_dn = (float*)r[11];
+    ws.rowmax_dn = (uint32_t*)r[12];
+  }
+  return ws;
+}
+
+int verify_ws_clear_padding(const lopa_model* m, int32_t n_branches, int32_t L, const VerifyWs& ws,
+                            hipStream_t s) {
+  // packed operands are [column block][row block] fragments, so a matrix's
+  // padding columns are one contiguous tail: bf16 blocks of 32 columns x 16
+  // rows (1 KiB), E4M3 blocks of 64 columns x 16 rows (1 KiB)
+  const lopa_model_cfg& c = m->cfg;
+  const size_t rb = (size_t)padded_rows(n_branches * L) / 16;
+  auto tail = [&](void* buf, size_t cols, size_t padded, size_t per_block) -> hipError_t {
+    if (padded == cols) return hipSuccess;
+    const size_t from = cols / per_block * rb * 1024, to = padded / per_block * rb * 1024;
+    return launch_fill_zero((char*)buf + from, to - from, s);
+  };
+  hipError_t e;
+  if ((e = tail(ws.fbuf, c.ffn, round256(c.ffn), 32)) != hipSuccess ||
+      (m->fp8 && ((e = tail(ws.a8_gu, c.hidden, round512(c.hidden), 64)) != hipSuccess ||
+                  (e = tail(ws.a8_dn, c.ffn, round512(c.ffn), 64)) != hipSuccess)))
+    return fail(LOPA_EHIP, "clearing the padding columns: %s", hipGetErrorString(e));
+  return LOPA_OK;
+}

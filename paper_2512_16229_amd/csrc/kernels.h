@@ -43,6 +43,9 @@ hipError_t launch_repack(const uint16_t* s0, int r0, const uint16_t* s1, int r1,
                          const uint16_t* s2, int r2, int K, int KP, int blocks, int nb, int pairs,
                          uint16_t* dst, hipStream_t s);
 hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_t s);
+// bytes [0, bytes) of device memory p set to zero by a kernel (p and bytes
+// multiples of 16)
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 
 // ---------------------------------------------------------------- per-row
 // x[r] = embed[tokens[r]] (fp32) and a[r] = pack(rmsnorm(x[r]) * w) for r < M.

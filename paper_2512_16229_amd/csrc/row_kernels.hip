@@ -509,3 +509,18 @@ hipError_t launch_bf16_to_f32(const uint16_t* src, float* dst, int n, hipStream_
   hipLaunchKernelGGL(bf16_to_f32_kernel, dim3((n + 255) / 256), dim3(256), 0, s, src, dst, n);
   return hipGetLastError();
 }
+
+// bytes [0, n) of p set to zero, 16 bytes per thread (p and n multiples of 16)
+__global__ __launch_bounds__(256) void fill_zero_kernel(uint4* p, int64_t n16) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n16) p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+  if (bytes == 0) return hipSuccess;
+  if (((uintptr_t)p | bytes) & 15) return hipErrorInvalidValue;
+  const int64_t n16 = (int64_t)(bytes / 16);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n16 + 255) / 256)), dim3(256), 0, s,
+                     (uint4*)p, n16);
+  return hipGetLastError();
+}

@@ -56,6 +56,8 @@ def test_build_branches_validation(lp, L, mask, tau, k, code):
 def test_null_pointers(lp):
     assert lp.lib.lopa_build_branches(None, FAKE, FAKE, 16, 5, 0.9, 3, FAKE, FAKE, FAKE, FAKE, None) == -1
     assert lp.lib.lopa_verify_forward(None, None, 0, FAKE, 1, 16, FAKE, FAKE, None) == -1
+    assert lp.lib.lopa_verify_forward_noalloc(None, None, 0, FAKE, 1, 16, FAKE, FAKE, None) == -1
+    assert lp.lib.lopa_verify_forward_noalloc(FAKE, FAKE, 0, FAKE, 1, 16, None, FAKE, None) == -1
     assert lp.lib.lopa_branch_confidence_select(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, FAKE, None,
                                                 FAKE, FAKE, FAKE, FAKE, None) == -1
     assert lp.lib.lopa_commit_kv(None, FAKE, 0, 16, FAKE, None) == -1
