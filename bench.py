@@ -8,7 +8,12 @@ uniform-random prompt), block 32, k = 7 (8 branches, 256 rows), tau = 0.9. The
 timed state is the block's first iteration (all 32 positions masked, conf /
 pred from the initial forward), replayed K times (commit rewrites the same rows).
 
-Prints one JSON line: value = branch-tokens/s = 8 * 32 / step seconds.
+Prints one JSON line: value = branch-tokens/s = 8 * 32 / mean step seconds,
+with the median / p10 / p90 of the per-step times (an event before every step),
+per-kind launch times, the gate/up roofline, end-to-end decode figures, the
+FP8 variants, three further shapes (the 2-layer tiny model at prefix 64, k = 3;
+the same 7B model at prefix 2048, k = 15; the LLaDA-8B layout at prefix 1024,
+k = 7) and the float64 oracle's time for the same whole step on the host CPU.
 """
 from __future__ import annotations
 
@@ -172,56 +177,221 @@ def hbm_counter_run(cfg, P, L, k, reps=3):
     print(json.dumps({"verify_forwards": reps, "rows": nb * L, "prefix": P}))
 
 
-def cpu_baseline(cfg_full, weights_dev, P, L, k, layers_sample=4, min_seconds=10.0, max_reps=8):
-    """Time the oracle (float64 numpy) on a bounded sample of the same step:
-    `layers_sample` decoder layers of the full shape + the LM head and softmax for
-    all (k+1)*L rows, against a random prefix cache; the layer pass is repeated
-    until about `min_seconds` of CPU work, and the mean is scaled to all layers."""
+def host_info():
+    """The CPU model, the BLAS library numpy calls (and its thread count) and
+    the cores this process may run on."""
+    import subprocess
+    model = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except (OSError, subprocess.SubprocessError):
+        pass
+    blas = []
+    try:
+        import numpy  # noqa: F401  (loads the BLAS that threadpoolctl inspects)
+        from threadpoolctl import threadpool_info
+        blas = [{"api": i.get("internal_api"), "version": i.get("version"),
+                 "threads": i.get("num_threads")}
+                for i in threadpool_info() if i.get("user_api") == "blas"]
+    except ImportError:
+        pass
+    return {"cpu_model": model, "blas": blas, "affinity_cores": len(os.sched_getaffinity(0))}
+
+
+class _HostLayers:
+    """The device layers as float64 host tensors, converted on access."""
+
+    def __init__(self, layers):
+        self.layers = layers
+
+    def __len__(self):
+        return len(self.layers)
+
+    def __getitem__(self, i):
+        return {kk: v.double().cpu() for kk, v in self.layers[i].items()}
+
+
+def cpu_baseline(cfg, weights_dev, state, P, L, k, tau, runs=3):
+    """Time the oracle (float64 numpy, as it stands) on the same step: one
+    LoPA iteration (build, batched forward of all k+1 branches through every
+    layer and the LM head, select, commit) from the GPU's first-iteration
+    state, against a random prefix cache of length P. Median of `runs` runs.
+    The weights are converted to float64 host arrays before the timed region
+    when host memory allows, else one layer at a time inside it (said in the
+    sample text)."""
     import numpy as np
-    import torch
+    import psutil
 
     import synth
     from oracle import KVCache, OracleModel
+    from oracle.lopa import lopa_step
 
-    cfg = dict(cfg_full)
-    cfg["layers"] = layers_sample
-    host = {"embed": weights_dev["embed"].float().cpu(),
-            "layers": [{kk: v.float().cpu() for kk, v in weights_dev["layers"][i].items()}
-                       for i in range(layers_sample)],
-            "final_norm": weights_dev["final_norm"].float().cpu(),
-            "lm_head": weights_dev["lm_head"].float().cpu()}
-    model = OracleModel(cfg, host, "pure")
+    n_layer = sum(v.numel() for v in weights_dev["layers"][0].values())
+    need = 8 * (cfg["layers"] * n_layer + weights_dev["embed"].numel() +
+                weights_dev["lm_head"].numel())
+    resident = psutil.virtual_memory().available > 1.25 * need + (16 << 30)
+    host = {"embed": weights_dev["embed"].double().cpu(),
+            "layers": _HostLayers(weights_dev["layers"]),
+            "final_norm": weights_dev["final_norm"].double().cpu(),
+            "lm_head": weights_dev["lm_head"].double().cpu()}
+    model = OracleModel(cfg, host, "pure", keep_layers=True if resident else 1)
     del host
+    t0 = time.perf_counter()
+    if resident:
+        for i in range(cfg["layers"]):
+            model.layer(i)
+    t_conv = time.perf_counter() - t0
+    print(f"cpu baseline: weights {'converted' if resident else 'left bf16'} in {t_conv:.1f}s",
+          file=sys.stderr, flush=True)
     cache = KVCache(cfg, P + L)
     g = synth.irwin_hall(synth.stream_key(7, 1), cache.k[:, :, :P].size, 1.0).double().numpy()
     cache.k[:, :, :P] = g.reshape(cache.k[:, :, :P].shape)
     cache.v[:, :, :P] = -g.reshape(cache.v[:, :, :P].shape)
-    nb = k + 1
-    tokens = synth.prompt(cfg, nb * L, seed=3).numpy().reshape(nb, L)
-    tokens[:, ::2] = cfg["mask_id"]
-    threads = len(os.sched_getaffinity(0))
-    torch.set_num_threads(threads)
-    # layers (repeated for a stable mean)
-    t_all, reps = 0.0, 0
-    while reps < max_reps and (reps == 0 or t_all < min_seconds):
+    st = (np.asarray(state[0], dtype=np.int64), np.asarray(state[1], dtype=np.float64),
+          np.asarray(state[2], dtype=np.int64))
+    times = []
+    for _ in range(runs):
         t0 = time.perf_counter()
-        out = model.forward_block(tokens, P, cache, n_layers=layers_sample)
-        t_all += time.perf_counter() - t0
-        reps += 1
-    t_layers = t_all / reps
-    # LM head + softmax for every row (final norm included)
-    from oracle.model import confidence, rms_norm
-    t0 = time.perf_counter()
-    hf = rms_norm(out["x"], model.final_norm, cfg["rms_eps"])
-    confidence(hf @ model.lm_head.T, cfg["mask_id"])
-    t_head = time.perf_counter() - t0
-    step_s = t_layers / layers_sample * cfg_full["layers"] + t_head
-    return {"value": nb * L / step_s, "unit": "branch-tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": (f"float64 numpy oracle, {layers_sample} of {cfg_full['layers']} decoder layers "
-                       f"+ LM head/softmax of the Dream-7B shape at {nb}x{L} rows, prefix {P}; "
-                       f"mean of {reps} runs {t_layers:.2f}s layers + {t_head:.2f}s head, scaled to "
-                       f"{step_s:.1f}s per step")}
+        lopa_step(model, cache, P, st, k, tau)
+        times.append(time.perf_counter() - t0)
+        print(f"cpu baseline: oracle step {len(times)} in {times[-1]:.2f}s", file=sys.stderr,
+              flush=True)
+    step_s = sorted(times)[len(times) // 2]
+    info = host_info()
+    threads = max([b["threads"] for b in info["blas"] if b["threads"]] or [1])
+    nb = k + 1
+    return {"value": round(nb * L / step_s, 3), "unit": "branch-tokens/s", "cores": threads,
+            "kind": "oracle", "ms_per_step": round(step_s * 1e3, 1),
+            "runs_s": [round(t, 3) for t in times],
+            "cpu_model": info["cpu_model"], "blas": info["blas"],
+            "affinity_cores": info["affinity_cores"],
+            "sample": (f"the whole step, not a sample: float64 numpy oracle, one LoPA iteration "
+                       f"(build, forward of {nb}x{L} rows through all {cfg['layers']} layers + "
+                       f"LM head / softmax, select, commit) on the {cfg['name']} shape, prefix {P} "
+                       f"(random cache), median of {runs} runs; weights "
+                       + (f"converted to float64 before the timed region ({t_conv:.1f}s)"
+                          if resident else "upcast from bf16 one layer at a time inside it"))}
+
+
+def cpu_tiny_step(cfg, weights_dev, state, P, L, k, tau, runs=20):
+    """The oracle's step time on a small shape (median of `runs`, seconds)."""
+    import numpy as np
+
+    from oracle import KVCache, OracleModel
+    from oracle.lopa import lopa_step
+
+    host = {"embed": weights_dev["embed"].double().cpu(),
+            "layers": [{kk: v.double().cpu() for kk, v in lw.items()}
+                       for lw in weights_dev["layers"]],
+            "final_norm": weights_dev["final_norm"].double().cpu(),
+            "lm_head": weights_dev["lm_head"].double().cpu()}
+    model = OracleModel(cfg, host, "pure")
+    cache = KVCache(cfg, P + L)
+    rng = np.random.default_rng(7)
+    cache.k[:, :, :P] = rng.standard_normal(cache.k[:, :, :P].shape)
+    cache.v[:, :, :P] = rng.standard_normal(cache.v[:, :, :P].shape)
+    st = (np.asarray(state[0], dtype=np.int64), np.asarray(state[1], dtype=np.float64),
+          np.asarray(state[2], dtype=np.int64))
+    times = []
+    for _ in range(runs):
+        t0 = time.perf_counter()
+        lopa_step(model, cache, P, st, k, tau)
+        times.append(time.perf_counter() - t0)
+    return sorted(times)[runs // 2]
+
+
+class StepRunner:
+    """The timed workload: the four calls of one LoPA iteration (build, verify
+    forward of all k+1 branches, select, commit) on the block's first state
+    (all L positions masked, conf / pred from the initial forward), replayed;
+    the commit rewrites the same cache rows, so every replay is the same step."""
+
+    def __init__(self, lp, synth, model, cfg, P, L, k, tau):
+        import torch
+        self.lp, self.model, self.cfg = lp, model, cfg
+        self.P, self.L, self.k, self.tau, self.nb = P, L, k, tau, k + 1
+        dev = "cuda"
+        self.kv = lp.KV(model, P + L, self.nb, L)
+        dec = lp.Decoder(model, self.kv, L, k, tau)
+        assert dec.prefill(synth.prompt(cfg, P, device=dev)) == P
+        dec.init_block(P)
+        self.dec = dec
+        i32 = dict(dtype=torch.int32, device=dev)
+        nb = self.nb
+        self.tokens, self.conf, self.pred = dec.tokens.clone(), dec.conf.clone(), dec.pred.clone()
+        self.bt, self.fp = torch.empty(nb * L, **i32), torch.empty(nb, **i32)
+        self.va, self.nv = torch.empty(nb, dtype=torch.uint8, device=dev), torch.empty(1, **i32)
+        self.cb = torch.empty(nb * L, dtype=torch.float32, device=dev)
+        self.pb = torch.empty(nb * L, **i32)
+        self.sc, self.win = torch.empty(nb, dtype=torch.float32, device=dev), torch.empty(1, **i32)
+        self.nt, self.nc = torch.empty(L, **i32), torch.empty(L, dtype=torch.float32, device=dev)
+        self.npd, self.nu, self.off = torch.empty(L, **i32), torch.empty(1, **i32), torch.empty(1, **i32)
+
+    def step(self):
+        lp, L, k, nb, P, mask = self.lp, self.L, self.k, self.nb, self.P, self.cfg["mask_id"]
+        lp.lopa_build_branches(self.tokens, self.conf, self.pred, L, mask, self.tau, k, self.bt,
+                               self.fp, self.va, self.nv)
+        lp.lopa_verify_forward(self.model, self.kv, P, self.bt, nb, L, self.cb, self.pb)
+        lp.lopa_branch_confidence_select(self.bt, self.cb, self.pb, self.va, nb, L, mask, self.sc,
+                                         self.win, self.nt, self.nc, self.npd, self.nu)
+        lp.lopa_commit_kv(self.kv, self.win, P, L, self.off)
+
+    def time(self, steps, warmup):
+        """Per-step times from an event before each step and after the last:
+        mean over the run (= (last - first) / steps) and the step quantiles."""
+        import torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        ev[0].record()
+        for i in range(steps):
+            self.step()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        per = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+        q = lambda f: per[min(steps - 1, int(round(f * (steps - 1))))]
+        return {"mean": ev[0].elapsed_time(ev[steps]) / steps, "median": q(0.5), "p10": q(0.1),
+                "p90": q(0.9), "steps": steps}
+
+    def kinds(self, steps):
+        """Per-kind launch times (HIP events on the library's stream) per step."""
+        import torch
+        self.kv.profile(self.lp.PROF_KINDS)
+        for _ in range(steps):
+            self.step()
+        torch.cuda.synchronize()
+        prof = self.kv.profile_read()
+        self.kv.profile(())
+        return {kd: round(t / steps, 4) for kd, (t, n) in prof.items()}
+
+
+def shape_figure(lp, synth, model, cfg, P, L, k, tau, steps, warmup, what, precision="bf16"):
+    """One line per further measured shape: ms/step (mean, median, p10, p90),
+    branch-tokens/s, the step's algorithmic HBM bytes and FLOPs against the
+    peaks, per-kind times."""
+    import torch
+    run = StepRunner(lp, synth, model, cfg, P, L, k, tau)
+    t = run.time(steps, warmup)
+    kinds = run.kinds(steps)
+    nb = k + 1
+    sb, sf = step_bytes(cfg, P, L, nb, precision), step_flops(cfg, P, L, nb)
+    ms = t["mean"]
+    out = {"workload": what, "ms_per_step": round(ms, 4),
+           "ms_median": round(t["median"], 4), "ms_p10": round(t["p10"], 4),
+           "ms_p90": round(t["p90"], 4), "steps": t["steps"],
+           "branch_tokens_per_s": round(nb * L / (ms * 1e-3), 1),
+           "step_roofline": {"hbm_bytes": sb, "flops": sf,
+                             "hbm_frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                             "mfma_frac": round(sf / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)},
+           "kernel_ms_per_step": kinds}
+    del run
+    torch.cuda.empty_cache()
+    return out
 
 
 def e2e_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7, tau=0.9):
@@ -300,61 +470,31 @@ def fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, steps, warmup, precision):
     also QKV and the LM head): a second model from the same weights; ms/step,
     branch-tokens/s and per-kind times."""
     import torch
-    nb, dev = k + 1, "cuda"
     model = lp.Model(cfg, w, precision=precision)
-    kv = lp.KV(model, P + L, nb, L)
-    dec = lp.Decoder(model, kv, L, k, tau)
-    assert dec.prefill(synth.prompt(cfg, P, device=dev)) == P
-    dec.init_block(P)
-    i32 = dict(dtype=torch.int32, device=dev)
-    tokens, conf, pred = dec.tokens.clone(), dec.conf.clone(), dec.pred.clone()
-    bt, fp = torch.empty(nb * L, **i32), torch.empty(nb, **i32)
-    va, nv = torch.empty(nb, dtype=torch.uint8, device=dev), torch.empty(1, **i32)
-    cb, pb = torch.empty(nb * L, dtype=torch.float32, device=dev), torch.empty(nb * L, **i32)
-    sc, win = torch.empty(nb, dtype=torch.float32, device=dev), torch.empty(1, **i32)
-    nt, nc = torch.empty(L, **i32), torch.empty(L, dtype=torch.float32, device=dev)
-    npd, nu, off = torch.empty(L, **i32), torch.empty(1, **i32), torch.empty(1, **i32)
-    mask = cfg["mask_id"]
-
-    def step():
-        lp.lopa_build_branches(tokens, conf, pred, L, mask, tau, k, bt, fp, va, nv)
-        lp.lopa_verify_forward(model, kv, P, bt, nb, L, cb, pb)
-        lp.lopa_branch_confidence_select(bt, cb, pb, va, nb, L, mask, sc, win, nt, nc, npd, nu)
-        lp.lopa_commit_kv(kv, win, P, L, off)
-
-    for _ in range(warmup):
-        step()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / steps
-    kv.profile(lp.PROF_KINDS)
-    for _ in range(steps):
-        step()
-    torch.cuda.synchronize()
-    prof = kv.profile_read()
-    kv.profile(())
     what = ("gate / up / down" if precision == "fp8_mlp"
             else "QKV, gate / up / down and the LM head")
     rest = ("attention, QKV / O and the LM head bf16" if precision == "fp8_mlp"
             else "attention and the output projection bf16")
-    out = {"workload": f"the headline step with {what} in W8A8 E4M3 (per-channel weight "
-                       f"and per-row activation scales); {rest}",
-           "ms_per_step": round(ms, 4), "branch_tokens_per_s": round(nb * L / (ms * 1e-3), 1),
-           "kernel_ms_per_step": {kd: round(t / steps, 4) for kd, (t, n) in prof.items()}}
-    del dec, kv, model
+    out = shape_figure(lp, synth, model, cfg, P, L, k, tau, steps, warmup,
+                       f"the headline step with {what} in W8A8 E4M3 (per-channel weight "
+                       f"and per-row activation scales); {rest}", precision)
+    del model
     torch.cuda.empty_cache()
     return out
+
+
+def describe(cfg, P, L, k, tau):
+    nb = k + 1
+    return (f"LoPA verify step, {cfg['name']} shape ({cfg['layers']}L H{cfg['hidden']} "
+            f"{cfg['heads']}q/{cfg['kv_heads']}kv d{cfg['head_dim']} F{cfg['ffn']} "
+            f"V{cfg['vocab']}), random bf16 weights, prefix {P}, block {L}, "
+            f"k={k} ({nb} branches, {nb * L} rows), tau {tau}")
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="dream7b", help="synth config name (model shape)")
     ap.add_argument("--prefix", type=int, default=512)
@@ -362,8 +502,10 @@ def main():
     ap.add_argument("--k", type=int, default=7)
     ap.add_argument("--tau", type=float, default=0.9)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=4)
-    ap.add_argument("--no-e2e", action="store_true", help="skip the end-to-end decode run")
+    ap.add_argument("--cpu-runs", type=int, default=3)
+    ap.add_argument("--no-e2e", action="store_true", help="skip the end-to-end decode runs")
+    ap.add_argument("--no-shapes", action="store_true",
+                    help="skip the further shapes (tiny; k=15 at prefix 2048; LLaDA-8B)")
     ap.add_argument("--precision", default="bf16", choices=["bf16", "fp8_mlp", "fp8"],
                     help="projection precision of the timed model (the headline is bf16; "
                          "fp8_mlp: gate / up / down in W8A8 E4M3; fp8: also QKV and the LM head)")
@@ -410,65 +552,29 @@ def main():
     t0 = time.perf_counter()
     model = lp.Model(cfg, w, precision=args.precision)
     log(f"model repacked in {time.perf_counter() - t0:.1f}s ({args.precision})")
-    kv = lp.KV(model, P + L, nb, L)
-    dec = lp.Decoder(model, kv, L, k, tau)
     t0 = time.perf_counter()
-    assert dec.prefill(synth.prompt(cfg, P, device=dev)) == P
-    dec.init_block(P)
+    run = StepRunner(lp, synth, model, cfg, P, L, k, tau)
     torch.cuda.synchronize()
     log(f"prefill of {P} positions + initial forward in {time.perf_counter() - t0:.1f}s")
 
-    i32 = dict(dtype=torch.int32, device=dev)
-    tokens, conf, pred = dec.tokens.clone(), dec.conf.clone(), dec.pred.clone()
-    bt = torch.empty(nb * L, **i32)
-    fp = torch.empty(nb, **i32)
-    va = torch.empty(nb, dtype=torch.uint8, device=dev)
-    nv = torch.empty(1, **i32)
-    cb = torch.empty(nb * L, dtype=torch.float32, device=dev)
-    pb = torch.empty(nb * L, **i32)
-    sc = torch.empty(nb, dtype=torch.float32, device=dev)
-    win = torch.empty(1, **i32)
-    nt, nc, npd, nu = (torch.empty(L, **i32), torch.empty(L, dtype=torch.float32, device=dev),
-                       torch.empty(L, **i32), torch.empty(1, **i32))
-    off = torch.empty(1, **i32)
-    mask = cfg["mask_id"]
-
-    def step():
-        lp.lopa_build_branches(tokens, conf, pred, L, mask, tau, k, bt, fp, va, nv)
-        lp.lopa_verify_forward(model, kv, P, bt, nb, L, cb, pb)
-        lp.lopa_branch_confidence_select(bt, cb, pb, va, nb, L, mask, sc, win, nt, nc, npd, nu)
-        lp.lopa_commit_kv(kv, win, P, L, off)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
-    ev0.record()
-    for _ in range(args.steps):
-        step()
-    ev1.record()
-    torch.cuda.synchronize()
+    t = run.time(args.steps, args.warmup)
     wall = time.perf_counter() - t0
-    ms = ev0.elapsed_time(ev1) / args.steps
-    log(f"{args.steps} steps: {ms:.3f} ms/step (events), {wall / args.steps * 1e3:.3f} ms/step (wall)")
+    ms = t["mean"]
+    log(f"{args.steps} steps: {ms:.3f} ms/step mean, median {t['median']:.3f}, p10 {t['p10']:.3f}, "
+        f"p90 {t['p90']:.3f} (events); {wall / (args.steps + args.warmup) * 1e3:.3f} ms/step (wall)")
 
     # launch times with HIP events on the library's stream: first the gate/up
     # launches alone (the roofline kernel; one event pair per launch), then
     # every kind for the per-step breakdown
-    kv.profile(("gateup",))
+    run.kv.profile(("gateup",))
     for _ in range(args.steps):
-        step()
+        run.step()
     torch.cuda.synchronize()
-    t, n = kv.profile_read()["gateup"]
-    gu_ms = t / n
-    kv.profile(lp.PROF_KINDS)
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    prof = kv.profile_read()
-    kv.profile(())
-    per_step_ms = {kd: t / args.steps for kd, (t, n) in prof.items()}
+    tg, n = run.kv.profile_read()["gateup"]
+    gu_ms = tg / n
+    run.kv.profile(())
+    per_step_ms = run.kinds(args.steps)
     log("per-step ms by kind: " + ", ".join(f"{kd} {v:.3f}" for kd, v in per_step_ms.items()))
 
     # the box's own copy bandwidth (device-to-device copy of 1 GiB, read + write
@@ -495,14 +601,13 @@ def main():
         "unit": "branch-tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
+        "ms_median": round(t["median"], 4), "ms_p10": round(t["p10"], 4),
+        "ms_p90": round(t["p90"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": {"bf16": "bf16", "fp8_mlp": "bf16 + fp8(e4m3) MLP",
                   "fp8": "bf16 + fp8(e4m3) QKV/MLP/LM head"}[args.precision], "data": "synthetic",
-        "config": {"workload": (f"LoPA verify step, {args.config} shape ({cfg['layers']}L H{cfg['hidden']} "
-                                f"{cfg['heads']}q/{cfg['kv_heads']}kv d{cfg['head_dim']} F{cfg['ffn']} "
-                                f"V{cfg['vocab']}), random bf16 weights, prefix {P}, block {L}, "
-                                f"k={k} ({nb} branches, {M} rows), tau {tau}"),
-                   "prefix": P, "block": L, "k": k, "rows": M},
+        "config": {"workload": describe(cfg, P, L, k, tau), "prefix": P, "block": L, "k": k,
+                   "rows": M},
         "roofline": {"bound": "hbm", "kernel": "gate/up projection + SwiGLU (gemm_kernel<EPI_SWIGLU>)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
@@ -515,8 +620,11 @@ def main():
         "step_roofline": {"hbm_bytes": sb, "flops": sf,
                           "hbm_frac": round(sb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "mfma_frac": round(sf / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFS, 4)},
-        "kernel_ms_per_step": {kd: round(v, 4) for kd, v in per_step_ms.items()},
+        "kernel_ms_per_step": per_step_ms,
     }
+    state = (run.tokens.cpu().numpy(), run.conf.cpu().numpy(), run.pred.cpu().numpy())
+    del run
+    torch.cuda.empty_cache()
     if not args.no_e2e:
         t0 = time.perf_counter()
         result["e2e_decode"] = e2e_decode(lp, synth, model, cfg, L=L, k=k, tau=tau)
@@ -542,10 +650,50 @@ def main():
                                            args.warmup, prec)
             log(f"{prec} step in {time.perf_counter() - t0:.1f}s: "
                 f"{result[key]['ms_per_step']} ms/step")
+    if not args.no_shapes and args.config == "dream7b":
+        shapes = {}
+        # the same model at 16 branches and a 2048-position prefix
+        t0 = time.perf_counter()
+        shapes["dream7b_p2048_k15"] = shape_figure(
+            lp, synth, model, cfg, 2048, 32, 15, tau, args.steps, args.warmup,
+            describe(cfg, 2048, 32, 15, tau))
+        log(f"dream7b p2048 k15 in {time.perf_counter() - t0:.1f}s: "
+            f"{shapes['dream7b_p2048_k15']['ms_per_step']} ms/step")
+        # the parity workhorse: launch-bound, microseconds per step
+        t0 = time.perf_counter()
+        ct = synth.config("tiny")
+        wt = synth.model_weights(ct, device=dev, dtype=torch.bfloat16)
+        mt = lp.Model(ct, wt)
+        fig = shape_figure(lp, synth, mt, ct, 64, 16, 3, tau, max(args.steps, 200),
+                           args.warmup, describe(ct, 64, 16, 3, tau))
+        fig["us_per_step"] = round(fig["ms_per_step"] * 1e3, 1)
+        fig["us_median"] = round(fig["ms_median"] * 1e3, 1)
+        if not args.no_cpu_baseline:
+            rt = StepRunner(lp, synth, mt, ct, 64, 16, 3, tau)
+            st = (rt.tokens.cpu().numpy(), rt.conf.cpu().numpy(), rt.pred.cpu().numpy())
+            del rt
+            fig["cpu_oracle_us_per_step"] = round(
+                cpu_tiny_step(ct, wt, st, 64, 16, 3, tau) * 1e6, 1)
+        shapes["tiny_p64_k3"] = fig
+        del mt, wt
+        log(f"tiny in {time.perf_counter() - t0:.1f}s: {fig['us_per_step']} us/step")
+        # LLaDA-8B layout (MHA, 32 layers) at prefix 1024
+        t0 = time.perf_counter()
+        cl = synth.config("llada8b")
+        wl = synth.model_weights(cl, device=dev, dtype=torch.bfloat16)
+        ml = lp.Model(cl, wl)
+        shapes["llada8b_p1024_k7"] = shape_figure(
+            lp, synth, ml, cl, 1024, 32, 7, tau, args.steps, args.warmup,
+            describe(cl, 1024, 32, 7, tau))
+        del ml, wl
+        torch.cuda.empty_cache()
+        log(f"llada8b p1024 k7 in {time.perf_counter() - t0:.1f}s: "
+            f"{shapes['llada8b_p1024_k7']['ms_per_step']} ms/step")
+        result["shapes"] = shapes
     if not args.no_cpu_baseline:
         t0 = time.perf_counter()
         try:
-            result["cpu_baseline"] = cpu_baseline(cfg, w, P, L, k, args.cpu_layers)
+            result["cpu_baseline"] = cpu_baseline(cfg, w, state, P, L, k, tau, args.cpu_runs)
         except Exception as e:  # the GPU number stands; say why the baseline is missing
             result["cpu_baseline"] = {"value": None, "error": repr(e)}
         log(f"cpu baseline in {time.perf_counter() - t0:.1f}s")
