@@ -487,8 +487,236 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Single-load form, for key ranges short enough that every score of the
+// workgroup fits in registers (at most SL_WAVES x NT tiles). Eight wavefronts
+// split the key tiles; each loads its tiles' K straight into registers in
+// MFMA operand layout, forms and keeps the scores, then loads V into the same
+// registers while the row maxima are exchanged through LDS. The probabilities
+// are formed once, against the exact maximum, from the kept scores, so K and V
+// cross the memory system once and the path has two memory round trips
+// instead of one per tile.
+//
+// Key order inside a tile: A-operand row i of key block kb holds key
+// 8 (i / 4) + 4 kb + i % 4, so the scores of lane (c16, g) are keys
+// 8 g .. 8 g + 7 of the tile (kb = 0: j = 0..3, kb = 1: j = 0..3), for query
+// c16; the same lane then needs V^T at keys 8 g .. 8 g + 7: one 16-byte load
+// per 16 dimensions.
+constexpr int SL_WAVES = 8;
+
+template <int D, int QB, int NT>
+struct SlSmem {
+  static constexpr int NDB = D / 16;
+  static constexpr int OV = NDB * QB * 64;  // f32x4 partial-output values of one wavefront
+};
+
+template <int D, int QB, int NT>
+__global__ __launch_bounds__(64 * SL_WAVES) void attn_sl_kernel(AttnArgs a) {
+  constexpr int NDB = D / 16, NKK = D / 32;
+  using SM = SlSmem<D, QB, NT>;
+  __shared__ f32x4 s_o[SL_WAVES][SM::OV];
+  __shared__ float s_max[SL_WAVES][QB * 16];
+  __shared__ float s_l[SL_WAVES][QB * 16];
+  const int h = blockIdx.x, br = blockIdx.y;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g = lane >> 4, c16 = lane & 15;
+  const int kvh = h / (a.Hq / a.Hkv);
+  const int L = a.L, P = a.P;
+  const int pt = (P + KT - 1) / KT, bt = (L + KT - 1) / KT, T = pt + bt;
+  const int t_lo = wv * T / SL_WAVES, nt = (wv + 1) * T / SL_WAVES - t_lo;  // nt <= NT
+  const float sl2 = a.scale * 1.4426950408889634f;
+
+  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;  // [pos][D]
+  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;  // [D][vld]
+  const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
+  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
+  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
+
+  // K of the wavefront's tiles; rows past the end of a source read its last
+  // row (masked below)
+  u32x4 kv[NT][2][NKK];
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    if (i >= nt) break;
+    const int t = t_lo + i;
+    const bool pre = t < pt;
+    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
+    const uint16_t* kb_ = pre ? kc : ks;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int r = min(p0 + 8 * (c16 >> 2) + 4 * kb + (c16 & 3), lim - 1);
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+        kv[i][kb][kk] = *(const u32x4*)(kb_ + (int64_t)r * D + kk * 32 + g * 8);
+    }
+  }
+  // Q^T operand: query column 16 qb + c16, dims 32 kk + 8 g .. +8
+  u32x4 qf[QB][NKK];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int row = qb * 16 + c16;
+    const uint16_t* qrow = a.q + (((int64_t)br * a.Hq + h) * L + (row < L ? row : 0)) * D;
+    const unsigned keep = row < L ? ~0u : 0u;  // rows past L: zero queries
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) qf[qb][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
+  }
+
+  // scores S^T = K Q^T, kept: sc[i][qb][kb][j] is key p0 + 8 g + 4 kb + j of
+  // tile i, query 16 qb + c16; masked keys -inf
+  f32x4 sc[NT][QB][2];
+  float mraw[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) mraw[qb] = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    if (i >= nt) break;
+    const int t = t_lo + i;
+    const bool pre = t < pt;
+    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      int lq = lim;  // block-causal: rows 16 qb .. lie in one sub-block
+      if (!pre && a.cblk) lq = min(lim, ((qb * 16) / a.cblk + 1) * a.cblk);
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < NKK; ++kk) acc = mfma16(kv[i][kb][kk], qf[qb][kk], acc);
+        if (p0 + KT > lq) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            acc[j] = p0 + 8 * g + 4 * kb + j < lq ? acc[j] : -INFINITY;
+        }
+        sc[i][qb][kb] = acc;
+        mraw[qb] = max2(mraw[qb], max2(max2(acc[0], acc[1]), max2(acc[2], acc[3])));
+      }
+    }
+  }
+  // V^T of the same keys (the K registers are free now): lane (c16, g) takes
+  // dims 16 db + c16, keys 8 g .. 8 g + 7; a run that starts past the end of
+  // its source reads the source's first run instead (its probabilities are 0)
+  u32x4 vf[NT][NDB];
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    if (i >= nt) break;
+    const int t = t_lo + i;
+    const bool pre = t < pt;
+    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
+    const int64_t ld = pre ? a.vld : a.vlds;
+    const uint16_t* vb_ = (pre ? vc : vs) + p0 + (p0 + 8 * g < lim ? 8 * g : 0);
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+      vf[i][db] = *(const u32x4*)(vb_ + (int64_t)(db * 16 + c16) * ld);
+  }
+
+  // the exact row maximum over the eight wavefronts (the V loads stay in
+  // flight across the barrier)
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float mw = pair32_max(pair16_max(mraw[qb]));
+    if (g == 0) s_max[wv][qb * 16 + c16] = mw;
+  }
+  lds_barrier();
+  float m[QB], l[QB];
+  f32x4 o[NDB][QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    float mx = s_max[0][qb * 16 + c16];
+#pragma unroll
+    for (int w = 1; w < SL_WAVES; ++w) mx = max2(mx, s_max[w][qb * 16 + c16]);
+    m[qb] = mx * sl2;  // every probability 2^(s sl2 - m) <= 1
+    l[qb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // probabilities against the exact maximum; V meets them rounded to bf16
+#pragma unroll
+  for (int i = 0; i < NT; ++i) {
+    if (i >= nt) break;
+    const int t = t_lo + i;
+    const bool pre = t < pt;
+    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
+    if (p0 + KT > lim) {
+      // zero V at keys past the end of the source (0 * inf would poison o)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int pos = p0 + 8 * g + 2 * e;
+        const unsigned mk = (pos < lim ? 0xFFFFu : 0u) | (pos + 1 < lim ? 0xFFFF0000u : 0u);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) vf[i][db][e] &= mk;
+      }
+    }
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const float nm = -m[qb];
+      uint16_t pb[8];
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const float p = fast_exp2(__builtin_fmaf(sc[i][qb][kb][j], sl2, nm));  // -inf: 0
+          l[qb] += p;
+          pb[kb * 4 + j] = f2bf_bits(p);
+        }
+      const u32x4 pf = *(const u32x4*)pb;  // keys 8 g .. 8 g + 7
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) o[db][qb] = mfma16(vf[i][db], pf, o[db][qb]);
+    }
+  }
+
+  // the eight partial states share the maximum: they add up, in wavefront
+  // order (deterministic); every thread then finishes a share of the outputs
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float lw = pair32_sum(pair16_sum(l[qb]));
+    if (g == 0) s_l[wv][qb * 16 + c16] = lw;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) s_o[wv][(db * QB + qb) * 64 + lane] = o[db][qb];
+  }
+  lds_barrier();
+  for (int f = tid; f < SM::OV; f += 64 * SL_WAVES) {
+    const int ln = f & 63, qb = (f >> 6) % QB, db = (f >> 6) / QB;
+    const int q16 = ln & 15, g4 = ln >> 4;
+    const int row = qb * 16 + q16;
+    if (row >= L) continue;
+    f32x4 acc = s_o[0][f];
+    float ls = s_l[0][qb * 16 + q16];
+#pragma unroll
+    for (int w = 1; w < SL_WAVES; ++w) {
+      acc += s_o[w][f];
+      ls += s_l[w][qb * 16 + q16];
+    }
+    const float inv = 1.0f / ls;
+    uint16_t ob[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) ob[j] = f2bf_bits(acc[j] * inv);
+    const int col = h * D + db * 16 + g4 * 4;
+    *(uint2*)(a.out + packA_off(br * L + row, col, a.Mp)) = *(const uint2*)ob;
+  }
+}
+
+template <int D, int QB>
+hipError_t launch_sl(const AttnArgs& a, int nt, hipStream_t s) {
+  const dim3 grid(a.Hq, a.nb), block(64 * SL_WAVES);
+  switch (nt) {
+    case 1: hipLaunchKernelGGL((attn_sl_kernel<D, QB, 1>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((attn_sl_kernel<D, QB, 2>), grid, block, 0, s, a); break;
+    case 3: hipLaunchKernelGGL((attn_sl_kernel<D, QB, 3>), grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 template <int D>
 hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
+  const int T = (a.P + KT - 1) / KT + (a.L + KT - 1) / KT;
+  const int nt = (T + SL_WAVES - 1) / SL_WAVES;  // most tiles of one wavefront
+  if (a.L <= 32 && nt <= 3) {
+    if (a.L <= 16) return launch_sl<D, 1>(a, nt, s);
+    return launch_sl<D, 2>(a, nt, s);
+  }
   const dim3 grid(a.Hq, a.nb);
   switch ((a.L + 15) / 16) {
     case 1: hipLaunchKernelGGL((attn_kernel<D, 1>), grid, dim3(256), 0, s, a); break;
