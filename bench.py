@@ -457,7 +457,8 @@ def e2e_window_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7,
     torch.cuda.synchronize()
     t = time.perf_counter() - t0
     return {"workload": (f"{cfg['name']} shape, {prompt_len}-token uniform-random prompt (prefill "
-                         f"included), {gen} generated tokens, window of up to {w_max} blocks of {L}, "
+                         f"included), {gen} generated tokens, window of up to {w_max} blocks of {L} "
+                         f"(gates on the device), "
                          f"k={k}, tau {tau}, tau_add {tau_add}, tau_act {tau_act}"
                          + (", block-causal attention inside the window" if block_causal else "")),
             "tokens_per_s": round(gen / t, 1), "tokens_per_forward": round(out["tpf"], 3),
@@ -636,6 +637,13 @@ def main():
             log(f"end-to-end window decode in {time.perf_counter() - t0:.1f}s: "
                 f"{result['e2e_window_decode']['tokens_per_s']} tok/s, "
                 f"TPF {result['e2e_window_decode']['tokens_per_forward']}")
+            if 4 * L <= lp.MAX_BLOCK:
+                t0 = time.perf_counter()
+                result["e2e_window_decode_w4"] = e2e_window_decode(lp, synth, model, cfg, L=L, k=k,
+                                                                   tau=tau, w_max=4)
+                log(f"end-to-end window decode (4 blocks) in {time.perf_counter() - t0:.1f}s: "
+                    f"{result['e2e_window_decode_w4']['tokens_per_s']} tok/s, "
+                    f"TPF {result['e2e_window_decode_w4']['tokens_per_forward']}")
             t0 = time.perf_counter()
             result["e2e_window_decode_block_causal"] = e2e_window_decode(
                 lp, synth, model, cfg, L=L, k=k, tau=tau, block_causal=True)

@@ -53,8 +53,9 @@ enum {
 };
 
 /* Largest supported values (checked by the calls). */
-#define LOPA_MAX_BLOCK 64    /* L: positions of the active block            */
-#define LOPA_MAX_ROWS 512    /* n_branches * L rows in one verify forward   */
+#define LOPA_MAX_BLOCK 256   /* L: positions of the active block (window)   */
+#define LOPA_MAX_ROWS 2048   /* n_branches * L rows in one verify forward   */
+#define LOPA_WINDOW_MAX_BLOCKS 16  /* blocks of a multi-block window        */
 
 /* Decoder shape (Qwen2.5 / LLaMA-style pre-norm decoder, the layout of the
  * paper's Dream-7B / DiffuCoder-7B backbones; the paper names only the
@@ -261,6 +262,73 @@ int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32
  * length); otherwise as lopa_commit_kv. */
 int lopa_commit_kv_rows(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,
                         int32_t n_rows, int32_t* append_offset, void* stream);
+
+/* -------------------------------------------- multi-block window (D2F) */
+
+/* Sec. 3.3, integration with D2F: the active blocks form one window whose
+ * positions are explored together, blocks join the window by the tau_add gate
+ * and become fully activated by the tau_act gate, and a completed leading
+ * block leaves it (its K/V enter the prefix). The window's state lives in
+ * device memory in this struct (caller-allocated, device); the three calls
+ * below read and write it on the stream, so the gates need no host copy of the
+ * window. A host loop reads the first words (blocks, eligible, prefix_len,
+ * need_initial, done) once per iteration: the next iteration's launch shapes
+ * depend on them. Gates in the library's readings (tau as fractions of a
+ * block's L positions, compared in double on the host and kept as counts):
+ *   - an empty window with blocks left opens one, fully activated, with
+ *     need_initial = 1 (its initial forward, one branch over its L rows, has
+ *     not run); then blocks are appended, not activated, while the window has
+ *     fewer than w_max blocks, blocks remain, and the last block has at least
+ *     add_min = ceil(tau_add L) filled positions;
+ *   - after a selection (lopa_window_update): block b >= 1 becomes fully
+ *     activated when block b - 1 is and has at least act_min = ceil(tau_act L)
+ *     filled positions (block order); the leading blocks with no masked
+ *     position leave the window (tokens to the output, K/V committed by
+ *     lopa_window_commit), the rest moves to the front with its new first
+ *     block fully activated; then the opening / appending above.
+ * Opened and appended blocks hold mask_id, conf 0 and pred mask_id. */
+typedef struct lopa_window {
+  int32_t blocks;          /* blocks in the window (its length is blocks * L)       */
+  int32_t eligible;        /* positions of its fully activated leading blocks:       */
+                           /* the n_eligible of lopa_build_branches_window          */
+  int32_t prefix_len;      /* committed positions (the verify forwards' prefix_len) */
+  int32_t need_initial;    /* 1: block 0 was just opened; run its initial forward    */
+  int32_t done;            /* 1: all n_blocks blocks committed                      */
+  int32_t added;           /* blocks opened or appended so far                      */
+  int32_t committed;       /* blocks committed so far                               */
+  int32_t last_commit;     /* blocks the last update moved out of the window        */
+  int32_t last_commit_at;  /* the prefix_len they are committed at                  */
+  int32_t error;           /* 1: lopa_window_commit found its inputs invalid        */
+  int32_t L, w_max, n_blocks, mask_id, add_min, act_min;
+  int32_t active[LOPA_WINDOW_MAX_BLOCKS];  /* 1: block fully activated               */
+} lopa_window;
+
+/* Start a window for n_blocks blocks of L positions after prefix_len committed
+ * positions: writes the header and opens block 0 into tokens / conf / pred
+ * (device, capacity w_max * L each) by the rules above. Host checks: null
+ * pointers, 1 <= w_max <= LOPA_WINDOW_MAX_BLOCKS, w_max * L <= LOPA_MAX_BLOCK,
+ * n_blocks >= 1, prefix_len >= 0, tau_add and tau_act in [0, 1] (LOPA_EINVAL /
+ * LOPA_ESHAPE). */
+int lopa_window_init(lopa_window* win, int32_t* tokens, float* conf, int32_t* pred, int32_t L,
+                     int32_t w_max, int32_t n_blocks, int32_t prefix_len, int32_t mask_id,
+                     double tau_add, double tau_act, void* stream);
+
+/* The gates after a selection: tokens / conf / pred (device) hold the winner's
+ * window rows (the next_tokens / next_conf / next_pred of
+ * lopa_branch_confidence_select over the window); they are updated in place
+ * to the next window. Tokens of completed leading blocks are appended to
+ * out_tokens (device, n_blocks * L int32, block order). */
+int lopa_window_update(lopa_window* win, int32_t* tokens, float* conf, int32_t* pred,
+                       int32_t* out_tokens, void* stream);
+
+/* Commit the K/V of the blocks the last lopa_window_update moved out of the
+ * window: the first last_commit * L staged rows of branch *winner (device) of
+ * the last lopa_verify_forward on kv (which must be that of the window's
+ * iteration) go to cache rows [last_commit_at, ...). Nothing if none left.
+ * The row count is read on the device: inputs that do not fit (winner outside
+ * the forward's branches, more rows than it staged, past max_len) commit
+ * nothing and set win->error = 1. */
+int lopa_window_commit(lopa_kv* kv, const int32_t* winner, lopa_window* win, void* stream);
 
 /* ---------------------------------------------------------- inspection */
 

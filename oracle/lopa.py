@@ -261,6 +261,147 @@ def decode(model, prompt, gen_len: int, L: int, k: int, tau: float, max_len=None
 #       unfilled position leave the window and their K/V (from that forward)
 #       enter the prefix; an empty window takes a new block with one initial
 #       forward, as a single block does.
+class WindowGates:
+    """The window bookkeeping of R27-R30, model-free: which blocks form the
+    window, which are fully activated, when blocks join and leave. Driven by
+    the window's tokens after each selection; the caller runs the forwards.
+    (R29's coverage condition always holds where it is tested: every block in
+    the window at a selection was covered by that selection's forward.)"""
+
+    def __init__(self, L: int, w_max: int, n_blocks: int, tau_add: float, tau_act: float,
+                 mask_id: int):
+        self.L, self.w_max, self.n_blocks = L, w_max, n_blocks
+        self.tau_add, self.tau_act, self.mask_id = tau_add, tau_act, mask_id
+        self.active, self.added, self.committed = [], 0, 0
+
+    def filled(self, tokens, b) -> float:
+        return float(np.mean(tokens[b * self.L:(b + 1) * self.L] != self.mask_id))
+
+    def eligible(self) -> int:
+        """Positions of the fully activated leading blocks (R29)."""
+        return self.L * next((i for i, a in enumerate(self.active) if not a), len(self.active))
+
+    def fill(self, tokens, conf, pred):
+        """R27 / R30: an empty window with blocks left opens one (fully
+        activated; its initial forward is due), then blocks are appended while
+        the window has room, blocks remain and the last block is at least
+        tau_add filled. Returns (tokens, conf, pred, opened)."""
+        L, m = self.L, self.mask_id
+
+        def append():
+            nonlocal tokens, conf, pred
+            tokens = np.concatenate([tokens, np.full(L, m, dtype=np.int64)])
+            conf = np.concatenate([conf, np.zeros(L)])
+            pred = np.concatenate([pred, np.full(L, m, dtype=np.int64)])
+            self.active.append(len(self.active) == 0)
+            self.added += 1
+
+        opened = False
+        if not self.active and self.added < self.n_blocks:
+            append()
+            opened = True
+        while (len(self.active) < self.w_max and self.added < self.n_blocks
+               and self.filled(tokens, len(self.active) - 1) >= self.tau_add):
+            append()
+        return tokens, conf, pred, opened
+
+    def after_select(self, tokens):
+        """R29 / R30 after a selection over the window: activation in block
+        order, then c = the leading blocks with no unfilled position, which
+        leave (the new first block is fully activated). Returns c; the caller
+        commits their K/V and drops their rows."""
+        for i in range(1, len(self.active)):
+            if not self.active[i] and self.active[i - 1] and self.filled(tokens, i - 1) >= self.tau_act:
+                self.active[i] = True
+        c = 0
+        while c < len(self.active) and not np.any(tokens[c * self.L:(c + 1) * self.L] == self.mask_id):
+            c += 1
+        if c:
+            del self.active[:c]
+            if self.active:
+                self.active[0] = True
+            self.committed += c
+        return c
+
+
+def decode_window(model: OracleModel, prompt, gen_len: int, L: int, k: int, tau: float,
+                  tau_add: float, tau_act: float, w_max: int, metric: int = METRIC_MEAN,
+                  window: int = 4, eta: float = 0.25, trace=None, max_len=None,
+                  block_causal: bool = False):
+    """Generate gen_len tokens (gen_len / L blocks) with a sliding window of up
+    to w_max active blocks. Returns tokens, iterations, forwards, tpf, cache.
+    block_causal: the window's blocks attend block-causally (a block sees the
+    prefix, the earlier window blocks and itself; Sec. 3.4, LoPA-Dist-Ascend)
+    instead of with full attention inside the window."""
+    cblk = L if block_causal else 0
+    mask_id = model.cfg["mask_id"]
+    prompt = np.asarray(prompt, dtype=np.int64)
+    cache = KVCache(model.cfg, max_len or (len(prompt) + gen_len))
+    P = prefill(model, cache, prompt, L)
+    n_blocks = gen_len // L
+    gates = WindowGates(L, w_max, n_blocks, tau_add, tau_act, mask_id)
+    tokens = np.zeros(0, dtype=np.int64)
+    conf = np.zeros(0)
+    pred = np.zeros(0, dtype=np.int64)
+    out, iters, forwards = [], 0, 0
+
+    while gates.committed < n_blocks:
+        tokens, conf, pred, opened = gates.fill(tokens, conf, pred)
+        if opened:
+            # the new block's initial forward (the block alone)
+            o = model.forward_block(tokens[None, :L], P, cache, causal_blk=cblk)
+            conf[:L], pred[:L] = o["conf"][0], o["pred"][0]
+            forwards += 1
+        n_el = gates.eligible()
+        state_in = (tokens.copy(), conf.copy(), pred.copy())
+        bt, fill_pos, valid, n_valid = build_branches(tokens, conf, pred, mask_id, tau, k, n_el)
+        o = model.forward_block(bt[:n_valid], P, cache, causal_blk=cblk)
+        nb, Lw = k + 1, len(tokens)
+        conf_b = np.zeros((nb, Lw))
+        pred_b = np.zeros((nb, Lw), dtype=np.int64)
+        conf_b[:n_valid], pred_b[:n_valid] = o["conf"], o["pred"]
+        scores, w = select(bt, conf_b, valid, mask_id, metric, window, eta)
+        forwards += 1
+        iters += 1
+        tokens, conf, pred = bt[w].copy(), conf_b[w].copy(), pred_b[w].copy()
+        c = gates.after_select(tokens)
+        if trace is not None:
+            trace.append(dict(prefix_len=P, state=state_in, branch_tokens=bt, valid=valid,
+                              n_valid=n_valid, n_eligible=n_el, conf=conf_b, pred=pred_b,
+                              scores=scores, winner=w, committed_blocks=c, k=o["k"], v=o["v"]))
+        if c:
+            cache.commit(P, o["k"][w][:, :, :c * L], o["v"][w][:, :, :c * L])
+            out.append(tokens[:c * L].copy())
+            tokens, conf, pred = tokens[c * L:], conf[c * L:], pred[c * L:]
+            P += c * L
+        if iters > 2 * gen_len + 2 * n_blocks:
+            raise RuntimeError("window decode did not converge")
+    gen = np.concatenate(out) if out else np.zeros(0, dtype=np.int64)
+    return dict(tokens=gen, iterations=iters, forwards=forwards,
+                tpf=(len(gen) / forwards) if forwards else 0.0, cache=cache)
+
+
+# ------------------------------------------- multi-block window (Sec. 3.3)
+# LoPA on D2F treats all active blocks as one window for branch exploration,
+# with full attention inside the window (Sec. 3.3); the appendix's tables give
+# the D2F gates tau_add and tau_act next to tau_conf but not their rules.
+# Readings (the oracle and the GPU decoder follow both):
+#   R27 window: up to w_max consecutive blocks of L after the committed prefix;
+#       Eq. 1, the lookahead branches, the verify forward and Eq. 2 run over
+#       all its positions at once.
+#   R28 adding (tau_add): before an iteration, while the window holds fewer
+#       than w_max blocks, blocks remain, and the last block's filled fraction
+#       is >= tau_add, an all-mask block is appended; until a forward covers it
+#       its positions carry Conf 0.
+#   R29 activation (tau_act): the window's first block is fully activated;
+#       block i becomes so once block i-1 is, block i has been covered by a
+#       forward, and block i-1's filled fraction is >= tau_act. The Eq. 1
+#       fallback and the lookahead positions are taken in the fully activated
+#       blocks (a prefix of the window); the others fill only above tau.
+#   R30 commit: after an iteration the leading blocks of the winner with no
+#       unfilled position leave the window and their K/V (from that forward)
+#       enter the prefix; an empty window takes a new block with one initial
+#       forward, as a single block does.
 def decode_window(model: OracleModel, prompt, gen_len: int, L: int, k: int, tau: float,
                   tau_add: float, tau_act: float, w_max: int, metric: int = METRIC_MEAN,
                   window: int = 4, eta: float = 0.25, trace=None, max_len=None,

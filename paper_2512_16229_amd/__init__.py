@@ -20,8 +20,8 @@ import torch
 
 from ._abi import (EXPORTS, LIB_PATH, LOPA_ECAPACITY, LOPA_EHIP, LOPA_EINVAL, LOPA_ENOMEM,  # noqa: F401
                    LOPA_ESHAPE, LOPA_OK, MAX_BLOCK, MAX_ROWS, METRIC_LOWEST_SEGMENT, METRIC_MEAN,
-                   METRIC_WINDOW_MIN, PRECISIONS, PROF_KINDS, LopaError, lib,
-                   lopa_layer_weights, lopa_model_cfg, lopa_weight_ptrs)
+                   METRIC_WINDOW_MIN, PRECISIONS, PROF_KINDS, WINDOW_MAX_BLOCKS, LopaError, lib,
+                   lopa_layer_weights, lopa_model_cfg, lopa_weight_ptrs, lopa_window)
 
 
 def _check(status: int):
@@ -221,6 +221,40 @@ def lopa_commit_kv(kv: KV, winner, prefix_len, L, append_offset, stream=None):
 def lopa_commit_kv_rows(kv: KV, winner, prefix_len, L, n_rows, append_offset, stream=None):
     _check(lib.lopa_commit_kv_rows(kv.handle, _ptr(winner, I32, "winner"), prefix_len, L, n_rows,
                                    _ptr(append_offset, I32, "append_offset"), _stream(stream)))
+
+
+# ---------------------------------------------------- multi-block window
+WINDOW_WORDS = C.sizeof(lopa_window) // 4  # int32 words of the device window state
+
+
+def window_state(device="cuda") -> torch.Tensor:
+    """Device memory for one lopa_window (int32 words)."""
+    return torch.zeros(WINDOW_WORDS, dtype=torch.int32, device=device)
+
+
+def window_read(win: torch.Tensor) -> lopa_window:
+    """The window state copied to the host (a synchronising read)."""
+    host = win.cpu().numpy()
+    return lopa_window.from_buffer_copy(host.tobytes())
+
+
+def lopa_window_init(win, tokens, conf, pred, L, w_max, n_blocks, prefix_len, mask_id, tau_add,
+                     tau_act, stream=None):
+    _check(lib.lopa_window_init(_ptr(win, I32, "win"), _ptr(tokens, I32, "tokens"),
+                                _ptr(conf, F32, "conf"), _ptr(pred, I32, "pred"), L, w_max,
+                                n_blocks, prefix_len, mask_id, float(tau_add), float(tau_act),
+                                _stream(stream)))
+
+
+def lopa_window_update(win, tokens, conf, pred, out_tokens, stream=None):
+    _check(lib.lopa_window_update(_ptr(win, I32, "win"), _ptr(tokens, I32, "tokens"),
+                                  _ptr(conf, F32, "conf"), _ptr(pred, I32, "pred"),
+                                  _ptr(out_tokens, I32, "out_tokens"), _stream(stream)))
+
+
+def lopa_window_commit(kv: KV, winner, win, stream=None):
+    _check(lib.lopa_window_commit(kv.handle, _ptr(winner, I32, "winner"), _ptr(win, I32, "win"),
+                                  _stream(stream)))
 
 
 from .decoder import Decoder, WindowDecoder  # noqa: E402,F401

@@ -12,7 +12,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblopa.so")
 
 LOPA_OK, LOPA_EINVAL, LOPA_ESHAPE, LOPA_ECAPACITY, LOPA_EHIP, LOPA_ENOMEM = 0, -1, -2, -3, -4, -5
-MAX_BLOCK, MAX_ROWS = 64, 512
+MAX_BLOCK, MAX_ROWS, WINDOW_MAX_BLOCKS = 256, 2048, 16
 
 
 class LopaError(RuntimeError):
@@ -33,6 +33,14 @@ class lopa_layer_weights(C.Structure):
                                            "w_up", "w_down", "ln1", "ln2")]
 
 
+class lopa_window(C.Structure):
+    """The device-resident window state of include/lopa.h (field order)."""
+    _fields_ = [(n, C.c_int32) for n in ("blocks", "eligible", "prefix_len", "need_initial", "done",
+                                          "added", "committed", "last_commit", "last_commit_at",
+                                          "error", "L", "w_max", "n_blocks", "mask_id", "add_min",
+                                          "act_min")] + [("active", C.c_int32 * 16)]
+
+
 class lopa_weight_ptrs(C.Structure):
     _fields_ = [("embed", C.c_void_p), ("layers", C.POINTER(lopa_layer_weights)),
                 ("final_norm", C.c_void_p), ("lm_head", C.c_void_p)]
@@ -45,7 +53,8 @@ EXPORTS = ["lopa_model_create", "lopa_model_create_ex", "lopa_model_destroy", "l
            "lopa_commit_kv_rows", "lopa_kv_read", "lopa_kv_write",
            "lopa_kv_read_staging", "lopa_debug_hidden",
            "lopa_kv_set_block_causal", "lopa_kv_profile",
-           "lopa_kv_profile_read", "lopa_verify_forward_noalloc"]
+           "lopa_kv_profile_read", "lopa_verify_forward_noalloc", "lopa_window_init",
+           "lopa_window_update", "lopa_window_commit"]
 METRIC_MEAN, METRIC_WINDOW_MIN, METRIC_LOWEST_SEGMENT = 0, 1, 2
 PRECISIONS = {"bf16": 0, "fp8_mlp": 1, "fp8": 2}
 PROF_KINDS = ["qkv", "attn", "oproj", "gateup", "down", "lmhead", "norm", "merge"]
@@ -82,6 +91,9 @@ def _load():
         "lopa_kv_profile": (C.c_int, [P, I32]),
         "lopa_kv_profile_read": (C.c_int, [P, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
         "lopa_verify_forward_noalloc": (C.c_int, [P, P, I32, P, I32, I32, P, P, P]),
+        "lopa_window_init": (C.c_int, [P, P, P, P, I32, I32, I32, I32, I32, C.c_double, C.c_double, P]),
+        "lopa_window_update": (C.c_int, [P, P, P, P, P, P]),
+        "lopa_window_commit": (C.c_int, [P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)

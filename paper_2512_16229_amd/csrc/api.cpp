@@ -850,6 +850,48 @@ int lopa_commit_kv_rows(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, 
   return LOPA_OK;
 }
 
+// smallest filled count n of an L-position block with n / L >= tau (the
+// gate's fraction in double), L + 1 if none
+static int32_t gate_count(double tau, int32_t L) {
+  for (int32_t n = 0; n <= L; ++n)
+    if ((double)n / (double)L >= tau) return n;
+  return L + 1;
+}
+
+int lopa_window_init(lopa_window* win, int32_t* tokens, float* conf, int32_t* pred, int32_t L,
+                     int32_t w_max, int32_t n_blocks, int32_t prefix_len, int32_t mask_id,
+                     double tau_add, double tau_act, void* stream) {
+  if (!win || !tokens || !conf || !pred) return fail(LOPA_EINVAL, "null pointer argument");
+  if (L < 1 || w_max < 1 || w_max > LOPA_WINDOW_MAX_BLOCKS || (int64_t)w_max * L > LOPA_MAX_BLOCK)
+    return fail(LOPA_ESHAPE, "window of %d blocks of %d positions (at most %d blocks, %d positions)",
+                w_max, L, LOPA_WINDOW_MAX_BLOCKS, LOPA_MAX_BLOCK);
+  if (n_blocks < 1 || prefix_len < 0) return fail(LOPA_EINVAL, "n_blocks %d, prefix_len %d", n_blocks, prefix_len);
+  if (!(tau_add >= 0.0 && tau_add <= 1.0) || !(tau_act >= 0.0 && tau_act <= 1.0))
+    return fail(LOPA_EINVAL, "tau_add %g / tau_act %g outside [0, 1]", tau_add, tau_act);
+  const hipStream_t s = (hipStream_t)stream;
+  HIP_TRY(launch_window_init(win, L, w_max, n_blocks, prefix_len, mask_id, gate_count(tau_add, L),
+                             gate_count(tau_act, L), s));
+  HIP_TRY(launch_window_update(win, tokens, conf, pred, nullptr, s));
+  return LOPA_OK;
+}
+
+int lopa_window_update(lopa_window* win, int32_t* tokens, float* conf, int32_t* pred,
+                       int32_t* out_tokens, void* stream) {
+  if (!win || !tokens || !conf || !pred || !out_tokens) return fail(LOPA_EINVAL, "null pointer argument");
+  HIP_TRY(launch_window_update(win, tokens, conf, pred, out_tokens, (hipStream_t)stream));
+  return LOPA_OK;
+}
+
+int lopa_window_commit(lopa_kv* kv, const int32_t* winner, lopa_window* win, void* stream) {
+  if (!kv || !winner || !win) return fail(LOPA_EINVAL, "null pointer argument");
+  if (kv->last_nb < 0) return fail(LOPA_EINVAL, "no verify forward has staged K/V yet");
+  const lopa_model_cfg& c = kv->m->cfg;
+  HIP_TRY(launch_window_commit(kv->staging, kv->cache, winner, win, kv->last_nb, kv->last_L,
+                               kv->max_len, c.layers, c.kv_heads, kv->vlds, kv->vld, c.head_dim,
+                               (hipStream_t)stream));
+  return LOPA_OK;
+}
+
 int lopa_commit_kv(lopa_kv* kv, const int32_t* winner, int32_t prefix_len, int32_t L,
                    int32_t* append_offset, void* stream) {
   if (!kv || !winner || !append_offset) return fail(LOPA_EINVAL, "null pointer argument");

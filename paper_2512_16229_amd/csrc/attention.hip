@@ -304,6 +304,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   constexpr int NDB = D / 16, NKK = D / 32;
   __shared__ __attribute__((aligned(1024))) char smem[SM::BYTES];
   const int h = blockIdx.x, br = blockIdx.y;
+  const int row0 = blockIdx.z * QB * 16;  // first query row of this workgroup's group
   const int tid = threadIdx.x, lane = tid & 63;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, c16 = lane & 15;
@@ -370,7 +371,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   u32x4 qf[QB][NKK];
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    const int row = qb * 16 + c16;
+    const int row = row0 + qb * 16 + c16;
     const uint16_t* qrow = a.q + (((int64_t)br * a.Hq + h) * L + (row < L ? row : 0)) * D;
     const unsigned keep = row < L ? ~0u : 0u;  // rows past L: zero queries
 #pragma unroll
@@ -388,7 +389,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int t = tile_of(i);
     const bool pre = t < pt;
     tile_max<D, QB>(smem + (wv * 2 + (i & 1)) * TileLds<D>::TILE, lane, qf, mraw,
-                    (pre ? t : t - pt) * KT, pre ? P : L, g, pre ? 0 : a.cblk, 0);
+                    (pre ? t : t - pt) * KT, pre ? P : L, g, pre ? 0 : a.cblk, row0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     issue_k(tile_of(i + 2 < n ? i + 2 : n - 1), i & 1);
   }
@@ -429,7 +430,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int t = tile_of(i);
     const bool pre = t < pt;
     tile_update<D, QB, false>(x, qf, m, l, o, (pre ? t : t - pt) * KT, pre ? P : L, sl2, g,
-                              pre ? 0 : a.cblk, 0);
+                              pre ? 0 : a.cblk, row0);
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     issue(tile_of(i + 2 < n ? i + 2 : n - 1), i & 1);
   }
@@ -472,7 +473,7 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
-    const int row = qb * 16 + c16;
+    const int row = row0 + qb * 16 + c16;
     if (row >= L) continue;
     const float inv = 1.0f / l[qb];
     const int r = br * L + row;
@@ -717,8 +718,10 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
     if (a.L <= 16) return launch_sl<D, 1>(a, nt, s);
     return launch_sl<D, 2>(a, nt, s);
   }
-  const dim3 grid(a.Hq, a.nb);
-  switch ((a.L + 15) / 16) {
+  // up to 64 query rows per workgroup; longer blocks (multi-block windows) in
+  // groups of 64 rows, each group reading all of the branch's keys
+  const dim3 grid(a.Hq, a.nb, (a.L + 63) / 64);
+  switch (a.L > 64 ? 4 : (a.L + 15) / 16) {
     case 1: hipLaunchKernelGGL((attn_kernel<D, 1>), grid, dim3(256), 0, s, a); break;
     case 2: hipLaunchKernelGGL((attn_kernel<D, 2>), grid, dim3(256), 0, s, a); break;
     case 3: hipLaunchKernelGGL((attn_kernel<D, 3>), grid, dim3(256), 0, s, a); break;
@@ -731,7 +734,7 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
-  if (a.L < 1 || a.L > 64 || a.P < 0 || a.Hq % a.Hkv || a.vld % 8 || a.vlds % 8 ||
+  if (a.L < 1 || a.L > 256 || a.P < 0 || a.Hq % a.Hkv || a.vld % 8 || a.vlds % 8 ||
       a.L > a.vlds || a.P > a.vld)
     return hipErrorInvalidValue;
   if (a.cblk < 0 || (a.cblk > 0 && (a.cblk % 16 || a.L % a.cblk))) return hipErrorInvalidValue;

@@ -3,15 +3,17 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/lopa.h"
+
 // ----------------------------------------------------------- step kernels
-// Positions [0, n_elig) (1 <= n_elig <= L <= 64) are eligible for the Eq. 1
+// Positions [0, n_elig) (1 <= n_elig <= L <= 256) are eligible for the Eq. 1
 // fallback and the lookahead fills.
 hipError_t launch_build_branches(const int32_t* tokens, const float* conf, const int32_t* pred,
                                  int L, int n_elig, int mask_id, float tau, int k,
                                  int32_t* branch_tokens, int32_t* fill_pos, uint8_t* valid,
                                  int32_t* n_valid, hipStream_t s);
 // metric 0: Eq. 2 mean; 1: window minimum (window >= 1); 2: lowest-segment
-// mean (0 < eta <= 1). nb <= 1024, L <= 64.
+// mean (0 < eta <= 1). nb <= 1024, L <= 256.
 hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pred,
                          const uint8_t* valid, int nb, int L, int mask_id, int metric,
                          int window, float eta, float* scores, int32_t* winner, int32_t* nt,
@@ -28,6 +30,18 @@ hipError_t launch_commit(const uint16_t* staging, uint16_t* cache, const int32_t
 hipError_t launch_kv_rows(uint16_t* cache_k, uint16_t* cache_v, int64_t head_stride, int ld,
                           int Hkv, int d, int start, int len, uint16_t* buf_k, uint16_t* buf_v,
                           int to_cache, hipStream_t s);
+// Multi-block window (lopa_window in device memory; see step_kernels.hip):
+// the header of a new window; the gates after a selection (tokens / conf /
+// pred: the window rows, capacity w_max * L <= 256; out: the generated
+// tokens); the commit of the blocks the last update moved out (rows [0, n) of
+// the winner's staging of the last verify forward, n <= last_L).
+hipError_t launch_window_init(lopa_window* win, int L, int w_max, int n_blocks, int prefix_len,
+                              int mask_id, int add_min, int act_min, hipStream_t s);
+hipError_t launch_window_update(lopa_window* win, int32_t* tokens, float* conf, int32_t* pred,
+                                int32_t* out, hipStream_t s);
+hipError_t launch_window_commit(const uint16_t* staging, uint16_t* cache, const int32_t* winner,
+                                lopa_window* win, int nb_last, int last_L, int max_len,
+                                int layers, int Hkv, int vlds, int vld, int d, hipStream_t s);
 
 // ------------------------------------------------------------ weight repack
 // Pack the rows of up to three [rows_i, K] bf16 sources (stacked in order) into

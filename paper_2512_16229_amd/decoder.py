@@ -10,10 +10,11 @@ from __future__ import annotations
 
 import torch
 
-from . import (KV, METRIC_MEAN, Model, lopa_branch_confidence_select,
-               lopa_branch_confidence_select_metric, lopa_build_branches,
-               lopa_build_branches_window, lopa_commit_kv, lopa_commit_kv_rows,
-               lopa_verify_forward)
+from . import (KV, MAX_BLOCK, METRIC_MEAN, WINDOW_MAX_BLOCKS, Model,
+               lopa_branch_confidence_select, lopa_branch_confidence_select_metric,
+               lopa_build_branches, lopa_build_branches_window, lopa_commit_kv,
+               lopa_verify_forward, lopa_window_commit, lopa_window_init, lopa_window_update,
+               window_read, window_state)
 
 
 class Decoder:
@@ -134,17 +135,21 @@ class Decoder:
 class WindowDecoder:
     """LoPA over a window of up to w_max active blocks (Sec. 3.3, integration
     with D2F: the active blocks form one window for branch exploration, full
-    attention inside it). The gates follow the library's readings: a block is
-    appended while the last one is at least tau_add filled; block i becomes
-    fully activated (eligible for the Eq. 1 fallback and the lookahead fills)
-    once block i-1 is fully activated and at least tau_act filled and a forward
-    has covered block i; leading blocks with no unfilled position are committed
-    (lopa_commit_kv_rows) and leave the window. The host reads the winner's
-    tokens after every iteration to apply the gates."""
+    attention inside it). The gates run on the device, in the library's
+    readings (lopa_window_init / lopa_window_update / lopa_window_commit and
+    the lopa_window state): blocks join while the last one is at least tau_add
+    filled, become fully activated (eligible for the Eq. 1 fallback and the
+    lookahead fills) once the block before is fully activated and at least
+    tau_act filled, and leave with their K/V committed once they have no
+    unfilled position. The host reads the window's header (a few words) once
+    per iteration: the next iteration's launch shapes depend on it."""
 
     def __init__(self, model: Model, kv: KV, L: int, k: int, tau: float, tau_add: float,
                  tau_act: float, w_max: int, metric: int = METRIC_MEAN, window: int = 4,
                  eta: float = 0.25, block_causal: bool = False):
+        if w_max * L > MAX_BLOCK or w_max > WINDOW_MAX_BLOCKS:
+            raise ValueError(f"a window of {w_max} blocks of {L} exceeds the library's "
+                             f"{WINDOW_MAX_BLOCKS} blocks / {MAX_BLOCK} positions")
         self.model, self.kv, self.L, self.k = model, kv, L, k
         # block_causal: the window's blocks attend block-causally (Sec. 3.4,
         # the Ascend system's mask) instead of with full attention
@@ -170,7 +175,7 @@ class WindowDecoder:
         self.next_conf = torch.empty(W, **f32)
         self.next_pred = torch.empty(W, **i32)
         self.next_unfilled = torch.empty(1, **i32)
-        self.append_offset = torch.empty(1, **i32)
+        self.win = window_state(dev)
         self.forwards = self.iterations = 0
 
     def decode(self, prompt: torch.Tensor, gen_len: int, trace=None) -> dict:
@@ -178,35 +183,21 @@ class WindowDecoder:
         self.kv.set_block_causal(L if self.block_causal else 0)
         P = Decoder(self.model, self.kv, L, 0, self.tau).prefill(prompt)
         n_blocks = gen_len // L
-        active, covered, out = [], [], []
-        added = committed = 0
-        host = None  # host copy of the window's tokens
-
-        def filled(b):
-            return float((host[b * L:(b + 1) * L] != mask).float().mean())
-
-        def append_block():
-            nonlocal added, host
-            w = len(active)
-            self.tokens[w * L:(w + 1) * L] = mask
-            self.conf[w * L:(w + 1) * L] = 0.0
-            self.pred[w * L:(w + 1) * L] = mask
-            host = self.tokens[:(w + 1) * L].cpu()
-            active.append(w == 0)
-            covered.append(False)
-            added += 1
-
-        while committed < n_blocks:
-            if not active:
-                append_block()
+        out = torch.empty(max(1, n_blocks * L), dtype=torch.int32, device="cuda")
+        lopa_window_init(self.win, self.tokens, self.conf, self.pred, L, self.w_max, n_blocks, P,
+                         mask, self.tau_add, self.tau_act)
+        while True:
+            h = window_read(self.win)
+            if h.error:
+                raise RuntimeError("window commit found invalid inputs")
+            if h.done:
+                break
+            P, Lw, n_el = h.prefix_len, h.blocks * L, h.eligible
+            if h.need_initial:
+                # the new first block's initial forward (the block alone)
                 lopa_verify_forward(self.model, self.kv, P, self.tokens[:L], 1, L, self.conf[:L],
                                     self.pred[:L])
-                covered[:] = [True] * len(covered)
                 self.forwards += 1
-            while len(active) < self.w_max and added < n_blocks and filled(len(active) - 1) >= self.tau_add:
-                append_block()
-            Lw = len(active) * L
-            n_el = L * next((i for i, a in enumerate(active) if not a), len(active))
             state = ((self.tokens[:Lw].cpu(), self.conf[:Lw].cpu(), self.pred[:Lw].cpu())
                      if trace is not None else None)
             lopa_build_branches_window(self.tokens[:Lw], self.conf[:Lw], self.pred[:Lw], Lw, n_el,
@@ -228,38 +219,21 @@ class WindowDecoder:
             self.pred, self.next_pred = self.next_pred, self.pred
             self.forwards += 1
             self.iterations += 1
-            host = self.tokens[:Lw].cpu()
-            covered[:] = [True] * len(covered)
-            for i in range(1, len(active)):
-                if not active[i] and active[i - 1] and covered[i] and filled(i - 1) >= self.tau_act:
-                    active[i] = True
-            c = 0
-            while c < len(active) and not bool((host[c * L:(c + 1) * L] == mask).any()):
-                c += 1
+            selected = self.tokens[:Lw].cpu() if trace is not None else None
+            lopa_window_update(self.win, self.tokens, self.conf, self.pred, out)
+            lopa_window_commit(self.kv, self.winner, self.win)
             if trace is not None:
-                trace.append(dict(prefix_len=P, n_eligible=n_el, winner=int(self.winner.item()),
-                                  tokens=host.clone(), committed_blocks=c,
+                trace.append(dict(prefix_len=P, n_eligible=n_el, window_len=Lw,
+                                  initial_forward=bool(h.need_initial),
+                                  winner=int(self.winner.item()), tokens=selected,
+                                  committed_blocks=window_read(self.win).last_commit,
                                   scores=self.scores.cpu(), state=state,
                                   branch_tokens=self.bt[:nb * Lw].view(nb, Lw).cpu(),
                                   valid=self.valid.cpu(), n_valid=int(self.n_valid.item()),
                                   conf=self.conf_b[:nb * Lw].view(nb, Lw).cpu(),
                                   pred=self.pred_b[:nb * Lw].view(nb, Lw).cpu()))
-            if c:
-                lopa_commit_kv_rows(self.kv, self.winner, P, Lw, c * L, self.append_offset)
-                out.append(host[:c * L].clone())
-                rest = Lw - c * L
-                if rest:
-                    self.tokens[:rest] = self.tokens[c * L:Lw].clone()
-                    self.conf[:rest] = self.conf[c * L:Lw].clone()
-                    self.pred[:rest] = self.pred[c * L:Lw].clone()
-                    host = host[c * L:]
-                del active[:c], covered[:c]
-                if active:
-                    active[0] = True
-                P += c * L
-                committed += c
             if self.iterations > 2 * gen_len + 2 * n_blocks:
                 raise RuntimeError("window decode did not converge")
-        toks = torch.cat(out) if out else torch.zeros(0, dtype=torch.int32)
+        toks = out[:n_blocks * L].cpu() if n_blocks else torch.zeros(0, dtype=torch.int32)
         return dict(tokens=toks, iterations=self.iterations, forwards=self.forwards,
                     tpf=(toks.numel() / self.forwards) if self.forwards else 0.0)

@@ -46,7 +46,7 @@ FAKE = C.c_void_p(0x1000)  # never dereferenced: every case fails validation fir
 
 
 @pytest.mark.parametrize("L,mask,tau,k,code", [
-    (0, 5, 0.9, 3, -2), (65, 5, 0.9, 3, -2), (16, 5, 1.5, 3, -1), (16, 5, -0.1, 3, -1),
+    (0, 5, 0.9, 3, -2), (257, 5, 0.9, 3, -2), (16, 5, 1.5, 3, -1), (16, 5, -0.1, 3, -1),
     (16, 5, float("nan"), 3, -1), (16, 5, 0.9, -1, -1), (16, -1, 0.9, 3, -1)])
 def test_build_branches_validation(lp, L, mask, tau, k, code):
     rc = lp.lib.lopa_build_branches(FAKE, FAKE, FAKE, L, mask, tau, k, FAKE, FAKE, FAKE, FAKE, None)
@@ -67,7 +67,7 @@ def test_null_pointers(lp):
 def test_select_validation(lp):
     f = lp.lib.lopa_branch_confidence_select
     assert f(FAKE, FAKE, FAKE, FAKE, 0, 16, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -2
-    assert f(FAKE, FAKE, FAKE, FAKE, 4, 65, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -2
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 257, 5, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -2
     assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, -3, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == -1
 
 
@@ -80,7 +80,7 @@ def test_select_metric_validation(lp):
     assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 2, 1, 0.0, *o) == -1        # eta outside (0, 1]
     assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 2, 1, 1.5, *o) == -1
     assert f(FAKE, FAKE, FAKE, FAKE, 4, 16, 5, 2, 1, float("nan"), *o) == -1
-    assert f(FAKE, FAKE, FAKE, FAKE, 4, 65, 5, 1, 2, 1.0, *o) == -2        # L too large
+    assert f(FAKE, FAKE, FAKE, FAKE, 4, 257, 5, 1, 2, 1.0, *o) == -2       # L too large
     assert f(None, FAKE, FAKE, FAKE, 4, 16, 5, 0, 1, 1.0, *o) == -1
 
 
@@ -126,8 +126,8 @@ def test_kv_create_validation(lp):
     h = C.c_void_p()
     assert lp.lib.lopa_kv_create(None, 128, 8, 32, C.byref(h)) == -1
     assert lp.lib.lopa_kv_create(FAKE, 0, 8, 32, C.byref(h)) == -1
-    assert lp.lib.lopa_kv_create(FAKE, 128, 8, 65, C.byref(h)) == -2
-    assert lp.lib.lopa_kv_create(FAKE, 128, 16, 64, C.byref(h)) == -2   # 1024 rows > 512
+    assert lp.lib.lopa_kv_create(FAKE, 128, 8, 257, C.byref(h)) == -2
+    assert lp.lib.lopa_kv_create(FAKE, 128, 16, 256, C.byref(h)) == -2  # 4096 rows > 2048
 
 
 def test_window_entry_points_validation(lp):
@@ -135,6 +135,35 @@ def test_window_entry_points_validation(lp):
     o = (FAKE, FAKE, FAKE, FAKE, None)
     assert f(FAKE, FAKE, FAKE, 32, 0, 5, 0.9, 3, *o) == -1        # n_eligible < 1
     assert f(FAKE, FAKE, FAKE, 32, 33, 5, 0.9, 3, *o) == -1       # n_eligible > L
-    assert f(FAKE, FAKE, FAKE, 65, 32, 5, 0.9, 3, *o) == -2       # L too large
+    assert f(FAKE, FAKE, FAKE, 257, 32, 5, 0.9, 3, *o) == -2      # L too large
     assert f(None, FAKE, FAKE, 32, 16, 5, 0.9, 3, *o) == -1
     assert lp.lib.lopa_commit_kv_rows(None, FAKE, 0, 32, 16, FAKE, None) == -1
+
+
+def test_window_state_validation(lp):
+    """lopa_window_init / _update / _commit reject bad arguments on the host,
+    before any launch (the window's sizes and gates; null pointers)."""
+    init = lp.lib.lopa_window_init
+    t = (FAKE, FAKE, FAKE)
+    assert init(None, *t, 32, 2, 4, 0, 5, 0.1, 0.9, None) == -1
+    assert init(FAKE, None, FAKE, FAKE, 32, 2, 4, 0, 5, 0.1, 0.9, None) == -1
+    assert init(FAKE, *t, 32, 0, 4, 0, 5, 0.1, 0.9, None) == -2                 # w_max < 1
+    assert init(FAKE, *t, 16, lp.WINDOW_MAX_BLOCKS + 1, 4, 0, 5, 0.1, 0.9, None) == -2
+    assert init(FAKE, *t, 32, 9, 4, 0, 5, 0.1, 0.9, None) == -2                 # 288 positions
+    assert init(FAKE, *t, 0, 2, 4, 0, 5, 0.1, 0.9, None) == -2                  # L < 1
+    assert init(FAKE, *t, 32, 2, 0, 0, 5, 0.1, 0.9, None) == -1                 # no blocks
+    assert init(FAKE, *t, 32, 2, 4, -1, 5, 0.1, 0.9, None) == -1                # prefix < 0
+    assert init(FAKE, *t, 32, 2, 4, 0, 5, 1.5, 0.9, None) == -1                 # tau_add > 1
+    assert init(FAKE, *t, 32, 2, 4, 0, 5, 0.1, float("nan"), None) == -1
+    assert lp.lib.lopa_window_update(None, *t, FAKE, None) == -1
+    assert lp.lib.lopa_window_update(FAKE, *t, None, None) == -1
+    assert lp.lib.lopa_window_commit(None, FAKE, FAKE, None) == -1
+    assert lp.lib.lopa_window_commit(FAKE, None, FAKE, None) == -1
+
+
+def test_window_struct_layout(lp):
+    """The ctypes mirror of lopa_window has the header's field order and size
+    (16 header words, then the activation flags)."""
+    assert C.sizeof(lp.lopa_window) == 4 * (16 + lp.WINDOW_MAX_BLOCKS)
+    assert [f[0] for f in lp.lopa_window._fields_][:5] == ["blocks", "eligible", "prefix_len",
+                                                            "need_initial", "done"]

@@ -171,7 +171,13 @@ def test_free_running_block(cfgname, P, L, k, tau, metric, min_iters):
 
 # ---------------------------------------------- multi-block window (R27-R30)
 WINDOW_CASES = [("tiny", 32, 16, 3, 0.9, 0.1, 0.5, 2, 48), ("tiny", 32, 16, 2, 0.9, 0.0, 0.3, 4, 64),
-                ("small", 64, 32, 3, 0.9, 0.1, 0.5, 2, 64)]
+                ("small", 64, 32, 3, 0.9, 0.1, 0.5, 2, 64),
+                # windows past 64 positions: 6 x 16, 4 x 32 and 8 x 32 (row groups of
+                # the attention, 256-position build / select)
+                ("tiny", 32, 16, 3, 0.9, 0.0, 0.3, 6, 96), ("small", 64, 32, 3, 0.9, 0.0, 0.5, 4, 128),
+                ("small", 16, 32, 1, 0.9, 0.0, 0.5, 8, 256)]
+FREE_WINDOW_CASES = [WINDOW_CASES[i] for i in (0, 1, 3, 4, 5)]
+FORWARD_CHECKS_LONG = 6  # forwards compared with the oracle per long-window case
 
 
 def _load_rows(s, cache, upto):
@@ -213,7 +219,7 @@ def _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, 
     assert len(res["tokens"]) == gen and not np.any(res["tokens"] == mask)
     cache = res["cache"]
     checked = windows = 0
-    for it in otrace:
+    for t_idx, it in enumerate(otrace):
         P_t, (tokens, conf, pred), n_el = it["prefix_len"], it["state"], it["n_eligible"]
         Lw = len(tokens)
         windows += Lw > L
@@ -235,8 +241,12 @@ def _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, 
         lp.lopa_verify_forward(s.model, s.kv, P_t, _d(obt.ravel(), I32), nb, Lw, conf_b, pred_b)
         gc = conf_b.view(nb, Lw).cpu().numpy().astype(np.float64)
         gp = pred_b.view(nb, Lw).cpu().numpy()
-        check_forward(s, obt, gc, gp, P=P_t, cache_f=cache, causal_blk=cblk,
-                      layers=Lw > L, label=f"window {Lw} rows, prefix {P_t}")
+        # per-layer comparisons on the first two multi-block windows; for
+        # windows past 64 positions the whole-forward checks on the first
+        # FORWARD_CHECKS_LONG iterations (every decision is replayed below)
+        if L * w_max <= 64 or t_idx < FORWARD_CHECKS_LONG:
+            check_forward(s, obt, gc, gp, P=P_t, cache_f=cache, causal_blk=cblk,
+                          layers=Lw > L and windows <= 2, label=f"window {Lw} rows, prefix {P_t}")
         scores = torch.empty(nb, dtype=F32, device="cuda")
         win = torch.empty(1, dtype=I32, device="cuda")
         nt = torch.empty(Lw, dtype=I32, device="cuda")
@@ -263,10 +273,12 @@ def _window_teacher_forced(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, 
 
 
 @pytest.mark.parametrize("block_causal", [False, True])
-@pytest.mark.parametrize("cfgname,P,L,k,tau,tau_add,tau_act,w_max,gen", WINDOW_CASES[:2])
+@pytest.mark.parametrize("cfgname,P,L,k,tau,tau_add,tau_act,w_max,gen", FREE_WINDOW_CASES)
 def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_max, gen, block_causal):
-    """The GPU WindowDecoder end to end: a filled, committed sequence, and the
-    oracle's trajectory until a decision the oracle calls a near-tie."""
+    """The GPU WindowDecoder end to end: a filled, committed sequence; the
+    device gates (lopa_window_update / _commit) against the oracle's window
+    bookkeeping (WindowGates) driven by the GPU's own selections; every
+    iteration's decisions replayed; the oracle's trajectory logged."""
     log(f"window free-running {cfgname} P={P} L={L} k={k} w_max={w_max} block_causal={block_causal}")
     s = Setup(cfgname, 0, L * w_max, k, max_len=P + gen)
     mask = s.cfg["mask_id"]
@@ -290,6 +302,35 @@ def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_
         cache.k[layer, :, :end] = kk.float().cpu().numpy()
         cache.v[layer, :, :end] = vv.float().cpu().numpy()
     cblk = L if block_causal else 0
+    # the device gates: each iteration's window (prefix, length, eligible
+    # positions, rows) and its committed blocks as the oracle's bookkeeping
+    # gives them from the GPU's selections
+    gates = lopa.WindowGates(L, w_max, gen // L, tau_add, tau_act, mask)
+    wt, wc, wp = np.zeros(0, np.int64), np.zeros(0), np.zeros(0, np.int64)
+    Pg, grown = P, 0
+    for t, g in enumerate(gtrace):
+        wt, wc, wp, opened = gates.fill(wt, wc, wp)
+        assert g["initial_forward"] == opened, f"iteration {t}: initial forward"
+        assert (g["prefix_len"], g["window_len"], g["n_eligible"]) == (Pg, len(wt), gates.eligible()), \
+            f"iteration {t}: window"
+        st_t, st_c, st_p = (v.numpy() for v in g["state"])
+        assert np.array_equal(st_t, wt), f"iteration {t}: window tokens"
+        if not opened:
+            assert np.array_equal(st_c, wc.astype(np.float32)) and np.array_equal(st_p, wp)
+        grown = max(grown, len(wt))
+        sel = g["tokens"].numpy().astype(np.int64)
+        w = g["winner"]
+        c = gates.after_select(sel)
+        assert g["committed_blocks"] == c, f"iteration {t}: committed blocks"
+        wt = sel[c * L:]
+        wc = g["conf"].numpy()[w, c * L:].astype(np.float64)
+        wp = g["pred"].numpy()[w, c * L:].astype(np.int64)
+        Pg += c * L
+    assert gates.committed == gen // L and grown > L
+    if tau_add == 0.0:  # the window fills at once: it reached its full length
+        assert grown == L * min(w_max, gen // L)
+    log(f"  device gates as the oracle's bookkeeping over {len(gtrace)} iterations; "
+        f"longest window {grown} positions")
     excused = 0
     for t, g in enumerate(gtrace):
         tokens, conf, pred = (v.numpy() for v in g["state"])
@@ -298,17 +339,19 @@ def test_window_decoder_free_running(cfgname, P, L, k, tau, tau_add, tau_act, w_
         assert np.array_equal(g["branch_tokens"].numpy(), rbt), f"iteration {t}: branches differ"
         assert np.array_equal(g["valid"].numpy(), rva) and g["n_valid"] == rnv
         gc = g["conf"].numpy().astype(np.float64)
-        check_forward(s, rbt, gc, g["pred"].numpy(), P=g["prefix_len"], cache_f=cache,
-                      causal_blk=cblk, layers=False, label=f"iteration {t}")
+        if L * w_max <= 64 or t < FORWARD_CHECKS_LONG:
+            check_forward(s, rbt, gc, g["pred"].numpy(), P=g["prefix_len"], cache_f=cache,
+                          causal_blk=cblk, layers=False, label=f"iteration {t}")
         ts, tw = lopa.select(rbt, gc, rva, mask)
         if score_margin(ts) >= NEAR_TIE:
             assert g["winner"] == tw or np.array_equal(rbt[g["winner"]], rbt[tw])
         else:
             excused += 1
         assert np.array_equal(g["tokens"].numpy(), rbt[g["winner"]])
-    otrace = []
-    res = lopa.decode_window(s.faith, prompt.numpy(), gen, L, k, f32(tau), tau_add, tau_act, w_max,
-                             trace=otrace, block_causal=block_causal)
-    same = np.array_equal(g_tokens, res["tokens"])
+    own = "not run (long window)"
+    if L * w_max <= 64:  # the oracle's own trajectory, for the log
+        res = lopa.decode_window(s.faith, prompt.numpy(), gen, L, k, f32(tau), tau_add, tau_act,
+                                 w_max, block_causal=block_causal)
+        own = "identical" if np.array_equal(g_tokens, res["tokens"]) else "differs"
     log(f"  {out['iterations']} iterations, {out['forwards']} forwards, TPF {out['tpf']:.2f}; "
-        f"{excused} winner near-ties; oracle's own trajectory {'identical' if same else 'differs'}")
+        f"{excused} winner near-ties; oracle's own trajectory {own}")

@@ -27,7 +27,7 @@ def _dev(a, dtype):
 def _cases():
     rng = np.random.default_rng(1234)
     out = []
-    for L in (1, 5, 16, 32, 33, 64):
+    for L in (1, 5, 16, 32, 33, 64, 65, 96, 128, 200, 256):
         for k in (0, 1, 3, 7, 15):
             for tau in (0.3, 0.9, 0.99):
                 for style in ("cont", "ties"):
@@ -68,7 +68,8 @@ METRICS = [(0, 1, 1.0), (1, 1, 1.0), (1, 3, 1.0), (1, 8, 1.0), (2, 1, 0.1), (2, 
 
 @pytest.mark.parametrize("metric,window,eta", METRICS, ids=lambda v: str(v))
 @pytest.mark.parametrize("nb,L,seed", [(1, 16, 0), (4, 16, 1), (8, 32, 2), (16, 32, 3),
-                                       (3, 7, 4), (8, 64, 5), (33, 9, 6)])
+                                       (3, 7, 4), (8, 64, 5), (33, 9, 6), (4, 65, 7),
+                                       (8, 128, 8), (2, 200, 9), (8, 256, 10)])
 def test_select_matches_oracle(lp, nb, L, seed, metric, window, eta):
     """Eq. 2 (metric 0) and the alternative branch confidences (1: window
     minimum, 2: lowest-segment mean) against the oracle."""
