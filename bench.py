@@ -370,6 +370,40 @@ class StepRunner:
         return {kd: round(t / steps, 4) for kd, (t, n) in prof.items()}
 
 
+def blas_reference(reps_per_copy=20):
+    """The same GEMM shapes (256 rows, the verify step at the 7B shape) through
+    torch.matmul (the vendor BLAS, hipBLASLt / rocBLAS) in bf16, with enough
+    distinct weight copies that every call streams its weights from HBM, as
+    the model's layers do. The library GEMMs here carry no epilogue (no
+    SwiGLU, bias, RoPE or softmax statistics)."""
+    import torch
+    out = {}
+    for name, (M, K, N) in {"qkv": (256, 3584, 4608), "o": (256, 3584, 3584),
+                            "gateup": (256, 3584, 37888), "down": (256, 18944, 3584),
+                            "lmhead": (256, 3584, 152064)}.items():
+        copies = max(2, int(600e6 // (K * N * 2)))
+        g = torch.Generator(device="cuda").manual_seed(0)
+        A = torch.randn(M, K, device="cuda", dtype=torch.bfloat16, generator=g) * 0.1
+        Ws = [torch.randn(N, K, device="cuda", dtype=torch.bfloat16, generator=g) * 0.02
+              for _ in range(copies)]
+        for W in Ws:
+            C = A @ W.t()
+        torch.cuda.synchronize()
+        reps = reps_per_copy * copies
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for i in range(reps):
+            C = A @ Ws[i % copies].t()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / reps
+        out[name] = {"M": M, "K": K, "N": N, "us": round(us, 1),
+                     "weight_gbs": round(K * N * 2 / us / 1e3, 1)}
+        del Ws, A, C
+        torch.cuda.empty_cache()
+    print(json.dumps({"blas_reference": out}))
+
+
 def shape_figure(lp, synth, model, cfg, P, L, k, tau, steps, warmup, what, precision="bf16"):
     """One line per further measured shape: ms/step (mean, median, p10, p90),
     branch-tokens/s, the step's algorithmic HBM bytes and FLOPs against the
@@ -515,6 +549,8 @@ def main():
                     help="only run a 1 GiB device copy 5 times (HBM counter calibration)")
     ap.add_argument("--hbm-counters", action="store_true",
                     help="only run 3 torch-free verify forwards (for rocprofv3 --pmc)")
+    ap.add_argument("--blas-reference", action="store_true",
+                    help="only time the step's GEMM shapes through torch.matmul (vendor BLAS)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -535,6 +571,10 @@ def main():
         return
 
     import torch
+
+    if args.blas_reference:
+        blas_reference()
+        return
 
     import synth
     import paper_2512_16229_amd as lp
