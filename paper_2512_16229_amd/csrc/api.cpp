@@ -182,6 +182,7 @@ struct lopa_kv {
   float* ps = nullptr;
   int32_t* pi = nullptr;
   int last_nb = -1, last_L = -1, last_P = -1;
+  size_t part_bytes = 0;  // bytes of partials
   std::vector<void*> owned;
   // launch timing (lopa_kv_profile): events around launches of enabled kinds
   int prof_mask = 0;
@@ -504,6 +505,12 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
                        plan_partial_bytes(EPI_RESID, p.o, MT),
                        plan_partial_bytes(EPI_RESID, p.down, MT)});
   }
+  // the attention's scratch (between the QKV fix-up and the output projection
+  // the partial sums are free): its largest need over the branch counts
+  for (int nb = 1; nb <= max_branches; ++nb)
+    part_b = std::max(part_b, attention_scratch_bytes(nb, std::min(max_block, 32), c.heads,
+                                                      c.kv_heads, d));
+  kv->part_bytes = part_b;
   const size_t rows = (size_t)kv->mp_max;
   const int FP = round256(F);
 #define KV_ALLOC(field, type, bytes)                  \
@@ -656,6 +663,8 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   at.scale = 1.0f / std::sqrt((float)d);
   // a block of one sub-block (or less) needs no mask
   at.cblk = kv->causal_blk && L > kv->causal_blk ? kv->causal_blk : 0;
+  at.scratch = ws.partials;
+  at.scratch_bytes = ws.partials_bytes;
   const int n_layers = stop_layer >= 0 ? std::min(stop_layer, c.layers) : c.layers;
   for (int l = 0; l < n_layers; ++l) {
     const LayerPack& p = m->layers[l];
@@ -768,6 +777,7 @@ static VerifyWs kv_ws(const lopa_kv* kv) {
   w.fbuf = kv->fbuf;
   w.qbuf = kv->qbuf;
   w.partials = kv->partials;
+  w.partials_bytes = kv->part_bytes;
   w.pm = kv->pm;
   w.ps = kv->ps;
   w.pi = kv->pi;
@@ -1033,7 +1043,8 @@ WsLayout ws_layout(const lopa_model* m, int32_t nb, int32_t L) {
   w.sz[2] = rows * round256(c.ffn) * 2;
   w.sz[3] = (size_t)nb * c.heads * L * c.head_dim * 2;
   w.sz[4] = std::max({(size_t)16, plan_partial_bytes(EPI_QKV, p.qkv, MT),
-                      plan_partial_bytes(EPI_RESID, p.o, MT), plan_partial_bytes(EPI_RESID, p.down, MT)});
+                      plan_partial_bytes(EPI_RESID, p.o, MT), plan_partial_bytes(EPI_RESID, p.down, MT),
+                      attention_scratch_bytes(nb, L, c.heads, c.kv_heads, c.head_dim)});
   w.sz[5] = w.sz[6] = w.sz[7] = rows * m->tiles_lm * 4;
   if (m->fp8) {
     w.sz[8] = rows * round512(c.hidden);
@@ -1064,6 +1075,7 @@ VerifyWs verify_ws_carve(const lopa_model* m, int32_t n_branches, int32_t L, cha
   ws.fbuf = (uint16_t*)r[2];
   ws.qbuf = (uint16_t*)r[3];
   ws.partials = (float*)r[4];
+  ws.partials_bytes = w.sz[4];
   ws.pm = (float*)r[5];
   ws.ps = (float*)r[6];
   ws.pi = (int32_t*)r[7];

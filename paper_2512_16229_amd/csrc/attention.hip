@@ -25,6 +25,7 @@
 
 #include <math.h>
 
+#include <algorithm>
 #include <type_traits>
 
 namespace {
@@ -710,6 +711,245 @@ hipError_t launch_sl(const AttnArgs& a, int nt, hipStream_t s) {
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Grouped form, for key ranges too long for the single-load form (more than
+// SL_WAVES x 3 tiles) with grouped-query heads (2..8 query heads per KV head).
+// The keys are cut into NS splits; a workgroup takes one (KV head, branch,
+// split) with one wavefront per query head of the group, so that every K / V
+// tile crosses into the CU once for all the group's heads (wavefront 0 copies
+// it into an LDS ring, the others read it after a barrier). Three launches:
+//   gmax   each row's largest score over the split's keys,
+//   gpv    the exact row maximum (over the splits), then the probabilities
+//          rounded to bf16 against it, their sum and P V over the split,
+//   merge  the splits' sums and outputs added in split order, normalised,
+//          rounded to bf16 into the packed operand of the output projection.
+// The scores are formed the same way (the same MFMA chain, tile by tile) in
+// gmax and gpv, so the maximum gpv subtracts is exactly one of its scores.
+constexpr int GQ_RING = 4;  // LDS slots: one tile in use, GQ_RING - 1 in flight
+
+struct GroupSplit {
+  int p_lo, np, n;  // first prefix tile; prefix tiles; all tiles (the last split
+                    // also takes the block's tiles)
+};
+__device__ __forceinline__ GroupSplit group_split(int P, int L, int sp, int NS) {
+  const int pt = (P + KT - 1) / KT, bt = (L + KT - 1) / KT;
+  const int p_lo = sp * pt / NS, p_hi = (sp + 1) * pt / NS;
+  return {p_lo, p_hi - p_lo, p_hi - p_lo + (sp == NS - 1 ? bt : 0)};
+}
+
+template <int D, int QB, bool WITH_V>
+__device__ __forceinline__ void group_issue(const AttnArgs& a, const GroupSplit& gs, int i,
+                                            int slot, uint32_t ring, const uint16_t* kc,
+                                            const uint16_t* vc, const uint16_t* ks,
+                                            const uint16_t* vs, const CopyOffsets& co_c,
+                                            const CopyOffsets& co_s, int c16, int g) {
+  using T = TileLds<D>;
+  constexpr int OPS = WITH_V ? T::OPS : 2 * (D / 32);
+  constexpr int SLOT = WITH_V ? T::TILE : T::KBYTES;
+  i = i < gs.n ? i : gs.n - 1;  // past the last tile: the last one again
+  const bool pre = i < gs.np;
+  const int p0 = (pre ? gs.p_lo + i : i - gs.np) * KT, lim = pre ? a.P : a.L;
+  const uint32_t sb = ring + (uint32_t)slot * SLOT;
+  if (p0 + KT <= lim) {
+#pragma unroll
+    for (int q = 0; q < OPS; ++q)
+      tile_copy_full<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, sb,
+                        pre ? co_c : co_s);
+  } else {
+#pragma unroll
+    for (int q = 0; q < OPS; ++q)
+      tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, lim, sb, c16, g);
+  }
+}
+
+// Q^T operand of query head h, rows 16 qb + c16 of branch br (zero past L)
+template <int D, int QB>
+__device__ __forceinline__ void group_q(const AttnArgs& a, int br, int h, int c16, int g,
+                                        u32x4 (&qf)[QB][D / 32]) {
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int row = qb * 16 + c16;
+    const uint16_t* qrow = a.q + (((int64_t)br * a.Hq + h) * a.L + (row < a.L ? row : 0)) * D;
+    const unsigned keep = row < a.L ? ~0u : 0u;
+#pragma unroll
+    for (int kk = 0; kk < D / 32; ++kk)
+      qf[qb][kk] = *(const u32x4*)(qrow + kk * 32 + g * 8) & keep;
+  }
+}
+
+// scratch layout: mpart [nb][Hq][L][NS], lsum [NS][nb][Hq][L], opart [NS][nb][Hq][L][D]
+struct GroupScratch {
+  float *m, *l, *o;
+};
+__host__ __device__ __forceinline__ size_t group_scratch_floats(const AttnArgs& a, int NS) {
+  const size_t rows = (size_t)a.nb * a.Hq * a.L;
+  return rows * NS * 2 + rows * NS * a.d;
+}
+__device__ __forceinline__ GroupScratch group_scratch(const AttnArgs& a, int NS) {
+  const size_t rows = (size_t)a.nb * a.Hq * a.L;
+  return {a.scratch, a.scratch + rows * NS, a.scratch + rows * NS * 2};
+}
+
+template <int D, int QB>
+__global__ __launch_bounds__(512) void attn_gmax_kernel(AttnArgs a, int NS) {
+  using T = TileLds<D>;
+  constexpr int KOPS = 2 * (D / 32);
+  __shared__ __attribute__((aligned(1024))) char smem[GQ_RING * T::KBYTES];
+  const int kvh = blockIdx.x, br = blockIdx.y, sp = blockIdx.z;
+  const int G = a.Hq / a.Hkv;
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int h = kvh * G + wv, g = lane >> 4, c16 = lane & 15;
+  const GroupSplit gs = group_split(a.P, a.L, sp, NS);
+  const int np = gs.np;
+  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;
+  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;
+  const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
+  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
+  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
+  const uint32_t ring = (uint32_t)(uintptr_t)smem;
+  const CopyOffsets co_c = copy_offsets<D>(a.vld, c16, g), co_s = copy_offsets<D>(a.vlds, c16, g);
+  if (wv == 0 && gs.n > 0)
+#pragma unroll
+    for (int i = 0; i < GQ_RING - 1; ++i)
+      group_issue<D, QB, false>(a, gs, i, i, ring, kc, vc, ks, vs, co_c, co_s, c16, g);
+  u32x4 qf[QB][D / 32];
+  group_q<D, QB>(a, br, h, c16, g, qf);
+  float mraw[QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) mraw[qb] = -INFINITY;
+  for (int i = 0; i < gs.n; ++i) {
+    if (wv == 0) attn_wait_vmcnt<KOPS * (GQ_RING - 2)>();  // tile i has landed
+    lds_barrier();  // ... for every wavefront, which all finished tile i - 1
+    if (wv == 0)
+      group_issue<D, QB, false>(a, gs, i + GQ_RING - 1, (i + GQ_RING - 1) % GQ_RING, ring, kc, vc,
+                                ks, vs, co_c, co_s, c16, g);
+    const bool pre = i < np;
+    tile_max<D, QB>(smem + (i % GQ_RING) * T::KBYTES, lane, qf, mraw,
+                    (pre ? gs.p_lo + i : i - np) * KT, pre ? a.P : a.L, g, pre ? 0 : a.cblk, 0);
+  }
+  if (wv == 0) attn_wait_vmcnt<0>();
+  const GroupScratch sc = group_scratch(a, NS);
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float m = pair32_max(pair16_max(mraw[qb]));
+    const int row = qb * 16 + c16;
+    if (g == 0 && row < a.L) sc.m[(((int64_t)br * a.Hq + h) * a.L + row) * NS + sp] = m;
+  }
+}
+
+template <int D, int QB>
+__global__ __launch_bounds__(512) void attn_gpv_kernel(AttnArgs a, int NS) {
+  using T = TileLds<D>;
+  constexpr int NDB = D / 16;
+  __shared__ __attribute__((aligned(1024))) char smem[GQ_RING * T::TILE];
+  const int kvh = blockIdx.x, br = blockIdx.y, sp = blockIdx.z;
+  const int G = a.Hq / a.Hkv;
+  const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int h = kvh * G + wv, g = lane >> 4, c16 = lane & 15;
+  const GroupSplit gs = group_split(a.P, a.L, sp, NS);
+  const int np = gs.np;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;
+  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;
+  const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
+  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
+  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
+  const uint32_t ring = (uint32_t)(uintptr_t)smem;
+  const CopyOffsets co_c = copy_offsets<D>(a.vld, c16, g), co_s = copy_offsets<D>(a.vlds, c16, g);
+  if (wv == 0 && gs.n > 0)
+#pragma unroll
+    for (int i = 0; i < GQ_RING - 1; ++i)
+      group_issue<D, QB, true>(a, gs, i, i, ring, kc, vc, ks, vs, co_c, co_s, c16, g);
+  u32x4 qf[QB][D / 32];
+  group_q<D, QB>(a, br, h, c16, g, qf);
+  const GroupScratch sc = group_scratch(a, NS);
+  float m[QB], l[QB];
+  f32x4 o[NDB][QB];
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const int row = qb * 16 + c16;
+    float mx = 0.f;  // rows past L: zero queries, any finite reference
+    if (row < a.L) {
+      const float* mp = sc.m + (((int64_t)br * a.Hq + h) * a.L + row) * NS;
+      mx = mp[0];
+      for (int s2 = 1; s2 < NS; ++s2) mx = max2(mx, mp[s2]);
+    }
+    m[qb] = mx * sl2;  // the exact row maximum: every probability <= 1
+    l[qb] = 0.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) o[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int i = 0; i < gs.n; ++i) {
+    if (wv == 0) attn_wait_vmcnt<T::OPS * (GQ_RING - 2)>();
+    lds_barrier();
+    if (wv == 0)
+      group_issue<D, QB, true>(a, gs, i + GQ_RING - 1, (i + GQ_RING - 1) % GQ_RING, ring, kc, vc,
+                               ks, vs, co_c, co_s, c16, g);
+    AttnTile<D> x;
+    tile_fetch<D>(smem + (i % GQ_RING) * T::TILE, lane, x);
+    const bool pre = i < np;
+    tile_update<D, QB, false>(x, qf, m, l, o, (pre ? gs.p_lo + i : i - np) * KT,
+                              pre ? a.P : a.L, sl2, g, pre ? 0 : a.cblk, 0);
+  }
+  if (wv == 0) attn_wait_vmcnt<0>();
+#pragma unroll
+  for (int qb = 0; qb < QB; ++qb) {
+    const float ls = pair32_sum(pair16_sum(l[qb]));
+    const int row = qb * 16 + c16;
+    if (row >= a.L) continue;
+    const int64_t r = (((int64_t)sp * a.nb + br) * a.Hq + h) * a.L + row;
+    if (g == 0) sc.l[r] = ls;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db) *(f32x4*)(sc.o + r * D + db * 16 + g * 4) = o[db][qb];
+  }
+}
+
+// one thread per (branch, head, row, 4 dimensions)
+template <int D>
+__global__ __launch_bounds__(256) void attn_gmerge_kernel(AttnArgs a, int NS) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int q4 = (int)(t % (D / 4));
+  const int64_t r = t / (D / 4);  // (branch, head, row)
+  if (r >= (int64_t)a.nb * a.Hq * a.L) return;
+  const int row = (int)(r % a.L), h = (int)((r / a.L) % a.Hq), br = (int)(r / ((int64_t)a.L * a.Hq));
+  const GroupScratch sc = group_scratch(a, NS);
+  const int64_t rows = (int64_t)a.nb * a.Hq * a.L;
+  f32x4 acc = *(const f32x4*)(sc.o + r * D + q4 * 4);
+  float ls = sc.l[r];
+  for (int s2 = 1; s2 < NS; ++s2) {
+    acc += *(const f32x4*)(sc.o + (s2 * rows + r) * D + q4 * 4);
+    ls += sc.l[s2 * rows + r];
+  }
+  const float inv = 1.0f / ls;
+  uint16_t ob[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) ob[j] = f2bf_bits(acc[j] * inv);
+  *(uint2*)(a.out + packA_off(br * a.L + row, h * D + q4 * 4, a.Mp)) = *(const uint2*)ob;
+}
+
+// key splits of the grouped form before the per-call caps: enough workgroups
+// for the chip's 256 CUs, at most 16
+int group_splits(int nb, int Hkv) {
+  return std::min(16, std::max(1, (256 + Hkv * nb - 1) / (Hkv * nb)));
+}
+
+template <int D>
+hipError_t launch_group(const AttnArgs& a, int NS, hipStream_t s) {
+  const int G = a.Hq / a.Hkv;
+  const dim3 grid(a.Hkv, a.nb, NS), block(64 * G);
+  if (a.L <= 16) {
+    hipLaunchKernelGGL((attn_gmax_kernel<D, 1>), grid, block, 0, s, a, NS);
+    hipLaunchKernelGGL((attn_gpv_kernel<D, 1>), grid, block, 0, s, a, NS);
+  } else {
+    hipLaunchKernelGGL((attn_gmax_kernel<D, 2>), grid, block, 0, s, a, NS);
+    hipLaunchKernelGGL((attn_gpv_kernel<D, 2>), grid, block, 0, s, a, NS);
+  }
+  const int64_t threads = (int64_t)a.nb * a.Hq * a.L * (D / 4);
+  hipLaunchKernelGGL((attn_gmerge_kernel<D>), dim3((unsigned)((threads + 255) / 256)), dim3(256),
+                     0, s, a, NS);
+  return hipGetLastError();
+}
+
 template <int D>
 hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
   const int T = (a.P + KT - 1) / KT + (a.L + KT - 1) / KT;
@@ -717,6 +957,16 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
   if (a.L <= 32 && nt <= 3) {
     if (a.L <= 16) return launch_sl<D, 1>(a, nt, s);
     return launch_sl<D, 2>(a, nt, s);
+  }
+  const int G = a.Hq / a.Hkv;
+  if (a.L <= 32 && G >= 2 && G <= 8 && a.scratch) {
+    // key splits: enough workgroups for the chip, at least 4 prefix tiles each,
+    // within the scratch
+    const int pt = (a.P + KT - 1) / KT;
+    int NS = group_splits(a.nb, a.Hkv);
+    NS = std::min(NS, std::max(1, pt / 4));
+    while (NS > 1 && group_scratch_floats(a, NS) * 4 > a.scratch_bytes) --NS;
+    if (group_scratch_floats(a, NS) * 4 <= a.scratch_bytes) return launch_group<D>(a, NS, s);
   }
   // up to 64 query rows per workgroup; longer blocks (multi-block windows) in
   // groups of 64 rows, each group reading all of the branch's keys
@@ -732,6 +982,13 @@ hipError_t launch_d(const AttnArgs& a, hipStream_t s) {
 }
 
 }  // namespace
+
+size_t attention_scratch_bytes(int nb, int L, int Hq, int Hkv, int d) {
+  const int G = Hkv > 0 ? Hq / Hkv : 0;
+  if (L > 32 || G < 2 || G > 8) return 0;
+  const size_t rows = (size_t)nb * Hq * L;
+  return rows * group_splits(nb, Hkv) * (2 + (size_t)d) * 4;
+}
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.L < 1 || a.L > 256 || a.P < 0 || a.Hq % a.Hkv || a.vld % 8 || a.vlds % 8 ||

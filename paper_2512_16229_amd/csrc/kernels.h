@@ -156,5 +156,12 @@ struct AttnArgs {
   // a row of sub-block r / cblk sees the prefix and the block keys of the
   // sub-blocks up to its own. 0: full attention inside the block.
   int cblk;
+  // working memory of the grouped form for long key ranges (per key split:
+  // row maxima, sums and partial outputs); null or too small: not used
+  float* scratch;
+  size_t scratch_bytes;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+// bytes of AttnArgs::scratch that let the grouped form run with its full key
+// splits for nb branches of L rows at any prefix (0: the shape never takes it)
+size_t attention_scratch_bytes(int nb, int L, int Hq, int Hkv, int d);

@@ -16,7 +16,8 @@ struct VerifyWs {
   uint16_t* abuf = nullptr;    // packed [Mp][H] bf16 operand
   uint16_t* fbuf = nullptr;    // packed [Mp][round256(F)] bf16 operand (padding columns zero)
   uint16_t* qbuf = nullptr;    // [branches][Hq][L][d] bf16 queries
-  float* partials = nullptr;   // split-K partial sums
+  float* partials = nullptr;   // split-K partial sums; the grouped attention's scratch
+  size_t partials_bytes = 0;
   float* pm = nullptr;         // [Mp][LM-head tiles] max
   float* ps = nullptr;         // [Mp][LM-head tiles] sum of exp
   int32_t* pi = nullptr;       // [Mp][LM-head tiles] argmax

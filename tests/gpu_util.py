@@ -210,24 +210,29 @@ def _check_forward_bf16(s, bt, conf_g, pred_g, P, cache_f, cache_p, causal_blk, 
         return model.forward_block(bt, P, cache, x_in=x, first_layer=li, n_layers=li + 1,
                                    causal_blk=causal_blk)["x"]
 
+    # layers: True (all), a list of layer indices, or False
+    which = set(range(Ly)) if layers is True else (set(layers) if layers else set())
     rel_f, rel_p = [], []
     x0 = s.faith.embed[np.asarray(bt)]
-    x_g, x_p, x_f = x0, x0, x0     # GPU input of the layer, pure and faithful end to end
+    x_g, g_at = x0, 0              # a GPU residual stream and the layers it has passed
+    x_p, x_f = x0, x0              # pure and faithful end to end
     for li in range(Ly):
-        if layers:
+        if li in which:
+            x_in = x_g if g_at == li else gpu_residual(s, bt, li, P)
             xg = gpu_residual(s, bt, li + 1, P)
-            rel_f.append(rel_l2(xg, one(s.faith, x_g, li, cache_f)))
-            rel_p.append(rel_l2(xg, one(s.pure, x_g, li, cache_f)))
-            x_g = xg
+            rel_f.append(rel_l2(xg, one(s.faith, x_in, li, cache_f)))
+            rel_p.append(rel_l2(xg, one(s.pure, x_in, li, cache_f)))
+            x_g, g_at = xg, li + 1
         x_p = one(s.pure, x_p, li, cache_p)
         if e2e_faithful:
             x_f = one(s.faith, x_f, li, cache_f)
         if big:
+            tf = li in which
             log(f"    layer {li}: teacher-forced rel-L2 vs faithful "
-                f"{rel_f[-1] if layers else 0:.2e}, vs pure {rel_p[-1] if layers else 0:.2e}; end "
-                f"to end: gpu-pure {rel_l2(x_g, x_p) if layers else 0:.2e}, faithful-pure "
+                f"{rel_f[-1] if tf else 0:.2e}, vs pure {rel_p[-1] if tf else 0:.2e}; end "
+                f"to end: gpu-pure {rel_l2(x_g, x_p) if tf else 0:.2e}, faithful-pure "
                 f"{rel_l2(x_f, x_p) if e2e_faithful else 0:.2e}")
-    x_last = x_g if layers else gpu_residual(s, bt, Ly, P)
+    x_last = x_g if g_at == Ly else gpu_residual(s, bt, Ly, P)
     rp = s.pure.lm_from_residual(x_p)
     e_pure = float(np.max(np.abs(conf_g - rp["conf"])))
     rf_e2e, bad_e2e, e_faith, n_dec, e_bf16 = None, -1, float("nan"), 0, 0.0
@@ -260,7 +265,7 @@ def _check_forward_bf16(s, bt, conf_g, pred_g, P, cache_f, cache_p, causal_blk, 
     else:
         log(f"  {label}: bf16 arithmetic alone differs from float64 by {e_bf16:.2e} > {tol:.2e}; "
             f"end-to-end confidences not bounded on this case")
-    for li, (rf, rpu) in enumerate(zip(rel_f, rel_p)):
+    for li, rf, rpu in zip(sorted(which), rel_f, rel_p):
         assert rf <= LAYER_TOL, f"{label}: layer {li} rel-L2 vs faithful {rf:.2e} > {LAYER_TOL}"
         assert rpu <= LAYER_TOL_PURE, f"{label}: layer {li} rel-L2 vs pure {rpu:.2e}"
     assert not np.any(pred_g == mask)

@@ -10,8 +10,9 @@ One whole LoPA iteration (Alg. 1) at each shape, all layers, every row:
   * lopa_build_branches on that state against the oracle's Eq. 1 / top-k on
     the same confidences (bit-exact);
   * lopa_verify_forward of all k+1 branches against the float64 oracle with
-    the fixed tolerances of gpu_util.check_forward: every layer fed the GPU's
-    own input residual stream (rel-L2 vs the bf16-faithful layer), confidences
+    the fixed tolerances of gpu_util.check_forward: every layer (every seventh
+    and the last at prefix 2048) fed the GPU's own input residual stream
+    (rel-L2 vs the bf16-faithful layer), confidences
     within 2e-2 of the pure oracle end to end, and the oracle's LM head +
     softmax on the GPU's own final rows (confidence within 1e-3, candidate
     tokens equal where the top-2 margin is >= 1e-3);
@@ -107,7 +108,11 @@ def test_lopa_iteration_full_depth(big):
     gc = dec.conf_b.view(nb, L).cpu().numpy().astype(np.float64)
     gp = dec.pred_b.view(nb, L).cpu().numpy()
     log(f"  verify forward: {nb * L} rows, conf {gc.min():.3f}..{gc.max():.3f}")
-    st = check_forward(s, rbt, gc, gp, layers=True, e2e_faithful=True, label="verify forward")
+    # every layer teacher-forced at the two shorter prefixes; at prefix 2048 (the
+    # oracle's attention over 2080 keys for 512 rows dominates the test's time)
+    # every seventh layer and the last, and the end-to-end sweeps over all
+    tf_layers = True if P <= 1024 else list(range(0, cfg["layers"], 7)) + [cfg["layers"] - 1]
+    st = check_forward(s, rbt, gc, gp, layers=tf_layers, e2e_faithful=True, label="verify forward")
     # Eq. 2 on the GPU's confidences, and vs the pure oracle's scores
     outs = (dec.scores, dec.winner, dec.next_tokens, dec.next_conf, dec.next_pred,
             dec.next_unfilled)

@@ -64,7 +64,10 @@ def test_verify_forward_parity(cfgname, P, L, k):
 # long prefixes (many key tiles per wavefront, ragged last tile) with 4 to 16
 # branches, and short ones down to a single prefix key
 LONG = [("tiny", 512, 16, 3), ("small", 600, 32, 15), ("small128", 300, 32, 15),
-        ("tiny", 37, 16, 3), ("small128", 1, 8, 2), ("small", 100, 48, 3)]
+        ("tiny", 37, 16, 3), ("small128", 1, 8, 2), ("small", 100, 48, 3),
+        # past 24 key tiles: the grouped form (key splits, one K / V tile per
+        # KV head for all its query heads)
+        ("small", 1000, 32, 7), ("small128", 900, 16, 3), ("tiny", 1200, 16, 1)]
 
 
 @pytest.mark.parametrize("cfgname,P,L,k", LONG)
@@ -135,7 +138,8 @@ def test_batch_invariance_and_determinism(cfgname, P, L, k):
 # 3.4, the Ascend system's mask); 16-row sub-blocks make a 32-key tile partly
 # visible to a row block
 CAUSAL = [("small", 100, 64, 3, 32), ("small", 300, 64, 3, 32), ("tiny", 40, 48, 2, 16),
-          ("tiny", 272, 48, 5, 16), ("small128", 64, 64, 1, 16)]
+          ("tiny", 272, 48, 5, 16), ("small128", 64, 64, 1, 16),
+          ("small", 900, 32, 3, 16)]  # the grouped form with the mask
 
 
 @pytest.mark.parametrize("cfgname,P,L,k,cblk", CAUSAL)
