@@ -160,8 +160,8 @@ struct lopa_model {
 struct lopa_kv {
   const lopa_model* m = nullptr;
   int max_len = 0, max_branches = 0, max_block = 0, mp_max = 0;
-  int vld = 0, vlds = 0;        // V leading dimensions: max_len, max_block rounded up to 8
-  uint16_t* cache = nullptr;    // [layers][2][Hkv][d * vld]: K [pos][d], V [d][vld]
+  int vld = 0, vlds = 0;        // positions per head region: max_len, max_block rounded up to 32
+  uint16_t* cache = nullptr;    // [layers][2][Hkv][d * vld], KV tile layout (common.h)
   uint16_t* staging = nullptr;  // [max_branches][layers][2][Hkv][d * vlds]
   float* rope = nullptr;        // [max_len][d/2][2]
   float* x = nullptr;           // [mp_max][H]
@@ -494,8 +494,8 @@ int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches, i
   };
   DevBuf b;
   int rc;
-  kv->vld = round_up(max_len, 8);
-  kv->vlds = round_up(max_block, 8);
+  kv->vld = round_up(max_len, 32);  // whole KV tiles (32 positions)
+  kv->vlds = round_up(max_block, 32);
   const size_t cache_e = (size_t)c.layers * 2 * Hkv * d * kv->vld;
   const size_t stag_e = (size_t)max_branches * c.layers * 2 * Hkv * d * kv->vlds;
   size_t part_b = 16;

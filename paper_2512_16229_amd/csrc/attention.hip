@@ -12,14 +12,13 @@
 // LDS); pass 2 forms them again (the same instructions, the same bits) and
 // rounds each probability to bf16 against that exact maximum before it meets
 // V, so no state is rescaled and the four partial states add up.
-// Tiles go global -> LDS by asynchronous copies, then into registers in MFMA
-// operand layout. Scores are formed transposed, S^T = K Q^T, so a lane owns one
-// query column and the probabilities land directly in the operand layout of
-// O^T = V^T P^T; V is stored transposed ([d][position]) in the cache and the
-// staging so that a copy lane's 8 keys of one dimension are 16 contiguous
-// bytes. Prefix tiles and block tiles are kept apart (a tile reads one source,
-// with positions aligned to 8) and keys past the end of either are masked:
-// their probability and their V values are zero.
+// K and V live in the KV tile layout (common.h): every 1 KiB MFMA operand
+// fragment of a 32-key tile is one contiguous run, so tiles go global -> LDS
+// (or straight into registers) by fully coalesced 16-byte lane copies, and a
+// lane's scores S^T = K Q^T come out as keys 8 g .. 8 g + 7 of the tile for
+// query c16, the order in which the probabilities meet V in O^T = V^T P^T.
+// Keys past the end of a source (the last prefix tile, a block shorter than
+// 32) are masked: their scores are -inf and their V values zero.
 #include "common.h"
 #include "kernels.h"
 
@@ -34,8 +33,8 @@ constexpr int KT = 32;  // keys per tile
 
 template <int D>
 struct AttnTile {
-  u32x4 k[2][D / 32];  // K fragments: key block kb, dims 32 kk + 8 g .. +8
-  uint2 v[D / 16][2];  // V^T: dims 16 db + c16, keys {4g .. 4g+3} and {16 + 4g ..}
+  u32x4 k[2][D / 32];  // K fragments (kb, kk) in the KV tile layout
+  u32x4 v[D / 16];     // V^T: dims 16 db + c16, keys 8 g .. 8 g + 7
 };
 
 // Asynchronous copy of 16 bytes per lane, from base + voff(lane) (base
@@ -95,82 +94,29 @@ struct TileLds {
   static constexpr int OPS = 2 * NKK + NDB;         // 1 KiB copies per tile
 };
 
-// Copy q (0 <= q < OPS) of the tile whose first position is p0 in a source of
-// lim positions (K rows [pos][D] at kbase, V^T rows [D][vld] at vbase) into the
-// LDS slot at sb. A K copy lane takes key row 16 kb + c16, dims 32 kk + 8 g .. +8;
-// a V copy lane dimension 16 db + c16, keys 8 g .. 8 g + 7. In a tile that runs
-// past the end of its source, K rows past the end read the last row and V runs
-// that start past the end read the first run (tile_update masks both): every
-// copy stays inside the source, whose row lengths are multiples of 8.
+// Copy q (0 <= q < OPS) of the tile whose K and V (KV tile layout) start at
+// kt and vt into the LDS slot at sb: K fragment q, or V fragment q - 2 D/32;
+// each a contiguous 1 KiB, lane l taking bytes [16 l, 16 l + 16).
 template <int D>
-__device__ __forceinline__ void tile_copy(int q, const uint16_t* kbase, const uint16_t* vbase,
-                                          int64_t vld, int p0, int lim, uint32_t sb, int c16,
-                                          int g) {
+__device__ __forceinline__ void tile_copy(int q, const uint16_t* kt, const uint16_t* vt,
+                                          uint32_t sb, int lane) {
   using T = TileLds<D>;
-  const uint16_t* kb_ = kbase + (int64_t)p0 * D;
-  const uint16_t* vb_ = vbase + p0;
-  if (q < 2 * T::NKK) {
-    const int kb = q / T::NKK, kk = q % T::NKK;
-    int r = kb * 16 + c16;
-    r = r < lim - p0 ? r : lim - 1 - p0;
-    attn_dma16(kb_ + kk * 32, (uint32_t)((r * D + g * 8) * 2), sb + q * 1024);
-  } else {
-    const int db = q - 2 * T::NKK;
-    const uint32_t voff = (uint32_t)((c16 * vld + (8 * g < lim - p0 ? 8 * g : 0)) * 2);
-    attn_dma16(vb_ + (int64_t)db * 16 * vld, voff, sb + q * 1024);
-  }
-}
-
-// Lane byte offsets of the copies of a tile that lies wholly inside its source
-// (no clamping): k0 / k1 for the K copies of key block 0 / 1, v for the V
-// copies of a source whose V^T rows are vld positions long. (Scalars, not an
-// array: the copy index may be known only at run time, and a dynamically
-// indexed array would live in scratch memory.)
-struct CopyOffsets {
-  uint32_t k0, k1, v;
-};
-template <int D>
-__device__ __forceinline__ CopyOffsets copy_offsets(int64_t vld, int c16, int g) {
-  CopyOffsets c;
-  c.k0 = (uint32_t)((c16 * D + g * 8) * 2);
-  c.k1 = (uint32_t)(((16 + c16) * D + g * 8) * 2);
-  c.v = (uint32_t)((c16 * vld + 8 * g) * 2);
-  return c;
-}
-// tile_copy of a tile with p0 + 32 <= lim: the same copies, addresses from the
-// wave-uniform base and the precomputed lane offsets
-template <int D>
-__device__ __forceinline__ void tile_copy_full(int q, const uint16_t* kbase, const uint16_t* vbase,
-                                               int64_t vld, int p0, uint32_t sb,
-                                               const CopyOffsets& co) {
-  using T = TileLds<D>;
-  if (q < 2 * T::NKK) {
-    const int kb = q / T::NKK, kk = q % T::NKK;
-    attn_dma16(kbase + (int64_t)p0 * D + kk * 32, kb ? co.k1 : co.k0, sb + q * 1024);
-  } else {
-    const int db = q - 2 * T::NKK;
-    attn_dma16(vbase + (int64_t)db * 16 * vld + p0, co.v, sb + q * 1024);
-  }
+  const uint16_t* src = q < 2 * T::NKK ? kt + q * 512 : vt + (q - 2 * T::NKK) * 512;
+  attn_dma16(src, (uint32_t)lane * 16u, sb + q * 1024);
 }
 
 // LDS slot -> registers (operand layouts)
 template <int D>
 __device__ __forceinline__ void tile_fetch(const char* sb, int lane, AttnTile<D>& x) {
   using T = TileLds<D>;
-  const int g = lane >> 4, c16 = lane & 15;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int kk = 0; kk < T::NKK; ++kk)
       x.k[kb][kk] = *(const u32x4*)(sb + ((kb * T::NKK + kk) * 64 + lane) * 16);
-  // keys 4g .. 4g+3 sit in copy lane c16 + 16 (g / 2) at byte 8 (g % 2);
-  // keys 16 + 4g .. in copy lane c16 + 16 (2 + g / 2)
-  const char* vb = sb + T::KBYTES + (c16 + 16 * (g >> 1)) * 16 + 8 * (g & 1);
 #pragma unroll
-  for (int db = 0; db < T::NDB; ++db) {
-    x.v[db][0] = *(const uint2*)(vb + db * 1024);
-    x.v[db][1] = *(const uint2*)(vb + db * 1024 + 32 * 16);
-  }
+  for (int db = 0; db < T::NDB; ++db)
+    x.v[db] = *(const u32x4*)(sb + T::KBYTES + (db * 64 + lane) * 16);
 }
 
 // Pass 2 of one key tile (keys p0 .. p0 + 31 of a source of lim positions) for
@@ -190,15 +136,11 @@ __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR
     // zero V of masked keys (stale cache or staging contents may be
     // non-finite, and 0 * inf would poison the sums); branch-free
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int pos = p0 + hf * 16 + g * 4;
-      const unsigned m01 = (pos < lim ? 0xFFFFu : 0u) | (pos + 1 < lim ? 0xFFFF0000u : 0u);
-      const unsigned m23 = (pos + 2 < lim ? 0xFFFFu : 0u) | (pos + 3 < lim ? 0xFFFF0000u : 0u);
+    for (int e = 0; e < 4; ++e) {
+      const int pos = p0 + 8 * g + 2 * e;
+      const unsigned mk = (pos < lim ? 0xFFFFu : 0u) | (pos + 1 < lim ? 0xFFFF0000u : 0u);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        x.v[db][hf].x &= m01;
-        x.v[db][hf].y &= m23;
-      }
+      for (int db = 0; db < NDB; ++db) x.v[db][e] &= mk;
     }
   }
 #pragma unroll
@@ -217,13 +159,13 @@ __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) s[kb] = mfma16(x.k[kb][kk], qf[qb][kk], s[kb]);
     }
-    // s[kb][j]: key p0 + 16 kb + 4 g + j, query 16 qb + c16
+    // s[kb][j]: key p0 + 8 g + 4 kb + j, query 16 qb + c16
     if (!full || p0 + KT > lq) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int pos = p0 + kb * 16 + g * 4 + j;
+          const int pos = p0 + 8 * g + 4 * kb + j;
           s[kb][j] = pos < lq ? s[kb][j] : -INFINITY;
         }
     }
@@ -237,12 +179,10 @@ __device__ __forceinline__ void tile_update(AttnTile<D>& x, const u32x4 (&qf)[NR
         l[qb] += p;
         pb[kb * 4 + j] = f2bf_bits(p);
       }
-    const u32x4 pf = *(const u32x4*)pb;  // keys {4g .. 4g+3} then {16 + 4g ..}
+    const u32x4 pf = *(const u32x4*)pb;  // keys 8 g .. 8 g + 7
 #pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      const u32x4 vf = {x.v[db][0].x, x.v[db][0].y, x.v[db][1].x, x.v[db][1].y};
-      o[db][qb] = mfma16(vf, pf, o[db][qb]);  // O^T(dim 16 db + 4g + j, query)
-    }
+    for (int db = 0; db < NDB; ++db)
+      o[db][qb] = mfma16(x.v[db], pf, o[db][qb]);  // O^T(dim 16 db + 4g + j, query)
   }
 }
 
@@ -279,7 +219,7 @@ __device__ __forceinline__ void tile_max(const char* sb, int lane, const u32x4 (
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int pos = p0 + kb * 16 + g * 4 + j;
+          const int pos = p0 + 8 * g + 4 * kb + j;
           s[kb][j] = pos < lq ? s[kb][j] : -INFINITY;
         }
     }
@@ -315,46 +255,28 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
   const int t_lo = wv * T / 4, t_hi = (wv + 1) * T / 4;
   const float sl2 = a.scale * 1.4426950408889634f;  // scale * log2(e)
 
-  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;  // [pos][D]
-  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;  // [D][vld]
+  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;  // KV tile layout
+  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;
   const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
-  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;  // [pos][D]
-  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;  // [D][vlds]
+  const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
+  const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
   const uint32_t ring = (uint32_t)(uintptr_t)smem + (uint32_t)(wv * 2) * TileLds<D>::TILE;
 
-  // tile t -> this wavefront's ring slot (all OPS copies)
-  const CopyOffsets co_c = copy_offsets<D>(a.vld, c16, g), co_s = copy_offsets<D>(a.vlds, c16, g);
+  // tile t -> this wavefront's ring slot: all OPS copies, or the K copies only
+  // (pass 1); tiles are whole in memory (positions past the source are masked)
   auto issue = [&](int t, int slot) {
     const bool pre = t < pt;
-    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
+    const int64_t off = (int64_t)(pre ? t : t - pt) * KT * D;
     const uint32_t sb = ring + (uint32_t)slot * TileLds<D>::TILE;
-    if (p0 + KT <= lim) {
 #pragma unroll
-      for (int q = 0; q < SM::OPS; ++q)
-        tile_copy_full<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, sb,
-                          pre ? co_c : co_s);
-    } else {
-#pragma unroll
-      for (int q = 0; q < SM::OPS; ++q)
-        tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, lim, sb, c16, g);
-    }
+    for (int q = 0; q < SM::OPS; ++q) tile_copy<D>(q, (pre ? kc : ks) + off, (pre ? vc : vs) + off, sb, lane);
   };
-
-  // K copies of tile t only (pass 1)
   auto issue_k = [&](int t, int slot) {
     const bool pre = t < pt;
-    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
+    const int64_t off = (int64_t)(pre ? t : t - pt) * KT * D;
     const uint32_t sb = ring + (uint32_t)slot * TileLds<D>::TILE;
-    if (p0 + KT <= lim) {
 #pragma unroll
-      for (int q = 0; q < 2 * NKK; ++q)
-        tile_copy_full<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, sb,
-                          pre ? co_c : co_s);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 2 * NKK; ++q)
-        tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, lim, sb, c16, g);
-    }
+    for (int q = 0; q < 2 * NKK; ++q) tile_copy<D>(q, (pre ? kc : ks) + off, (pre ? vc : vs) + off, sb, lane);
   };
 
   // the first two tiles are in flight while Q is loaded. The query heads of
@@ -499,11 +421,10 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // cross the memory system once and the path has two memory round trips
 // instead of one per tile.
 //
-// Key order inside a tile: A-operand row i of key block kb holds key
-// 8 (i / 4) + 4 kb + i % 4, so the scores of lane (c16, g) are keys
-// 8 g .. 8 g + 7 of the tile (kb = 0: j = 0..3, kb = 1: j = 0..3), for query
-// c16; the same lane then needs V^T at keys 8 g .. 8 g + 7: one 16-byte load
-// per 16 dimensions.
+// In the KV tile layout every K and V fragment a lane needs is its 16 bytes
+// of one contiguous 1 KiB run: the loads are fully coalesced, and the scores
+// of lane (c16, g) are keys 8 g .. 8 g + 7 of the tile, the keys of its V^T
+// fragments.
 constexpr int SL_WAVES = 8;
 
 template <int D, int QB, int NT>
@@ -529,29 +450,25 @@ __global__ __launch_bounds__(64 * SL_WAVES) void attn_sl_kernel(AttnArgs a) {
   const int t_lo = wv * T / SL_WAVES, nt = (wv + 1) * T / SL_WAVES - t_lo;  // nt <= NT
   const float sl2 = a.scale * 1.4426950408889634f;
 
-  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;  // [pos][D]
-  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;  // [D][vld]
+  const uint16_t* kc = a.kcache + (int64_t)kvh * D * a.vld;  // KV tile layout
+  const uint16_t* vc = a.vcache + (int64_t)kvh * D * a.vld;
   const int64_t st_base = (((int64_t)br * a.layers + a.layer) * 2) * a.Hkv;
   const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
   const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
 
-  // K of the wavefront's tiles; rows past the end of a source read its last
-  // row (masked below)
+  // K of the wavefront's tiles (whole tiles; keys past a source's end are
+  // masked below)
   u32x4 kv[NT][2][NKK];
 #pragma unroll
   for (int i = 0; i < NT; ++i) {
     if (i >= nt) break;
     const int t = t_lo + i;
     const bool pre = t < pt;
-    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
-    const uint16_t* kb_ = pre ? kc : ks;
+    const uint16_t* kt = (pre ? kc : ks) + (int64_t)(pre ? t : t - pt) * KT * D + lane * 8;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int r = min(p0 + 8 * (c16 >> 2) + 4 * kb + (c16 & 3), lim - 1);
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-        kv[i][kb][kk] = *(const u32x4*)(kb_ + (int64_t)r * D + kk * 32 + g * 8);
-    }
+      for (int kk = 0; kk < NKK; ++kk) kv[i][kb][kk] = *(const u32x4*)(kt + (kb * NKK + kk) * 512);
   }
   // Q^T operand: query column 16 qb + c16, dims 32 kk + 8 g .. +8
   u32x4 qf[QB][NKK];
@@ -596,20 +513,16 @@ __global__ __launch_bounds__(64 * SL_WAVES) void attn_sl_kernel(AttnArgs a) {
     }
   }
   // V^T of the same keys (the K registers are free now): lane (c16, g) takes
-  // dims 16 db + c16, keys 8 g .. 8 g + 7; a run that starts past the end of
-  // its source reads the source's first run instead (its probabilities are 0)
+  // dims 16 db + c16, keys 8 g .. 8 g + 7
   u32x4 vf[NT][NDB];
 #pragma unroll
   for (int i = 0; i < NT; ++i) {
     if (i >= nt) break;
     const int t = t_lo + i;
     const bool pre = t < pt;
-    const int p0 = (pre ? t : t - pt) * KT, lim = pre ? P : L;
-    const int64_t ld = pre ? a.vld : a.vlds;
-    const uint16_t* vb_ = (pre ? vc : vs) + p0 + (p0 + 8 * g < lim ? 8 * g : 0);
+    const uint16_t* vt = (pre ? vc : vs) + (int64_t)(pre ? t : t - pt) * KT * D + lane * 8;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
-      vf[i][db] = *(const u32x4*)(vb_ + (int64_t)(db * 16 + c16) * ld);
+    for (int db = 0; db < NDB; ++db) vf[i][db] = *(const u32x4*)(vt + db * 512);
   }
 
   // the exact row maximum over the eight wavefronts (the V loads stay in
@@ -741,25 +654,16 @@ template <int D, int QB, bool WITH_V>
 __device__ __forceinline__ void group_issue(const AttnArgs& a, const GroupSplit& gs, int i,
                                             int slot, uint32_t ring, const uint16_t* kc,
                                             const uint16_t* vc, const uint16_t* ks,
-                                            const uint16_t* vs, const CopyOffsets& co_c,
-                                            const CopyOffsets& co_s, int c16, int g) {
+                                            const uint16_t* vs, int lane) {
   using T = TileLds<D>;
   constexpr int OPS = WITH_V ? T::OPS : 2 * (D / 32);
   constexpr int SLOT = WITH_V ? T::TILE : T::KBYTES;
   i = i < gs.n ? i : gs.n - 1;  // past the last tile: the last one again
   const bool pre = i < gs.np;
-  const int p0 = (pre ? gs.p_lo + i : i - gs.np) * KT, lim = pre ? a.P : a.L;
+  const int64_t off = (int64_t)(pre ? gs.p_lo + i : i - gs.np) * KT * D;
   const uint32_t sb = ring + (uint32_t)slot * SLOT;
-  if (p0 + KT <= lim) {
 #pragma unroll
-    for (int q = 0; q < OPS; ++q)
-      tile_copy_full<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, sb,
-                        pre ? co_c : co_s);
-  } else {
-#pragma unroll
-    for (int q = 0; q < OPS; ++q)
-      tile_copy<D>(q, pre ? kc : ks, pre ? vc : vs, pre ? a.vld : a.vlds, p0, lim, sb, c16, g);
-  }
+  for (int q = 0; q < OPS; ++q) tile_copy<D>(q, (pre ? kc : ks) + off, (pre ? vc : vs) + off, sb, lane);
 }
 
 // Q^T operand of query head h, rows 16 qb + c16 of branch br (zero past L)
@@ -807,11 +711,10 @@ __global__ __launch_bounds__(512) void attn_gmax_kernel(AttnArgs a, int NS) {
   const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
   const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
   const uint32_t ring = (uint32_t)(uintptr_t)smem;
-  const CopyOffsets co_c = copy_offsets<D>(a.vld, c16, g), co_s = copy_offsets<D>(a.vlds, c16, g);
   if (wv == 0 && gs.n > 0)
 #pragma unroll
     for (int i = 0; i < GQ_RING - 1; ++i)
-      group_issue<D, QB, false>(a, gs, i, i, ring, kc, vc, ks, vs, co_c, co_s, c16, g);
+      group_issue<D, QB, false>(a, gs, i, i, ring, kc, vc, ks, vs, lane);
   u32x4 qf[QB][D / 32];
   group_q<D, QB>(a, br, h, c16, g, qf);
   float mraw[QB];
@@ -822,7 +725,7 @@ __global__ __launch_bounds__(512) void attn_gmax_kernel(AttnArgs a, int NS) {
     lds_barrier();  // ... for every wavefront, which all finished tile i - 1
     if (wv == 0)
       group_issue<D, QB, false>(a, gs, i + GQ_RING - 1, (i + GQ_RING - 1) % GQ_RING, ring, kc, vc,
-                                ks, vs, co_c, co_s, c16, g);
+                                ks, vs, lane);
     const bool pre = i < np;
     tile_max<D, QB>(smem + (i % GQ_RING) * T::KBYTES, lane, qf, mraw,
                     (pre ? gs.p_lo + i : i - np) * KT, pre ? a.P : a.L, g, pre ? 0 : a.cblk, 0);
@@ -855,11 +758,10 @@ __global__ __launch_bounds__(512) void attn_gpv_kernel(AttnArgs a, int NS) {
   const uint16_t* ks = a.staging + (st_base + 0 * a.Hkv + kvh) * D * a.vlds;
   const uint16_t* vs = a.staging + (st_base + 1 * a.Hkv + kvh) * D * a.vlds;
   const uint32_t ring = (uint32_t)(uintptr_t)smem;
-  const CopyOffsets co_c = copy_offsets<D>(a.vld, c16, g), co_s = copy_offsets<D>(a.vlds, c16, g);
   if (wv == 0 && gs.n > 0)
 #pragma unroll
     for (int i = 0; i < GQ_RING - 1; ++i)
-      group_issue<D, QB, true>(a, gs, i, i, ring, kc, vc, ks, vs, co_c, co_s, c16, g);
+      group_issue<D, QB, true>(a, gs, i, i, ring, kc, vc, ks, vs, lane);
   u32x4 qf[QB][D / 32];
   group_q<D, QB>(a, br, h, c16, g, qf);
   const GroupScratch sc = group_scratch(a, NS);
@@ -884,7 +786,7 @@ __global__ __launch_bounds__(512) void attn_gpv_kernel(AttnArgs a, int NS) {
     lds_barrier();
     if (wv == 0)
       group_issue<D, QB, true>(a, gs, i + GQ_RING - 1, (i + GQ_RING - 1) % GQ_RING, ring, kc, vc,
-                               ks, vs, co_c, co_s, c16, g);
+                               ks, vs, lane);
     AttnTile<D> x;
     tile_fetch<D>(smem + (i % GQ_RING) * T::TILE, lane, x);
     const bool pre = i < np;
@@ -991,7 +893,7 @@ size_t attention_scratch_bytes(int nb, int L, int Hq, int Hkv, int d) {
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
-  if (a.L < 1 || a.L > 256 || a.P < 0 || a.Hq % a.Hkv || a.vld % 8 || a.vlds % 8 ||
+  if (a.L < 1 || a.L > 256 || a.P < 0 || a.Hq % a.Hkv || a.vld % KT || a.vlds % KT ||
       a.L > a.vlds || a.P > a.vld)
     return hipErrorInvalidValue;
   if (a.cblk < 0 || (a.cblk > 0 && (a.cblk % 16 || a.L % a.cblk))) return hipErrorInvalidValue;

@@ -42,6 +42,27 @@ __device__ __forceinline__ f32x4 mfma16(const uint4& a, const uint4& b, f32x4 c)
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// KV tile layout (cache and staging). A head's K region and its V region each
+// hold tiles of KV_TILE = 32 positions, d x 32 elements per tile, stored in
+// the order the attention's MFMAs take them, so that every 1 KiB operand
+// fragment is one contiguous run:
+//   K: fragment (kb, kk) of a tile (kb < 2, kk < d / 32) at elements
+//      ((kb d/32 + kk) 64 + lane) 8; lane = c16 + 16 g holds position
+//      8 (c16 / 4) + 4 kb + c16 % 4 of the tile, dimensions 32 kk + 8 g .. + 7
+//      (an S^T = K Q^T tile then gives lane (c16, g) positions 8 g .. 8 g + 7);
+//   V: fragment db (< d / 16) at elements (db 64 + lane) 8; lane = c16 + 16 g
+//      holds dimension 16 db + c16, positions 8 g .. 8 g + 7.
+constexpr int KV_TILE = 32;
+__host__ __device__ __forceinline__ int64_t kv_k_off(int p, int e, int d) {
+  const int p32 = p & 31, kb = (p32 >> 2) & 1, c16 = 4 * (p32 >> 3) + (p32 & 3);
+  return (int64_t)(p >> 5) * 32 * d +
+         ((((kb * (d >> 5) + (e >> 5)) * 64 + c16 + 16 * ((e >> 3) & 3)) << 3) | (e & 7));
+}
+__host__ __device__ __forceinline__ int64_t kv_v_off(int p, int e, int d) {
+  const int p32 = p & 31;
+  return (int64_t)(p >> 5) * 32 * d + ((((e >> 4) * 64 + (e & 15) + 16 * (p32 >> 3)) << 3) | (p32 & 7));
+}
+
 // element offset of (row r, column c) in an activation matrix packed with Mp rows
 __device__ __forceinline__ int64_t packA_off(int r, int c, int Mp) {
   int rb = r >> 4, kb = c >> 5;

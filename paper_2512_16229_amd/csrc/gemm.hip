@@ -633,14 +633,14 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
         qo[dim] = f2bf_bits(o1);
         qo[dim + HD] = f2bf_bits(o2);
       } else {
-        // staging head (K or V) of this branch and layer: K [Lcap][D], V [D][vlds]
+        // staging head (K or V) of this branch and layer, in the KV tile layout
         uint16_t* st = a.staging + ((((int64_t)br * a.layers + a.layer) * 2 + (sect - 1)) *
                                         a.Hkv + head) * D * a.vlds;
         if (sect == 1) {
-          st[(int64_t)i * D + dim] = f2bf_bits(o1);
-          st[(int64_t)i * D + dim + HD] = f2bf_bits(o2);
+          st[kv_k_off(i, dim, D)] = f2bf_bits(o1);
+          st[kv_k_off(i, dim + HD, D)] = f2bf_bits(o2);
         } else {
-          st[(int64_t)dim * a.vlds + i] = f2bf_bits(o1);
+          st[kv_v_off(i, dim, D)] = f2bf_bits(o1);
         }
       }
     }

@@ -19,14 +19,16 @@ hipError_t launch_select(const int32_t* bt, const float* conf, const int32_t* pr
                          int window, float eta, float* scores, int32_t* winner, int32_t* nt,
                          float* nc, int32_t* np, int32_t* nu, hipStream_t s);
 // KV layouts. Cache: [layers][2][Hkv][d * vld] (vld = max_len rounded up to
-// 8): K position p, dim e at p * d + e; V (transposed) at e * vld + p.
-// Staging: [branches][layers][2][Hkv][d * vlds], the same with Lcap, vlds.
+// 32); each head's K and V region in the KV tile layout of common.h
+// (kv_k_off / kv_v_off). Staging: [branches][layers][2][Hkv][d * vlds], the
+// same with Lcap rounded up to 32.
 hipError_t launch_commit(const uint16_t* staging, uint16_t* cache, const int32_t* winner,
                          int nb_last, int layers, int Hkv, int vlds, int vld, int d, int P,
                          int L, int32_t* append_offset, hipStream_t s);
 // Copy positions of one layer between the cache (or staging) and a caller
 // buffer [Hkv][len][d] for K and V. to_cache: caller -> cache. head_stride:
-// elements between heads of the cache side; ld: its V leading dimension.
+// elements between heads of the cache side; ld: positions a head region holds
+// (a multiple of 32; start + len <= ld).
 hipError_t launch_kv_rows(uint16_t* cache_k, uint16_t* cache_v, int64_t head_stride, int ld,
                           int Hkv, int d, int start, int len, uint16_t* buf_k, uint16_t* buf_v,
                           int to_cache, hipStream_t s);
@@ -112,7 +114,7 @@ struct GemmArgs {
   const float* bias;   // [N] or null
   const float* rope;   // [max_pos][d/2][2] (cos, sin)
   uint16_t* q_out;     // [nb][Hq][L][d]
-  uint16_t* staging;   // [nb][layers][2][Hkv][d * vlds] (see the KV layouts)
+  uint16_t* staging;   // [nb][layers][2][Hkv][d * vlds] (the KV tile layout)
   int layer, layers, Hq, Hkv, d, L, P;
   int vlds;            // staging V leading dimension
   // EPI_RESID
@@ -146,8 +148,8 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s);
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
   const uint16_t* q;       // [nb][Hq][L][d] bf16 (post-RoPE)
-  const uint16_t* kcache;  // layer's K cache, heads d * vld apart, [pos][d]
-  const uint16_t* vcache;  // layer's V cache, heads d * vld apart, [d][vld]
+  const uint16_t* kcache;  // layer's K cache, heads d * vld apart (KV tile layout)
+  const uint16_t* vcache;  // layer's V cache, heads d * vld apart (KV tile layout)
   const uint16_t* staging; // [nb][layers][2][Hkv][d * vlds]
   uint16_t* out;           // packed activations (Mp rows, Hq*d columns)
   int nb, L, P, Hq, Hkv, d, vld, layer, layers, vlds, Mp;

@@ -203,8 +203,10 @@ __global__ __launch_bounds__(256) void select_kernel(
 }
 
 // Copy n rows of the winner's staged K/V of one (layer, K/V, head) lhg into
-// cache positions [P, P + n) (the KV layouts of kernels.h: V transposed,
-// leading dimensions vlds / vld).
+// cache positions [P, P + n) (both in the KV tile layout of common.h; head
+// regions d x vlds and d x vld elements). Whole tiles on both sides (P and n
+// multiples of 32, the usual block commit) are one contiguous run; otherwise
+// element by element.
 __device__ __forceinline__ void commit_rows(const uint16_t* __restrict__ staging,
                                             uint16_t* __restrict__ cache, int w, int lhg,
                                             int layers, int Hkv, int vlds, int vld, int d, int P,
@@ -212,24 +214,16 @@ __device__ __forceinline__ void commit_rows(const uint16_t* __restrict__ staging
   const bool is_v = (lhg / Hkv) & 1;
   const uint16_t* src = staging + ((int64_t)w * layers * 2 * Hkv + lhg) * d * vlds;
   uint16_t* dst = cache + (int64_t)lhg * d * vld;
-  if (!is_v) {
+  if (((P | n) & (KV_TILE - 1)) == 0) {
     const uint4* s4 = (const uint4*)src;
     uint4* d4 = (uint4*)(dst + (int64_t)P * d);
     for (int e = threadIdx.x; e < n * d / 8; e += blockDim.x) d4[e] = s4[e];
-  } else if (n <= 256) {
-    // V^T rows: dimension dim holds its positions contiguously. With lp the
-    // power of two >= n, thread t copies position t % lp of dimensions
-    // t / lp, t / lp + 256 / lp, ... (shifts and masks, no division)
-    const int lg = 32 - __builtin_clz(n - 1 > 0 ? n - 1 : 1) - (n == 1 ? 1 : 0);
-    const int i = threadIdx.x & ((1 << lg) - 1);
-    if (i < n)
-      for (int dim = threadIdx.x >> lg; dim < d; dim += 256 >> lg)
-        dst[(int64_t)dim * vld + P + i] = src[(int64_t)dim * vlds + i];
-  } else {
-    for (int e = threadIdx.x; e < n * d; e += blockDim.x) {
-      const int dim = e / n, i = e % n;
-      dst[(int64_t)dim * vld + P + i] = src[(int64_t)dim * vlds + i];
-    }
+    return;
+  }
+  for (int e = threadIdx.x; e < n * d; e += blockDim.x) {
+    const int i = e / d, dim = e % d;
+    if (is_v) dst[kv_v_off(P + i, dim, d)] = src[kv_v_off(i, dim, d)];
+    else dst[kv_k_off(P + i, dim, d)] = src[kv_k_off(i, dim, d)];
   }
 }
 
@@ -387,11 +381,11 @@ __global__ __launch_bounds__(256) void window_commit_kernel(
 }
 
 // Positions [start, start + len) of one layer's K and V between the cache
-// side (heads head_stride apart; K [pos][d], V [d][ld]) and a caller buffer
+// side (heads head_stride apart, KV tile layout) and a caller buffer
 // [Hkv][len][d]. One workgroup per (head, K/V).
 __global__ __launch_bounds__(256) void kv_rows_kernel(uint16_t* __restrict__ ck,
                                                       uint16_t* __restrict__ cv,
-                                                      int64_t head_stride, int ld, int d,
+                                                      int64_t head_stride, int d,
                                                       int start, int len,
                                                       uint16_t* __restrict__ bk,
                                                       uint16_t* __restrict__ bv, int to_cache) {
@@ -400,7 +394,7 @@ __global__ __launch_bounds__(256) void kv_rows_kernel(uint16_t* __restrict__ ck,
   uint16_t* b = (is_v ? bv : bk) + (int64_t)head * len * d;
   for (int e = threadIdx.x; e < len * d; e += blockDim.x) {
     const int i = e / d, dim = e % d;  // buffer element (i, dim)
-    const int64_t co = is_v ? (int64_t)dim * ld + start + i : (int64_t)(start + i) * d + dim;
+    const int64_t co = is_v ? kv_v_off(start + i, dim, d) : kv_k_off(start + i, dim, d);
     if (to_cache) c[co] = b[e];
     else b[e] = c[co];
   }
@@ -461,7 +455,8 @@ hipError_t launch_window_commit(const uint16_t* staging, uint16_t* cache, const 
 hipError_t launch_kv_rows(uint16_t* cache_k, uint16_t* cache_v, int64_t head_stride, int ld,
                           int Hkv, int d, int start, int len, uint16_t* buf_k, uint16_t* buf_v,
                           int to_cache, hipStream_t s) {
+  if (ld % KV_TILE || start < 0 || start + len > ld) return hipErrorInvalidValue;
   hipLaunchKernelGGL(kv_rows_kernel, dim3(2 * Hkv), dim3(256), 0, s, cache_k, cache_v,
-                     head_stride, ld, d, start, len, buf_k, buf_v, to_cache);
+                     head_stride, d, start, len, buf_k, buf_v, to_cache);
   return hipGetLastError();
 }
