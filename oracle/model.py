@@ -36,9 +36,10 @@ Precision modes:
     oracle/fp8.py): gate / up / down weights quantised per output channel, the
     normed input of gate/up quantised per row from its unrounded value, the
     SwiGLU output (stored bf16) quantised per row before the down projection.
-  * "fp8": "fp8_mlp", and the QKV projection and the LM head in FP8 as well
-    (their weights per output channel, their normed inputs per row from the
-    unrounded values); the output projection stays bf16.
+  * "fp8": "fp8_mlp", and every other projection in FP8 as well: QKV and the
+    LM head (their weights per output channel, their normed inputs per row
+    from the unrounded values) and the output projection (its weights per
+    output channel, the attention output, stored bf16, per row over all heads).
 """
 from __future__ import annotations
 
@@ -164,7 +165,7 @@ class OracleModel:
         lw = self._raw_layers[li]
         w = {k: (self._r(_np(v)) if k not in ("ln1", "ln2") else _np(v)) for k, v in lw.items()}
         quantized = (("w_gate", "w_up", "w_down") if self.fp8_mlp else ()) + \
-            (("wq", "wk", "wv") if self.fp8_qkv_lm else ())
+            (("wq", "wk", "wv", "wo") if self.fp8_qkv_lm else ())
         for key in quantized:
             w[key + "_q"], w[key + "_s"] = quantize_rows(w[key])
         if self._keep is True or (self._keep and not isinstance(self._keep, bool)):
@@ -272,7 +273,11 @@ class OracleModel:
                                trace=(lambda p_, li=li: tr("p", li, p_)))
             o = self._store(o.transpose(0, 2, 1, 3).reshape(nb, L, Hq * d))
             tr("o", li, o)
-            x = x + o @ w["wo"].T
+            if self.fp8_qkv_lm:
+                x = x + fp8_matmul(o, w["wo_q"], w["wo_s"])
+            else:
+                x = x + o @ w["wo"].T
+            tr("x1", li, x)
             if self.fp8_mlp:
                 h2 = rms_norm(x, w["ln2"], cfg["rms_eps"])
                 a = self._store(silu(fp8_matmul(h2, w["w_gate_q"], w["w_gate_s"]))

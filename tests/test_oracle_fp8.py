@@ -127,20 +127,19 @@ def test_fp8_mode_decodes(k):
     assert len(res["tokens"]) == 32 and not np.any(res["tokens"] == cfg["mask_id"])
 
 
-def test_fp8_full_mode_quantizes_qkv_and_lm_head():
-    """The "fp8" mode adds the QKV projection and the LM head: their weights
-    dequantise to the bf16 weights within the E4M3 step, the LM head's logits
-    are the quantised product of the final-normed rows, and the output
-    projection keeps its bf16 weights."""
+def test_fp8_full_mode_quantizes_every_projection():
+    """The "fp8" mode adds the QKV projection, the output projection and the
+    LM head: their weights dequantise to the bf16 weights within the E4M3
+    step, and the LM head's logits are the quantised product of the
+    final-normed rows."""
     cfg = synth.config("tiny")
     w = synth.model_weights(cfg)
     f = OracleModel(cfg, w, "faithful")
     q = OracleModel(cfg, w, "fp8")
-    for key in ("wq", "wk", "wv"):
+    for key in ("wq", "wk", "wv", "wo"):
         l0, f0 = q.layers[0], f.layers[0]
         err = np.abs(l0[key + "_q"] * l0[key + "_s"][:, None] - f0[key])
         assert np.all(err <= 2.0 ** -4 * np.abs(f0[key]) + 2.0 ** -10 * l0[key + "_s"][:, None] * 1.0001)
-    assert "wo_q" not in q.layers[0]
     err = np.abs(q.lm_head_q * q.lm_head_s[:, None] - f.lm_head)
     assert np.all(err <= 2.0 ** -4 * np.abs(f.lm_head) + 2.0 ** -10 * q.lm_head_s[:, None] * 1.0001)
     cache = KVCache(cfg, 48)
@@ -150,3 +149,32 @@ def test_fp8_full_mode_quantizes_qkv_and_lm_head():
                                rtol=0, atol=1e-12)
     res = lopa.decode(q, synth.prompt(cfg, 32).numpy(), 32, 16, 3, 0.9)
     assert len(res["tokens"]) == 32 and not np.any(res["tokens"] == cfg["mask_id"])
+
+
+def test_fp8_output_projection_within_quantization_bound():
+    """In the "fp8" mode the output projection's contribution to the residual
+    stream (the value after the attention block minus the layer's input) stays
+    within the error the two E4M3 roundings allow of the exact product of the
+    stored attention output and the bf16 weights: each factor within relative
+    2^-4 plus its subnormal step, the activation scaled per row over all heads."""
+    cfg = synth.config("tiny")
+    w = synth.model_weights(cfg)
+    q = OracleModel(cfg, w, "fp8")
+    f = OracleModel(cfg, w, "faithful")
+    cache = KVCache(cfg, 48)
+    bt = np.random.default_rng(3).integers(0, cfg["vocab"] - 1, (2, 16))
+    trace = []
+    q.forward_block(bt, 0, cache, trace=trace)
+    val = {(n, li): v for n, li, v in trace}
+    o = val[("o", 0)].reshape(-1, val[("o", 0)].shape[-1])
+    x_in = q.embed[bt].reshape(-1, cfg["hidden"])
+    got = val[("x1", 0)].reshape(-1, cfg["hidden"]) - x_in
+    wo = f.layers[0]["wo"]
+    exact = o @ wo.T
+    s_row = np.max(np.abs(o), axis=1) / E4M3_MAX
+    e_o = 2.0 ** -4 * np.abs(o) + 2.0 ** -10 * s_row[:, None] * 1.0001
+    s_w = np.max(np.abs(wo), axis=1) / E4M3_MAX
+    e_w = 2.0 ** -4 * np.abs(wo) + 2.0 ** -10 * s_w[:, None] * 1.0001
+    bound = e_o @ np.abs(wo).T + np.abs(o) @ e_w.T + e_o @ e_w.T
+    assert np.all(np.abs(got - exact) <= bound * (1 + 1e-9) + 1e-9)
+    assert np.max(np.abs(got - exact)) > 0
