@@ -502,14 +502,14 @@ def e2e_window_decode(lp, synth, model, cfg, prompt_len=256, gen=256, L=32, k=7,
 def fp8_step_figures(lp, synth, cfg, w, P, L, k, tau, steps, warmup, precision):
     """The same verify step (the block's first iteration, replayed) with the
     projections of `precision` in W8A8 E4M3 ("fp8_mlp": gate / up / down; "fp8":
-    also QKV and the LM head): a second model from the same weights; ms/step,
+    also QKV, O and the LM head): a second model from the same weights; ms/step,
     branch-tokens/s and per-kind times."""
     import torch
     model = lp.Model(cfg, w, precision=precision)
     what = ("gate / up / down" if precision == "fp8_mlp"
-            else "QKV, gate / up / down and the LM head")
+            else "QKV, O, gate / up / down and the LM head")
     rest = ("attention, QKV / O and the LM head bf16" if precision == "fp8_mlp"
-            else "attention and the output projection bf16")
+            else "attention bf16")
     out = shape_figure(lp, synth, model, cfg, P, L, k, tau, steps, warmup,
                        f"the headline step with {what} in W8A8 E4M3 (per-channel weight "
                        f"and per-row activation scales); {rest}", precision)

@@ -123,11 +123,12 @@ int lopa_model_create(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w,
  * requantisation of the bf16 SwiGLU output for down); the products are summed
  * in fp32 and the scales applied after the sum. Attention, QKV / O and the LM
  * head stay bf16. The caller's weights are still bf16.
- * LOPA_PRECISION_FP8: as FP8_MLP, and the QKV projection and the LM head in
- * W8A8 FP8 with the same rules (their activation rows are RMSNorm outputs, so
- * the norm writes the E4M3 rows and scales). The output projection stays bf16:
- * its input rows are written by the attention kernels in per-head pieces, so a
- * per-row scale would need one more pass over them; attention stays bf16. */
+ * LOPA_PRECISION_FP8: as FP8_MLP, and every other projection in W8A8 FP8 with
+ * the same rules: QKV and the LM head (their activation rows are RMSNorm
+ * outputs, so the norm writes the E4M3 rows and scales) and the output
+ * projection (its activation rows are the bf16 attention output, quantised
+ * with one scale per row over all heads by one more pass over them); the
+ * attention itself stays bf16. */
 enum { LOPA_PRECISION_BF16 = 0, LOPA_PRECISION_FP8_MLP = 1, LOPA_PRECISION_FP8 = 2 };
 int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* weights,
                          int32_t precision, void* stream, lopa_model** out);

@@ -66,9 +66,12 @@ struct LayerPack {
   uint8_t* down8 = nullptr;
   float* sw_gu = nullptr;
   float* sw_down = nullptr;
-  // FP8 models: E4M3 QKV weights (K = round512(H)) and their column scales
+  // FP8 models: E4M3 QKV and output-projection weights (K = round512(H)) and
+  // their column scales
   uint8_t* qkv8 = nullptr;
   float* sw_qkv = nullptr;
+  uint8_t* o8 = nullptr;
+  float* sw_o = nullptr;
   float* bias;     // [Nqkv] or null
   float* ln1;
   float* ln2;
@@ -145,6 +148,7 @@ struct lopa_model {
   int fp8 = 0;       // FP8 MLP (LOPA_PRECISION_FP8_MLP and LOPA_PRECISION_FP8)
   int fp8_qkv_lm = 0;  // FP8 QKV projection and LM head too (LOPA_PRECISION_FP8)
   int nb_down8 = 0;                                     // FP8 down-projection tile width
+  int nb_o8 = 0;                                        // FP8 output-projection tile width
   std::vector<LayerPack> layers;
   uint16_t* embed = nullptr;
   uint16_t* lm = nullptr;   // bf16 LM head (when not FP8)
@@ -237,7 +241,9 @@ StepPlans step_plans(const lopa_model* m, int MT) {
   StepPlans p;
   const int kch = m->fp8_qkv_lm ? round512(c.hidden) / 128 : c.hidden / 64;
   p.qkv = plan_gemm(EPI_QKV, m->blk_qkv, kch, MT, m->num_cu, m->nb_qkv);
-  p.o = plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu, m->nb_o);
+  p.o = m->fp8_qkv_lm
+            ? plan_gemm(EPI_RESID, m->blk_h, round512(c.heads * c.head_dim) / 128, MT, m->num_cu, m->nb_o8)
+            : plan_gemm(EPI_RESID, m->blk_h, c.heads * c.head_dim / 64, MT, m->num_cu, m->nb_o);
   p.gu = plan_gemm(EPI_SWIGLU, m->blk_gu, c.hidden / 64, MT, m->num_cu, 10);
   p.down = m->fp8 ? plan_gemm(EPI_RESID, m->blk_h, round512(c.ffn) / 128, MT, m->num_cu, m->nb_down8)
                   : plan_gemm(EPI_RESID, m->blk_h, round256(c.ffn) / 64, MT, m->num_cu, m->nb_down);
@@ -349,6 +355,7 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
   m->fp8 = precision == LOPA_PRECISION_FP8_MLP || precision == LOPA_PRECISION_FP8;
   m->fp8_qkv_lm = precision == LOPA_PRECISION_FP8;
   m->nb_down8 = plan_gemm(EPI_RESID, m->blk_h, round512(F) / 128, 1, m->num_cu, 0).nb;
+  m->nb_o8 = plan_gemm(EPI_RESID, m->blk_h, round512(c.heads * d) / 128, 1, m->num_cu, 0).nb;
   auto alloc16 = [&](uint16_t** p, size_t elems) -> int {
     DevBuf b;
     int r = dalloc(b, elems * 2, m->owned);
@@ -390,7 +397,9 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
     if ((!m->fp8_qkv_lm && (rc = alloc16(&p.qkv, wsize(m->blk_qkv, H)))) ||
         (m->fp8_qkv_lm && (rc = alloc8(&p.qkv8, wsize(m->blk_qkv, KPH8)))) ||
         (m->fp8_qkv_lm && (rc = allocf(&p.sw_qkv, (size_t)m->blk_qkv * 16))) ||
-        (rc = alloc16(&p.o, wsize(m->blk_h, c.heads * d))) ||
+        (!m->fp8_qkv_lm && (rc = alloc16(&p.o, wsize(m->blk_h, c.heads * d)))) ||
+        (m->fp8_qkv_lm && (rc = alloc8(&p.o8, wsize(m->blk_h, round512(c.heads * d))))) ||
+        (m->fp8_qkv_lm && (rc = allocf(&p.sw_o, (size_t)m->blk_h * 16))) ||
         (!m->fp8 && (rc = alloc16(&p.gu, wsize(m->blk_gu, H)))) ||
         (!m->fp8 && (rc = alloc16(&p.down, wsize(m->blk_h, FP)))) ||
         (m->fp8 && (rc = alloc8(&p.gu8, wsize(m->blk_gu, KPH8)))) ||
@@ -415,8 +424,15 @@ int lopa_model_create_ex(const lopa_model_cfg* cfg, const lopa_weight_ptrs* w, i
           (e = launch_repack8(wq, inv_q, sc_q, nq, wk, inv_q + nq, sc_q + nq, nk, wv,
                               inv_q + nq + nk, sc_q + nq + nk, nk, H, KPH8, m->blk_qkv,
                               m->nb_qkv, 0, p.qkv8, p.sw_qkv, s)) != hipSuccess)) ||
-        (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
-                           c.heads * d, m->blk_h, m->nb_o, 0, p.o, s)) != hipSuccess ||
+        (!m->fp8_qkv_lm &&
+         (e = launch_repack((const uint16_t*)lw.wo, H, nullptr, 0, nullptr, 0, c.heads * d,
+                            c.heads * d, m->blk_h, m->nb_o, 0, p.o, s)) != hipSuccess) ||
+        (m->fp8_qkv_lm &&  // the row-scale buffers are free again: the QKV repack ran before
+         ((e = launch_rowscale((const uint16_t*)lw.wo, H, c.heads * d, inv_q, sc_q, s)) !=
+              hipSuccess ||
+          (e = launch_repack8((const uint16_t*)lw.wo, inv_q, sc_q, H, nullptr, nullptr, nullptr, 0,
+                              nullptr, nullptr, nullptr, 0, c.heads * d, round512(c.heads * d),
+                              m->blk_h, m->nb_o8, 0, p.o8, p.sw_o, s)) != hipSuccess)) ||
         (!m->fp8 &&
          (e = launch_repack((const uint16_t*)lw.w_gate, F, (const uint16_t*)lw.w_up, F, nullptr,
                             0, H, H, m->blk_gu, 10, 1, p.gu, s)) != hipSuccess) ||
@@ -642,7 +658,7 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   { ProfScope ps_(kv, LOPA_PROF_NORM, s);
     if (f8x)
       HIP_TRY(launch_embed_norm8(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M,
-                                 Mp, H, ws.x, ws.a8_gu, ws.sa_gu, s));
+                                 Mp, H, ws.x, ws.a8_gu, ws.sa_gu, ws.rowmax_dn, s));
     else
       HIP_TRY(launch_embed_norm(branch_tokens, m->embed, c.vocab, m->layers[0].ln1, c.rms_eps, M,
                                 Mp, H, ws.x, ws.abuf, s)); }
@@ -665,6 +681,10 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
   at.cblk = kv->causal_blk && L > kv->causal_blk ? kv->causal_blk : 0;
   at.scratch = ws.partials;
   at.scratch_bytes = ws.partials_bytes;
+  // FP8 output projection: the attention output's row maxima, in the buffer
+  // the norm ahead of each layer's QKV projection zeroes (the gate/up GEMM's
+  // row maxima use it again after the second norm zeroes it)
+  at.rowmax = f8x ? ws.rowmax_dn : nullptr;
   const int n_layers = stop_layer >= 0 ? std::min(stop_layer, c.layers) : c.layers;
   for (int l = 0; l < n_layers; ++l) {
     const LayerPack& p = m->layers[l];
@@ -692,8 +712,21 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     { ProfScope ps_(kv, LOPA_PROF_ATTN, s);
       HIP_TRY(launch_attention(at, s)); }
     g.x = ws.x;
-    { ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
-      HIP_TRY(gemm(EPI_RESID, ws.abuf, p.o, H, c.heads * d, plan.o)); }
+    if (f8x) {
+      // FP8 output projection: the attention output (bf16) to E4M3 with a
+      // scale per row over all heads (the row maxima the attention kernels
+      // merged), in the operand buffer of the QKV projection, which has read
+      // it by now
+      { ProfScope ps_(kv, LOPA_PROF_NORM, s);
+        HIP_TRY(launch_quant_rows8(ws.abuf, c.heads * d, M, Mp, ws.rowmax_dn, ws.a8_gu, ws.sa_gu,
+                                   s)); }
+      { ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
+        HIP_TRY(gemm8(EPI_RESID, ws.a8_gu, p.o8, H, round512(c.heads * d), ws.sa_gu, p.sw_o,
+                      plan.o)); }
+    } else {
+      ProfScope ps_(kv, LOPA_PROF_OPROJ, s);
+      HIP_TRY(gemm(EPI_RESID, ws.abuf, p.o, H, c.heads * d, plan.o));
+    }
     g.a_out = ws.fbuf;
     if (m->fp8) {
       // FP8 MLP: the normed rows straight to E4M3 with their scales, gate/up,
@@ -722,9 +755,9 @@ static int verify_impl(const lopa_model* m, lopa_kv* kv, int32_t prefix_len,
     const float* next_w = (l + 1 < c.layers) ? m->layers[l + 1].ln1 : m->final_norm;
     const int dsplits = plan.down.splits > 1 ? plan.down.splits : 0;
     { ProfScope ps_(kv, LOPA_PROF_NORM, s);
-      if (f8x)
+      if (f8x)  // also zeroes the row maxima for the next layer's attention output
         HIP_TRY(launch_resnorm8(ws.partials, dsplits, next_w, c.rms_eps, M, Mp, H, ws.x,
-                                ws.a8_gu, ws.sa_gu, nullptr, s));
+                                ws.a8_gu, ws.sa_gu, ws.rowmax_dn, s));
       else
         HIP_TRY(launch_resnorm(ws.partials, dsplits, next_w, c.rms_eps, M, Mp, H, ws.x,
                                ws.abuf, s)); }

@@ -397,16 +397,25 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     const int row = row0 + qb * 16 + c16;
-    if (row >= L) continue;
-    const float inv = 1.0f / l[qb];
+    const bool ok = row < L;
+    const float inv = ok ? 1.0f / l[qb] : 0.f;
     const int r = br * L + row;
+    float mrow = 0.f;  // largest |stored value| of this lane's part of the row
 #pragma unroll
     for (int db = 0; db < NDB; ++db) {
       uint16_t ob[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) ob[j] = f2bf_bits(o[db][qb][j] * inv);
+      for (int j = 0; j < 4; ++j) {
+        ob[j] = f2bf_bits(o[db][qb][j] * inv);
+        mrow = fmaxf(mrow, fabsf(bf2f_bits(ob[j])));
+      }
       const int col = h * D + db * 16 + g * 4;
-      *(uint2*)(a.out + packA_off(r, col, a.Mp)) = *(const uint2*)ob;
+      if (ok) *(uint2*)(a.out + packA_off(r, col, a.Mp)) = *(const uint2*)ob;
+    }
+    if (a.rowmax) {  // lanes c16 + 16 g hold the row's 4 column groups of this head
+      mrow = fmaxf(mrow, __shfl_xor(mrow, 16));
+      mrow = fmaxf(mrow, __shfl_xor(mrow, 32));
+      if (ok && g == 0) atomicMax(a.rowmax + r, __float_as_uint(mrow));
     }
   }
 }
@@ -591,6 +600,10 @@ __global__ __launch_bounds__(64 * SL_WAVES) void attn_sl_kernel(AttnArgs a) {
     for (int db = 0; db < NDB; ++db) s_o[wv][(db * QB + qb) * 64 + lane] = o[db][qb];
   }
   lds_barrier();
+  // f = tid + 64 SL_WAVES i: every entry of a thread has the lane tid % 64 and
+  // the row block (tid / 64) % QB, so a thread's entries are one row
+  static_assert((64 * SL_WAVES) % (64 * QB) == 0, "a thread's entries share their row");
+  float mrow = 0.f;  // largest |stored value| of this thread's part of its row
   for (int f = tid; f < SM::OV; f += 64 * SL_WAVES) {
     const int ln = f & 63, qb = (f >> 6) % QB, db = (f >> 6) / QB;
     const int q16 = ln & 15, g4 = ln >> 4;
@@ -606,9 +619,29 @@ __global__ __launch_bounds__(64 * SL_WAVES) void attn_sl_kernel(AttnArgs a) {
     const float inv = 1.0f / ls;
     uint16_t ob[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) ob[j] = f2bf_bits(acc[j] * inv);
+    for (int j = 0; j < 4; ++j) {
+      ob[j] = f2bf_bits(acc[j] * inv);
+      mrow = fmaxf(mrow, fabsf(bf2f_bits(ob[j])));
+    }
     const int col = h * D + db * 16 + g4 * 4;
     *(uint2*)(a.out + packA_off(br * L + row, col, a.Mp)) = *(const uint2*)ob;
+  }
+  if (a.rowmax) {
+    // over the row's 4 column groups (lanes q16 + 16 g4), then over the
+    // wavefronts of the same row block (through LDS, reusing s_l: every
+    // thread has read it above), one atomic per row
+    mrow = fmaxf(mrow, __shfl_xor(mrow, 16));
+    mrow = fmaxf(mrow, __shfl_xor(mrow, 32));
+    lds_barrier();
+    float* s_m = &s_l[0][0];
+    if (lane < 16) s_m[wv * 16 + lane] = mrow;
+    lds_barrier();
+    if (tid < 16 * QB) {
+      const int qb = tid >> 4, row = qb * 16 + (tid & 15);
+      float m = 0.f;
+      for (int w = qb; w < SL_WAVES; w += QB) m = fmaxf(m, s_m[w * 16 + (tid & 15)]);
+      if (row < L) atomicMax(a.rowmax + br * L + row, __float_as_uint(m));
+    }
   }
 }
 
@@ -811,8 +844,9 @@ template <int D>
 __global__ __launch_bounds__(256) void attn_gmerge_kernel(AttnArgs a, int NS) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int q4 = (int)(t % (D / 4));
-  const int64_t r = t / (D / 4);  // (branch, head, row)
-  if (r >= (int64_t)a.nb * a.Hq * a.L) return;
+  const int64_t rr = t / (D / 4);  // (branch, head, row)
+  const bool ok = rr < (int64_t)a.nb * a.Hq * a.L;
+  const int64_t r = ok ? rr : 0;
   const int row = (int)(r % a.L), h = (int)((r / a.L) % a.Hq), br = (int)(r / ((int64_t)a.L * a.Hq));
   const GroupScratch sc = group_scratch(a, NS);
   const int64_t rows = (int64_t)a.nb * a.Hq * a.L;
@@ -824,9 +858,18 @@ __global__ __launch_bounds__(256) void attn_gmerge_kernel(AttnArgs a, int NS) {
   }
   const float inv = 1.0f / ls;
   uint16_t ob[4];
+  float mrow = 0.f;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) ob[j] = f2bf_bits(acc[j] * inv);
-  *(uint2*)(a.out + packA_off(br * a.L + row, h * D + q4 * 4, a.Mp)) = *(const uint2*)ob;
+  for (int j = 0; j < 4; ++j) {
+    ob[j] = f2bf_bits(acc[j] * inv);
+    mrow = fmaxf(mrow, fabsf(bf2f_bits(ob[j])));
+  }
+  if (ok) *(uint2*)(a.out + packA_off(br * a.L + row, h * D + q4 * 4, a.Mp)) = *(const uint2*)ob;
+  if (a.rowmax) {  // the D / 4 threads of one (branch, head, row) are adjacent lanes
+#pragma unroll
+    for (int o = 1; o < D / 4; o <<= 1) mrow = fmaxf(mrow, __shfl_xor(mrow, o));
+    if (ok && q4 == 0) atomicMax(a.rowmax + br * a.L + row, __float_as_uint(mrow));
+  }
 }
 
 // key splits of the grouped form before the per-call caps: enough workgroups

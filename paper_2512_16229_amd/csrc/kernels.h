@@ -90,7 +90,7 @@ hipError_t launch_repack8(const uint16_t* s0, const float* inv0, const float* sc
                           hipStream_t s);
 hipError_t launch_embed_norm8(const int32_t* tokens, const uint16_t* embed, int vocab,
                               const float* w, float eps, int M, int Mp, int H, float* x,
-                              uint8_t* a8, float* sa, hipStream_t s);
+                              uint8_t* a8, float* sa, uint32_t* rowmax_zero, hipStream_t s);
 // merge per-tile softmax partials into conf / pred
 hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, int M,
                            int tiles, float* conf, int32_t* pred, hipStream_t s);
@@ -162,6 +162,11 @@ struct AttnArgs {
   // row maxima, sums and partial outputs); null or too small: not used
   float* scratch;
   size_t scratch_bytes;
+  // non-null: the largest |value| of each output row (over all heads, of the
+  // stored bf16 values) merged into rowmax[row] as float bits by an atomic
+  // unsigned maximum (order-free; zeroed beforehand): the row scales of the
+  // FP8 output projection
+  uint32_t* rowmax;
 };
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 // bytes of AttnArgs::scratch that let the grouped form run with its full key

@@ -394,11 +394,11 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
 
 hipError_t launch_embed_norm8(const int32_t* tokens, const uint16_t* embed, int vocab,
                               const float* w, float eps, int M, int Mp, int H, float* x,
-                              uint8_t* a8, float* sa, hipStream_t s) {
+                              uint8_t* a8, float* sa, uint32_t* rz, hipStream_t s) {
   if (H % 256 || H > 1024 * CPT || !a8 || !sa) return hipErrorInvalidValue;
 #define EMBEDNORM8(NG)                                                                    \
   hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, true>), dim3(M), dim3(256), 0, s, tokens,  \
-                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, nullptr, a8, sa, nullptr)
+                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, nullptr, a8, sa, rz)
   switch (resnorm_groups(H)) {
     case 1: EMBEDNORM8(1); break;
     case 2: EMBEDNORM8(2); break;
