@@ -139,12 +139,13 @@ void lopa_model_destroy(lopa_model* m);
  * max_branches branches of a block of up to max_block positions, plus the
  * verify workspace. Cache layout (bf16, library-owned; read and write rows
  * through lopa_kv_read / lopa_kv_write, which use [kv_heads][len][head_dim]
- * whatever the internal layout): per layer and KV head, K as
- * [max_len rounded up to 8][head_dim] (position-major) and V transposed as
- * [head_dim][max_len rounded up to 8] (8 consecutive positions of one
- * dimension are one aligned 16-byte run, the attention kernel's copy unit);
- * layers outermost, then K / V, then KV heads. The per-branch staging has the
- * same two layouts with max_block. Zero-initialised. */
+ * whatever the internal layout): layers outermost, then K / V, then KV heads;
+ * each head's K region and V region hold tiles of 32 consecutive positions
+ * (max_len rounded up to 32), head_dim x 32 values per tile, stored in the
+ * order the attention kernels' matrix-core instructions take them: every
+ * 1 KiB operand fragment (K: 16 positions x 32 dimensions; V: 16 dimensions x
+ * 32 positions) is one contiguous run, 16 bytes per lane of a wavefront. The
+ * per-branch staging has the same layout with max_block. Zero-initialised. */
 int lopa_kv_create(const lopa_model* m, int32_t max_len, int32_t max_branches,
                    int32_t max_block, lopa_kv** out);
 void lopa_kv_destroy(lopa_kv* kv);
