@@ -23,8 +23,12 @@ pytestmark = pytest.mark.gpu
 
 # (config, P, L, k): two head dims, a ragged block, and the shared-prefix
 # attention path (P = 300, 16 branches)
+# the attention form varies with the key range and the block: single-load (the
+# first five), grouped (26 key tiles, 4 query heads per KV head) and
+# per-(head, branch) (64-row blocks); with LOPA_PRECISION_FP8 each writes the
+# row maxima of the FP8 output projection
 CASES = [("tiny", 64, 16, 3), ("small", 100, 32, 7), ("small128", 40, 16, 2), ("tiny", 23, 7, 2),
-         ("small", 300, 32, 15)]
+         ("small", 300, 32, 15), ("small", 800, 32, 3), ("small", 100, 64, 3)]
 PRECS = ["fp8_mlp", "fp8"]
 
 
