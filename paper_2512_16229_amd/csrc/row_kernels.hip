@@ -7,19 +7,20 @@
 
 #include <math.h>
 
-// One workgroup (256 threads) per row; thread t holds the 4-column groups
-// q = t + 256 i, i < NG (columns 4 q .. 4 q + 3, q < H / 4, H % 256 == 0,
-// H <= 1024 NG).
+// One workgroup of TPB threads (256, 512 or 1024: the launcher takes the
+// fewest that cover the row once, so a row's loads are spread over up to 16
+// wavefronts) per row; thread t holds the 4-column groups q = t + TPB i,
+// i < NG (columns 4 q .. 4 q + 3, q < H / 4, H % 256 == 0, H <= TPB NG 4).
 // The row is formed in registers:
 //   EMBED:  x = embedding of the token (bf16 -> fp32)
 //   else:   x += sum of the S split-K partial sums of the preceding projection
 //           (row-major fp32 [S][Mp][H], summed in split order first)
 // then x is stored back and a = pack(x / rms(x) * w) (RMSNorm; the sum of
-// squares is reduced in a fixed order: lanes, then wavefronts 0..3). Groups
+// squares is reduced in a fixed order: lanes, then wavefronts 0, 1, ...). Groups
 // past the row read the row's last group again and are discarded by a
 // select: no load sits under a branch, so all of them can be in flight
 // together.
-constexpr int CPT = 8;  // 4-column groups per thread at most
+constexpr int H_MAX = 8192;  // widest row: 1024 threads x 2 groups of 4 columns
 
 // E4M3 (no infinities, max 448) of x, round to nearest even, saturating:
 // subnormals (|x| < 2^-6) are multiples of 2^-9, and a normal value of binade
@@ -43,8 +44,8 @@ __device__ __forceinline__ int64_t packA8_off(int r, int c, int Mp) {
 __device__ __forceinline__ float e4m3_inv(float amax) { return amax > 0.f ? __fdiv_rn(448.f, amax) : 0.f; }
 __device__ __forceinline__ float e4m3_scale(float amax) { return amax > 0.f ? __fdiv_rn(amax, 448.f) : 0.f; }
 
-template <bool EMBED, int SC, int NG, bool A8>
-__global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict__ tokens,
+template <bool EMBED, int SC, int NG, bool A8, int TPB>
+__global__ __launch_bounds__(TPB) void resnorm_kernel(const int32_t* __restrict__ tokens,
                                                       const uint16_t* __restrict__ embed,
                                                       int vocab, const float* __restrict__ part,
                                                       int S, const float* __restrict__ w,
@@ -54,8 +55,9 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
                                                       uint8_t* __restrict__ a8,
                                                       float* __restrict__ sa,
                                                       uint32_t* __restrict__ rowmax_zero) {
-  __shared__ float red[4];
-  __shared__ float redm[4];
+  constexpr int NW = TPB / 64;
+  __shared__ float red[NW];
+  __shared__ float redm[NW];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int r = blockIdx.x;
   const int nq = H >> 2;
@@ -67,7 +69,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   float4 wt[NG];
 #pragma unroll
   for (int i = 0; i < NG; ++i) {
-    const int q = tid + 256 * i;
+    const int q = tid + TPB * i;
     wt[i] = ((const float4*)w)[q < nq ? q : nq - 1];
   }
   if (EMBED) {
@@ -77,7 +79,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
     const uint16_t* er = embed + (int64_t)tok * H;
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      const int q = tid + 256 * i;
+      const int q = tid + TPB * i;
       const bool ok = q < nq;
       const uint2 raw = *(const uint2*)(er + (ok ? q : nq - 1) * 4);
       v[i] = make_float4(ok ? bf2f_bits(raw.x & 0xffff) : 0.f, ok ? bf2f_bits(raw.x >> 16) : 0.f,
@@ -89,23 +91,29 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
     float4 t[NG], res[NG];
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      const int q = tid + 256 * i;
+      const int q = tid + TPB * i;
       res[i] = ((const float4*)xr)[q < nq ? q : nq - 1];  // the residual, loaded up front
       t[i] = make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    const int ns = SC >= 0 ? SC : S;
-    for (int sp = 0; sp < ns; ++sp) {
+    auto add_split = [&](int sp) {
       const float4* pr = (const float4*)(part + ((int64_t)sp * Mp + r) * H);
 #pragma unroll
       for (int i = 0; i < NG; ++i) {
-        const int q = tid + 256 * i;
+        const int q = tid + TPB * i;
         const float4 u = pr[q < nq ? q : nq - 1];
         t[i].x += u.x; t[i].y += u.y; t[i].z += u.z; t[i].w += u.w;
       }
+    };
+    if constexpr (SC >= 0) {
+      // unrolled: every split's loads are issued before the first add
+#pragma unroll
+      for (int sp = 0; sp < SC; ++sp) add_split(sp);
+    } else {
+      for (int sp = 0; sp < S; ++sp) add_split(sp);
     }
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      const int q = tid + 256 * i;
+      const int q = tid + TPB * i;
       const bool ok = q < nq;
       const float4 u = res[i];
       v[i] = make_float4(ok ? u.x + t[i].x : 0.f, ok ? u.y + t[i].y : 0.f,
@@ -114,23 +122,25 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   }
 #pragma unroll
   for (int i = 0; i < NG; ++i) {
-    const int q = tid + 256 * i;
+    const int q = tid + TPB * i;
     if (q < nq && (EMBED || (SC >= 0 ? SC : S) > 0)) ((float4*)xr)[q] = v[i];
     ss += v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
   }
   ss = wave_sum(ss);
   if (lane == 0) red[wv] = ss;
   __syncthreads();
-  const float tot = red[0] + red[1] + red[2] + red[3];
+  float tot = red[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) tot += red[w];
   const float inv = 1.0f / sqrtf(tot / (float)H + eps);
   if constexpr (A8) {
     // FP8 operand: the normed row, its largest magnitude (lanes, then
-    // wavefronts 0..3), then E4M3 of each value times 448 / max
+    // wavefronts 0, 1, ...), then E4M3 of each value times 448 / max
     float4 y[NG];
     float mx = 0.f;
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      const int q = tid + 256 * i;
+      const int q = tid + TPB * i;
       y[i] = make_float4(v[i].x * inv * wt[i].x, v[i].y * inv * wt[i].y, v[i].z * inv * wt[i].z,
                          v[i].w * inv * wt[i].w);
       if (q < nq)
@@ -139,11 +149,13 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
     mx = wave_max(mx);
     if (lane == 0) redm[wv] = mx;
     __syncthreads();
-    mx = fmaxf(fmaxf(redm[0], redm[1]), fmaxf(redm[2], redm[3]));
+    mx = redm[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) mx = fmaxf(mx, redm[w]);
     const float si = e4m3_inv(mx);
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      const int q = tid + 256 * i;
+      const int q = tid + TPB * i;
       if (q < nq) {
         const uint32_t b = f32_to_e4m3(y[i].x * si) | (f32_to_e4m3(y[i].y * si) << 8) |
                            (f32_to_e4m3(y[i].z * si) << 16) | (f32_to_e4m3(y[i].w * si) << 24);
@@ -157,7 +169,7 @@ __global__ __launch_bounds__(256) void resnorm_kernel(const int32_t* __restrict_
   } else {
 #pragma unroll
     for (int i = 0; i < NG; ++i) {
-      const int q = tid + 256 * i;
+      const int q = tid + TPB * i;
       if (q < nq) {
         const uint32_t lo = (uint32_t)f2bf_bits(v[i].x * inv * wt[i].x) |
                             ((uint32_t)f2bf_bits(v[i].y * inv * wt[i].y) << 16);
@@ -371,22 +383,24 @@ __global__ void bf16_to_f32_kernel(const uint16_t* __restrict__ s, float* __rest
 
 // ------------------------------------------------------------ launchers
 namespace {
-// 4-column groups per thread for a row of H columns
-int resnorm_groups(int H) { return H <= 1024 ? 1 : H <= 2048 ? 2 : H <= 4096 ? 4 : 8; }
+// threads per row and 4-column groups per thread for a row of H columns:
+// 1: (256, 1), 2: (512, 1), 3: (1024, 1), 4: (1024, 2)
+int resnorm_shape(int H) { return H <= 1024 ? 1 : H <= 2048 ? 2 : H <= 4096 ? 3 : 4; }
 }  // namespace
 
 hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int vocab,
                              const float* w, float eps, int M, int Mp, int H, float* x,
                              uint16_t* a, hipStream_t s) {
-  if (H % 256 || H > 1024 * CPT) return hipErrorInvalidValue;
-#define EMBEDNORM(NG)                                                                     \
-  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, false>), dim3(M), dim3(256), 0, s, tokens,   \
-                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr)
-  switch (resnorm_groups(H)) {
-    case 1: EMBEDNORM(1); break;
-    case 2: EMBEDNORM(2); break;
-    case 4: EMBEDNORM(4); break;
-    default: EMBEDNORM(8); break;
+  if (H % 256 || H > H_MAX) return hipErrorInvalidValue;
+#define EMBEDNORM(NG, TPB)                                                                \
+  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, false, TPB>), dim3(M), dim3(TPB), 0, s,      \
+                     tokens, embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, a, nullptr, nullptr, \
+                     nullptr)
+  switch (resnorm_shape(H)) {
+    case 1: EMBEDNORM(1, 256); break;
+    case 2: EMBEDNORM(1, 512); break;
+    case 3: EMBEDNORM(1, 1024); break;
+    default: EMBEDNORM(2, 1024); break;
   }
 #undef EMBEDNORM
   return hipGetLastError();
@@ -395,26 +409,26 @@ hipError_t launch_embed_norm(const int32_t* tokens, const uint16_t* embed, int v
 hipError_t launch_embed_norm8(const int32_t* tokens, const uint16_t* embed, int vocab,
                               const float* w, float eps, int M, int Mp, int H, float* x,
                               uint8_t* a8, float* sa, uint32_t* rz, hipStream_t s) {
-  if (H % 256 || H > 1024 * CPT || !a8 || !sa) return hipErrorInvalidValue;
-#define EMBEDNORM8(NG)                                                                    \
-  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, true>), dim3(M), dim3(256), 0, s, tokens,  \
-                     embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, nullptr, a8, sa, rz)
-  switch (resnorm_groups(H)) {
-    case 1: EMBEDNORM8(1); break;
-    case 2: EMBEDNORM8(2); break;
-    case 4: EMBEDNORM8(4); break;
-    default: EMBEDNORM8(8); break;
+  if (H % 256 || H > H_MAX || !a8 || !sa) return hipErrorInvalidValue;
+#define EMBEDNORM8(NG, TPB)                                                               \
+  hipLaunchKernelGGL((resnorm_kernel<true, 0, NG, true, TPB>), dim3(M), dim3(TPB), 0, s,       \
+                     tokens, embed, vocab, nullptr, 0, w, eps, M, Mp, H, x, nullptr, a8, sa, rz)
+  switch (resnorm_shape(H)) {
+    case 1: EMBEDNORM8(1, 256); break;
+    case 2: EMBEDNORM8(1, 512); break;
+    case 3: EMBEDNORM8(1, 1024); break;
+    default: EMBEDNORM8(2, 1024); break;
   }
 #undef EMBEDNORM8
   return hipGetLastError();
 }
 
 namespace {
-template <int NG, bool A8>
+template <int NG, bool A8, int TPB>
 void resnorm_ng(const float* part, int S, const float* w, float eps, int M, int Mp, int H,
                 float* x, uint16_t* a, uint8_t* a8, float* sa, uint32_t* rz, hipStream_t s) {
 #define RESNORM(SC)                                                                         \
-  hipLaunchKernelGGL((resnorm_kernel<false, SC, NG, A8>), dim3(M), dim3(256), 0, s, nullptr, \
+  hipLaunchKernelGGL((resnorm_kernel<false, SC, NG, A8, TPB>), dim3(M), dim3(TPB), 0, s, nullptr, \
                      nullptr, 0, part, S, w, eps, M, Mp, H, x, a, a8, sa, rz)
   switch (S) {
     case 0: RESNORM(0); break;
@@ -434,24 +448,24 @@ void resnorm_ng(const float* part, int S, const float* w, float eps, int M, int 
 
 hipError_t launch_resnorm(const float* part, int S, const float* w, float eps, int M, int Mp,
                           int H, float* x, uint16_t* a, hipStream_t s) {
-  if (H % 256 || H > 1024 * CPT || S < 0) return hipErrorInvalidValue;
-  switch (resnorm_groups(H)) {
-    case 1: resnorm_ng<1, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
-    case 2: resnorm_ng<2, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
-    case 4: resnorm_ng<4, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
-    default: resnorm_ng<8, false>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
+  if (H % 256 || H > H_MAX || S < 0) return hipErrorInvalidValue;
+  switch (resnorm_shape(H)) {
+    case 1: resnorm_ng<1, false, 256>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
+    case 2: resnorm_ng<1, false, 512>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
+    case 3: resnorm_ng<1, false, 1024>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
+    default: resnorm_ng<2, false, 1024>(part, S, w, eps, M, Mp, H, x, a, nullptr, nullptr, nullptr, s); break;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_resnorm8(const float* part, int S, const float* w, float eps, int M, int Mp,
                            int H, float* x, uint8_t* a8, float* sa, uint32_t* rz, hipStream_t s) {
-  if (H % 256 || H > 1024 * CPT || S < 0 || !a8 || !sa) return hipErrorInvalidValue;
-  switch (resnorm_groups(H)) {
-    case 1: resnorm_ng<1, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
-    case 2: resnorm_ng<2, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
-    case 4: resnorm_ng<4, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
-    default: resnorm_ng<8, true>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
+  if (H % 256 || H > H_MAX || S < 0 || !a8 || !sa) return hipErrorInvalidValue;
+  switch (resnorm_shape(H)) {
+    case 1: resnorm_ng<1, true, 256>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
+    case 2: resnorm_ng<1, true, 512>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
+    case 3: resnorm_ng<1, true, 1024>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
+    default: resnorm_ng<2, true, 1024>(part, S, w, eps, M, Mp, H, x, nullptr, a8, sa, rz, s); break;
   }
   return hipGetLastError();
 }
