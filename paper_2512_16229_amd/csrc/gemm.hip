@@ -567,8 +567,11 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
 // QKV: sum the S partials of one f32x4 of the output (4 rows, 1 column) in
 // split order and run the epilogue. One thread per (row tile, column tile, wave,
 // 16-row block, 16-column block, lane): the same indexing as gemm_kernel's
-// partial store, so each warp-wide load is 1 KiB contiguous.
-template <int EPI, int NB>
+// partial store, so each warp-wide load is 1 KiB contiguous. SC > 0: the split
+// count as a constant, so that every load of a thread (the split sums of its
+// column and of its rotation partner, the rotary rows, bias and scales) is in
+// flight before the first add; SC = 0: any split count, summed in a loop.
+template <int EPI, int NB, int SC>
 __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int lane = (int)(gid & 63);
@@ -586,62 +589,81 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
   const int r0 = mt * 256 + wv * 64 + mb * 16 + g * 4;
   const int n = (tile * NB + nb) * 16 + c16;
   if (n >= a.N || r0 >= a.M) return;
+  const int D = a.d, HD = D >> 1;
+  const int qcols = a.Hq * D, kcols = a.Hkv * D;
+  const int sect = n < qcols ? 0 : (n < qcols + kcols ? 1 : 2);
+  const int base = sect == 0 ? 0 : (sect == 1 ? qcols : qcols + kcols);
+  const int head = (n - base) / D, dim = (n - base) % D;
+  if (sect < 2 && dim >= HD) return;  // written with its rotation partner
+  const bool rot = sect < 2;
+  const int n2 = rot ? n + HD : n;  // the partner column (V: the column itself, unused)
   const int64_t sstride = (int64_t)4 * 4 * NB * 64;  // f32x4 between consecutive splits
-  auto sum = [&](int t2, int nb2) {
-    const f32x4* p = (const f32x4*)a.partials +
-                     ((((int64_t)mt * a.tiles + t2) * a.splits * 4 + wv) * 4 * NB + mb * NB + nb2) *
-                         64 + lane;
-    f32x4 v = p[0];
-    for (int s = 1; s < a.splits; ++s) v += p[s * sstride];
-    return v;
+  auto first = [&](int col) {
+    const int t2 = (col >> 4) / NB, nb2 = (col >> 4) % NB;
+    return (const f32x4*)a.partials +
+           ((((int64_t)mt * a.tiles + t2) * a.splits * 4 + wv) * 4 * NB + mb * NB + nb2) * 64 + lane;
   };
-  {
-    const int D = a.d, HD = D >> 1;
-    const int qcols = a.Hq * D, kcols = a.Hkv * D;
-    const int sect = n < qcols ? 0 : (n < qcols + kcols ? 1 : 2);
-    const int base = sect == 0 ? 0 : (sect == 1 ? qcols : qcols + kcols);
-    const int head = (n - base) / D, dim = (n - base) % D;
-    if (sect < 2 && dim >= HD) return;  // written with its rotation partner
-    f32x4 v1 = sum(tile, nb);
-    f32x4 v2 = {0.f, 0.f, 0.f, 0.f};
-    const int n2 = n + HD;
-    if (sect < 2) v2 = sum((n2 >> 4) / NB, (n2 >> 4) % NB);
-    if (a.f8) {  // FP8 operands: the sums of products times the row and column scales
+  const f32x4* p1 = first(n);
+  const f32x4* p2 = first(n2);
+  f32x4 v1 = p1[0], v2 = p2[0];
+  if constexpr (SC > 0) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float sr = r0 + j < a.M ? a.sa[r0 + j] : 0.f;
-        v1[j] = v1[j] * sr * a.sw[n];
-        if (sect < 2) v2[j] = v2[j] * sr * a.sw[n2];
-      }
+    for (int s = 1; s < SC; ++s) {
+      v1 += p1[s * sstride];
+      v2 += p2[s * sstride];
     }
-    const float b1 = a.bias ? a.bias[n] : 0.f;
-    const float b2 = (a.bias && sect < 2) ? a.bias[n2] : 0.f;
+  } else {
+    for (int s = 1; s < a.splits; ++s) {
+      v1 += p1[s * sstride];
+      v2 += p2[s * sstride];
+    }
+  }
+  // rows r0 .. r0 + 3 (those past M read row M - 1's table entries and are not stored)
+  int br[4], pos[4];
+  float2 cs[4];
+  float sr[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = r0 + j < a.M ? r0 + j : a.M - 1;
+    br[j] = r / a.L;
+    pos[j] = r % a.L;
+    cs[j] = rot ? *(const float2*)(a.rope + ((int64_t)(a.P + pos[j]) * HD + dim) * 2)
+                : make_float2(1.f, 0.f);
+    sr[j] = a.f8 && r0 + j < a.M ? a.sa[r0 + j] : 0.f;
+  }
+  const float b1 = a.bias ? a.bias[n] : 0.f;
+  const float b2 = (a.bias && rot) ? a.bias[n2] : 0.f;
+  const float sw1 = a.f8 ? a.sw[n] : 0.f, sw2 = a.f8 && rot ? a.sw[n2] : 0.f;
+  if (a.f8) {  // FP8 operands: the sums of products times the row and column scales
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int r = r0 + j;
-      if (r >= a.M) continue;
-      const int br = r / a.L, i = r % a.L;
-      float o1 = v1[j] + b1, o2 = 0.f;
-      if (sect < 2) {
-        const float2 cs = *(const float2*)(a.rope + ((int64_t)(a.P + i) * HD + dim) * 2);
-        const float x1 = o1, x2 = v2[j] + b2;
-        o1 = x1 * cs.x - x2 * cs.y;
-        o2 = x2 * cs.x + x1 * cs.y;
-      }
-      if (sect == 0) {
-        uint16_t* qo = a.q_out + (((int64_t)br * a.Hq + head) * a.L + i) * D;
-        qo[dim] = f2bf_bits(o1);
-        qo[dim + HD] = f2bf_bits(o2);
+      v1[j] = v1[j] * sr[j] * sw1;
+      if (rot) v2[j] = v2[j] * sr[j] * sw2;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (r0 + j >= a.M) continue;
+    const int i = pos[j];
+    float o1 = v1[j] + b1, o2 = 0.f;
+    if (rot) {
+      const float x1 = o1, x2 = v2[j] + b2;
+      o1 = x1 * cs[j].x - x2 * cs[j].y;
+      o2 = x2 * cs[j].x + x1 * cs[j].y;
+    }
+    if (sect == 0) {
+      uint16_t* qo = a.q_out + (((int64_t)br[j] * a.Hq + head) * a.L + i) * D;
+      qo[dim] = f2bf_bits(o1);
+      qo[dim + HD] = f2bf_bits(o2);
+    } else {
+      // staging head (K or V) of this branch and layer, in the KV tile layout
+      uint16_t* st = a.staging + ((((int64_t)br[j] * a.layers + a.layer) * 2 + (sect - 1)) *
+                                      a.Hkv + head) * D * a.vlds;
+      if (sect == 1) {
+        st[kv_k_off(i, dim, D)] = f2bf_bits(o1);
+        st[kv_k_off(i, dim + HD, D)] = f2bf_bits(o2);
       } else {
-        // staging head (K or V) of this branch and layer, in the KV tile layout
-        uint16_t* st = a.staging + ((((int64_t)br * a.layers + a.layer) * 2 + (sect - 1)) *
-                                        a.Hkv + head) * D * a.vlds;
-        if (sect == 1) {
-          st[kv_k_off(i, dim, D)] = f2bf_bits(o1);
-          st[kv_k_off(i, dim + HD, D)] = f2bf_bits(o2);
-        } else {
-          st[kv_v_off(i, dim, D)] = f2bf_bits(o1);
-        }
+        st[kv_v_off(i, dim, D)] = f2bf_bits(o1);
       }
     }
   }
@@ -655,8 +677,20 @@ hipError_t launch_nb(const GemmArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   if constexpr (EPI == EPI_QKV) {
     const int64_t threads = (int64_t)a.mtiles * a.tiles * 4 * 4 * NB * 64;
-    hipLaunchKernelGGL((gemm_fixup_kernel<EPI, NB>), dim3((unsigned)((threads + 255) / 256)),
-                       dim3(256), 0, s, a);
+    const dim3 fg((unsigned)((threads + 255) / 256));
+    switch (a.splits) {
+#define FIXUP(SC) hipLaunchKernelGGL((gemm_fixup_kernel<EPI, NB, SC>), fg, dim3(256), 0, s, a)
+      case 1: FIXUP(1); break;
+      case 2: FIXUP(2); break;
+      case 3: FIXUP(3); break;
+      case 4: FIXUP(4); break;
+      case 5: FIXUP(5); break;
+      case 6: FIXUP(6); break;
+      case 7: FIXUP(7); break;
+      case 8: FIXUP(8); break;
+      default: FIXUP(0); break;
+#undef FIXUP
+    }
     e = hipGetLastError();
   }
   return e;
