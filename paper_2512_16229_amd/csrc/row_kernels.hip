@@ -320,12 +320,22 @@ __global__ __launch_bounds__(256) void lm_merge_kernel(const float* __restrict__
   const float* rm = pm + (int64_t)r * tiles;
   const float* rs = ps + (int64_t)r * tiles;
   const int32_t* ri = pi + (int64_t)r * tiles;
-#pragma unroll 4
-  for (int t = tid; t < tiles; t += 256) {
-    const float tm = rm[t], ts = rs[t];
-    const int ti = ri[t];
-    if (tm == -INFINITY) continue;
-    st = lm_combine(st, {tm, ts, ti});
+  // a thread's tiles tid, tid + 256, ... in order, LM_BATCH of them loaded
+  // (index clamped, no load under a branch) before any is merged
+  constexpr int LM_BATCH = 4;
+  for (int t0 = tid; t0 < tiles; t0 += 256 * LM_BATCH) {
+    float tm[LM_BATCH], ts[LM_BATCH];
+    int ti[LM_BATCH];
+#pragma unroll
+    for (int b = 0; b < LM_BATCH; ++b) {
+      const int t = min(t0 + 256 * b, tiles - 1);
+      tm[b] = rm[t];
+      ts[b] = rs[t];
+      ti[b] = ri[t];
+    }
+#pragma unroll
+    for (int b = 0; b < LM_BATCH; ++b)
+      if (t0 + 256 * b < tiles && tm[b] != -INFINITY) st = lm_combine(st, {tm[b], ts[b], ti[b]});
   }
   for (int o = 1; o < 64; o <<= 1) {
     const LmState ot{__shfl_xor(st.m, o), __shfl_xor(st.s, o), __shfl_xor(st.idx, o)};
