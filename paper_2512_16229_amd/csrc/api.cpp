@@ -109,7 +109,7 @@ GemmPlan plan_gemm(int epi, int nblocks, int KC, int MT, int num_cu, int fixed_n
   for (int nb : {4, 8}) {
     if (fixed_nb && nb != fixed_nb) continue;
     const int tiles = nblocks / nb;
-    for (int S = 1; S <= Q; ++S) {
+    for (int S = 1; S <= (epi == EPI_QKV ? std::min(Q, QKV_MAX_SPLITS) : Q); ++S) {
       const int64_t wgs = (int64_t)MT * tiles * S;
       const int64_t rounds = (wgs + num_cu - 1) / num_cu;
       const double iters = 4.0 * ((Q + S - 1) / S);

@@ -567,10 +567,10 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) __attribute__((amdgpu_waves_per_eu
 // QKV: sum the S partials of one f32x4 of the output (4 rows, 1 column) in
 // split order and run the epilogue. One thread per (row tile, column tile, wave,
 // 16-row block, 16-column block, lane): the same indexing as gemm_kernel's
-// partial store, so each warp-wide load is 1 KiB contiguous. SC > 0: the split
-// count as a constant, so that every load of a thread (the split sums of its
-// column and of its rotation partner, the rotary rows, bias and scales) is in
-// flight before the first add; SC = 0: any split count, summed in a loop.
+// partial store, so each warp-wide load is 1 KiB contiguous. The split count SC
+// (1..8, QKV_MAX_SPLITS) is a constant, so that every load of a thread (the
+// split sums of its column and of its rotation partner, the rotary rows, bias
+// and scales) is in flight before the first add.
 template <int EPI, int NB, int SC>
 __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
   const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -606,17 +606,10 @@ __global__ __launch_bounds__(256) void gemm_fixup_kernel(GemmArgs a) {
   const f32x4* p1 = first(n);
   const f32x4* p2 = first(n2);
   f32x4 v1 = p1[0], v2 = p2[0];
-  if constexpr (SC > 0) {
 #pragma unroll
-    for (int s = 1; s < SC; ++s) {
-      v1 += p1[s * sstride];
-      v2 += p2[s * sstride];
-    }
-  } else {
-    for (int s = 1; s < a.splits; ++s) {
-      v1 += p1[s * sstride];
-      v2 += p2[s * sstride];
-    }
+  for (int s = 1; s < SC; ++s) {
+    v1 += p1[s * sstride];
+    v2 += p2[s * sstride];
   }
   // rows r0 .. r0 + 3 (those past M read row M - 1's table entries and are not stored)
   int br[4], pos[4];
@@ -688,7 +681,7 @@ hipError_t launch_nb(const GemmArgs& a, hipStream_t s) {
       case 6: FIXUP(6); break;
       case 7: FIXUP(7); break;
       case 8: FIXUP(8); break;
-      default: FIXUP(0); break;
+      default: return hipErrorInvalidValue;  // launch_gemm admits at most QKV_MAX_SPLITS
 #undef FIXUP
     }
     e = hipGetLastError();
@@ -719,6 +712,7 @@ hipError_t launch_gemm(int epi, const GemmArgs& a, hipStream_t s) {
       a.gcols < 1 || a.Mp != 256 * a.mtiles)
     return hipErrorInvalidValue;
   if (a.gcols != a.tiles * a.splits) return hipErrorInvalidValue;
+  if (epi == EPI_QKV && a.splits > QKV_MAX_SPLITS) return hipErrorInvalidValue;
   if (a.f8) {
     if (!a.sa || !a.sw || (epi == EPI_SWIGLU && !a.rowmax)) return hipErrorInvalidValue;
     switch (epi * 16 + a.nb) {

@@ -97,6 +97,8 @@ hipError_t launch_lm_merge(const float* pm, const float* ps, const int32_t* pi, 
 
 // ---------------------------------------------------------------- GEMM
 enum { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
+// most k-splits of the QKV projection (its fix-up sums them with the count as a constant)
+constexpr int QKV_MAX_SPLITS = 8;
 
 struct GemmArgs {
   const uint16_t* A;   // packed activations, Mp rows, K columns
