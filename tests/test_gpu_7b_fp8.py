@@ -1,6 +1,7 @@
-"""GPU parity of the FP8 model mode (LOPA_PRECISION_FP8: QKV, gate / up / down
-and the LM head in W8A8 E4M3) at the full Dream-7B shape, prefix 512, k = 7, in
-the launch configuration bench.py times for its FP8 step figure: one verify
+"""GPU parity of the FP8 model mode (LOPA_PRECISION_FP8: QKV, O, gate / up /
+down and the LM head in W8A8 E4M3) at the full Dream-7B shape, prefix 512, k = 7,
+in the launch configuration bench.py times for its FP8 step figure, and at the
+LLaDA-8B layout (multi-head attention, other tile widths), prefix 1024: one verify
 forward of all 8 x 32 rows, every layer fed the GPU's own input residual stream
 against the oracle's "fp8" mode layer (fixed rel-L2), and the oracle's FP8 LM
 head + softmax on the GPU's own final rows (confidences within 1e-3, candidate
@@ -22,7 +23,7 @@ from oracle.model import rms_norm
 
 pytestmark = pytest.mark.gpu
 
-L, P, K = 32, 512, 7
+L, K = 32, 7
 
 
 class _Layers:
@@ -49,9 +50,10 @@ def _tie_free(rows, n, rng, eps):
     raise AssertionError("not enough tie-free tokens")
 
 
-def test_fp8_full_depth_all_rows():
+@pytest.mark.parametrize("cfgname,P", [("dream7b_spread", 512), ("llada8b_spread", 1024)])
+def test_fp8_full_depth_all_rows(cfgname, P):
     import paper_2512_16229_amd as lp
-    cfg = synth.config("dream7b_spread")
+    cfg = synth.config(cfgname)
     log(f"full shape {cfg['name']} fp8: prefix {P}, k {K}")
     w = synth.model_weights(cfg, device="cuda", dtype=torch.bfloat16)
     model = lp.Model(cfg, w, precision="fp8")
@@ -85,4 +87,4 @@ def test_fp8_full_depth_all_rows():
     # the first, a middle and the last layer fed the GPU's own input (the FP8
     # oracle quantises a layer's 233 M weights in tens of seconds)
     check_forward(s, bt, conf_g, pred_g, layers=[0, cfg["layers"] // 2, cfg["layers"] - 1],
-                  label="dream7b fp8 verify forward")
+                  label=f"{cfgname} fp8 verify forward")
