@@ -1,7 +1,8 @@
 """GPU parity of the FP8 model mode (LOPA_PRECISION_FP8: QKV, O, gate / up /
 down and the LM head in W8A8 E4M3) at the full Dream-7B shape, prefix 512, k = 7,
-in the launch configuration bench.py times for its FP8 step figure, and at the
-LLaDA-8B layout (multi-head attention, other tile widths), prefix 1024: one verify
+in the launch configuration bench.py times for its FP8 step figure, at prefix
+2048, k = 15 (two row tiles, the grouped attention form) and at the LLaDA-8B
+layout (multi-head attention, other tile widths), prefix 1024: one verify
 forward of all 8 x 32 rows, every layer fed the GPU's own input residual stream
 against the oracle's "fp8" mode layer (fixed rel-L2), and the oracle's FP8 LM
 head + softmax on the GPU's own final rows (confidences within 1e-3, candidate
@@ -23,7 +24,7 @@ from oracle.model import rms_norm
 
 pytestmark = pytest.mark.gpu
 
-L, K = 32, 7
+L = 32
 
 
 class _Layers:
@@ -50,8 +51,9 @@ def _tie_free(rows, n, rng, eps):
     raise AssertionError("not enough tie-free tokens")
 
 
-@pytest.mark.parametrize("cfgname,P", [("dream7b_spread", 512), ("llada8b_spread", 1024)])
-def test_fp8_full_depth_all_rows(cfgname, P):
+@pytest.mark.parametrize("cfgname,P,K", [("dream7b_spread", 512, 7), ("dream7b_spread", 2048, 15),
+                                         ("llada8b_spread", 1024, 7)])
+def test_fp8_full_depth_all_rows(cfgname, P, K):
     import paper_2512_16229_amd as lp
     cfg = synth.config(cfgname)
     log(f"full shape {cfg['name']} fp8: prefix {P}, k {K}")
@@ -61,7 +63,7 @@ def test_fp8_full_depth_all_rows(cfgname, P):
     dec = lp.Decoder(model, kv, L, K, 0.9)
     assert dec.prefill(synth.prompt(cfg, P, device="cuda")) == P
     rng = np.random.default_rng(12)
-    cand = rng.choice(cfg["vocab"] - 1, 2048, replace=False)
+    cand = rng.choice(cfg["vocab"] - 1, 4096, replace=False)
     emb = w["embed"][torch.tensor(cand, device="cuda")].float().cpu().numpy().astype(np.float64)
     bt = cand[_tie_free(emb, (K + 1) * L, rng, cfg["rms_eps"])].reshape(K + 1, L)
     host = {"embed": w["embed"].float().cpu(), "layers": _Layers(w),
