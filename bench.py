@@ -135,7 +135,7 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}))
 
 
-def hbm_counter_run(cfg, P, L, k, reps=3):
+def hbm_counter_run(cfg, P, L, k, reps=3, precision="bf16"):
     """Torch-free verify forwards on the given shape for the HBM counter runs
     (rocprofv3 --pmc): weights are constant fills, which changes no traffic."""
     import ctypes as C
@@ -164,7 +164,8 @@ def hbm_counter_run(cfg, P, L, k, reps=3):
             raise RuntimeError(lib.lopa_last_error().decode())
 
     model, kv = C.c_void_p(), C.c_void_p()
-    ok(lib.lopa_model_create(C.byref(c), C.byref(wp), None, C.byref(model)))
+    prec = {"bf16": 0, "fp8_mlp": 1, "fp8": 2}[precision]  # LOPA_PRECISION_*
+    ok(lib.lopa_model_create_ex(C.byref(c), C.byref(wp), prec, None, C.byref(model)))
     nb = k + 1
     ok(lib.lopa_kv_create(model, P + L, nb, L, C.byref(kv)))
     tokens = hip.alloc(4 * nb * L)  # token 0 everywhere
@@ -174,7 +175,7 @@ def hbm_counter_run(cfg, P, L, k, reps=3):
     hip.check(hip.rt.hipDeviceSynchronize(), "hipDeviceSynchronize")
     lib.lopa_kv_destroy(kv)
     lib.lopa_model_destroy(model)
-    print(json.dumps({"verify_forwards": reps, "rows": nb * L, "prefix": P}))
+    print(json.dumps({"verify_forwards": reps, "rows": nb * L, "prefix": P, "precision": precision}))
 
 
 def host_info():
@@ -567,7 +568,8 @@ def main():
                                                       os.path.join(ROOT, "synth", "shapes.py"))
         shapes = importlib.util.module_from_spec(spec)
         spec.loader.exec_module(shapes)
-        hbm_counter_run(shapes.config(args.config), args.prefix, args.block, args.k)
+        hbm_counter_run(shapes.config(args.config), args.prefix, args.block, args.k,
+                        precision=args.precision)
         return
 
     import torch
