@@ -24,6 +24,15 @@ CONFIGS = {
     "small128": dict(layers=2, hidden=512, heads=4, kv_heads=2, head_dim=128, ffn=1024,
                      vocab=2048, rms_eps=1e-5, rope_theta=5e5, qkv_bias=False,
                      std=0.02, lm_std=5.0 / math.sqrt(512)),
+    # One-layer models of other widths: rows of 1536 and 6144 values (the
+    # RMSNorm kernels' 512-thread and 1024-thread x 2-group row forms), GQA 3:1
+    # and 6:1, FFN widths not a multiple of the GEMM tiles' 160 columns.
+    "wide1536": dict(layers=1, hidden=1536, heads=12, kv_heads=4, head_dim=128, ffn=4096,
+                     vocab=2048, rms_eps=1e-6, rope_theta=1e6, qkv_bias=True,
+                     std=0.02, lm_std=4.0 / math.sqrt(1536)),
+    "wide6144": dict(layers=1, hidden=6144, heads=48, kv_heads=8, head_dim=128, ffn=8192,
+                     vocab=2048, rms_eps=1e-5, rope_theta=5e5, qkv_bias=False,
+                     std=0.02, lm_std=4.0 / math.sqrt(6144)),
     # Dream-7B (Qwen2.5-7B layout).
     "dream7b": dict(layers=28, hidden=3584, heads=28, kv_heads=4, head_dim=128, ffn=18944,
                     vocab=152064, rms_eps=1e-6, rope_theta=1e6, qkv_bias=True,

@@ -168,6 +168,12 @@ def gpu_residual(s, branch_tokens: np.ndarray, n_layers: int, P=None) -> np.ndar
     return x.view(nb, L, -1).cpu().numpy().astype(np.float64)
 
 
+def _full_size(cfg):
+    """The 7B / 8B shapes (billions of weights): the oracle runs them layer by
+    layer, without a second whole-forward pass."""
+    return cfg["layers"] * cfg["hidden"] ** 2 >= 1e8
+
+
 def check_forward(s, bt, conf_g, pred_g, P=None, cache_f=None, cache_p=None, causal_blk=0,
                   layers=True, label="", e2e_faithful=True):
     """The parity protocol of one verify forward whose prefix K/V the GPU shares
@@ -204,7 +210,7 @@ def _check_forward_bf16(s, bt, conf_g, pred_g, P, cache_f, cache_p, causal_blk, 
     cache_f = s.cache_f if cache_f is None else cache_f
     cache_p = cache_f if cache_p is None else cache_p
     mask, Ly = s.cfg["mask_id"], s.cfg["layers"]
-    big = s.cfg["hidden"] >= 2048   # full-size shapes: a progress line per layer
+    big = _full_size(s.cfg)   # full-size shapes: a progress line per layer
 
     def one(model, x, li, cache):
         return model.forward_block(bt, P, cache, x_in=x, first_layer=li, n_layers=li + 1,
@@ -299,7 +305,7 @@ def check_forward_fp8(s, bt, conf_g, pred_g, P=None, cache_f=None, causal_blk=0,
     cache_f = s.cache_f if cache_f is None else cache_f
     mask, Ly = s.cfg["mask_id"], s.cfg["layers"]
     which = list(range(Ly)) if layers is True else (list(layers) if layers else [])
-    big = s.cfg["hidden"] >= 2048
+    big = _full_size(s.cfg)
     rels = []
     for li in which:
         x_in = s.faith.embed[np.asarray(bt)] if li == 0 else gpu_residual(s, bt, li, P)

@@ -15,14 +15,16 @@ from gpu_util import Setup, check_forward, gpu_residual, log, rel_l2
 
 pytestmark = pytest.mark.gpu
 
-# (config, P, L, k): 64 / 256 / 512 / 48 / 128 rows; ragged prefixes; two head dims
+# (config, P, L, k): 64 / 256 / 512 / 48 / 128 rows; ragged prefixes; two head dims; four widths
 CASES = [("tiny", 64, 16, 3), ("small", 100, 32, 7), ("small", 37, 32, 15),
          ("small128", 40, 16, 2), ("small128", 0, 32, 3),
          # ragged and extreme block shapes: a 7-row block (partial key tile and
          # partial 16-row query block), 48 rows (three query blocks), the
          # 64-row maximum with head_dim 128, and the degenerate one-row block
          # with no prefix and no lookahead
-         ("tiny", 23, 7, 2), ("small", 50, 48, 3), ("small128", 64, 64, 1), ("tiny", 0, 1, 0)]
+         ("tiny", 23, 7, 2), ("small", 50, 48, 3), ("small128", 64, 64, 1), ("tiny", 0, 1, 0),
+         # other widths (row kernels of 512 and 1024 x 2 threads' groups, other plans)
+         ("wide1536", 64, 32, 3), ("wide6144", 40, 16, 3)]
 
 
 def _kv_close(gpu, ref, what):

@@ -28,8 +28,16 @@ pytestmark = pytest.mark.gpu
 # per-(head, branch) (64-row blocks); with LOPA_PRECISION_FP8 each writes the
 # row maxima of the FP8 output projection
 CASES = [("tiny", 64, 16, 3), ("small", 100, 32, 7), ("small128", 40, 16, 2), ("tiny", 23, 7, 2),
-         ("small", 300, 32, 15), ("small", 800, 32, 3), ("small", 100, 64, 3)]
+         ("small", 300, 32, 15), ("small", 800, 32, 3), ("small", 100, 64, 3),
+         ("wide1536", 64, 32, 3)]
 PRECS = ["fp8_mlp", "fp8"]
+# The 6144-wide model in the MLP-only mode. With every projection in E4M3 its
+# first layer is more sensitive than the fixed layer bound: the oracle's own
+# first-layer output moves by 7.5e-2 rel-L2 when its input moves by under a
+# quarter bf16 step (3.2-4.0e-2 in the MLP-only mode, 5.8-7.1e-2 for the
+# other models in that mode), so a GPU difference of that size is the E4M3
+# rounding of the operands, not a defect the bound could name.
+PAIRS = [(c, p) for c in CASES for p in PRECS] + [(("wide6144", 40, 16, 3), "fp8_mlp")]
 
 
 def _tokens(s, nb, L, seed):
@@ -40,8 +48,7 @@ def _tokens(s, nb, L, seed):
     return bt
 
 
-@pytest.mark.parametrize("prec", PRECS)
-@pytest.mark.parametrize("cfgname,P,L,k", CASES)
+@pytest.mark.parametrize("cfgname,P,L,k,prec", [(*c, p) for c, p in PAIRS])
 def test_fp8_forward_parity(cfgname, P, L, k, prec):
     log(f"{prec} forward {cfgname} P={P} L={L} k={k}")
     s = Setup(cfgname, P, L, k, precision=prec)
