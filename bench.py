@@ -554,8 +554,9 @@ def main():
                     help="only time the step's GEMM shapes through torch.matmul (vendor BLAS)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(multi-GPU branch parallelism is a design note, not built)", file=sys.stderr)
+        print(f"bench.py: the library runs the verify step on one GPU; --gpus {args.gpus} is "
+              "not supported (branch parallelism over several GPUs is not implemented)",
+              file=sys.stderr)
         sys.exit(2)
 
     if args.copy_calibration:
